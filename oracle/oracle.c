@@ -1,0 +1,247 @@
+/*
+ * CPU oracle of the data-parallel update -- TEST INFRASTRUCTURE ONLY.
+ *
+ * Only the tests, the smoke check and the benchmark's CPU-baseline leg load
+ * this file's library.  The HIP library never includes or calls it and the
+ * two share no code.
+ *
+ * What it computes, per call over a list of flat layer segments that all have
+ * R gradient buffers:
+ *   1. g_bar[i] = fp32( (sum over ranks r of bf16 G_r[i], in FP64) / R )
+ *      -- the rank gradients are summed and averaged into one gradient
+ *      (Design, shared host state and communication routes: gradient return
+ *      by GPU reduction).
+ *   2. S = sum over every element of every segment of g_bar[i]^2 in FP64;
+ *      norm = sqrt(S).  The paper never mentions clipping; the global L2
+ *      norm of the mean gradient is taken as the quantity to clip by.
+ *   3. c = min(1, max_norm / (norm + 1e-6)) when max_norm > 0, else 1.
+ *      A non-finite norm leaves every state unchanged.
+ *   4. AdamW per element in FP64 (Loshchilov & Hutter, decoupled weight
+ *      decay; Kingma & Ba bias correction), with g = g_bar[i] * c:
+ *        p1 = p - (lr * wd) * p
+ *        m' = beta1 * m + (1 - beta1) * g
+ *        v' = beta2 * v + (1 - beta2) * g^2
+ *        p' = p1 - lr * (m' / (1 - beta1^t)) / (sqrt(v' / (1 - beta2^t)) + eps)
+ *      The paper calls the update mixed-precision Adam over FP32 master
+ *      weights and FP32 moments (Background, training states table; Design,
+ *      the rank-0 update worker).
+ *   5. master = fp32(p'), exp_avg = fp32(m'), exp_avg_sq = fp32(v'),
+ *      param_bf16 = bf16(master) -- BF16 compute weights for the next
+ *      dispatch (training states table; Design, overlap within a layer).
+ * fp32() is the C conversion from double (round to nearest, ties to even);
+ * bf16() is round to nearest even on the 8-bit significand, written below
+ * from that definition.
+ *
+ * Parallelism: the per-element update loop (independent elements) runs under
+ * OpenMP; the norm is one sequential FP64 sum in index order.
+ */
+#include "oracle.h"
+
+#include <math.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+static double f32_bits_value(uint32_t bits)
+{
+    float f;
+    memcpy(&f, &bits, sizeof f);
+    return (double)f;
+}
+
+/* Round an FP32 value to the nearest BF16 value, ties to the BF16 value
+ * whose last significand bit is zero.  BF16 keeps the FP32 sign and exponent
+ * and the top 7 stored significand bits, so its values are exactly the FP32
+ * values whose low 16 bits are zero.  The two candidates are the truncation
+ * of |x| and the next BF16 value above it; an FP32 value above the largest
+ * finite BF16 value by half a BF16 step or more rounds to infinity.  NaN
+ * stays NaN with the quiet bit set; infinities and signed zeros are kept;
+ * subnormals are rounded like any other value. */
+uint16_t orc_bf16_from_f32(float x)
+{
+    uint32_t u;
+    memcpy(&u, &x, sizeof u);
+    uint32_t sign = u & 0x80000000u;
+    uint32_t mag = u & 0x7fffffffu;
+    if (mag > 0x7f800000u)
+        return (uint16_t)((u >> 16) | 0x0040u);
+    uint32_t lo = mag & 0xffff0000u;
+    if (lo == mag)
+        return (uint16_t)(u >> 16);
+    uint32_t hi = lo + 0x10000u;
+    double a = f32_bits_value(mag);
+    double vlo = f32_bits_value(lo);
+    /* one step above the largest finite BF16 magnitude is 2^128 */
+    double vhi = (hi == 0x7f800000u) ? ldexp(1.0, 128) : f32_bits_value(hi);
+    double dlo = a - vlo, dhi = vhi - a;
+    uint32_t pick;
+    if (dlo < dhi)
+        pick = lo;
+    else if (dhi < dlo)
+        pick = hi;
+    else
+        pick = ((lo >> 16) & 1u) ? hi : lo;
+    return (uint16_t)((sign | pick) >> 16);
+}
+
+float orc_f32_from_bf16(uint16_t b)
+{
+    uint32_t u = (uint32_t)b << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return f;
+}
+
+void orc_bf16_array(const float *x, uint16_t *out, int64_t n)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i)
+        out[i] = orc_bf16_from_f32(x[i]);
+}
+
+/* Step 1: mean over ranks of one element's gradients, rounded once to FP32.
+ * Ranks are added in rank order in FP64 (exact for BF16 inputs whose
+ * magnitudes span less than about 2^45). */
+float orc_mean_grad(const uint16_t *const *grads, int32_t R, int64_t i)
+{
+    double s = 0.0;
+    for (int32_t r = 0; r < R; ++r)
+        s += (double)orc_f32_from_bf16(grads[r][i]);
+    return (float)(s / (double)R);
+}
+
+void orc_mean_grads(const uint16_t *const *grads, int32_t R, int64_t n, float *out)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i)
+        out[i] = orc_mean_grad(grads, R, i);
+}
+
+/* Step 2: global L2 norm of the mean gradient over all segments. */
+double orc_grad_norm(const orc_segment *segs, int32_t n_segs, int32_t R)
+{
+    double S = 0.0;
+    for (int32_t s = 0; s < n_segs; ++s) {
+        for (int64_t i = 0; i < segs[s].numel; ++i) {
+            double g = (double)orc_mean_grad(segs[s].grads, R, i);
+            S += g * g;
+        }
+    }
+    return sqrt(S);
+}
+
+/* Step 3: clip coefficient. */
+double orc_clip_coef(double norm, double max_grad_norm)
+{
+    if (!(max_grad_norm > 0.0))
+        return 1.0;
+    double c = max_grad_norm / (norm + 1e-6);
+    return c < 1.0 ? c : 1.0;
+}
+
+/* Step 4 for one element, no rounding. */
+static void adamw_element(double p, double m, double v, double g,
+                          const orc_hparams *hp, double bc1, double bc2,
+                          double *po, double *mo, double *vo)
+{
+    double p1 = p - (hp->lr * hp->weight_decay) * p;
+    double m1 = hp->beta1 * m + (1.0 - hp->beta1) * g;
+    double v1 = hp->beta2 * v + (1.0 - hp->beta2) * (g * g);
+    double m_hat = m1 / bc1;
+    double v_hat = v1 / bc2;
+    *po = p1 - hp->lr * m_hat / (sqrt(v_hat) + hp->eps);
+    *mo = m1;
+    *vo = v1;
+}
+
+static void bias_corrections(const orc_hparams *hp, double *bc1, double *bc2)
+{
+    *bc1 = 1.0 - pow(hp->beta1, (double)hp->step);
+    *bc2 = 1.0 - pow(hp->beta2, (double)hp->step);
+}
+
+/* Step 4 on FP64 arrays with FP64 results (used by the library cross-check). */
+void orc_adamw_f64(int64_t n, const double *p, const double *m, const double *v,
+                   const double *g, const orc_hparams *hp,
+                   double *p_out, double *m_out, double *v_out)
+{
+    double bc1, bc2;
+    bias_corrections(hp, &bc1, &bc2);
+    for (int64_t i = 0; i < n; ++i)
+        adamw_element(p[i], m[i], v[i], g[i], hp, bc1, bc2,
+                      &p_out[i], &m_out[i], &v_out[i]);
+}
+
+/* Steps 4 and 5 for one element given its mean gradient and clip coefficient. */
+static void update_one(float *p, float *m, float *v, uint16_t *pb, float g_bar,
+                       double c, const orc_hparams *hp, double bc1, double bc2)
+{
+    double po, mo, vo;
+    adamw_element((double)*p, (double)*m, (double)*v, (double)g_bar * c, hp,
+                  bc1, bc2, &po, &mo, &vo);
+    *p = (float)po;
+    *m = (float)mo;
+    *v = (float)vo;
+    *pb = orc_bf16_from_f32(*p);
+}
+
+/* One full optimizer step over all segments; states are updated in place.
+ * Returns ORC_NONFINITE (states untouched) when the norm is not finite. */
+int orc_step(orc_segment *segs, int32_t n_segs, int32_t R, const orc_hparams *hp,
+             double *norm_out)
+{
+    if (R < 1 || n_segs < 0 || hp->step < 1)
+        return ORC_INVALID;
+    double norm = orc_grad_norm(segs, n_segs, R);
+    if (norm_out)
+        *norm_out = norm;
+    if (!isfinite(norm))
+        return ORC_NONFINITE;
+    double c = orc_clip_coef(norm, hp->max_grad_norm);
+    double bc1, bc2;
+    bias_corrections(hp, &bc1, &bc2);
+    for (int32_t s = 0; s < n_segs; ++s) {
+        orc_segment *sg = &segs[s];
+#pragma omp parallel for schedule(static)
+        for (int64_t i = 0; i < sg->numel; ++i)
+            update_one(&sg->master[i], &sg->exp_avg[i], &sg->exp_avg_sq[i],
+                       &sg->param_bf16[i], orc_mean_grad(sg->grads, R, i), c,
+                       hp, bc1, bc2);
+    }
+    return ORC_OK;
+}
+
+/* Steps 1, 4 and 5 at n independent points whose clip coefficient is already
+ * known (for sampled checks of large states).  g_rows holds the R BF16
+ * gradients of point k at g_rows[k * R + r]. */
+void orc_update_points(int64_t n, const float *p, const float *m, const float *v,
+                       const uint16_t *g_rows, int32_t R, double clip_coef,
+                       const orc_hparams *hp, float *p_out, float *m_out,
+                       float *v_out, uint16_t *pb_out)
+{
+    double bc1, bc2;
+    bias_corrections(hp, &bc1, &bc2);
+    if (R < 1 || R > ORC_MAX_RANKS)
+        return;
+    for (int64_t k = 0; k < n; ++k) {
+        const uint16_t *rows[ORC_MAX_RANKS];
+        for (int32_t r = 0; r < R; ++r)
+            rows[r] = &g_rows[k * R + r];
+        float g_bar = orc_mean_grad(rows, R, 0);
+        p_out[k] = p[k];
+        m_out[k] = m[k];
+        v_out[k] = v[k];
+        update_one(&p_out[k], &m_out[k], &v_out[k], &pb_out[k], g_bar,
+                   clip_coef, hp, bc1, bc2);
+    }
+}
+
+int orc_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

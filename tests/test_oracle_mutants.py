@@ -1,0 +1,78 @@
+"""Planted mistakes in copies of the oracle must each fail some pin.
+
+Every mutation below is a plausible slip (a dropped term, a wrong sign, a
+wrong index, a misplaced constant).  Each is applied to a copy of oracle.c in
+a temporary directory, compiled, and run through the pins; the test passes
+only if some pin rejects it.  The real oracle is never modified.
+"""
+import os
+import shutil
+
+import pytest
+
+import oracle
+import pins
+
+MUTATIONS = {
+    "decay_dropped": ("double p1 = p - (hp->lr * hp->weight_decay) * p;", "double p1 = p;"),
+    "decay_sign": ("double p1 = p - (hp->lr", "double p1 = p + (hp->lr"),
+    "decay_uses_lr_only": ("(hp->lr * hp->weight_decay) * p", "(hp->weight_decay) * p"),
+    "m_history_dropped": ("double m1 = hp->beta1 * m +", "double m1 = 0.0 * m +"),
+    "m_wrong_coef": ("(1.0 - hp->beta1) * g;", "hp->beta1 * g;"),
+    "v_not_squared": ("(1.0 - hp->beta2) * (g * g)", "(1.0 - hp->beta2) * fabs(g)"),
+    "v_uses_beta1": ("double v1 = hp->beta2 * v", "double v1 = hp->beta1 * v"),
+    "eps_inside_sqrt": ("(sqrt(v_hat) + hp->eps)", "sqrt(v_hat + hp->eps)"),
+    "no_bias_correction_1": ("double m_hat = m1 / bc1;", "double m_hat = m1;"),
+    "no_bias_correction_2": ("double v_hat = v1 / bc2;", "double v_hat = v1;"),
+    "step_sign": ("*po = p1 - hp->lr", "*po = p1 + hp->lr"),
+    "bias_uses_step_minus_1": ("pow(hp->beta1, (double)hp->step)", "pow(hp->beta1, (double)(hp->step + 1))"),
+    "mean_not_divided": ("return (float)(s / (double)R);", "return (float)s;"),
+    "mean_rank0_only": ("s += (double)orc_f32_from_bf16(grads[r][i]);",
+                        "s += (double)orc_f32_from_bf16(grads[0][i]);"),
+    "mean_fp32_sum": ("double s = 0.0;\n    for (int32_t r = 0; r < R; ++r)\n        s += (double)orc_f32_from_bf16(grads[r][i]);",
+                      "float s = 0.0f;\n    for (int32_t r = 0; r < R; ++r)\n        s += orc_f32_from_bf16(grads[r][i]);"),
+    "norm_no_sqrt": ("return sqrt(S);", "return S;"),
+    "norm_first_segment_only": ("for (int32_t s = 0; s < n_segs; ++s) {\n        for (int64_t i = 0; i < segs[s].numel; ++i) {",
+                                "for (int32_t s = 0; s < 1; ++s) {\n        for (int64_t i = 0; i < segs[s].numel; ++i) {"),
+    "clip_uncapped": ("return c < 1.0 ? c : 1.0;", "return c;"),
+    "clip_no_guard": ("max_grad_norm / (norm + 1e-6)", "max_grad_norm / norm"),
+    "clip_applied_to_square": ("(double)g_bar * c, hp,", "(double)g_bar * c * c, hp,"),
+    "nonfinite_not_skipped": ("if (!isfinite(norm))\n        return ORC_NONFINITE;", ""),
+    "bf16_ties_odd": ("pick = ((lo >> 16) & 1u) ? hi : lo;", "pick = ((lo >> 16) & 1u) ? lo : hi;"),
+    "bf16_truncates": ("if (dlo < dhi)\n        pick = lo;", "if (1)\n        pick = lo;"),
+    "bf16_nan_not_quiet": ("return (uint16_t)((u >> 16) | 0x0040u);", "return (uint16_t)(u >> 16);"),
+    "bf16_no_overflow_to_inf": ("ldexp(1.0, 128)", "ldexp(1.0, 200)"),
+    "param_from_unrounded": ("*pb = orc_bf16_from_f32(*p);", "*pb = orc_bf16_from_f32((float)(po + 1e-9));"),
+}
+
+# cheap pins first so that most mutants are rejected quickly
+ORDER = ["pin_bf16_special_values", "pin_mean_closed_forms", "pin_norm_constant",
+         "pin_clip_coef", "pin_first_step_sign", "pin_zero_gradient", "pin_sign_descent",
+         "pin_lr_zero", "pin_identical_ranks", "pin_clip_noop", "pin_nonfinite",
+         "pin_param_is_bf16_of_master", "pin_mean_vs_numpy", "pin_norm_vs_torch",
+         "pin_adamw_f64_vs_torch", "pin_bf16_random_vs_torch", "pin_step_vs_torch",
+         "pin_brute_force"]
+
+
+def test_order_covers_all_pins():
+    assert sorted(ORDER) == sorted(p.__name__ for p in pins.ALL_PINS)
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_mutant_is_rejected(name, tmp_path):
+    here = os.path.dirname(oracle.__file__)
+    src = open(os.path.join(here, "oracle.c")).read()
+    old, new = MUTATIONS[name]
+    assert src.count(old) == 1, "mutation anchor not found exactly once"
+    shutil.copy(os.path.join(here, "oracle.h"), tmp_path / "oracle.h")
+    (tmp_path / "oracle.c").write_text(src.replace(old, new))
+    lib = oracle.load(oracle.build(src=str(tmp_path / "oracle.c"),
+                                   out=str(tmp_path / "liboracle_mutant.so")))
+    failed_by = None
+    for pname in ORDER:
+        try:
+            getattr(pins, pname)(lib)
+        except AssertionError:
+            failed_by = pname
+            break
+    assert failed_by is not None, f"mutation {name} passed every pin"
