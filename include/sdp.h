@@ -1,0 +1,236 @@
+/*
+ * sdp.h -- C ABI of libsdp, the MI355X (gfx950) library for the data-parallel
+ * optimizer update of SlideDP (arxiv 2609.34162): aggregate the BF16
+ * gradients of R data-parallel ranks, clip by the global L2 norm, apply
+ * mixed-precision AdamW to FP32 master weights and moments, and re-emit BF16
+ * parameters.
+ *
+ * The paper keeps one FP32 master copy and two FP32 Adam moments per layer,
+ * updated once per iteration from the gradient averaged over all ranks, and
+ * hands BF16 copies of the weights to the ranks for the next forward pass
+ * (Background, training-state table; Design, shared host state and
+ * communication routes; Design, cross-rank pipelining and chunked overlap).
+ * The paper runs that update on host CPUs.  This library runs it on the GPU,
+ * either on states in device memory (sdp_agg_adam_step) or on states in
+ * pinned host memory streamed through the GPU in double-buffered chunks
+ * (sdp_stream_step).
+ *
+ * Conventions for every call:
+ *  - Return value: SDP_OK (0) or a negative SDP_ERR_* status.  A failing call
+ *    validates before it enqueues anything, so it has no side effects, except
+ *    SDP_ERR_HIP, which reports a HIP runtime failure (text in
+ *    sdp_last_error()).
+ *  - sdp_last_error() returns the detail of the last failure on the calling
+ *    thread (thread-local, valid until the next call on that thread).
+ *  - A "stream" argument is a hipStream_t passed as void*; NULL is the null
+ *    stream.  The header needs no HIP include.
+ *  - The caller owns every state and gradient buffer.  The library never
+ *    frees them and keeps no pointer to them after the work it enqueued
+ *    completes.  The context owns its workspace.
+ *  - One context is not thread-safe; different contexts are independent.
+ *
+ * Numerics (the paper never states the optimizer formulas; these follow
+ * AdamW with decoupled decay, Loshchilov & Hutter, and Kingma & Ba bias
+ * correction):
+ *    g_bar[i] = fp32( (sum_r bf16 G_r[i], summed in FP64 in rank order) / R )
+ *    norm     = sqrt( sum over all elements of all segments of g_bar^2 ) (FP64)
+ *    c        = min(1, max_grad_norm / (norm + 1e-6)) if max_grad_norm > 0, else 1
+ *    g        = g_bar * c
+ *    p1 = p - lr*wd*p ; m' = b1*m + (1-b1)*g ; v' = b2*v + (1-b2)*g^2
+ *    p' = p1 - (lr / (1 - b1^t)) * m' / (sqrt(v' / (1 - b2^t)) + eps)
+ *    master = fp32(p'), exp_avg = fp32(m'), exp_avg_sq = fp32(v'),
+ *    param_bf16 = bf16_rne(master)
+ *  The per-element update is evaluated in FP64 registers and rounded once.
+ *  A non-finite norm leaves every state and parameter unchanged.
+ *  Results do not depend on the chunk size, on the mode (device or
+ *  streamed) or on run-to-run scheduling: the norm is a fixed-order tree
+ *  over fixed 65,536-element tiles of each segment.
+ */
+#ifndef SDP_H
+#define SDP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+#define SDP_OK 0
+#define SDP_ERR_INVALID_ARGUMENT (-1)  /* NULL pointer, bad size, R out of range, aliasing */
+#define SDP_ERR_ALIGNMENT (-2)         /* a buffer is not 16-byte aligned */
+#define SDP_ERR_NOT_DEVICE_MEMORY (-3) /* device mode got a pointer that is not device memory of ctx's GPU, or a range that overruns its allocation */
+#define SDP_ERR_NOT_PINNED (-4)        /* streamed mode got host memory that is not pinned */
+#define SDP_ERR_CHUNK_TOO_LARGE (-5)   /* chunk_elems exceeds the context's staging */
+#define SDP_ERR_OUT_OF_MEMORY (-6)     /* workspace allocation failed */
+#define SDP_ERR_HIP (-7)               /* HIP runtime error; see sdp_last_error() */
+#define SDP_ERR_NONFINITE (-8)         /* gradient norm is NaN or Inf; nothing was updated */
+
+/* ---- constants --------------------------------------------------------- */
+#define SDP_NORM_TILE 65536 /* elements per norm partial; chunk sizes are multiples of it */
+#define SDP_MAX_RANKS 16    /* largest R */
+#define SDP_ALIGN 16        /* byte alignment required of every buffer */
+
+/* ---- context flags ----------------------------------------------------- */
+/* Device mode: whether the norm pass stores g_bar (4 B/element of workspace)
+ * so that the update pass reads 4 B instead of 2R B per element.  Default
+ * (neither flag): stored when R > 4, where it moves fewer bytes. */
+#define SDP_FLAG_DEVICE_GBAR_NEVER 0x1u
+#define SDP_FLAG_DEVICE_GBAR_ALWAYS 0x2u
+/* Streamed mode: by default g_bar is kept in device memory between the norm
+ * pass and the update pass, so each gradient crosses the host link once.
+ * With this flag the gradients are streamed a second time instead. */
+#define SDP_FLAG_STREAM_GBAR_NEVER 0x4u
+/* Streamed mode: after each staging slot is released, fill it with a NaN
+ * pattern (debug aid: a missing wait then shows up as corrupted results). */
+#define SDP_FLAG_DEBUG_POISON 0x8u
+
+/* ---- types ------------------------------------------------------------- */
+typedef struct sdp_ctx sdp_ctx;
+
+/* Hyperparameters of one step.  step = t >= 1 is the 1-based optimizer step
+ * used for bias correction; max_grad_norm <= 0 disables clipping. */
+typedef struct {
+    double lr, beta1, beta2, eps, weight_decay, max_grad_norm;
+    int64_t step;
+} sdp_adamw_params;
+
+/* One flat layer state: all its tensors concatenated, numel elements.
+ * master / exp_avg / exp_avg_sq: FP32, updated in place.
+ * param_bf16: BF16 bit patterns (uint16), written.
+ * grads: array of n_ranks pointers, each to numel BF16 bit patterns (read only).
+ * n_ranks must be the same for every segment of a call, 1..SDP_MAX_RANKS.
+ * Gradients must not overlap any state; param_bf16 must not overlap master.
+ * Every pointer must be SDP_ALIGN-byte aligned; numel >= 1, any value. */
+typedef struct {
+    float *master;
+    float *exp_avg;
+    float *exp_avg_sq;
+    uint16_t *param_bf16;
+    const uint16_t *const *grads;
+    int32_t n_ranks;
+    int64_t numel;
+} sdp_segment;
+
+/* Accumulated kernel times of a context, from HIP events recorded around
+ * each launch on the stream the launch uses (only while timing is on). */
+typedef struct {
+    double norm_ms;       /* norm-partials kernel (step a3, first pass) */
+    double finalize_ms;   /* norm finalize kernel */
+    double update_ms;     /* fused aggregate + clip + AdamW + BF16 kernel */
+    int64_t norm_launches, finalize_launches, update_launches;
+    int64_t update_elems; /* elements processed by the timed update launches */
+} sdp_kernel_times;
+
+/* ---- context ----------------------------------------------------------- */
+
+/* Create a context on GPU `device`.  max_chunk_elems > 0 reserves two
+ * streamed-mode staging slots of (14 + 2*max_ranks) * max_chunk_elems bytes
+ * each (0: device mode only); it must be a multiple of SDP_NORM_TILE.
+ * max_ranks in 1..SDP_MAX_RANKS bounds R for streamed mode staging.  The
+ * context creates two streams (default priority) and its events.  Other
+ * workspace (norm partials, cached g_bar) grows on demand. */
+int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems,
+                   int32_t max_ranks, uint32_t flags);
+void sdp_ctx_destroy(sdp_ctx *ctx);
+
+/* ---- the update -------------------------------------------------------- */
+
+/* Device mode.  All state and gradient buffers are device memory of ctx's
+ * GPU.  Enqueues on `stream`: the norm pass over every tile of every segment
+ * (segment order, then tile order), the one-block norm finalize, and the
+ * fused update over every element; the update reads the clip coefficient and
+ * the non-finite flag from device memory, so nothing returns to the host.
+ * chunk_elems (0 or a multiple of SDP_NORM_TILE) names the unit the caller
+ * works in; results never depend on it, and each segment is covered by one
+ * launch per kernel.  Asynchronous unless grad_norm_out is non-NULL: then the
+ * call waits for the stream, stores the pre-clip norm, and returns
+ * SDP_ERR_NONFINITE if it is not finite (states unchanged).  Without
+ * grad_norm_out a non-finite norm still leaves the states unchanged, and
+ * sdp_ctx_last_norm() reports it after the stream has finished.  The caller
+ * keeps the buffers alive until the stream has finished the work. */
+int sdp_agg_adam_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs,
+                      const sdp_adamw_params *hp, int64_t chunk_elems,
+                      void *stream, double *grad_norm_out);
+
+/* Streamed mode.  All state and gradient buffers are pinned host memory
+ * (e.g. from sdp_host_alloc).  chunk_elems: a multiple of SDP_NORM_TILE,
+ * at most the context's max_chunk_elems, and n_ranks <= its max_ranks.
+ * Phase 1 copies each chunk's R gradients host-to-device on the copy
+ * stream and runs the norm pass on the compute stream, alternating two
+ * staging slots ordered by events; then the norm is finalized and read back.
+ * Phase 2 copies master/m/v of each chunk in, runs the fused update, and
+ * copies master/m/v and the BF16 parameters back to the same host locations
+ * on the compute stream, again double-buffered.  Blocks until every copy
+ * has landed.  Returns SDP_ERR_NONFINITE (states unchanged) for a
+ * non-finite norm.  grad_norm_out may be NULL. */
+int sdp_stream_step(sdp_ctx *ctx, const sdp_segment *host_segs, int32_t n_segs,
+                    const sdp_adamw_params *hp, int64_t chunk_elems,
+                    double *grad_norm_out);
+
+/* The global norm of the mean gradient alone (the first pass and finalize of
+ * either mode; device_resident selects device or pinned-host buffers; only
+ * grads, n_ranks and numel of each segment are read).  Blocks; chunk_elems
+ * is used in streamed mode only.  Stores the norm even if it is not finite
+ * and then returns SDP_ERR_NONFINITE. */
+int sdp_grad_norm(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs,
+                  int device_resident, int64_t chunk_elems, void *stream,
+                  double *norm_out);
+
+/* Norm, clip coefficient and non-finite flag of the last finished norm pass
+ * on this context (waits for the context's pending work). */
+int sdp_ctx_last_norm(sdp_ctx *ctx, double *norm, double *clip_coef, int *nonfinite);
+
+/* The BF16 re-emit on its own: dst[i] = bf16_rne(src[i]) for n elements of
+ * device memory (the same device routine the fused update uses).  NaN keeps
+ * its sign and top payload bits and gets the quiet bit. */
+int sdp_cast_bf16(sdp_ctx *ctx, const float *src, uint16_t *dst, int64_t n, void *stream);
+
+/* ---- planning (host only, no GPU needed) --------------------------------- */
+
+/* Chunks and norm tiles of a call: n_chunks = sum over segments of
+ * ceil(numel / chunk_elems), n_tiles = sum of ceil(numel / SDP_NORM_TILE). */
+int sdp_plan(const int64_t *numels, int32_t n_segs, int64_t chunk_elems,
+             int64_t *n_chunks_out, int64_t *n_tiles_out);
+
+/* Algorithmic bytes per element of one step: device mode HBM traffic, or
+ * streamed mode host-link traffic per direction (h2d, d2h), for R ranks and
+ * the given context flags' g_bar policy. */
+int sdp_bytes_per_elem(int streamed, int32_t n_ranks, uint32_t flags,
+                       double *hbm_or_h2d, double *d2h);
+
+/* ---- measurement support ---------------------------------------------- */
+
+/* Start (enable = 1, also clears) or stop (0) per-kernel event timing. */
+int sdp_ctx_set_timing(sdp_ctx *ctx, int enable);
+/* Sum of the recorded kernel times (waits for the recorded events). */
+int sdp_ctx_get_timing(sdp_ctx *ctx, sdp_kernel_times *out);
+
+/* Device-to-device copy of `bytes` (a multiple of 16) with the library's
+ * 16-byte-per-lane streaming pattern: the HBM ceiling and the scale for
+ * hardware traffic counters. */
+int sdp_probe_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, void *stream);
+
+/* Pinned host link bandwidth with the streamed engine's copy path:
+ * hipMemcpyAsync in chunk_bytes pieces over `bytes`, `reps` times, on the
+ * context's copy stream (H2D) and compute stream (D2H).  gbs_out[0] = H2D
+ * alone, [1] = D2H alone, [2] = H2D + D2H at once (sum of both directions).
+ * host_a/host_b: pinned host buffers, dev_a/dev_b: device buffers, each of
+ * at least `bytes`.  Blocks. */
+int sdp_probe_link(sdp_ctx *ctx, void *host_a, void *host_b, void *dev_a, void *dev_b,
+                   int64_t bytes, int64_t chunk_bytes, int32_t reps, double *gbs_out);
+
+/* Pinned host memory of exactly `bytes` (hipHostMalloc), for streamed-mode
+ * states; free with sdp_host_free. */
+int sdp_host_alloc(void **out, size_t bytes);
+int sdp_host_free(void *p);
+
+/* ---- errors ------------------------------------------------------------ */
+const char *sdp_status_string(int status);
+const char *sdp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SDP_H */

@@ -1,0 +1,64 @@
+// Internal interface between the C ABI (sdp_runtime.hip) and the gfx950
+// kernels (sdp_kernels.hip).  Not installed; not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "sdp.h"
+
+namespace sdp {
+
+// Result of the norm pass, kept in device memory so that the update kernel
+// reads the clip coefficient without a host round trip.
+struct NormState {
+    double sumsq;
+    double norm;
+    double clip;
+    int32_t nonfinite;
+    int32_t pad;
+};
+
+// One launch of the norm pass: `n` elements starting at a tile boundary of
+// a segment.  Block b covers elements [b*TILE, min((b+1)*TILE, n)) and writes
+// partials[b].  When gbar_out is non-null it also stores g_bar there.
+struct NormArgs {
+    const uint16_t *g[SDP_MAX_RANKS];
+    int64_t n;
+    double *partials;
+    float *gbar_out;
+};
+
+// One launch of the fused update over `n` elements.  Gradients come either
+// from the R BF16 buffers or, when gbar is non-null, from stored g_bar.
+struct UpdateArgs {
+    float *p, *m, *v;
+    uint16_t *pb;
+    const uint16_t *g[SDP_MAX_RANKS];
+    const float *gbar;
+    int64_t n;
+    const NormState *ns;
+    // per-step constants, computed once on the host in FP64
+    double lr_wd;      // lr * weight_decay
+    double beta1, one_minus_beta1;
+    double beta2, one_minus_beta2;
+    double step_size;  // lr / (1 - beta1^t)
+    double inv_bc2;    // 1 / (1 - beta2^t)
+    double eps;
+};
+
+constexpr int kTile = SDP_NORM_TILE;
+constexpr int kNormThreads = 256;
+constexpr int kFinalizeThreads = 1024;
+constexpr int kUpdateThreads = 256;
+constexpr int kVec = 8;  // elements per lane per access (16 B of BF16, 32 B of FP32)
+
+hipError_t launch_norm_partials(int R, const NormArgs &a, hipStream_t s);
+hipError_t launch_norm_finalize(const double *partials, int64_t n_partials,
+                                double max_grad_norm, NormState *ns, hipStream_t s);
+hipError_t launch_update(int R, const UpdateArgs &a, int max_blocks, hipStream_t s);
+hipError_t launch_cast_bf16(const float *src, uint16_t *dst, int64_t n, hipStream_t s);
+hipError_t launch_copy16(void *dst, const void *src, int64_t n16, int max_blocks, hipStream_t s);
+hipError_t launch_fill_u32(void *dst, int64_t n_words, uint32_t value, hipStream_t s);
+
+}  // namespace sdp

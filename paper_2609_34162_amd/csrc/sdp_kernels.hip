@@ -1,0 +1,380 @@
+// gfx950 kernels of the data-parallel update: norm partials over fixed tiles,
+// a one-block fixed-order finalize, and the fused aggregate + clip + AdamW +
+// BF16 re-emit pass.  All of them are bound by HBM bandwidth: every lane moves
+// 16-byte (dwordx4) accesses, eight elements at a time, and no MFMA is used.
+//
+// Element arithmetic (the paper names mixed-precision Adam over FP32 master
+// weights and moments, fed by the gradient averaged over the ranks, and BF16
+// compute weights; the formulas are AdamW with decoupled decay and
+// Kingma-Ba bias correction):
+//   g_bar = fp32(sum_r bf16 G_r, in FP64 in rank order, / R)
+//   g     = g_bar * c                               (c from the global norm)
+//   p1 = p - lr*wd*p ; m' = b1 m + (1-b1) g ; v' = b2 v + (1-b2) g^2
+//   p' = p1 - lr/(1-b1^t) * m' / (sqrt(v'/(1-b2^t)) + eps)
+// in FP64 registers, each output rounded once to FP32, BF16 from the FP32.
+#include "sdp_internal.h"
+
+namespace sdp {
+namespace {
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Round to nearest even on the top 16 bits.  NaN: keep sign and top payload
+// bits, set the quiet bit (adding the rounding bias could carry a NaN into
+// the infinity pattern).  Infinity stays infinity; overflow of the largest
+// finite values rounds to infinity as IEEE round-to-nearest does.
+__device__ __forceinline__ uint32_t bf16_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x0040u;
+    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+    return bf16_rne(lo) | (bf16_rne(hi) << 16);
+}
+
+template <int R>
+__device__ __forceinline__ float mean_of(double s) {
+    // R a power of two: the product by 1/R is exact and equals s / R.
+    if constexpr ((R & (R - 1)) == 0) {
+        return (float)(s * (1.0 / (double)R));
+    } else {
+        return (float)(s / (double)R);
+    }
+}
+
+// g_bar of the 8 elements held as BF16 in raw[r] (one dwordx4 per rank).
+template <int R>
+__device__ __forceinline__ void mean8(const uint4 (&raw)[R], float (&g)[kVec]) {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        double s_lo = 0.0, s_hi = 0.0;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            uint32_t word = (&raw[r].x)[w];
+            s_lo += (double)bf16_lo(word);
+            s_hi += (double)bf16_hi(word);
+        }
+        g[2 * w] = mean_of<R>(s_lo);
+        g[2 * w + 1] = mean_of<R>(s_hi);
+    }
+}
+
+template <int R>
+__device__ __forceinline__ float mean1(const uint16_t *const *g, int64_t i) {
+    double s = 0.0;
+#pragma unroll
+    for (int r = 0; r < R; ++r) s += (double)__uint_as_float((uint32_t)g[r][i] << 16);
+    return mean_of<R>(s);
+}
+
+__device__ __forceinline__ double wave_sum(double x) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+    return x;
+}
+
+// Sum of one double per thread over the block, in a fixed order: lanes by
+// a fixed butterfly inside each wave, then waves in index order.
+template <int THREADS>
+__device__ __forceinline__ double block_sum(double x) {
+    __shared__ double ws[THREADS / 64];
+    x = wave_sum(x);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0) ws[wave] = x;
+    __syncthreads();
+    double t = 0.0;
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int k = 0; k < THREADS / 64; ++k) t += ws[k];
+    }
+    return t;  // valid in thread 0
+}
+
+// ---------------------------------------------------------------------------
+// Norm partials: block b sums g_bar^2 over tile b.  Lane t of iteration it
+// handles elements 8*(b*8192 + it*256 + t) .. +7, so each pass of the block
+// reads a contiguous 4 KB per rank.  The per-lane order, the butterfly and
+// the wave order are fixed, so a tile's partial depends on its contents only.
+template <int R, bool WRITE_GBAR>
+__global__ __launch_bounds__(kNormThreads) void k_norm_partials(NormArgs a) {
+    constexpr int kGroupsPerTile = kTile / kVec;            // 8192
+    constexpr int kIters = kGroupsPerTile / kNormThreads;   // 32
+    const int64_t n = a.n;
+    const int64_t tile0 = (int64_t)blockIdx.x * kGroupsPerTile;
+    double acc = 0.0;
+    const uint16_t *const *gp = a.g;
+    for (int it = 0; it < kIters; ++it) {
+        const int64_t q = tile0 + (int64_t)it * kNormThreads + threadIdx.x;
+        const int64_t e0 = q * kVec;
+        if (e0 + kVec <= n) {
+            uint4 raw[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r) raw[r] = *reinterpret_cast<const uint4 *>(gp[r] + e0);
+            float g[kVec];
+            mean8<R>(raw, g);
+#pragma unroll
+            for (int e = 0; e < kVec; ++e) acc += (double)g[e] * (double)g[e];
+            if constexpr (WRITE_GBAR) {
+                float4 *o = reinterpret_cast<float4 *>(a.gbar_out + e0);
+                o[0] = make_float4(g[0], g[1], g[2], g[3]);
+                o[1] = make_float4(g[4], g[5], g[6], g[7]);
+            }
+        } else if (e0 < n) {
+            for (int64_t i = e0; i < n; ++i) {
+                float g = mean1<R>(a.g, i);
+                acc += (double)g * (double)g;
+                if constexpr (WRITE_GBAR) a.gbar_out[i] = g;
+            }
+        }
+    }
+    double t = block_sum<kNormThreads>(acc);
+    if (threadIdx.x == 0) a.partials[blockIdx.x] = t;
+}
+
+// One block: fixed-order sum of all tile partials, then the norm, the clip
+// coefficient and the non-finite flag.
+__global__ __launch_bounds__(kFinalizeThreads) void k_norm_finalize(
+    const double *__restrict__ partials, int64_t n_partials, double max_grad_norm,
+    NormState *__restrict__ ns) {
+    double acc = 0.0;
+    for (int64_t i = threadIdx.x; i < n_partials; i += kFinalizeThreads) acc += partials[i];
+    double S = block_sum<kFinalizeThreads>(acc);
+    if (threadIdx.x == 0) {
+        double norm = sqrt(S);
+        int bad = !isfinite(S);
+        double c = 1.0;
+        if (max_grad_norm > 0.0 && !bad) {
+            c = max_grad_norm / (norm + 1e-6);
+            if (c > 1.0) c = 1.0;
+        }
+        ns->sumsq = S;
+        ns->norm = norm;
+        ns->clip = c;
+        ns->nonfinite = bad;
+        ns->pad = 0;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Fused update.
+
+struct Consts {
+    double c, lr_wd, beta1, omb1, beta2, omb2, step_size, inv_bc2, eps;
+};
+
+// p1, m' and v' are each rounded after every product and sum, in the order
+// of their definition (no fused multiply-add).  m' cancels where b1*m is
+// close to -(1-b1)*g -- common, since the inputs sit on the coarse BF16 grid
+// -- and there a single-rounding fma and a two-rounding evaluation differ by
+// a large relative amount of a result that is pure rounding noise.  Fixing
+// the order makes m' (and v', p1) the same bits as the definition's.
+__device__ __forceinline__ void moments(double pd, double md, double vd, double g, const Consts &k,
+                                        double &p1, double &m1, double &v1) {
+#pragma clang fp contract(off)
+    p1 = pd - k.lr_wd * pd;
+    m1 = k.beta1 * md + k.omb1 * g;
+    v1 = k.beta2 * vd + k.omb2 * (g * g);
+}
+
+__device__ __forceinline__ void adamw(float &p, float &m, float &v, float g_bar, const Consts &k) {
+    const double g = (double)g_bar * k.c;
+    double p1, m1, v1;
+    moments((double)p, (double)m, (double)v, g, k, p1, m1, v1);
+    const double denom = sqrt(v1 * k.inv_bc2) + k.eps;
+    const double pn = p1 - k.step_size * (m1 / denom);
+    p = (float)pn;
+    m = (float)m1;
+    v = (float)v1;
+}
+
+template <int R, bool CACHED>
+__global__ __launch_bounds__(kUpdateThreads) void k_update(UpdateArgs a) {
+    const NormState *ns = a.ns;
+    if (ns->nonfinite) return;
+    Consts k;
+    k.c = ns->clip;
+    k.lr_wd = a.lr_wd;
+    k.beta1 = a.beta1;
+    k.omb1 = a.one_minus_beta1;
+    k.beta2 = a.beta2;
+    k.omb2 = a.one_minus_beta2;
+    k.step_size = a.step_size;
+    k.inv_bc2 = a.inv_bc2;
+    k.eps = a.eps;
+
+    float *__restrict__ P = a.p;
+    float *__restrict__ M = a.m;
+    float *__restrict__ V = a.v;
+    uint16_t *__restrict__ PB = a.pb;
+    const float *__restrict__ GB = a.gbar;
+    const int64_t n = a.n;
+    const int64_t groups = n / kVec;
+    const int64_t gid = (int64_t)blockIdx.x * kUpdateThreads + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * kUpdateThreads;
+
+    for (int64_t q = gid; q < groups; q += stride) {
+        const int64_t e0 = q * kVec;
+        float g[kVec];
+        if constexpr (CACHED) {
+            const float4 a0 = reinterpret_cast<const float4 *>(GB + e0)[0];
+            const float4 a1 = reinterpret_cast<const float4 *>(GB + e0)[1];
+            g[0] = a0.x; g[1] = a0.y; g[2] = a0.z; g[3] = a0.w;
+            g[4] = a1.x; g[5] = a1.y; g[6] = a1.z; g[7] = a1.w;
+        } else {
+            uint4 raw[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r) raw[r] = *reinterpret_cast<const uint4 *>(a.g[r] + e0);
+            mean8<R>(raw, g);
+        }
+        float4 *p4 = reinterpret_cast<float4 *>(P + e0);
+        float4 *m4 = reinterpret_cast<float4 *>(M + e0);
+        float4 *v4 = reinterpret_cast<float4 *>(V + e0);
+        float4 pv[2] = {p4[0], p4[1]};
+        float4 mv[2] = {m4[0], m4[1]};
+        float4 vv[2] = {v4[0], v4[1]};
+        float *pf = &pv[0].x, *mf = &mv[0].x, *vf = &vv[0].x;
+#pragma unroll
+        for (int e = 0; e < kVec; ++e) adamw(pf[e], mf[e], vf[e], g[e], k);
+        p4[0] = pv[0]; p4[1] = pv[1];
+        m4[0] = mv[0]; m4[1] = mv[1];
+        v4[0] = vv[0]; v4[1] = vv[1];
+        uint4 b;
+        b.x = pack_bf16(pf[0], pf[1]);
+        b.y = pack_bf16(pf[2], pf[3]);
+        b.z = pack_bf16(pf[4], pf[5]);
+        b.w = pack_bf16(pf[6], pf[7]);
+        *reinterpret_cast<uint4 *>(PB + e0) = b;
+    }
+    // ragged tail of fewer than 8 elements
+    if (gid == 0) {
+        for (int64_t i = groups * kVec; i < n; ++i) {
+            float gb;
+            if constexpr (CACHED) gb = GB[i];
+            else gb = mean1<R>(a.g, i);
+            float p = P[i], m = M[i], v = V[i];
+            adamw(p, m, v, gb, k);
+            P[i] = p; M[i] = m; V[i] = v;
+            PB[i] = (uint16_t)bf16_rne(p);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Small helpers.
+
+__global__ __launch_bounds__(256) void k_cast_bf16(const float *__restrict__ src,
+                                                   uint16_t *__restrict__ dst, int64_t n) {
+    const int64_t groups = n / kVec;
+    const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    for (int64_t q = gid; q < groups; q += stride) {
+        const float4 a0 = reinterpret_cast<const float4 *>(src + q * kVec)[0];
+        const float4 a1 = reinterpret_cast<const float4 *>(src + q * kVec)[1];
+        uint4 b;
+        b.x = pack_bf16(a0.x, a0.y);
+        b.y = pack_bf16(a0.z, a0.w);
+        b.z = pack_bf16(a1.x, a1.y);
+        b.w = pack_bf16(a1.z, a1.w);
+        *reinterpret_cast<uint4 *>(dst + q * kVec) = b;
+    }
+    if (gid == 0)
+        for (int64_t i = groups * kVec; i < n; ++i) dst[i] = (uint16_t)bf16_rne(src[i]);
+}
+
+__global__ __launch_bounds__(256) void k_copy16(uint4 *__restrict__ dst, const uint4 *__restrict__ src,
+                                                int64_t n16) {
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += stride) dst[i] = src[i];
+}
+
+__global__ __launch_bounds__(256) void k_fill_u32(uint32_t *__restrict__ dst, int64_t n_words, uint32_t value) {
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    const int64_t n4 = n_words / 4;
+    uint4 v4 = make_uint4(value, value, value, value);
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += stride)
+        reinterpret_cast<uint4 *>(dst)[i] = v4;
+    if (blockIdx.x == 0 && threadIdx.x == 0)
+        for (int64_t i = n4 * 4; i < n_words; ++i) dst[i] = value;
+}
+
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+template <int R>
+hipError_t norm_r(const NormArgs &a, hipStream_t s) {
+    const int64_t blocks = cdiv(a.n, kTile);
+    if (a.gbar_out)
+        hipLaunchKernelGGL((k_norm_partials<R, true>), dim3((uint32_t)blocks), dim3(kNormThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL((k_norm_partials<R, false>), dim3((uint32_t)blocks), dim3(kNormThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int R>
+hipError_t update_r(const UpdateArgs &a, int64_t blocks, hipStream_t s) {
+    if (a.gbar)
+        hipLaunchKernelGGL((k_update<1, true>), dim3((uint32_t)blocks), dim3(kUpdateThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL((k_update<R, false>), dim3((uint32_t)blocks), dim3(kUpdateThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+#define SDP_FOR_EACH_R(X) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15) X(16)
+
+hipError_t launch_norm_partials(int R, const NormArgs &a, hipStream_t s) {
+    switch (R) {
+#define CASE(r) case r: return norm_r<r>(a, s);
+        SDP_FOR_EACH_R(CASE)
+#undef CASE
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_norm_finalize(const double *partials, int64_t n_partials, double max_grad_norm,
+                                NormState *ns, hipStream_t s) {
+    hipLaunchKernelGGL(k_norm_finalize, dim3(1), dim3(kFinalizeThreads), 0, s, partials, n_partials,
+                       max_grad_norm, ns);
+    return hipGetLastError();
+}
+
+hipError_t launch_update(int R, const UpdateArgs &a, int max_blocks, hipStream_t s) {
+    int64_t blocks = cdiv(a.n / kVec, kUpdateThreads);
+    if (blocks < 1) blocks = 1;
+    if (max_blocks > 0 && blocks > max_blocks) blocks = max_blocks;
+    switch (R) {
+#define CASE(r) case r: return update_r<r>(a, blocks, s);
+        SDP_FOR_EACH_R(CASE)
+#undef CASE
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_cast_bf16(const float *src, uint16_t *dst, int64_t n, hipStream_t s) {
+    int64_t blocks = cdiv(n / kVec, 256);
+    if (blocks < 1) blocks = 1;
+    if (blocks > 65536) blocks = 65536;
+    hipLaunchKernelGGL(k_cast_bf16, dim3((uint32_t)blocks), dim3(256), 0, s, src, dst, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_copy16(void *dst, const void *src, int64_t n16, int max_blocks, hipStream_t s) {
+    int64_t blocks = cdiv(n16, 256);
+    if (blocks < 1) blocks = 1;
+    if (max_blocks > 0 && blocks > max_blocks) blocks = max_blocks;
+    hipLaunchKernelGGL(k_copy16, dim3((uint32_t)blocks), dim3(256), 0, s, (uint4 *)dst,
+                       (const uint4 *)src, n16);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_u32(void *dst, int64_t n_words, uint32_t value, hipStream_t s) {
+    int64_t blocks = cdiv(n_words / 4, 256);
+    if (blocks < 1) blocks = 1;
+    if (blocks > 16384) blocks = 16384;
+    hipLaunchKernelGGL(k_fill_u32, dim3((uint32_t)blocks), dim3(256), 0, s, (uint32_t *)dst, n_words, value);
+    return hipGetLastError();
+}
+
+}  // namespace sdp

@@ -1,0 +1,952 @@
+// C ABI of libsdp: context, argument validation, the device-mode driver and
+// the streamed engine.  Kernels live in sdp_kernels.hip.
+//
+// Device mode (sdp_agg_adam_step): per call, one norm-partials launch per
+// segment, one finalize launch, one fused-update launch per segment, all on
+// the caller's stream.  The clip coefficient stays in device memory.
+//
+// Streamed mode (sdp_stream_step): states live in pinned host memory and
+// move through two device staging slots.  A copy stream carries host-to-
+// device copies; a compute stream runs the kernels and the device-to-host
+// copies.  Events h2d_done[s] and slot_free[s] order each slot's reuse: a
+// slot is refilled only after its previous consumer finished (the paper's
+// buffer-reuse rule, Design, completion and buffer reuse), and the update of
+// a chunk starts as soon as its copy has landed (chunked overlap within a
+// layer).  Phase 1 streams the gradients for the global norm; phase 2
+// streams master/m/v through the fused update and back.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "sdp_internal.h"
+
+using sdp::NormState;
+
+namespace {
+
+thread_local std::string t_err;
+
+int fail(int status, const char *fmt, ...) {
+    char buf[1024];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    t_err = buf;
+    return status;
+}
+
+#define HIP_TRY(expr)                                                                        \
+    do {                                                                                     \
+        hipError_t e_ = (expr);                                                              \
+        if (e_ != hipSuccess)                                                                \
+            return fail(SDP_ERR_HIP, "%s failed: %s (%s:%d)", #expr, hipGetErrorString(e_),   \
+                        __FILE__, __LINE__);                                                 \
+    } while (0)
+
+#define SDP_TRY(expr)              \
+    do {                           \
+        int rc_ = (expr);          \
+        if (rc_ != SDP_OK) return rc_; \
+    } while (0)
+
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline int64_t round_up(int64_t a, int64_t b) { return cdiv(a, b) * b; }
+
+struct DeviceGuard {
+    int old = -1;
+    explicit DeviceGuard(int d) {
+        if (hipGetDevice(&old) != hipSuccess) old = -1;
+        if (old != d) (void)hipSetDevice(d);
+    }
+    ~DeviceGuard() {
+        int cur = -1;
+        if (old >= 0 && hipGetDevice(&cur) == hipSuccess && cur != old) (void)hipSetDevice(old);
+    }
+};
+
+enum TimedKind { kNorm = 0, kFinalize = 1, kUpdate = 2 };
+
+struct Timed {
+    int kind;
+    hipEvent_t a, b;
+    int64_t elems;
+};
+
+}  // namespace
+
+struct sdp_ctx {
+    int device = 0;
+    int64_t max_chunk = 0;
+    int32_t max_ranks = 0;
+    uint32_t flags = 0;
+    hipStream_t s_copy = nullptr, s_comp = nullptr;
+    hipEvent_t h2d_done[2] = {nullptr, nullptr};
+    hipEvent_t slot_free[2] = {nullptr, nullptr};
+    hipEvent_t last_done = nullptr;
+    bool last_done_valid = false;
+    char *staging = nullptr;
+    size_t slot_bytes = 0;
+    double *partials = nullptr;
+    int64_t partials_cap = 0;
+    float *gbar = nullptr;
+    int64_t gbar_cap = 0;
+    NormState *ns = nullptr;       // device
+    NormState *ns_host = nullptr;  // pinned mirror for read-back
+    int update_max_blocks = 0;     // 0: one 8-element group per lane
+    bool timing = false;
+    std::vector<Timed> timed;
+    std::vector<hipEvent_t> pool;
+};
+
+namespace {
+
+// ---- validation ---------------------------------------------------------
+
+int check_hparams(const sdp_adamw_params *hp) {
+    if (!hp) return fail(SDP_ERR_INVALID_ARGUMENT, "hyperparameters are NULL");
+    if (hp->step < 1) return fail(SDP_ERR_INVALID_ARGUMENT, "step must be >= 1 (got %lld)", (long long)hp->step);
+    const double v[] = {hp->lr, hp->beta1, hp->beta2, hp->eps, hp->weight_decay, hp->max_grad_norm};
+    for (double x : v)
+        if (!std::isfinite(x)) return fail(SDP_ERR_INVALID_ARGUMENT, "hyperparameters must be finite");
+    if (hp->beta1 < 0.0 || hp->beta1 >= 1.0 || hp->beta2 < 0.0 || hp->beta2 >= 1.0)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "betas must lie in [0, 1)");
+    if (hp->eps < 0.0) return fail(SDP_ERR_INVALID_ARGUMENT, "eps must be >= 0");
+    return SDP_OK;
+}
+
+bool aligned(const void *p) { return ((uintptr_t)p % SDP_ALIGN) == 0; }
+
+int check_device_ptr(const sdp_ctx *ctx, const void *p, size_t bytes, const char *what, int seg) {
+    hipPointerAttribute_t at;
+    hipError_t e = hipPointerGetAttributes(&at, p);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(SDP_ERR_NOT_DEVICE_MEMORY, "segment %d %s (%p) is not device memory", seg, what, p);
+    }
+    if (at.type != hipMemoryTypeDevice || at.device != ctx->device)
+        return fail(SDP_ERR_NOT_DEVICE_MEMORY, "segment %d %s (%p) is not device memory of GPU %d", seg, what, p,
+                    ctx->device);
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    if (hipMemGetAddressRange(&base, &size, (hipDeviceptr_t)p) == hipSuccess) {
+        if ((const char *)p + bytes > (const char *)base + size)
+            return fail(SDP_ERR_NOT_DEVICE_MEMORY, "segment %d %s: %zu bytes at %p overrun its allocation", seg, what,
+                        bytes, p);
+    } else {
+        (void)hipGetLastError();
+        return fail(SDP_ERR_NOT_DEVICE_MEMORY, "segment %d %s (%p): allocation range unknown", seg, what, p);
+    }
+    return SDP_OK;
+}
+
+int check_pinned_ptr(const void *p, size_t bytes, const char *what, int seg) {
+    const void *ends[2] = {p, (const char *)p + bytes - 1};
+    for (const void *q : ends) {
+        hipPointerAttribute_t at;
+        hipError_t e = hipPointerGetAttributes(&at, q);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(SDP_ERR_NOT_PINNED, "segment %d %s (%p, %zu bytes) is not pinned host memory", seg, what, p,
+                        bytes);
+        }
+        if (at.type != hipMemoryTypeHost)
+            return fail(SDP_ERR_NOT_PINNED, "segment %d %s (%p) is not pinned host memory", seg, what, p);
+    }
+    return SDP_OK;
+}
+
+struct Range {
+    uintptr_t a, b;
+    int seg;
+    const char *what;
+};
+
+bool overlap(const Range &x, const Range &y) { return x.a < y.b && y.a < x.b; }
+
+// Checks every segment of a call; returns R and the per-segment sizes.
+int validate_segments(const sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, bool device, bool grads_only,
+                      int32_t *R_out) {
+    if (!segs || n_segs < 1) return fail(SDP_ERR_INVALID_ARGUMENT, "need at least one segment");
+    int32_t R = segs[0].n_ranks;
+    if (R < 1 || R > SDP_MAX_RANKS)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "n_ranks must be in 1..%d (got %d)", SDP_MAX_RANKS, R);
+    std::vector<Range> states, grads;
+    for (int32_t s = 0; s < n_segs; ++s) {
+        const sdp_segment &g = segs[s];
+        if (g.n_ranks != R) return fail(SDP_ERR_INVALID_ARGUMENT, "segment %d has n_ranks %d, segment 0 has %d", s,
+                                        g.n_ranks, R);
+        if (g.numel < 1) return fail(SDP_ERR_INVALID_ARGUMENT, "segment %d: numel must be >= 1", s);
+        if (!g.grads) return fail(SDP_ERR_INVALID_ARGUMENT, "segment %d: grads is NULL", s);
+        const int64_t n = g.numel;
+        struct Buf {
+            const void *p;
+            size_t bytes;
+            const char *what;
+        };
+        std::vector<Buf> bufs;
+        if (!grads_only) {
+            bufs.push_back({g.master, (size_t)n * 4, "master"});
+            bufs.push_back({g.exp_avg, (size_t)n * 4, "exp_avg"});
+            bufs.push_back({g.exp_avg_sq, (size_t)n * 4, "exp_avg_sq"});
+            bufs.push_back({g.param_bf16, (size_t)n * 2, "param_bf16"});
+        }
+        const size_t n_state = bufs.size();
+        for (int32_t r = 0; r < R; ++r) bufs.push_back({g.grads[r], (size_t)n * 2, "grad"});
+        for (size_t k = 0; k < bufs.size(); ++k) {
+            const Buf &b = bufs[k];
+            if (!b.p) return fail(SDP_ERR_INVALID_ARGUMENT, "segment %d: %s is NULL", s, b.what);
+            if (!aligned(b.p))
+                return fail(SDP_ERR_ALIGNMENT, "segment %d: %s (%p) is not %d-byte aligned", s, b.what, b.p, SDP_ALIGN);
+        }
+        for (size_t k = 0; k < bufs.size(); ++k) {
+            const Buf &b = bufs[k];
+            SDP_TRY(device ? check_device_ptr(ctx, b.p, b.bytes, b.what, s) : check_pinned_ptr(b.p, b.bytes, b.what, s));
+            Range rg{(uintptr_t)b.p, (uintptr_t)b.p + b.bytes, s, b.what};
+            (k < n_state ? states : grads).push_back(rg);
+        }
+    }
+    // states pairwise disjoint; gradients disjoint from every state
+    std::sort(states.begin(), states.end(), [](const Range &x, const Range &y) { return x.a < y.a; });
+    for (size_t k = 1; k < states.size(); ++k)
+        if (overlap(states[k - 1], states[k]))
+            return fail(SDP_ERR_INVALID_ARGUMENT, "segment %d %s overlaps segment %d %s", states[k - 1].seg,
+                        states[k - 1].what, states[k].seg, states[k].what);
+    for (const Range &g : grads) {
+        auto it = std::upper_bound(states.begin(), states.end(), g.a,
+                                   [](uintptr_t v, const Range &x) { return v < x.a; });
+        if (it != states.end() && overlap(*it, g))
+            return fail(SDP_ERR_INVALID_ARGUMENT, "segment %d gradient overlaps segment %d %s", g.seg, it->seg, it->what);
+        if (it != states.begin() && overlap(*(it - 1), g))
+            return fail(SDP_ERR_INVALID_ARGUMENT, "segment %d gradient overlaps segment %d %s", g.seg, (it - 1)->seg,
+                        (it - 1)->what);
+    }
+    *R_out = R;
+    return SDP_OK;
+}
+
+int check_chunk(int64_t chunk, bool allow_zero) {
+    if (chunk < 0 || (chunk == 0 && !allow_zero) || chunk % SDP_NORM_TILE != 0)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "chunk_elems must be a %spositive multiple of %d (got %lld)",
+                    allow_zero ? "zero or " : "", SDP_NORM_TILE, (long long)chunk);
+    return SDP_OK;
+}
+
+// ---- workspace ----------------------------------------------------------
+
+int ensure_partials(sdp_ctx *ctx, int64_t n) {
+    if (n <= ctx->partials_cap) return SDP_OK;
+    HIP_TRY(hipDeviceSynchronize());
+    if (ctx->partials) HIP_TRY(hipFree(ctx->partials));
+    ctx->partials = nullptr;
+    ctx->partials_cap = 0;
+    int64_t cap = std::max<int64_t>(n, 4096);
+    if (hipMalloc(&ctx->partials, (size_t)cap * sizeof(double)) != hipSuccess) {
+        (void)hipGetLastError();
+        ctx->partials = nullptr;
+        return fail(SDP_ERR_OUT_OF_MEMORY, "cannot allocate %lld norm partials", (long long)cap);
+    }
+    ctx->partials_cap = cap;
+    return SDP_OK;
+}
+
+int ensure_gbar(sdp_ctx *ctx, int64_t n) {
+    if (n <= ctx->gbar_cap) return SDP_OK;
+    HIP_TRY(hipDeviceSynchronize());
+    if (ctx->gbar) HIP_TRY(hipFree(ctx->gbar));
+    ctx->gbar = nullptr;
+    ctx->gbar_cap = 0;
+    if (hipMalloc(&ctx->gbar, (size_t)n * sizeof(float)) != hipSuccess) {
+        (void)hipGetLastError();
+        ctx->gbar = nullptr;
+        return fail(SDP_ERR_OUT_OF_MEMORY, "cannot allocate %lld floats for the stored mean gradient", (long long)n);
+    }
+    ctx->gbar_cap = n;
+    return SDP_OK;
+}
+
+// Layout of one call: norm tiles and stored-g_bar offsets of each segment.
+struct Plan {
+    std::vector<int64_t> tile_base, gbar_base;
+    int64_t tiles = 0, gbar_elems = 0;
+};
+
+Plan make_plan(const sdp_segment *segs, int32_t n_segs) {
+    Plan p;
+    for (int32_t s = 0; s < n_segs; ++s) {
+        p.tile_base.push_back(p.tiles);
+        p.gbar_base.push_back(p.gbar_elems);
+        p.tiles += cdiv(segs[s].numel, SDP_NORM_TILE);
+        p.gbar_elems += round_up(segs[s].numel, 64);  // 256-byte aligned segment bases
+    }
+    return p;
+}
+
+bool device_gbar(const sdp_ctx *ctx, int32_t R) {
+    if (ctx->flags & SDP_FLAG_DEVICE_GBAR_ALWAYS) return true;
+    if (ctx->flags & SDP_FLAG_DEVICE_GBAR_NEVER) return false;
+    return R > 4;
+}
+
+// ---- timing -------------------------------------------------------------
+
+hipEvent_t take_event(sdp_ctx *ctx) {
+    if (!ctx->pool.empty()) {
+        hipEvent_t e = ctx->pool.back();
+        ctx->pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    return e;
+}
+
+hipEvent_t timed_begin(sdp_ctx *ctx, hipStream_t s) {
+    if (!ctx->timing) return nullptr;
+    hipEvent_t a = take_event(ctx);
+    if (a && hipEventRecord(a, s) != hipSuccess) {
+        (void)hipGetLastError();
+        ctx->pool.push_back(a);
+        return nullptr;
+    }
+    return a;
+}
+
+void timed_end(sdp_ctx *ctx, hipStream_t s, hipEvent_t a, int kind, int64_t elems) {
+    if (!ctx->timing || !a) return;
+    hipEvent_t b = take_event(ctx);
+    if (!b || hipEventRecord(b, s) != hipSuccess) {
+        (void)hipGetLastError();
+        ctx->pool.push_back(a);
+        if (b) ctx->pool.push_back(b);
+        return;
+    }
+    ctx->timed.push_back({kind, a, b, elems});
+}
+
+// ---- launches shared by both modes ---------------------------------------
+
+int norm_launch(sdp_ctx *ctx, int32_t R, const uint16_t *const *g, int64_t n, double *partials, float *gbar_out,
+                hipStream_t s) {
+    sdp::NormArgs a{};
+    for (int32_t r = 0; r < R; ++r) a.g[r] = g[r];
+    a.n = n;
+    a.partials = partials;
+    a.gbar_out = gbar_out;
+    hipEvent_t t0 = timed_begin(ctx, s);
+    HIP_TRY(sdp::launch_norm_partials(R, a, s));
+    timed_end(ctx, s, t0, kNorm, n);
+    return SDP_OK;
+}
+
+int finalize_launch(sdp_ctx *ctx, int64_t tiles, double max_grad_norm, hipStream_t s) {
+    hipEvent_t t0 = timed_begin(ctx, s);
+    HIP_TRY(sdp::launch_norm_finalize(ctx->partials, tiles, max_grad_norm, ctx->ns, s));
+    timed_end(ctx, s, t0, kFinalize, tiles);
+    return SDP_OK;
+}
+
+void fill_consts(const sdp_adamw_params *hp, sdp::UpdateArgs &a) {
+    const double t = (double)hp->step;
+    const double bc1 = 1.0 - std::pow(hp->beta1, t);
+    const double bc2 = 1.0 - std::pow(hp->beta2, t);
+    a.lr_wd = hp->lr * hp->weight_decay;
+    a.beta1 = hp->beta1;
+    a.one_minus_beta1 = 1.0 - hp->beta1;
+    a.beta2 = hp->beta2;
+    a.one_minus_beta2 = 1.0 - hp->beta2;
+    a.step_size = hp->lr / bc1;
+    a.inv_bc2 = 1.0 / bc2;
+    a.eps = hp->eps;
+}
+
+int update_launch(sdp_ctx *ctx, int32_t R, const sdp_adamw_params *hp, float *p, float *m, float *v, uint16_t *pb,
+                  const uint16_t *const *g, const float *gbar, int64_t n, hipStream_t s) {
+    sdp::UpdateArgs a{};
+    a.p = p;
+    a.m = m;
+    a.v = v;
+    a.pb = pb;
+    if (!gbar)
+        for (int32_t r = 0; r < R; ++r) a.g[r] = g[r];
+    a.gbar = gbar;
+    a.n = n;
+    a.ns = ctx->ns;
+    fill_consts(hp, a);
+    hipEvent_t t0 = timed_begin(ctx, s);
+    HIP_TRY(sdp::launch_update(R, a, ctx->update_max_blocks, s));
+    timed_end(ctx, s, t0, kUpdate, n);
+    return SDP_OK;
+}
+
+// Order this call's work after the previous call's (they share workspace).
+int order_after_last(sdp_ctx *ctx, hipStream_t s) {
+    if (ctx->last_done_valid) HIP_TRY(hipStreamWaitEvent(s, ctx->last_done, 0));
+    return SDP_OK;
+}
+
+int mark_done(sdp_ctx *ctx, hipStream_t s) {
+    HIP_TRY(hipEventRecord(ctx->last_done, s));
+    ctx->last_done_valid = true;
+    return SDP_OK;
+}
+
+int read_norm(sdp_ctx *ctx, hipStream_t s, NormState *out) {
+    HIP_TRY(hipMemcpyAsync(ctx->ns_host, ctx->ns, sizeof(NormState), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    *out = *ctx->ns_host;
+    return SDP_OK;
+}
+
+// ---- device mode ----------------------------------------------------------
+
+int device_norm(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R, const Plan &plan, bool store_gbar,
+                double max_grad_norm, hipStream_t s) {
+    for (int32_t k = 0; k < n_segs; ++k)
+        SDP_TRY(norm_launch(ctx, R, segs[k].grads, segs[k].numel, ctx->partials + plan.tile_base[k],
+                            store_gbar ? ctx->gbar + plan.gbar_base[k] : nullptr, s));
+    return finalize_launch(ctx, plan.tiles, max_grad_norm, s);
+}
+
+// ---- streamed mode --------------------------------------------------------
+
+struct Slot {
+    float *p, *m, *v;
+    uint16_t *pb;
+    uint16_t *g[SDP_MAX_RANKS];
+};
+
+Slot slot_at(const sdp_ctx *ctx, int k) {
+    Slot sl{};
+    const int64_t C = ctx->max_chunk;
+    char *b = ctx->staging + (size_t)k * ctx->slot_bytes;
+    sl.p = (float *)b;
+    sl.m = sl.p + C;
+    sl.v = sl.m + C;
+    sl.pb = (uint16_t *)(sl.v + C);
+    for (int r = 0; r < ctx->max_ranks; ++r) sl.g[r] = sl.pb + C + (size_t)r * C;
+    return sl;
+}
+
+struct Chunk {
+    int32_t seg;
+    int64_t off, len;
+};
+
+std::vector<Chunk> make_chunks(const sdp_segment *segs, int32_t n_segs, int64_t C) {
+    std::vector<Chunk> out;
+    for (int32_t s = 0; s < n_segs; ++s)
+        for (int64_t off = 0; off < segs[s].numel; off += C)
+            out.push_back({s, off, std::min(C, segs[s].numel - off)});
+    return out;
+}
+
+int poison(sdp_ctx *ctx, int k) {
+    if (!(ctx->flags & SDP_FLAG_DEBUG_POISON)) return SDP_OK;
+    HIP_TRY(sdp::launch_fill_u32(ctx->staging + (size_t)k * ctx->slot_bytes, (int64_t)(ctx->slot_bytes / 4),
+                                 0xFFC0FFC0u, ctx->s_comp));
+    return SDP_OK;
+}
+
+// Phase 1: gradients in, norm partials (and stored g_bar) out, then finalize.
+int stream_norm_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R, const Plan &plan,
+                      const std::vector<Chunk> &chunks, bool store_gbar, double max_grad_norm, bool used[2]) {
+    for (size_t k = 0; k < chunks.size(); ++k) {
+        const Chunk &c = chunks[k];
+        const int sl = (int)(k & 1);
+        Slot slot = slot_at(ctx, sl);
+        if (used[sl]) HIP_TRY(hipStreamWaitEvent(ctx->s_copy, ctx->slot_free[sl], 0));
+        for (int32_t r = 0; r < R; ++r)
+            HIP_TRY(hipMemcpyAsync(slot.g[r], segs[c.seg].grads[r] + c.off, (size_t)c.len * 2, hipMemcpyHostToDevice,
+                                   ctx->s_copy));
+        HIP_TRY(hipEventRecord(ctx->h2d_done[sl], ctx->s_copy));
+        HIP_TRY(hipStreamWaitEvent(ctx->s_comp, ctx->h2d_done[sl], 0));
+        const uint16_t *gp[SDP_MAX_RANKS];
+        for (int32_t r = 0; r < R; ++r) gp[r] = slot.g[r];
+        SDP_TRY(norm_launch(ctx, R, gp, c.len, ctx->partials + plan.tile_base[c.seg] + c.off / SDP_NORM_TILE,
+                            store_gbar ? ctx->gbar + plan.gbar_base[c.seg] + c.off : nullptr, ctx->s_comp));
+        SDP_TRY(poison(ctx, sl));
+        HIP_TRY(hipEventRecord(ctx->slot_free[sl], ctx->s_comp));
+        used[sl] = true;
+    }
+    return finalize_launch(ctx, plan.tiles, max_grad_norm, ctx->s_comp);
+}
+
+// Phase 2: master/m/v in (and the gradients again unless g_bar is stored),
+// fused update, master/m/v and BF16 parameters back out.
+int stream_update_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t R, const Plan &plan,
+                        const std::vector<Chunk> &chunks, bool stored_gbar, const sdp_adamw_params *hp, bool used[2],
+                        size_t k0) {
+    for (size_t j = 0; j < chunks.size(); ++j) {
+        const Chunk &c = chunks[j];
+        const sdp_segment &g = segs[c.seg];
+        const int sl = (int)((j + k0) & 1);
+        Slot slot = slot_at(ctx, sl);
+        const size_t f4 = (size_t)c.len * 4, b2 = (size_t)c.len * 2;
+        if (used[sl]) HIP_TRY(hipStreamWaitEvent(ctx->s_copy, ctx->slot_free[sl], 0));
+        HIP_TRY(hipMemcpyAsync(slot.p, g.master + c.off, f4, hipMemcpyHostToDevice, ctx->s_copy));
+        HIP_TRY(hipMemcpyAsync(slot.m, g.exp_avg + c.off, f4, hipMemcpyHostToDevice, ctx->s_copy));
+        HIP_TRY(hipMemcpyAsync(slot.v, g.exp_avg_sq + c.off, f4, hipMemcpyHostToDevice, ctx->s_copy));
+        if (!stored_gbar)
+            for (int32_t r = 0; r < R; ++r)
+                HIP_TRY(hipMemcpyAsync(slot.g[r], g.grads[r] + c.off, b2, hipMemcpyHostToDevice, ctx->s_copy));
+        HIP_TRY(hipEventRecord(ctx->h2d_done[sl], ctx->s_copy));
+        HIP_TRY(hipStreamWaitEvent(ctx->s_comp, ctx->h2d_done[sl], 0));
+        const uint16_t *gp[SDP_MAX_RANKS];
+        for (int32_t r = 0; r < R; ++r) gp[r] = slot.g[r];
+        SDP_TRY(update_launch(ctx, R, hp, slot.p, slot.m, slot.v, slot.pb, gp,
+                              stored_gbar ? ctx->gbar + plan.gbar_base[c.seg] + c.off : nullptr, c.len, ctx->s_comp));
+        HIP_TRY(hipMemcpyAsync(g.master + c.off, slot.p, f4, hipMemcpyDeviceToHost, ctx->s_comp));
+        HIP_TRY(hipMemcpyAsync(g.exp_avg + c.off, slot.m, f4, hipMemcpyDeviceToHost, ctx->s_comp));
+        HIP_TRY(hipMemcpyAsync(g.exp_avg_sq + c.off, slot.v, f4, hipMemcpyDeviceToHost, ctx->s_comp));
+        HIP_TRY(hipMemcpyAsync(g.param_bf16 + c.off, slot.pb, b2, hipMemcpyDeviceToHost, ctx->s_comp));
+        SDP_TRY(poison(ctx, sl));
+        HIP_TRY(hipEventRecord(ctx->slot_free[sl], ctx->s_comp));
+        used[sl] = true;
+    }
+    return SDP_OK;
+}
+
+int sync_streams(sdp_ctx *ctx) {
+    HIP_TRY(hipStreamSynchronize(ctx->s_copy));
+    HIP_TRY(hipStreamSynchronize(ctx->s_comp));
+    return SDP_OK;
+}
+
+int stream_common_checks(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int64_t chunk, bool grads_only,
+                         int32_t *R) {
+    if (!ctx->staging) return fail(SDP_ERR_CHUNK_TOO_LARGE, "context was created without streamed-mode staging");
+    SDP_TRY(check_chunk(chunk, false));
+    if (chunk > ctx->max_chunk)
+        return fail(SDP_ERR_CHUNK_TOO_LARGE, "chunk_elems %lld exceeds the context's %lld", (long long)chunk,
+                    (long long)ctx->max_chunk);
+    SDP_TRY(validate_segments(ctx, segs, n_segs, false, grads_only, R));
+    if (*R > ctx->max_ranks)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "n_ranks %d exceeds the context's max_ranks %d", *R, ctx->max_ranks);
+    return SDP_OK;
+}
+
+}  // namespace
+
+// ===========================================================================
+// exported
+
+extern "C" {
+
+const char *sdp_status_string(int status) {
+    switch (status) {
+        case SDP_OK: return "SDP_OK";
+        case SDP_ERR_INVALID_ARGUMENT: return "SDP_ERR_INVALID_ARGUMENT";
+        case SDP_ERR_ALIGNMENT: return "SDP_ERR_ALIGNMENT";
+        case SDP_ERR_NOT_DEVICE_MEMORY: return "SDP_ERR_NOT_DEVICE_MEMORY";
+        case SDP_ERR_NOT_PINNED: return "SDP_ERR_NOT_PINNED";
+        case SDP_ERR_CHUNK_TOO_LARGE: return "SDP_ERR_CHUNK_TOO_LARGE";
+        case SDP_ERR_OUT_OF_MEMORY: return "SDP_ERR_OUT_OF_MEMORY";
+        case SDP_ERR_HIP: return "SDP_ERR_HIP";
+        case SDP_ERR_NONFINITE: return "SDP_ERR_NONFINITE";
+        default: return "SDP_ERR_UNKNOWN";
+    }
+}
+
+const char *sdp_last_error(void) { return t_err.c_str(); }
+
+int sdp_plan(const int64_t *numels, int32_t n_segs, int64_t chunk_elems, int64_t *n_chunks_out, int64_t *n_tiles_out) {
+    t_err.clear();
+    if (!numels || n_segs < 1 || !n_chunks_out || !n_tiles_out)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_plan: NULL argument or no segments");
+    SDP_TRY(check_chunk(chunk_elems, false));
+    int64_t ch = 0, ti = 0;
+    for (int32_t s = 0; s < n_segs; ++s) {
+        if (numels[s] < 1) return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_plan: segment %d has numel < 1", s);
+        ch += cdiv(numels[s], chunk_elems);
+        ti += cdiv(numels[s], SDP_NORM_TILE);
+    }
+    *n_chunks_out = ch;
+    *n_tiles_out = ti;
+    return SDP_OK;
+}
+
+int sdp_bytes_per_elem(int streamed, int32_t n_ranks, uint32_t flags, double *hbm_or_h2d, double *d2h) {
+    t_err.clear();
+    if (!hbm_or_h2d || !d2h || n_ranks < 1 || n_ranks > SDP_MAX_RANKS)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_bytes_per_elem: bad argument");
+    const double R = n_ranks;
+    if (streamed) {
+        const bool cache = !(flags & SDP_FLAG_STREAM_GBAR_NEVER);
+        *hbm_or_h2d = cache ? 12.0 + 2.0 * R : 12.0 + 4.0 * R;
+        *d2h = 14.0;
+    } else {
+        bool cache = (flags & SDP_FLAG_DEVICE_GBAR_ALWAYS) ? true
+                     : (flags & SDP_FLAG_DEVICE_GBAR_NEVER) ? false
+                                                            : (n_ranks > 4);
+        // norm pass reads 2R (+ writes 4 if storing g_bar); update reads
+        // 12 + (2R or 4) and writes 14
+        *hbm_or_h2d = cache ? 2.0 * R + 4.0 + 4.0 + 12.0 + 14.0 : 2.0 * R + 2.0 * R + 12.0 + 14.0;
+        *d2h = 0.0;
+    }
+    return SDP_OK;
+}
+
+int sdp_host_alloc(void **out, size_t bytes) {
+    t_err.clear();
+    if (!out || bytes == 0) return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_host_alloc: bad argument");
+    *out = nullptr;
+    hipError_t e = hipHostMalloc(out, bytes, hipHostMallocDefault);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        *out = nullptr;
+        return fail(SDP_ERR_OUT_OF_MEMORY, "hipHostMalloc(%zu) failed: %s", bytes, hipGetErrorString(e));
+    }
+    return SDP_OK;
+}
+
+int sdp_host_free(void *p) {
+    t_err.clear();
+    if (!p) return SDP_OK;
+    HIP_TRY(hipHostFree(p));
+    return SDP_OK;
+}
+
+int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems, int32_t max_ranks, uint32_t flags) {
+    t_err.clear();
+    if (!out) return fail(SDP_ERR_INVALID_ARGUMENT, "out is NULL");
+    *out = nullptr;
+    if (max_ranks < 1 || max_ranks > SDP_MAX_RANKS)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "max_ranks must be in 1..%d", SDP_MAX_RANKS);
+    SDP_TRY(check_chunk(max_chunk_elems, true));
+    if ((flags & SDP_FLAG_DEVICE_GBAR_NEVER) && (flags & SDP_FLAG_DEVICE_GBAR_ALWAYS))
+        return fail(SDP_ERR_INVALID_ARGUMENT, "DEVICE_GBAR_NEVER and DEVICE_GBAR_ALWAYS are exclusive");
+    int ndev = 0;
+    HIP_TRY(hipGetDeviceCount(&ndev));
+    if (device < 0 || device >= ndev) return fail(SDP_ERR_INVALID_ARGUMENT, "device %d out of range (%d GPUs)", device, ndev);
+    DeviceGuard guard(device);
+    sdp_ctx *c = new sdp_ctx();
+    c->device = device;
+    c->max_chunk = max_chunk_elems;
+    c->max_ranks = max_ranks;
+    c->flags = flags;
+    if (const char *env = std::getenv("SDP_UPDATE_MAX_BLOCKS")) c->update_max_blocks = std::max(0, std::atoi(env));
+    int rc = SDP_OK;
+    auto bail = [&](int status) {
+        sdp_ctx_destroy(c);
+        return status;
+    };
+#define CTX_HIP(expr)                                                                                \
+    do {                                                                                             \
+        hipError_t e_ = (expr);                                                                      \
+        if (e_ != hipSuccess) {                                                                      \
+            (void)hipGetLastError();                                                                 \
+            return bail(fail(SDP_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(e_)));           \
+        }                                                                                            \
+    } while (0)
+    CTX_HIP(hipStreamCreateWithFlags(&c->s_copy, hipStreamNonBlocking));
+    CTX_HIP(hipStreamCreateWithFlags(&c->s_comp, hipStreamNonBlocking));
+    for (int k = 0; k < 2; ++k) {
+        CTX_HIP(hipEventCreateWithFlags(&c->h2d_done[k], hipEventDisableTiming));
+        CTX_HIP(hipEventCreateWithFlags(&c->slot_free[k], hipEventDisableTiming));
+    }
+    CTX_HIP(hipEventCreateWithFlags(&c->last_done, hipEventDisableTiming));
+    if (hipMalloc(&c->ns, sizeof(NormState)) != hipSuccess) {
+        (void)hipGetLastError();
+        return bail(fail(SDP_ERR_OUT_OF_MEMORY, "cannot allocate the norm state"));
+    }
+    CTX_HIP(hipMemset(c->ns, 0, sizeof(NormState)));
+    if (hipHostMalloc(&c->ns_host, sizeof(NormState), hipHostMallocDefault) != hipSuccess) {
+        (void)hipGetLastError();
+        return bail(fail(SDP_ERR_OUT_OF_MEMORY, "cannot allocate the pinned norm mirror"));
+    }
+    if (max_chunk_elems > 0) {
+        c->slot_bytes = (size_t)(14 + 2 * max_ranks) * (size_t)max_chunk_elems;
+        if (hipMalloc(&c->staging, 2 * c->slot_bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            c->staging = nullptr;
+            return bail(fail(SDP_ERR_OUT_OF_MEMORY, "cannot allocate 2 x %zu bytes of staging", c->slot_bytes));
+        }
+    }
+    rc = ensure_partials(c, 4096);
+    if (rc != SDP_OK) return bail(rc);
+#undef CTX_HIP
+    *out = c;
+    return SDP_OK;
+}
+
+void sdp_ctx_destroy(sdp_ctx *ctx) {
+    if (!ctx) return;
+    DeviceGuard guard(ctx->device);
+    (void)hipDeviceSynchronize();
+    for (const Timed &t : ctx->timed) {
+        (void)hipEventDestroy(t.a);
+        (void)hipEventDestroy(t.b);
+    }
+    for (hipEvent_t e : ctx->pool) (void)hipEventDestroy(e);
+    for (int k = 0; k < 2; ++k) {
+        if (ctx->h2d_done[k]) (void)hipEventDestroy(ctx->h2d_done[k]);
+        if (ctx->slot_free[k]) (void)hipEventDestroy(ctx->slot_free[k]);
+    }
+    if (ctx->last_done) (void)hipEventDestroy(ctx->last_done);
+    if (ctx->s_copy) (void)hipStreamDestroy(ctx->s_copy);
+    if (ctx->s_comp) (void)hipStreamDestroy(ctx->s_comp);
+    if (ctx->staging) (void)hipFree(ctx->staging);
+    if (ctx->partials) (void)hipFree(ctx->partials);
+    if (ctx->gbar) (void)hipFree(ctx->gbar);
+    if (ctx->ns) (void)hipFree(ctx->ns);
+    if (ctx->ns_host) (void)hipHostFree(ctx->ns_host);
+    (void)hipGetLastError();
+    delete ctx;
+}
+
+int sdp_agg_adam_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, const sdp_adamw_params *hp,
+                      int64_t chunk_elems, void *stream, double *grad_norm_out) {
+    t_err.clear();
+    if (!ctx) return fail(SDP_ERR_INVALID_ARGUMENT, "context is NULL");
+    SDP_TRY(check_hparams(hp));
+    SDP_TRY(check_chunk(chunk_elems, true));
+    DeviceGuard guard(ctx->device);
+    int32_t R = 0;
+    SDP_TRY(validate_segments(ctx, segs, n_segs, true, false, &R));
+    const Plan plan = make_plan(segs, n_segs);
+    const bool store = device_gbar(ctx, R);
+    SDP_TRY(ensure_partials(ctx, plan.tiles));
+    if (store) SDP_TRY(ensure_gbar(ctx, plan.gbar_elems));
+    hipStream_t s = (hipStream_t)stream;
+    SDP_TRY(order_after_last(ctx, s));
+    SDP_TRY(device_norm(ctx, segs, n_segs, R, plan, store, hp->max_grad_norm, s));
+    for (int32_t k = 0; k < n_segs; ++k) {
+        const sdp_segment &g = segs[k];
+        SDP_TRY(update_launch(ctx, R, hp, g.master, g.exp_avg, g.exp_avg_sq, g.param_bf16, g.grads,
+                              store ? ctx->gbar + plan.gbar_base[k] : nullptr, g.numel, s));
+    }
+    SDP_TRY(mark_done(ctx, s));
+    if (grad_norm_out) {
+        NormState st;
+        SDP_TRY(read_norm(ctx, s, &st));
+        *grad_norm_out = st.norm;
+        if (st.nonfinite) return fail(SDP_ERR_NONFINITE, "gradient norm is not finite (%g); nothing was updated", st.norm);
+    }
+    return SDP_OK;
+}
+
+int sdp_stream_step(sdp_ctx *ctx, const sdp_segment *host_segs, int32_t n_segs, const sdp_adamw_params *hp,
+                    int64_t chunk_elems, double *grad_norm_out) {
+    t_err.clear();
+    if (!ctx) return fail(SDP_ERR_INVALID_ARGUMENT, "context is NULL");
+    SDP_TRY(check_hparams(hp));
+    DeviceGuard guard(ctx->device);
+    int32_t R = 0;
+    SDP_TRY(stream_common_checks(ctx, host_segs, n_segs, chunk_elems, false, &R));
+    const Plan plan = make_plan(host_segs, n_segs);
+    const bool store = !(ctx->flags & SDP_FLAG_STREAM_GBAR_NEVER);
+    SDP_TRY(ensure_partials(ctx, plan.tiles));
+    if (store) SDP_TRY(ensure_gbar(ctx, plan.gbar_elems));
+    const std::vector<Chunk> chunks = make_chunks(host_segs, n_segs, chunk_elems);
+    SDP_TRY(order_after_last(ctx, ctx->s_copy));
+    SDP_TRY(order_after_last(ctx, ctx->s_comp));
+    bool used[2] = {false, false};
+    int rc = stream_norm_phase(ctx, host_segs, n_segs, R, plan, chunks, store, hp->max_grad_norm, used);
+    NormState st{};
+    if (rc == SDP_OK) rc = read_norm(ctx, ctx->s_comp, &st);
+    if (rc != SDP_OK) {
+        (void)sync_streams(ctx);
+        return rc;
+    }
+    if (grad_norm_out) *grad_norm_out = st.norm;
+    if (st.nonfinite) {
+        SDP_TRY(sync_streams(ctx));
+        SDP_TRY(mark_done(ctx, ctx->s_comp));
+        return fail(SDP_ERR_NONFINITE, "gradient norm is not finite (%g); nothing was updated", st.norm);
+    }
+    rc = stream_update_phase(ctx, host_segs, R, plan, chunks, store, hp, used, chunks.size());
+    int rc2 = sync_streams(ctx);
+    if (rc != SDP_OK) return rc;
+    if (rc2 != SDP_OK) return rc2;
+    return mark_done(ctx, ctx->s_comp);
+}
+
+int sdp_grad_norm(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int device_resident, int64_t chunk_elems,
+                  void *stream, double *norm_out) {
+    t_err.clear();
+    if (!ctx || !norm_out) return fail(SDP_ERR_INVALID_ARGUMENT, "context or norm_out is NULL");
+    DeviceGuard guard(ctx->device);
+    int32_t R = 0;
+    NormState st{};
+    if (device_resident) {
+        SDP_TRY(validate_segments(ctx, segs, n_segs, true, true, &R));
+        const Plan p = make_plan(segs, n_segs);
+        SDP_TRY(ensure_partials(ctx, p.tiles));
+        hipStream_t s = (hipStream_t)stream;
+        SDP_TRY(order_after_last(ctx, s));
+        SDP_TRY(device_norm(ctx, segs, n_segs, R, p, false, 0.0, s));
+        SDP_TRY(mark_done(ctx, s));
+        SDP_TRY(read_norm(ctx, s, &st));
+    } else {
+        SDP_TRY(stream_common_checks(ctx, segs, n_segs, chunk_elems, true, &R));
+        const Plan p = make_plan(segs, n_segs);
+        SDP_TRY(ensure_partials(ctx, p.tiles));
+        const std::vector<Chunk> chunks = make_chunks(segs, n_segs, chunk_elems);
+        SDP_TRY(order_after_last(ctx, ctx->s_copy));
+        SDP_TRY(order_after_last(ctx, ctx->s_comp));
+        bool used[2] = {false, false};
+        int rc = stream_norm_phase(ctx, segs, n_segs, R, p, chunks, false, 0.0, used);
+        if (rc == SDP_OK) rc = read_norm(ctx, ctx->s_comp, &st);
+        int rc2 = sync_streams(ctx);
+        if (rc != SDP_OK) return rc;
+        if (rc2 != SDP_OK) return rc2;
+        SDP_TRY(mark_done(ctx, ctx->s_comp));
+    }
+    *norm_out = st.norm;
+    if (st.nonfinite) return fail(SDP_ERR_NONFINITE, "gradient norm is not finite (%g)", st.norm);
+    return SDP_OK;
+}
+
+int sdp_ctx_last_norm(sdp_ctx *ctx, double *norm, double *clip_coef, int *nonfinite) {
+    t_err.clear();
+    if (!ctx) return fail(SDP_ERR_INVALID_ARGUMENT, "context is NULL");
+    DeviceGuard guard(ctx->device);
+    if (ctx->last_done_valid) HIP_TRY(hipEventSynchronize(ctx->last_done));
+    NormState st{};
+    HIP_TRY(hipMemcpy(&st, ctx->ns, sizeof st, hipMemcpyDeviceToHost));
+    if (norm) *norm = st.norm;
+    if (clip_coef) *clip_coef = st.clip;
+    if (nonfinite) *nonfinite = st.nonfinite;
+    return SDP_OK;
+}
+
+int sdp_cast_bf16(sdp_ctx *ctx, const float *src, uint16_t *dst, int64_t n, void *stream) {
+    t_err.clear();
+    if (!ctx || !src || !dst || n < 1) return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_cast_bf16: bad argument");
+    if (!aligned(src) || !aligned(dst)) return fail(SDP_ERR_ALIGNMENT, "sdp_cast_bf16: pointers must be 16-byte aligned");
+    DeviceGuard guard(ctx->device);
+    SDP_TRY(check_device_ptr(ctx, src, (size_t)n * 4, "src", 0));
+    SDP_TRY(check_device_ptr(ctx, dst, (size_t)n * 2, "dst", 0));
+    uintptr_t a0 = (uintptr_t)src, a1 = a0 + (size_t)n * 4, b0 = (uintptr_t)dst, b1 = b0 + (size_t)n * 2;
+    if (a0 < b1 && b0 < a1) return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_cast_bf16: src and dst overlap");
+    HIP_TRY(sdp::launch_cast_bf16(src, dst, n, (hipStream_t)stream));
+    return SDP_OK;
+}
+
+int sdp_ctx_set_timing(sdp_ctx *ctx, int enable) {
+    t_err.clear();
+    if (!ctx) return fail(SDP_ERR_INVALID_ARGUMENT, "context is NULL");
+    DeviceGuard guard(ctx->device);
+    if (enable) {
+        for (const Timed &t : ctx->timed) {
+            (void)hipEventSynchronize(t.b);
+            ctx->pool.push_back(t.a);
+            ctx->pool.push_back(t.b);
+        }
+        ctx->timed.clear();
+    }
+    ctx->timing = enable != 0;
+    return SDP_OK;
+}
+
+int sdp_ctx_get_timing(sdp_ctx *ctx, sdp_kernel_times *out) {
+    t_err.clear();
+    if (!ctx || !out) return fail(SDP_ERR_INVALID_ARGUMENT, "context or out is NULL");
+    DeviceGuard guard(ctx->device);
+    sdp_kernel_times r{};
+    for (const Timed &t : ctx->timed) {
+        HIP_TRY(hipEventSynchronize(t.b));
+        float ms = 0.f;
+        HIP_TRY(hipEventElapsedTime(&ms, t.a, t.b));
+        if (t.kind == kNorm) {
+            r.norm_ms += ms;
+            r.norm_launches++;
+        } else if (t.kind == kFinalize) {
+            r.finalize_ms += ms;
+            r.finalize_launches++;
+        } else {
+            r.update_ms += ms;
+            r.update_launches++;
+            r.update_elems += t.elems;
+        }
+    }
+    *out = r;
+    return SDP_OK;
+}
+
+int sdp_probe_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, void *stream) {
+    t_err.clear();
+    if (!ctx || !dst || !src || bytes < 16 || bytes % 16 != 0)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_probe_copy: bad argument (bytes must be a positive multiple of 16)");
+    if (!aligned(dst) || !aligned(src)) return fail(SDP_ERR_ALIGNMENT, "sdp_probe_copy: pointers must be 16-byte aligned");
+    DeviceGuard guard(ctx->device);
+    SDP_TRY(check_device_ptr(ctx, dst, (size_t)bytes, "dst", 0));
+    SDP_TRY(check_device_ptr(ctx, src, (size_t)bytes, "src", 0));
+    HIP_TRY(sdp::launch_copy16(dst, src, bytes / 16, ctx->update_max_blocks, (hipStream_t)stream));
+    return SDP_OK;
+}
+
+int sdp_probe_link(sdp_ctx *ctx, void *host_a, void *host_b, void *dev_a, void *dev_b, int64_t bytes,
+                   int64_t chunk_bytes, int32_t reps, double *gbs_out) {
+    t_err.clear();
+    if (!ctx || !host_a || !host_b || !dev_a || !dev_b || !gbs_out || bytes < 1 || chunk_bytes < 1 || reps < 1)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_probe_link: bad argument");
+    DeviceGuard guard(ctx->device);
+    SDP_TRY(check_pinned_ptr(host_a, (size_t)bytes, "host_a", 0));
+    SDP_TRY(check_pinned_ptr(host_b, (size_t)bytes, "host_b", 0));
+    SDP_TRY(check_device_ptr(ctx, dev_a, (size_t)bytes, "dev_a", 0));
+    SDP_TRY(check_device_ptr(ctx, dev_b, (size_t)bytes, "dev_b", 0));
+    HIP_TRY(hipDeviceSynchronize());
+    hipEvent_t e0, e1, e2, e3;
+    HIP_TRY(hipEventCreate(&e0));
+    HIP_TRY(hipEventCreate(&e1));
+    HIP_TRY(hipEventCreate(&e2));
+    HIP_TRY(hipEventCreate(&e3));
+    auto enqueue = [&](bool h2d, hipStream_t s) -> hipError_t {
+        for (int32_t k = 0; k < reps; ++k)
+            for (int64_t off = 0; off < bytes; off += chunk_bytes) {
+                const size_t len = (size_t)std::min(chunk_bytes, bytes - off);
+                hipError_t e = h2d ? hipMemcpyAsync((char *)dev_a + off, (const char *)host_a + off, len,
+                                                    hipMemcpyHostToDevice, s)
+                                   : hipMemcpyAsync((char *)host_b + off, (const char *)dev_b + off, len,
+                                                    hipMemcpyDeviceToHost, s);
+                if (e != hipSuccess) return e;
+            }
+        return hipSuccess;
+    };
+    float ms = 0.f;
+    const double total = (double)bytes * reps;
+    int rc = SDP_OK;
+    do {
+        // H2D alone on the copy stream
+        if (hipEventRecord(e0, ctx->s_copy) || enqueue(true, ctx->s_copy) || hipEventRecord(e1, ctx->s_copy) ||
+            hipEventSynchronize(e1) || hipEventElapsedTime(&ms, e0, e1)) {
+            rc = fail(SDP_ERR_HIP, "sdp_probe_link: H2D pass failed");
+            break;
+        }
+        gbs_out[0] = total / (ms * 1e-3) / 1e9;
+        // D2H alone on the compute stream
+        if (hipEventRecord(e0, ctx->s_comp) || enqueue(false, ctx->s_comp) || hipEventRecord(e1, ctx->s_comp) ||
+            hipEventSynchronize(e1) || hipEventElapsedTime(&ms, e0, e1)) {
+            rc = fail(SDP_ERR_HIP, "sdp_probe_link: D2H pass failed");
+            break;
+        }
+        gbs_out[1] = total / (ms * 1e-3) / 1e9;
+        // both at once: start together, stop when the later one ends
+        if (hipEventRecord(e0, ctx->s_copy) || hipStreamWaitEvent(ctx->s_comp, e0, 0) || enqueue(true, ctx->s_copy) ||
+            enqueue(false, ctx->s_comp) || hipEventRecord(e2, ctx->s_comp) || hipStreamWaitEvent(ctx->s_copy, e2, 0) ||
+            hipEventRecord(e3, ctx->s_copy) || hipEventSynchronize(e3) || hipEventElapsedTime(&ms, e0, e3)) {
+            rc = fail(SDP_ERR_HIP, "sdp_probe_link: bidirectional pass failed");
+            break;
+        }
+        gbs_out[2] = 2.0 * total / (ms * 1e-3) / 1e9;
+    } while (0);
+    (void)hipGetLastError();
+    (void)hipDeviceSynchronize();
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    (void)hipEventDestroy(e2);
+    (void)hipEventDestroy(e3);
+    return rc;
+}
+
+}  // extern "C"

@@ -1,0 +1,283 @@
+"""ctypes binding of libsdp (include/sdp.h): argument marshalling only.
+
+Every function here has the name of the C entry point it calls and does
+nothing but convert arguments, call it and turn a negative status into an
+exception.  All computation runs in the HIP library; if libsdp.so is not
+built this module raises on import.
+"""
+import ctypes
+import os
+from typing import List, Optional, Sequence, Tuple
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsdp.so")
+
+# status codes and constants, as in include/sdp.h
+SDP_OK = 0
+SDP_ERR_INVALID_ARGUMENT = -1
+SDP_ERR_ALIGNMENT = -2
+SDP_ERR_NOT_DEVICE_MEMORY = -3
+SDP_ERR_NOT_PINNED = -4
+SDP_ERR_CHUNK_TOO_LARGE = -5
+SDP_ERR_OUT_OF_MEMORY = -6
+SDP_ERR_HIP = -7
+SDP_ERR_NONFINITE = -8
+SDP_NORM_TILE = 65536
+SDP_MAX_RANKS = 16
+SDP_ALIGN = 16
+SDP_FLAG_DEVICE_GBAR_NEVER = 0x1
+SDP_FLAG_DEVICE_GBAR_ALWAYS = 0x2
+SDP_FLAG_STREAM_GBAR_NEVER = 0x4
+SDP_FLAG_DEBUG_POISON = 0x8
+
+
+class SdpError(RuntimeError):
+    def __init__(self, status: int, name: str, detail: str):
+        super().__init__(f"{name}: {detail}")
+        self.status = status
+        self.name = name
+        self.detail = detail
+
+
+class SdpNonFinite(SdpError):
+    def __init__(self, status, name, detail, norm):
+        super().__init__(status, name, detail)
+        self.norm = norm
+
+
+class sdp_adamw_params(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_double), ("beta1", ctypes.c_double), ("beta2", ctypes.c_double),
+                ("eps", ctypes.c_double), ("weight_decay", ctypes.c_double),
+                ("max_grad_norm", ctypes.c_double), ("step", ctypes.c_int64)]
+
+
+class sdp_segment(ctypes.Structure):
+    _fields_ = [("master", ctypes.c_void_p), ("exp_avg", ctypes.c_void_p),
+                ("exp_avg_sq", ctypes.c_void_p), ("param_bf16", ctypes.c_void_p),
+                ("grads", ctypes.c_void_p), ("n_ranks", ctypes.c_int32), ("numel", ctypes.c_int64)]
+
+
+class sdp_kernel_times(ctypes.Structure):
+    _fields_ = [("norm_ms", ctypes.c_double), ("finalize_ms", ctypes.c_double),
+                ("update_ms", ctypes.c_double), ("norm_launches", ctypes.c_int64),
+                ("finalize_launches", ctypes.c_int64), ("update_launches", ctypes.c_int64),
+                ("update_elems", ctypes.c_int64)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, dbl = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+    P = ctypes.POINTER
+    sig = {
+        "sdp_ctx_create": (ctypes.c_int, [P(vp), ctypes.c_int, i64, i32, ctypes.c_uint32]),
+        "sdp_ctx_destroy": (None, [vp]),
+        "sdp_agg_adam_step": (ctypes.c_int, [vp, vp, i32, P(sdp_adamw_params), i64, vp, P(dbl)]),
+        "sdp_stream_step": (ctypes.c_int, [vp, vp, i32, P(sdp_adamw_params), i64, P(dbl)]),
+        "sdp_grad_norm": (ctypes.c_int, [vp, vp, i32, ctypes.c_int, i64, vp, P(dbl)]),
+        "sdp_ctx_last_norm": (ctypes.c_int, [vp, P(dbl), P(dbl), P(ctypes.c_int)]),
+        "sdp_cast_bf16": (ctypes.c_int, [vp, vp, vp, i64, vp]),
+        "sdp_plan": (ctypes.c_int, [vp, i32, i64, P(i64), P(i64)]),
+        "sdp_bytes_per_elem": (ctypes.c_int, [ctypes.c_int, i32, ctypes.c_uint32, P(dbl), P(dbl)]),
+        "sdp_ctx_set_timing": (ctypes.c_int, [vp, ctypes.c_int]),
+        "sdp_ctx_get_timing": (ctypes.c_int, [vp, P(sdp_kernel_times)]),
+        "sdp_probe_copy": (ctypes.c_int, [vp, vp, vp, i64, vp]),
+        "sdp_probe_link": (ctypes.c_int, [vp, vp, vp, vp, vp, i64, i64, i32, P(dbl)]),
+        "sdp_host_alloc": (ctypes.c_int, [P(vp), ctypes.c_size_t]),
+        "sdp_host_free": (ctypes.c_int, [vp]),
+        "sdp_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "sdp_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    return L
+
+
+_lib = _load()
+
+
+def _check(rc: int, norm: Optional[float] = None) -> None:
+    if rc == SDP_OK:
+        return
+    name = _lib.sdp_status_string(rc).decode()
+    detail = _lib.sdp_last_error().decode()
+    if rc == SDP_ERR_NONFINITE:
+        raise SdpNonFinite(rc, name, detail, norm)
+    raise SdpError(rc, name, detail)
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return None
+    if hasattr(stream, "cuda_stream"):
+        return stream.cuda_stream or None
+    return int(stream) or None
+
+
+class Segments:
+    """A marshalled array of sdp_segment (keeps the pointer arrays alive).
+
+    Each entry is (master, exp_avg, exp_avg_sq, param_bf16, [grad ptrs], numel)
+    with integer addresses."""
+
+    def __init__(self, entries: Sequence[Tuple[int, int, int, int, Sequence[int], int]]):
+        self.n = len(entries)
+        self.arr = (sdp_segment * max(self.n, 1))()
+        self._keep = []
+        for k, (p, m, v, pb, grads, numel) in enumerate(entries):
+            g = (ctypes.c_void_p * len(grads))(*grads)
+            self._keep.append(g)
+            self.arr[k] = sdp_segment(p, m, v, pb, ctypes.cast(g, ctypes.c_void_p), len(grads), numel)
+
+    @property
+    def ptr(self):
+        return ctypes.cast(self.arr, ctypes.c_void_p)
+
+
+def segments_from_tensors(tensor_sets) -> Segments:
+    """tensor_sets: iterable of (master, exp_avg, exp_avg_sq, param_bf16, grads)
+    torch tensors (contiguous; FP32 states, 16-bit params and gradients)."""
+    entries = []
+    for master, m, v, pb, grads in tensor_sets:
+        for t in (master, m, v, pb, *grads):
+            if not t.is_contiguous():
+                raise ValueError("tensors must be contiguous")
+        entries.append((master.data_ptr(), m.data_ptr(), v.data_ptr(), pb.data_ptr(),
+                        [g.data_ptr() for g in grads], master.numel()))
+    return Segments(entries)
+
+
+def make_params(lr=1e-5, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01,
+                max_grad_norm=1.0, step=1) -> sdp_adamw_params:
+    return sdp_adamw_params(lr, beta1, beta2, eps, weight_decay, max_grad_norm, step)
+
+
+# ---- entry points ---------------------------------------------------------
+
+def sdp_ctx_create(device: int = 0, max_chunk_elems: int = 0, max_ranks: int = SDP_MAX_RANKS,
+                   flags: int = 0) -> ctypes.c_void_p:
+    ctx = ctypes.c_void_p()
+    _check(_lib.sdp_ctx_create(ctypes.byref(ctx), device, max_chunk_elems, max_ranks, flags))
+    return ctx
+
+
+def sdp_ctx_destroy(ctx) -> None:
+    _lib.sdp_ctx_destroy(ctx)
+
+
+def sdp_agg_adam_step(ctx, segs: Segments, hp: sdp_adamw_params, chunk_elems: int = 0,
+                      stream=None, want_norm: bool = False) -> Optional[float]:
+    norm = ctypes.c_double(float("nan"))
+    rc = _lib.sdp_agg_adam_step(ctx, segs.ptr, segs.n, ctypes.byref(hp), chunk_elems,
+                                _stream(stream), ctypes.byref(norm) if want_norm else None)
+    _check(rc, norm.value)
+    return norm.value if want_norm else None
+
+
+def sdp_stream_step(ctx, segs: Segments, hp: sdp_adamw_params, chunk_elems: int) -> float:
+    norm = ctypes.c_double(float("nan"))
+    rc = _lib.sdp_stream_step(ctx, segs.ptr, segs.n, ctypes.byref(hp), chunk_elems, ctypes.byref(norm))
+    _check(rc, norm.value)
+    return norm.value
+
+
+def sdp_grad_norm(ctx, segs: Segments, device_resident: bool, chunk_elems: int = 0,
+                  stream=None) -> float:
+    norm = ctypes.c_double(float("nan"))
+    rc = _lib.sdp_grad_norm(ctx, segs.ptr, segs.n, int(bool(device_resident)), chunk_elems,
+                            _stream(stream), ctypes.byref(norm))
+    _check(rc, norm.value)
+    return norm.value
+
+
+def sdp_ctx_last_norm(ctx) -> Tuple[float, float, bool]:
+    n, c, f = ctypes.c_double(), ctypes.c_double(), ctypes.c_int()
+    _check(_lib.sdp_ctx_last_norm(ctx, ctypes.byref(n), ctypes.byref(c), ctypes.byref(f)))
+    return n.value, c.value, bool(f.value)
+
+
+def sdp_cast_bf16(ctx, src: int, dst: int, n: int, stream=None) -> None:
+    _check(_lib.sdp_cast_bf16(ctx, src, dst, n, _stream(stream)))
+
+
+def sdp_plan(numels: Sequence[int], chunk_elems: int) -> Tuple[int, int]:
+    arr = (ctypes.c_int64 * len(numels))(*numels)
+    ch, ti = ctypes.c_int64(), ctypes.c_int64()
+    _check(_lib.sdp_plan(ctypes.cast(arr, ctypes.c_void_p), len(numels), chunk_elems,
+                         ctypes.byref(ch), ctypes.byref(ti)))
+    return ch.value, ti.value
+
+
+def sdp_bytes_per_elem(streamed: bool, n_ranks: int, flags: int = 0) -> Tuple[float, float]:
+    a, b = ctypes.c_double(), ctypes.c_double()
+    _check(_lib.sdp_bytes_per_elem(int(bool(streamed)), n_ranks, flags, ctypes.byref(a), ctypes.byref(b)))
+    return a.value, b.value
+
+
+def sdp_ctx_set_timing(ctx, enable: bool) -> None:
+    _check(_lib.sdp_ctx_set_timing(ctx, int(bool(enable))))
+
+
+def sdp_ctx_get_timing(ctx) -> sdp_kernel_times:
+    t = sdp_kernel_times()
+    _check(_lib.sdp_ctx_get_timing(ctx, ctypes.byref(t)))
+    return t
+
+
+def sdp_probe_copy(ctx, dst: int, src: int, nbytes: int, stream=None) -> None:
+    _check(_lib.sdp_probe_copy(ctx, dst, src, nbytes, _stream(stream)))
+
+
+def sdp_probe_link(ctx, host_a: int, host_b: int, dev_a: int, dev_b: int, nbytes: int,
+                   chunk_bytes: int, reps: int) -> List[float]:
+    out = (ctypes.c_double * 3)()
+    _check(_lib.sdp_probe_link(ctx, host_a, host_b, dev_a, dev_b, nbytes, chunk_bytes, reps,
+                               ctypes.cast(out, ctypes.POINTER(ctypes.c_double))))
+    return list(out)
+
+
+def sdp_host_alloc(nbytes: int) -> int:
+    p = ctypes.c_void_p()
+    _check(_lib.sdp_host_alloc(ctypes.byref(p), nbytes))
+    return p.value
+
+
+def sdp_host_free(ptr: int) -> None:
+    _check(_lib.sdp_host_free(ptr))
+
+
+def sdp_status_string(status: int) -> str:
+    return _lib.sdp_status_string(status).decode()
+
+
+def sdp_last_error() -> str:
+    return _lib.sdp_last_error().decode()
+
+
+class HostBuffer:
+    """Pinned host memory from sdp_host_alloc, viewable as numpy arrays."""
+
+    def __init__(self, nbytes: int):
+        self.nbytes = nbytes
+        self.ptr = sdp_host_alloc(nbytes)
+
+    def view(self, dtype, count: int, offset: int = 0):
+        import numpy as np
+        dt = np.dtype(dtype)
+        assert offset + count * dt.itemsize <= self.nbytes
+        buf = (ctypes.c_char * (count * dt.itemsize)).from_address(self.ptr + offset)
+        return np.frombuffer(buf, dtype=dt, count=count)
+
+    def close(self):
+        if self.ptr:
+            sdp_host_free(self.ptr)
+            self.ptr = 0
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

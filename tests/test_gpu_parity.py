@@ -1,0 +1,322 @@
+"""GPU parity: the HIP path through the C ABI against the oracle, on small
+inputs that span several tiles and ragged tails, plus bit-exact invariants.
+
+Criteria (per element, every step): FP32 master / exp_avg / exp_avg_sq within
+relative error 1e-5 of the oracle (an oracle zero requires a GPU zero); BF16
+params equal to bf16(GPU master) everywhere, equal to bf16(oracle master) on
+all but 1e-4 of elements and within 1 BF16 ulp everywhere; gradient norm
+within relative 1e-6.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_util import (DevState, HostState, check_norm, check_state, hp_pair, log, need_gpu,
+                      rand_inputs, states_equal, torch)
+
+pytestmark = pytest.mark.gpu
+
+TILE = 65536
+
+
+@pytest.fixture(scope="module")
+def sdp():
+    return need_gpu()
+
+
+@pytest.fixture(scope="module")
+def ctx(sdp):
+    c = sdp.sdp_ctx_create(0, 4 * TILE, 16, 0)
+    yield c
+    sdp.sdp_ctx_destroy(c)
+
+
+@pytest.fixture(scope="module")
+def ctx_store(sdp):
+    c = sdp.sdp_ctx_create(0, 4 * TILE, 16, sdp.SDP_FLAG_DEVICE_GBAR_ALWAYS)
+    yield c
+    sdp.sdp_ctx_destroy(c)
+
+
+@pytest.fixture(scope="module")
+def ctx_nostore(sdp):
+    c = sdp.sdp_ctx_create(0, 4 * TILE, 16, sdp.SDP_FLAG_DEVICE_GBAR_NEVER | sdp.SDP_FLAG_STREAM_GBAR_NEVER)
+    yield c
+    sdp.sdp_ctx_destroy(c)
+
+
+@pytest.fixture(scope="module")
+def ctx_poison(sdp):
+    c = sdp.sdp_ctx_create(0, 4 * TILE, 16, sdp.SDP_FLAG_DEBUG_POISON)
+    yield c
+    sdp.sdp_ctx_destroy(c)
+
+
+def stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def dev_step(sdp, ctx, dev, grads, hp, chunk=0, want_norm=True):
+    dev.set_grads(grads)
+    norm = sdp.sdp_agg_adam_step(ctx, dev.segments(sdp), hp, chunk, stream(), want_norm=want_norm)
+    torch.cuda.synchronize()
+    return norm
+
+
+def test_tiny_workload_free_running_and_teacher_forced(sdp, ctx):
+    w = synth.workload(0)
+    log(f"workload {w.name}")
+    master = synth.master(w, 0)
+    dev = DevState([master], w.ranks)
+    ref = oracle.State([master])
+    for t in range(1, w.steps + 1):
+        grads = [[synth.grad_bf16(w, 0, t, r) for r in range(w.ranks)]]
+        hs, ho = hp_pair(sdp, **w.hparams(t))
+        before = dev.host()
+        norm = dev_step(sdp, ctx, dev, grads, hs, chunk=w.chunk)
+        rc, onorm = oracle.step(ref, grads, ho)
+        assert rc == oracle.ORC_OK
+        check_norm(norm, onorm)
+        assert norm < w.max_grad_norm  # this workload's clip is a no-op
+        got = dev.host()
+        check_state(got, ref)                      # free running
+        forced = before.copy()
+        oracle.step(forced, grads, ho)
+        check_state(got, forced)                   # teacher forced
+
+
+SIZES = [1, 7, 8, 9, 63, 64, 65, 4095, 4097, TILE - 1, TILE, TILE + 1, 3 * TILE + 5]
+
+
+@pytest.mark.parametrize("R", [1, 2, 3, 4, 5, 8, 16])
+@pytest.mark.parametrize("store", [False, True])
+def test_sizes_and_ranks(sdp, ctx_store, ctx_nostore, R, store):
+    c = ctx_store if store else ctx_nostore
+    log(f"sizes/ranks R={R} store={store}")
+    for n in SIZES:
+        masters, grads = rand_inputs([n], R, 2, seed=1000 + 17 * n + R)
+        dev = DevState(masters, R)
+        ref = oracle.State(masters)
+        for t in (1, 2):
+            hs, ho = hp_pair(sdp, lr=1e-3, weight_decay=0.02, max_grad_norm=0.05, step=t)
+            norm = dev_step(sdp, c, dev, grads[t - 1], hs)
+            _, onorm = oracle.step(ref, grads[t - 1], ho)
+            check_norm(norm, onorm)
+            check_state(dev.host(), ref)
+
+
+def test_multi_segment_with_clipping(sdp, ctx):
+    sizes = [2 * TILE + 3, 1, 100000, 8]
+    R = 4
+    masters, grads = rand_inputs(sizes, R, 3, seed=5)
+    dev = DevState(masters, R)
+    ref = oracle.State(masters)
+    for t in (1, 2, 3):
+        hs, ho = hp_pair(sdp, lr=1e-4, weight_decay=0.1, max_grad_norm=0.1, step=t)
+        norm = dev_step(sdp, ctx, dev, grads[t - 1], hs)
+        _, onorm = oracle.step(ref, grads[t - 1], ho)
+        check_norm(norm, onorm)
+        assert norm > 0.1  # clipping active
+        check_state(dev.host(), ref)
+
+
+def test_bit_exact_invariants(sdp, ctx, ctx_store, ctx_nostore):
+    n = 3 * TILE + 77
+    masters, grads = rand_inputs([n], 4, 3, seed=9)
+    hs = [sdp.make_params(lr=1e-3, max_grad_norm=0.05, step=t) for t in (1, 2, 3)]
+
+    def run(c, R=4, g=None, params=None, chunk=0, steps=3):
+        dev = DevState(masters, R)
+        for t in range(steps):
+            gg = g[t] if g is not None else grads[t]
+            dev_step(sdp, c, dev, gg, (params or hs)[t], chunk=chunk)
+        return dev.host()
+
+    base = run(ctx)
+    assert states_equal(base, run(ctx)), "repeat run differs"
+    assert states_equal(base, run(ctx_store)), "stored g_bar path differs"
+    assert states_equal(base, run(ctx_nostore)), "no-store path differs"
+    assert states_equal(base, run(ctx, chunk=TILE)), "chunk size changed the result"
+    # R identical buffers == R = 1
+    one = [[[grads[t][0][0]]] for t in range(3)]
+    four = [[[grads[t][0][0]] * 4] for t in range(3)]
+    assert states_equal(run(ctx, R=1, g=one), run(ctx, R=4, g=four)), "identical ranks != one rank"
+    # clip no-op: a max norm above the norm equals no clipping
+    big = [sdp.make_params(lr=1e-3, max_grad_norm=1e6, step=t) for t in (1, 2, 3)]
+    off = [sdp.make_params(lr=1e-3, max_grad_norm=0.0, step=t) for t in (1, 2, 3)]
+    assert states_equal(run(ctx, params=big), run(ctx, params=off)), "clip no-op differs"
+    # resume: 2 steps, copy out, rebuild, step 3
+    dev = DevState(masters, 4)
+    for t in range(2):
+        dev_step(sdp, ctx, dev, grads[t], hs[t])
+    h = dev.host()
+    dev2 = DevState(h.master, 4, h.exp_avg, h.exp_avg_sq)
+    dev_step(sdp, ctx, dev2, grads[2], hs[2])
+    assert states_equal(base, dev2.host()), "resume after a state copy differs"
+    # lr = 0 leaves the master bit-unchanged
+    dev = DevState(masters, 4)
+    dev_step(sdp, ctx, dev, grads[0], sdp.make_params(lr=0.0, step=1))
+    got = dev.host()
+    assert np.array_equal(got.master[0], masters[0])
+    assert np.array_equal(got.param_bf16[0], oracle.bf16(masters[0]))
+
+
+@pytest.mark.parametrize("chunk_tiles", [1, 2, 4])
+def test_streamed_matches_oracle_and_device(sdp, ctx, ctx_poison, ctx_nostore, chunk_tiles):
+    sizes = [3 * TILE + 5, 1, 70000]
+    R = 3
+    steps = 2
+    masters, grads = rand_inputs(sizes, R, steps, seed=21 + chunk_tiles)
+    log(f"streamed chunk={chunk_tiles} tiles")
+    hps = [hp_pair(sdp, lr=1e-3, weight_decay=0.05, max_grad_norm=0.2, step=t) for t in range(1, steps + 1)]
+    dev = DevState(masters, R)
+    ref = oracle.State(masters)
+    dev_states, ref_states, norms = [], [], []
+    for t in range(steps):
+        dnorm = dev_step(sdp, ctx, dev, grads[t], hps[t][0])
+        _, onorm = oracle.step(ref, grads[t], hps[t][1])
+        check_norm(dnorm, onorm)
+        dev_states.append(dev.host())
+        ref_states.append(ref.copy())
+        norms.append(dnorm)
+    for c in (ctx_poison, ctx_nostore):
+        host = HostState(sdp, masters, R)
+        try:
+            for t in range(steps):
+                host.set_grads(grads[t])
+                snorm = sdp.sdp_stream_step(c, host.segments(), hps[t][0], chunk_tiles * TILE)
+                assert snorm == norms[t], "streamed norm differs from device norm"
+                got = host.host()
+                check_state(got, ref_states[t])
+                assert states_equal(got, dev_states[t]), "streamed differs from device mode"
+        finally:
+            host.close()
+
+
+def test_grad_norm_modes_agree(sdp, ctx):
+    sizes = [TILE * 2 + 1, 513]
+    R = 5
+    _, grads = rand_inputs(sizes, R, 1, seed=33)
+    dev = DevState([np.zeros(n, np.float32) for n in sizes], R)
+    dev.set_grads(grads[0])
+    dn = sdp.sdp_grad_norm(ctx, dev.segments(sdp), True, 0, stream())
+    host = HostState(sdp, [np.zeros(n, np.float32) for n in sizes], R)
+    try:
+        host.set_grads(grads[0])
+        hn = sdp.sdp_grad_norm(ctx, host.segments(), False, TILE)
+    finally:
+        host.close()
+    on = oracle.grad_norm(grads[0])
+    check_norm(dn, on)
+    assert dn == hn
+
+
+@pytest.mark.parametrize("mode", ["device", "streamed"])
+@pytest.mark.parametrize("bad", [np.nan, np.inf])
+def test_nonfinite_gradient_leaves_states_unchanged(sdp, ctx, mode, bad):
+    sizes = [TILE + 9]
+    R = 2
+    masters, grads = rand_inputs(sizes, R, 1, seed=44)
+    g = [[x.copy() for x in grads[0][0]]]
+    g[0][1][12345] = synth.to_bf16_bits(np.array([bad], np.float32))[0]
+    hs = sdp.make_params(step=1)
+    if mode == "device":
+        dev = DevState(masters, R)
+        dev.pb[0].fill_(7)
+        before = dev.host()
+        with pytest.raises(sdp.SdpNonFinite) as e:
+            dev_step(sdp, ctx, dev, g, hs)
+        assert not np.isfinite(e.value.norm)
+        assert states_equal(before, dev.host())
+        # without a norm request the call is asynchronous and still skips the update
+        dev_step(sdp, ctx, dev, g, hs, want_norm=False)
+        assert states_equal(before, dev.host())
+        norm, clip, nonfinite = sdp.sdp_ctx_last_norm(ctx)
+        assert nonfinite and not np.isfinite(norm)
+    else:
+        host = HostState(sdp, masters, R)
+        try:
+            host.pb[0][:] = 7
+            host.set_grads(g)
+            before = host.host()
+            with pytest.raises(sdp.SdpNonFinite):
+                sdp.sdp_stream_step(ctx, host.segments(), hs, TILE)
+            assert states_equal(before, host.host())
+        finally:
+            host.close()
+
+
+def test_argument_errors_have_no_side_effects(sdp, ctx):
+    n, R = 4096, 2
+    masters, grads = rand_inputs([n], R, 1, seed=55)
+    dev = DevState(masters, R)
+    dev.set_grads(grads[0])
+    torch.cuda.synchronize()
+    before = dev.host()
+    hs = sdp.make_params(step=1)
+    S = sdp.segments_from_tensors
+
+    def expect(status, segs, params=hs, chunk=0):
+        with pytest.raises(sdp.SdpError) as e:
+            sdp.sdp_agg_adam_step(ctx, segs, params, chunk, stream(), want_norm=True)
+        assert e.value.status == status, (e.value.name, e.value.detail)
+
+    p, m, v, pb, g = dev.p[0], dev.m[0], dev.v[0], dev.pb[0], dev.g[0]
+    expect(sdp.SDP_ERR_ALIGNMENT, S([(p[1:], m[1:], v[1:], pb[1:], [x[1:] for x in g])]))
+    expect(sdp.SDP_ERR_INVALID_ARGUMENT, S([(p, m, v, pb, [])]))                 # R = 0
+    expect(sdp.SDP_ERR_INVALID_ARGUMENT, S([(p, m, v, pb, g * 9)]))              # R = 18
+    expect(sdp.SDP_ERR_INVALID_ARGUMENT, S([(p, m, v, pb, [p.view(torch.int16)[:n], g[1]])]))  # grad aliases master
+    expect(sdp.SDP_ERR_INVALID_ARGUMENT, S([(p, p, v, pb, g)]))                  # master aliases exp_avg
+    expect(sdp.SDP_ERR_INVALID_ARGUMENT, S([(p, m, v, pb, g)]), params=sdp.make_params(step=0))
+    expect(sdp.SDP_ERR_INVALID_ARGUMENT, S([(p, m, v, pb, g)]), params=sdp.make_params(beta1=1.0, step=1))
+    expect(sdp.SDP_ERR_INVALID_ARGUMENT, S([(p, m, v, pb, g)]), chunk=1000)
+    expect(sdp.SDP_ERR_INVALID_ARGUMENT, S([(p, m, v, pb, g), (p, m, v, pb, g[:1])]))  # R differs
+    host = np.zeros(n, np.float32)
+    expect(sdp.SDP_ERR_NOT_DEVICE_MEMORY,
+           sdp.Segments([(host.ctypes.data, m.data_ptr(), v.data_ptr(), pb.data_ptr(), [x.data_ptr() for x in g], n)]))
+    expect(sdp.SDP_ERR_NOT_DEVICE_MEMORY,
+           sdp.Segments([(p.data_ptr(), m.data_ptr(), v.data_ptr(), pb.data_ptr(), [x.data_ptr() for x in g],
+                          1 << 34)]))                                            # far beyond the allocation
+    # streamed mode: device or pageable pointers are not pinned; chunk bounds
+    with pytest.raises(sdp.SdpError) as e:
+        sdp.sdp_stream_step(ctx, S([(p, m, v, pb, g)]), hs, TILE)
+    assert e.value.status == sdp.SDP_ERR_NOT_PINNED
+    hm = [np.zeros(n, np.float32) for _ in range(3)]
+    hb = [np.zeros(n, np.uint16) for _ in range(3)]
+    pageable = sdp.Segments([(hm[0].ctypes.data, hm[1].ctypes.data, hm[2].ctypes.data, hb[0].ctypes.data,
+                              [hb[1].ctypes.data, hb[2].ctypes.data], n)])
+    with pytest.raises(sdp.SdpError) as e:
+        sdp.sdp_stream_step(ctx, pageable, hs, TILE)
+    assert e.value.status == sdp.SDP_ERR_NOT_PINNED
+    with pytest.raises(sdp.SdpError) as e:
+        sdp.sdp_stream_step(ctx, pageable, hs, 8 * TILE)
+    assert e.value.status == sdp.SDP_ERR_CHUNK_TOO_LARGE
+    torch.cuda.synchronize()
+    assert states_equal(before, dev.host())
+
+
+def test_cast_bf16_exhaustive(sdp, ctx):
+    """The device BF16 re-emit over all 2^32 FP32 bit patterns, against the oracle."""
+    chunk = 1 << 28
+    src = torch.empty(chunk, dtype=torch.int32, device="cuda")
+    dst = torch.empty(chunk, dtype=torch.int16, device="cuda")
+    base = torch.arange(chunk, dtype=torch.int64, device="cuda")
+    bad = 0
+    for k in range((1 << 32) // chunk):
+        vals = base + k * chunk
+        vals = torch.where(vals >= (1 << 31), vals - (1 << 32), vals)
+        src.copy_(vals.to(torch.int32))
+        sdp.sdp_cast_bf16(ctx, src.data_ptr(), dst.data_ptr(), chunk, stream())
+        got = dst.cpu().numpy().view(np.uint16)
+        f = src.cpu().numpy().view(np.float32)
+        bad += int(np.count_nonzero(got != oracle.bf16(f)))
+        if k % 4 == 0:
+            log(f"cast chunk {k}")
+    assert bad == 0
+    # ragged sizes
+    for n in (1, 7, 9, 1000003):
+        x = torch.randn(n, device="cuda")
+        y = torch.empty(n, dtype=torch.int16, device="cuda")
+        sdp.sdp_cast_bf16(ctx, x.data_ptr(), y.data_ptr(), n, stream())
+        assert np.array_equal(y.cpu().numpy().view(np.uint16), oracle.bf16(x.cpu().numpy()))
