@@ -116,7 +116,7 @@ typedef struct {
 /* Accumulated kernel times of a context, from HIP events recorded around
  * each launch on the stream the launch uses (only while timing is on). */
 typedef struct {
-    double norm_ms;       /* norm-partials kernel (step a3, first pass) */
+    double norm_ms;       /* norm-partials kernel (first pass over the gradients) */
     double finalize_ms;   /* norm finalize kernel */
     double update_ms;     /* fused aggregate + clip + AdamW + BF16 kernel */
     int64_t norm_launches, finalize_launches, update_launches;
@@ -213,11 +213,14 @@ int sdp_ctx_get_timing(sdp_ctx *ctx, sdp_kernel_times *out);
 int sdp_probe_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, void *stream);
 
 /* Pinned host link bandwidth with the streamed engine's copy path:
- * hipMemcpyAsync in chunk_bytes pieces over `bytes`, `reps` times, on the
- * context's copy stream (H2D) and compute stream (D2H).  gbs_out[0] = H2D
- * alone, [1] = D2H alone, [2] = H2D + D2H at once (sum of both directions).
- * host_a/host_b: pinned host buffers, dev_a/dev_b: device buffers, each of
- * at least `bytes`.  Blocks. */
+ * hipMemcpyAsync in chunk_bytes pieces over `bytes`, `reps` times, host to
+ * device on the context's copy stream and device to host on its compute
+ * stream; when both run, their chunks are issued interleaved, as the engine
+ * issues them.  Each figure is timed on the host from the first enqueue to
+ * the end of both streams.  gbs_out[0] = H2D alone, [1] = D2H alone,
+ * [2] = H2D and D2H at once (sum of both directions).  host_a/host_b:
+ * pinned host buffers, dev_a/dev_b: device buffers, each of at least
+ * `bytes`.  Blocks. */
 int sdp_probe_link(sdp_ctx *ctx, void *host_a, void *host_b, void *dev_a, void *dev_b,
                    int64_t bytes, int64_t chunk_bytes, int32_t reps, double *gbs_out);
 

@@ -38,6 +38,7 @@
 #include "oracle.h"
 
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 #ifdef _OPENMP
 #include <omp.h>
@@ -118,16 +119,31 @@ void orc_mean_grads(const uint16_t *const *grads, int32_t R, int64_t n, float *o
         out[i] = orc_mean_grad(grads, R, i);
 }
 
-/* Step 2: global L2 norm of the mean gradient over all segments. */
+/* Step 2: global L2 norm of the mean gradient over all segments.  S is one
+ * sequential FP64 sum in element order; the mean gradients it adds are
+ * independent of each other, so they are formed a block at a time in
+ * parallel before the block is added in order. */
+#define ORC_NORM_BLOCK (1 << 20)
 double orc_grad_norm(const orc_segment *segs, int32_t n_segs, int32_t R)
 {
+    float *block = (float *)malloc(sizeof(float) * ORC_NORM_BLOCK);
+    if (!block)
+        return NAN;
     double S = 0.0;
     for (int32_t s = 0; s < n_segs; ++s) {
-        for (int64_t i = 0; i < segs[s].numel; ++i) {
-            double g = (double)orc_mean_grad(segs[s].grads, R, i);
-            S += g * g;
+        const uint16_t *const *g = segs[s].grads;
+        for (int64_t a = 0; a < segs[s].numel; a += ORC_NORM_BLOCK) {
+            int64_t len = segs[s].numel - a < ORC_NORM_BLOCK ? segs[s].numel - a : ORC_NORM_BLOCK;
+#pragma omp parallel for schedule(static)
+            for (int64_t k = 0; k < len; ++k)
+                block[k] = orc_mean_grad(g, R, a + k);
+            for (int64_t k = 0; k < len; ++k) {
+                double gb = (double)block[k];
+                S += gb * gb;
+            }
         }
     }
+    free(block);
     return sqrt(S);
 }
 

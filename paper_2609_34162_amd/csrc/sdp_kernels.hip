@@ -17,6 +17,8 @@
 namespace sdp {
 namespace {
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
@@ -93,40 +95,59 @@ __device__ __forceinline__ double block_sum(double x) {
 }
 
 // ---------------------------------------------------------------------------
-// Norm partials: block b sums g_bar^2 over tile b.  Lane t of iteration it
-// handles elements 8*(b*8192 + it*256 + t) .. +7, so each pass of the block
-// reads a contiguous 4 KB per rank.  The per-lane order, the butterfly and
+// Norm partials: block b sums g_bar^2 over tile b.  Lane t handles the
+// 8-element groups b*8192 + j*256 + t for j = 0..31 in increasing j, so each
+// pass of the block reads a contiguous 4 KB per rank; two passes are issued
+// before either is consumed.  The gradients are read with non-temporal loads:
+// they are not reused before the update pass, and the 256 MB last-level cache
+// cannot hold them.  The ragged tail of fewer than 8 elements is added by
+// lane 0 of its tile after the groups.  The per-lane order, the butterfly and
 // the wave order are fixed, so a tile's partial depends on its contents only.
+__device__ __forceinline__ uint4 load_stream(const uint16_t *p) {
+    const u32x4 t = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+    return make_uint4(t.x, t.y, t.z, t.w);
+}
+
 template <int R, bool WRITE_GBAR>
 __global__ __launch_bounds__(kNormThreads) void k_norm_partials(NormArgs a) {
-    constexpr int kGroupsPerTile = kTile / kVec;            // 8192
-    constexpr int kIters = kGroupsPerTile / kNormThreads;   // 32
+    constexpr int kGroupsPerTile = kTile / kVec;                    // 8192
+    constexpr int kUnroll = 2;
+    constexpr int kIters = kGroupsPerTile / (kNormThreads * kUnroll);  // 16
     const int64_t n = a.n;
+    const int64_t full_groups = n / kVec;
     const int64_t tile0 = (int64_t)blockIdx.x * kGroupsPerTile;
     double acc = 0.0;
-    const uint16_t *const *gp = a.g;
     for (int it = 0; it < kIters; ++it) {
-        const int64_t q = tile0 + (int64_t)it * kNormThreads + threadIdx.x;
-        const int64_t e0 = q * kVec;
-        if (e0 + kVec <= n) {
-            uint4 raw[R];
+        uint4 raw[kUnroll][R];
+        bool ok[kUnroll];
 #pragma unroll
-            for (int r = 0; r < R; ++r) raw[r] = *reinterpret_cast<const uint4 *>(gp[r] + e0);
+        for (int u = 0; u < kUnroll; ++u) {
+            const int64_t q = tile0 + (int64_t)(it * kUnroll + u) * kNormThreads + threadIdx.x;
+            ok[u] = q < full_groups;
+#pragma unroll
+            for (int r = 0; r < R; ++r) raw[u][r] = ok[u] ? load_stream(a.g[r] + q * kVec) : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            if (!ok[u]) continue;
             float g[kVec];
-            mean8<R>(raw, g);
+            mean8<R>(raw[u], g);
 #pragma unroll
             for (int e = 0; e < kVec; ++e) acc += (double)g[e] * (double)g[e];
             if constexpr (WRITE_GBAR) {
+                const int64_t e0 = (tile0 + (int64_t)(it * kUnroll + u) * kNormThreads + threadIdx.x) * kVec;
                 float4 *o = reinterpret_cast<float4 *>(a.gbar_out + e0);
                 o[0] = make_float4(g[0], g[1], g[2], g[3]);
                 o[1] = make_float4(g[4], g[5], g[6], g[7]);
             }
-        } else if (e0 < n) {
-            for (int64_t i = e0; i < n; ++i) {
-                float g = mean1<R>(a.g, i);
-                acc += (double)g * (double)g;
-                if constexpr (WRITE_GBAR) a.gbar_out[i] = g;
-            }
+        }
+    }
+    const int64_t tail0 = full_groups * kVec;
+    if (threadIdx.x == 0 && tail0 < n && tail0 / kTile == (int64_t)blockIdx.x) {
+        for (int64_t i = tail0; i < n; ++i) {
+            float g = mean1<R>(a.g, i);
+            acc += (double)g * (double)g;
+            if constexpr (WRITE_GBAR) a.gbar_out[i] = g;
         }
     }
     double t = block_sum<kNormThreads>(acc);

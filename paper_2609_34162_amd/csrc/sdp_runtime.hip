@@ -15,6 +15,7 @@
 // layer).  Phase 1 streams the gradients for the global norm; phase 2
 // streams master/m/v through the fused update and back.
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -896,57 +897,38 @@ int sdp_probe_link(sdp_ctx *ctx, void *host_a, void *host_b, void *dev_a, void *
     SDP_TRY(check_device_ptr(ctx, dev_a, (size_t)bytes, "dev_a", 0));
     SDP_TRY(check_device_ptr(ctx, dev_b, (size_t)bytes, "dev_b", 0));
     HIP_TRY(hipDeviceSynchronize());
-    hipEvent_t e0, e1, e2, e3;
-    HIP_TRY(hipEventCreate(&e0));
-    HIP_TRY(hipEventCreate(&e1));
-    HIP_TRY(hipEventCreate(&e2));
-    HIP_TRY(hipEventCreate(&e3));
-    auto enqueue = [&](bool h2d, hipStream_t s) -> hipError_t {
+    // Each pattern is timed on the host from its first enqueue to the end of
+    // both streams, with nothing else in flight; the two directions are
+    // issued chunk by chunk, interleaved, as the streamed engine issues them.
+    auto copy = [&](bool h2d, int64_t off) -> hipError_t {
+        const size_t len = (size_t)std::min(chunk_bytes, bytes - off);
+        return h2d ? hipMemcpyAsync((char *)dev_a + off, (const char *)host_a + off, len, hipMemcpyHostToDevice,
+                                    ctx->s_copy)
+                   : hipMemcpyAsync((char *)host_b + off, (const char *)dev_b + off, len, hipMemcpyDeviceToHost,
+                                    ctx->s_comp);
+    };
+    auto run = [&](bool do_h2d, bool do_d2h, double *seconds) -> hipError_t {
+        const auto t0 = std::chrono::steady_clock::now();
         for (int32_t k = 0; k < reps; ++k)
             for (int64_t off = 0; off < bytes; off += chunk_bytes) {
-                const size_t len = (size_t)std::min(chunk_bytes, bytes - off);
-                hipError_t e = h2d ? hipMemcpyAsync((char *)dev_a + off, (const char *)host_a + off, len,
-                                                    hipMemcpyHostToDevice, s)
-                                   : hipMemcpyAsync((char *)host_b + off, (const char *)dev_b + off, len,
-                                                    hipMemcpyDeviceToHost, s);
-                if (e != hipSuccess) return e;
+                hipError_t e = hipSuccess;
+                if (do_h2d && (e = copy(true, off)) != hipSuccess) return e;
+                if (do_d2h && (e = copy(false, off)) != hipSuccess) return e;
             }
-        return hipSuccess;
+        hipError_t e = hipStreamSynchronize(ctx->s_copy);
+        if (e == hipSuccess) e = hipStreamSynchronize(ctx->s_comp);
+        *seconds = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+        return e;
     };
-    float ms = 0.f;
     const double total = (double)bytes * reps;
-    int rc = SDP_OK;
-    do {
-        // H2D alone on the copy stream
-        if (hipEventRecord(e0, ctx->s_copy) || enqueue(true, ctx->s_copy) || hipEventRecord(e1, ctx->s_copy) ||
-            hipEventSynchronize(e1) || hipEventElapsedTime(&ms, e0, e1)) {
-            rc = fail(SDP_ERR_HIP, "sdp_probe_link: H2D pass failed");
-            break;
-        }
-        gbs_out[0] = total / (ms * 1e-3) / 1e9;
-        // D2H alone on the compute stream
-        if (hipEventRecord(e0, ctx->s_comp) || enqueue(false, ctx->s_comp) || hipEventRecord(e1, ctx->s_comp) ||
-            hipEventSynchronize(e1) || hipEventElapsedTime(&ms, e0, e1)) {
-            rc = fail(SDP_ERR_HIP, "sdp_probe_link: D2H pass failed");
-            break;
-        }
-        gbs_out[1] = total / (ms * 1e-3) / 1e9;
-        // both at once: start together, stop when the later one ends
-        if (hipEventRecord(e0, ctx->s_copy) || hipStreamWaitEvent(ctx->s_comp, e0, 0) || enqueue(true, ctx->s_copy) ||
-            enqueue(false, ctx->s_comp) || hipEventRecord(e2, ctx->s_comp) || hipStreamWaitEvent(ctx->s_copy, e2, 0) ||
-            hipEventRecord(e3, ctx->s_copy) || hipEventSynchronize(e3) || hipEventElapsedTime(&ms, e0, e3)) {
-            rc = fail(SDP_ERR_HIP, "sdp_probe_link: bidirectional pass failed");
-            break;
-        }
-        gbs_out[2] = 2.0 * total / (ms * 1e-3) / 1e9;
-    } while (0);
-    (void)hipGetLastError();
-    (void)hipDeviceSynchronize();
-    (void)hipEventDestroy(e0);
-    (void)hipEventDestroy(e1);
-    (void)hipEventDestroy(e2);
-    (void)hipEventDestroy(e3);
-    return rc;
+    double sec = 0.0;
+    HIP_TRY(run(true, false, &sec));
+    gbs_out[0] = total / sec / 1e9;
+    HIP_TRY(run(false, true, &sec));
+    gbs_out[1] = total / sec / 1e9;
+    HIP_TRY(run(true, true, &sec));
+    gbs_out[2] = 2.0 * total / sec / 1e9;
+    return SDP_OK;
 }
 
 }  // extern "C"

@@ -99,10 +99,10 @@ def to_bf16_bits(x: np.ndarray, out: np.ndarray = None,
     x = np.ascontiguousarray(x, dtype=np.float32)
     if out is None:
         out = np.empty(x.size, dtype=np.uint16)
-    ot = torch.from_numpy(out.view(np.int16))
+    ot = torch.from_numpy(out.view(np.int16)).view(torch.bfloat16)
     for a in range(0, x.size, block):
         b = min(a + block, x.size)
-        ot[a:b].copy_(torch.from_numpy(x[a:b]).to(torch.bfloat16).view(torch.int16))
+        ot[a:b].copy_(torch.from_numpy(x[a:b]))
     return out
 
 

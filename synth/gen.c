@@ -101,24 +101,52 @@ static inline void draw(uint64_t seed, int64_t i, double *z, double *u_out)
     }
 }
 
+/* Both normals and both outlier uniforms of counter block j (elements 2j
+ * and 2j+1); the same values draw() gives element by element. */
+static inline void draw_pair(uint64_t seed, int64_t j, double z[2], double u[2])
+{
+    uint32_t w[4];
+    synth_philox4x32_10(seed, (uint64_t)j, w);
+    double r = sqrt(-2.0 * log(u01(w[0])));
+    double th = TWO_PI * u01(w[1]);
+    z[0] = r * cos(th);
+    z[1] = r * sin(th);
+    u[0] = u01(w[2]);
+    u[1] = u01(w[3]);
+}
+
+static inline float scaled(double z, double u, double sigma, double outlier_p,
+                           double outlier_scale)
+{
+    double x = sigma * z;
+    if (outlier_p > 0.0 && u < outlier_p)
+        x *= outlier_scale;
+    return (float)x;
+}
+
 /*
  * out[k] = (float)(sigma * z(start + k)) for k in [0, n), where z is the
  * stream's standard normal; when outlier_p > 0 the value is first multiplied
  * by outlier_scale wherever that element's outlier uniform is below
- * outlier_p.  Parallel over elements; the result does not depend on the
- * number of threads.
+ * outlier_p.  Parallel over counter blocks; the result does not depend on
+ * the number of threads.
  */
 void synth_normal_f32(uint64_t seed, int64_t start, int64_t n, double sigma,
                       double outlier_p, double outlier_scale, float *out)
 {
+    if (n <= 0)
+        return;
+    int64_t end = start + n;
+    int64_t j0 = start >> 1, j1 = (end + 1) >> 1;
 #pragma omp parallel for schedule(static)
-    for (int64_t k = 0; k < n; ++k) {
-        double z, u;
-        draw(seed, start + k, &z, &u);
-        double x = sigma * z;
-        if (outlier_p > 0.0 && u < outlier_p)
-            x *= outlier_scale;
-        out[k] = (float)x;
+    for (int64_t j = j0; j < j1; ++j) {
+        double z[2], u[2];
+        draw_pair(seed, j, z, u);
+        for (int h = 0; h < 2; ++h) {
+            int64_t i = 2 * j + h;
+            if (i >= start && i < end)
+                out[i - start] = scaled(z[h], u[h], sigma, outlier_p, outlier_scale);
+        }
     }
 }
 

@@ -32,8 +32,10 @@ MUTATIONS = {
     "mean_fp32_sum": ("double s = 0.0;\n    for (int32_t r = 0; r < R; ++r)\n        s += (double)orc_f32_from_bf16(grads[r][i]);",
                       "float s = 0.0f;\n    for (int32_t r = 0; r < R; ++r)\n        s += orc_f32_from_bf16(grads[r][i]);"),
     "norm_no_sqrt": ("return sqrt(S);", "return S;"),
-    "norm_first_segment_only": ("for (int32_t s = 0; s < n_segs; ++s) {\n        for (int64_t i = 0; i < segs[s].numel; ++i) {",
-                                "for (int32_t s = 0; s < 1; ++s) {\n        for (int64_t i = 0; i < segs[s].numel; ++i) {"),
+    "norm_first_segment_only": ("for (int32_t s = 0; s < n_segs; ++s) {\n        const uint16_t *const *g = segs[s].grads;",
+                                "for (int32_t s = 0; s < 1; ++s) {\n        const uint16_t *const *g = segs[s].grads;"),
+    "norm_block_skips_last": ("            for (int64_t k = 0; k < len; ++k) {\n                double gb",
+                              "            for (int64_t k = 0; k + 1 < len; ++k) {\n                double gb"),
     "clip_uncapped": ("return c < 1.0 ? c : 1.0;", "return c;"),
     "clip_no_guard": ("max_grad_norm / (norm + 1e-6)", "max_grad_norm / norm"),
     "clip_applied_to_square": ("(double)g_bar * c, hp,", "(double)g_bar * c * c, hp,"),
