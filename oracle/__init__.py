@@ -57,6 +57,8 @@ def _declare(L):
     L.orc_mean_grads.argtypes = [vp, i32, i64, vp]
     L.orc_grad_norm.restype = dbl
     L.orc_grad_norm.argtypes = [vp, i32, i32]
+    L.orc_sum_squares_f32.restype = dbl
+    L.orc_sum_squares_f32.argtypes = [vp, i64]
     L.orc_clip_coef.restype = dbl
     L.orc_clip_coef.argtypes = [dbl, dbl]
     L.orc_adamw_f64.restype = None
@@ -165,6 +167,12 @@ def mean_grads(gs, lib=None) -> np.ndarray:
     out = np.empty(gs[0].size, np.float32)
     L.orc_mean_grads(ctypes.cast(ptrs, ctypes.c_void_p), R, out.size, out.ctypes.data)
     return out
+
+
+def sum_squares(x: np.ndarray, lib=None) -> float:
+    """Correctly rounded sum of the squares of FP32 values."""
+    x = np.ascontiguousarray(x, np.float32)
+    return (lib or load()).orc_sum_squares_f32(x.ctypes.data, x.size)
 
 
 def clip_coef(norm: float, max_grad_norm: float, lib=None) -> float:

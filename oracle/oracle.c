@@ -11,9 +11,10 @@
  *      -- the rank gradients are summed and averaged into one gradient
  *      (Design, shared host state and communication routes: gradient return
  *      by GPU reduction).
- *   2. S = sum over every element of every segment of g_bar[i]^2 in FP64;
- *      norm = sqrt(S).  The paper never mentions clipping; the global L2
- *      norm of the mean gradient is taken as the quantity to clip by.
+ *   2. S = sum over every element of every segment of g_bar[i]^2, the
+ *      exact sum rounded once to FP64; norm = sqrt(S).  The paper never
+ *      mentions clipping; the global L2 norm of the mean gradient is taken
+ *      as the quantity to clip by.
  *   3. c = min(1, max_norm / (norm + 1e-6)) when max_norm > 0, else 1.
  *      A non-finite norm leaves every state unchanged.
  *   4. AdamW per element in FP64 (Loshchilov & Hutter, decoupled weight
@@ -32,8 +33,8 @@
  * bf16() is round to nearest even on the 8-bit significand, written below
  * from that definition.
  *
- * Parallelism: the per-element update loop (independent elements) runs under
- * OpenMP; the norm is one sequential FP64 sum in index order.
+ * Parallelism: the per-element loops (independent elements) run under
+ * OpenMP; the norm's exact sum is split over threads and merged exactly.
  */
 #include "oracle.h"
 
@@ -119,32 +120,158 @@ void orc_mean_grads(const uint16_t *const *grads, int32_t R, int64_t n, float *o
         out[i] = orc_mean_grad(grads, R, i);
 }
 
-/* Step 2: global L2 norm of the mean gradient over all segments.  S is one
- * sequential FP64 sum in element order; the mean gradients it adds are
- * independent of each other, so they are formed a block at a time in
- * parallel before the block is added in order. */
-#define ORC_NORM_BLOCK (1 << 20)
+/* Exact summation.  S is defined as the exact sum of the squares rounded
+ * once to FP64.  Each square of an FP32 value is exact in FP64, so the sum
+ * is accumulated without rounding in a fixed-point integer whose bit 0 has
+ * weight 2^ACC_E0 (ACC_LIMBS little-endian 64-bit limbs: every finite
+ * double, plus 64 bits of headroom for carries), then rounded to nearest,
+ * ties to even.  Being exact, the sum does not depend on the order or
+ * grouping of its terms, so threads may each accumulate a share. */
+#define ACC_E0 (-1074)
+#define ACC_LIMBS 35
+typedef struct {
+    uint64_t limb[ACC_LIMBS];
+} orc_acc;
+
+static void acc_add_at(orc_acc *a, int k, uint64_t v)
+{
+    while (v != 0 && k < ACC_LIMBS) {
+        uint64_t old = a->limb[k];
+        a->limb[k] = old + v;
+        v = a->limb[k] < old; /* carry */
+        ++k;
+    }
+}
+
+/* Add a finite x >= 0. */
+static void acc_add(orc_acc *a, double x)
+{
+    uint64_t bits;
+    memcpy(&bits, &x, sizeof bits);
+    uint64_t e = (bits >> 52) & 0x7ff;
+    uint64_t m = bits & ((1ull << 52) - 1);
+    if (e == 0 && m == 0)
+        return;
+    int b; /* weight of m's least bit is 2^(b + ACC_E0) */
+    if (e == 0) {
+        b = 0; /* subnormal: m * 2^-1074 */
+    } else {
+        m |= 1ull << 52;
+        b = (int)e - 1075 - ACC_E0;
+    }
+    int k = b >> 6, s = b & 63;
+    acc_add_at(a, k, m << s);
+    if (s != 0)
+        acc_add_at(a, k + 1, m >> (64 - s));
+}
+
+static void acc_merge(orc_acc *a, const orc_acc *b)
+{
+    for (int k = 0; k < ACC_LIMBS; ++k)
+        acc_add_at(a, k, b->limb[k]);
+}
+
+static int acc_bit(const orc_acc *a, int pos)
+{
+    return pos >= 0 ? (int)((a->limb[pos >> 6] >> (pos & 63)) & 1u) : 0;
+}
+
+static int acc_any_below(const orc_acc *a, int pos) /* any bit at index < pos */
+{
+    if (pos <= 0)
+        return 0;
+    int k = pos >> 6, s = pos & 63;
+    for (int j = 0; j < k; ++j)
+        if (a->limb[j])
+            return 1;
+    return s ? (a->limb[k] & ((1ull << s) - 1)) != 0 : 0;
+}
+
+/* Round the accumulated value to the nearest double, ties to even.  (The
+ * values summed here are at least 2^-298, so the result is never in the
+ * subnormal range, where ldexp would round a second time.) */
+static double acc_round(const orc_acc *a)
+{
+    int top = ACC_LIMBS - 1;
+    while (top >= 0 && a->limb[top] == 0)
+        --top;
+    if (top < 0)
+        return 0.0;
+    int msb = top * 64 + 63 - __builtin_clzll(a->limb[top]);
+    int lsb = msb - 52; /* lowest bit kept in a 53-bit significand */
+    uint64_t mant = 0;
+    for (int pos = msb; pos >= lsb; --pos)
+        mant = (mant << 1) | (uint64_t)acc_bit(a, pos);
+    if (acc_bit(a, lsb - 1) && (acc_any_below(a, lsb - 1) || (mant & 1u)))
+        ++mant; /* may become 2^53, still exact */
+    return ldexp((double)mant, lsb + ACC_E0);
+}
+
+/* Correctly rounded sum of x[i]^2 (test hook for the exact summation). */
+double orc_sum_squares_f32(const float *x, int64_t n)
+{
+    orc_acc total;
+    memset(&total, 0, sizeof total);
+    double special = 0.0; /* non-finite terms propagate as in IEEE addition */
+#pragma omp parallel
+    {
+        orc_acc mine;
+        memset(&mine, 0, sizeof mine);
+        double sp = 0.0;
+#pragma omp for schedule(static)
+        for (int64_t i = 0; i < n; ++i) {
+            double g = (double)x[i];
+            double t = g * g;
+            if (isfinite(t))
+                acc_add(&mine, t);
+            else
+                sp += t;
+        }
+#pragma omp critical
+        {
+            acc_merge(&total, &mine);
+            special += sp;
+        }
+    }
+    if (special != 0.0 || isnan(special))
+        return special;
+    return acc_round(&total);
+}
+
+/* Step 2: global L2 norm of the mean gradient over all segments:
+ * sqrt of the exactly rounded sum of g_bar^2 over every element. */
 double orc_grad_norm(const orc_segment *segs, int32_t n_segs, int32_t R)
 {
-    float *block = (float *)malloc(sizeof(float) * ORC_NORM_BLOCK);
-    if (!block)
-        return NAN;
-    double S = 0.0;
+    orc_acc total;
+    memset(&total, 0, sizeof total);
+    double special = 0.0;
     for (int32_t s = 0; s < n_segs; ++s) {
         const uint16_t *const *g = segs[s].grads;
-        for (int64_t a = 0; a < segs[s].numel; a += ORC_NORM_BLOCK) {
-            int64_t len = segs[s].numel - a < ORC_NORM_BLOCK ? segs[s].numel - a : ORC_NORM_BLOCK;
-#pragma omp parallel for schedule(static)
-            for (int64_t k = 0; k < len; ++k)
-                block[k] = orc_mean_grad(g, R, a + k);
-            for (int64_t k = 0; k < len; ++k) {
-                double gb = (double)block[k];
-                S += gb * gb;
+        const int64_t n = segs[s].numel;
+#pragma omp parallel
+        {
+            orc_acc mine;
+            memset(&mine, 0, sizeof mine);
+            double sp = 0.0;
+#pragma omp for schedule(static)
+            for (int64_t i = 0; i < n; ++i) {
+                double gb = (double)orc_mean_grad(g, R, i);
+                double t = gb * gb;
+                if (isfinite(t))
+                    acc_add(&mine, t);
+                else
+                    sp += t;
+            }
+#pragma omp critical
+            {
+                acc_merge(&total, &mine);
+                special += sp;
             }
         }
     }
-    free(block);
-    return sqrt(S);
+    if (special != 0.0 || isnan(special))
+        return sqrt(special);
+    return sqrt(acc_round(&total));
 }
 
 /* Step 3: clip coefficient. */

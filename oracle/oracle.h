@@ -44,6 +44,7 @@ float orc_mean_grad(const uint16_t *const *grads, int32_t R, int64_t i);
 void orc_mean_grads(const uint16_t *const *grads, int32_t R, int64_t n, float *out);
 
 double orc_grad_norm(const orc_segment *segs, int32_t n_segs, int32_t R);
+double orc_sum_squares_f32(const float *x, int64_t n);
 double orc_clip_coef(double norm, double max_grad_norm);
 
 void orc_adamw_f64(int64_t n, const double *p, const double *m, const double *v,

@@ -21,7 +21,8 @@ struct NormState {
 
 // One launch of the norm pass: `n` elements starting at a tile boundary of
 // a segment.  Block b covers elements [b*TILE, min((b+1)*TILE, n)) and writes
-// partials[b].  When gbar_out is non-null it also stores g_bar there.
+// the double-double pair partials[2b], partials[2b+1].  When gbar_out is
+// non-null it also stores g_bar there.
 struct NormArgs {
     const uint16_t *g[SDP_MAX_RANKS];
     int64_t n;
@@ -54,7 +55,7 @@ constexpr int kUpdateThreads = 256;
 constexpr int kVec = 8;  // elements per lane per access (16 B of BF16, 32 B of FP32)
 
 hipError_t launch_norm_partials(int R, const NormArgs &a, hipStream_t s);
-hipError_t launch_norm_finalize(const double *partials, int64_t n_partials,
+hipError_t launch_norm_finalize(const double *partials /* pairs */, int64_t n_partials,
                                 double max_grad_norm, NormState *ns, hipStream_t s);
 hipError_t launch_update(int R, const UpdateArgs &a, int max_blocks, hipStream_t s);
 hipError_t launch_cast_bf16(const float *src, uint16_t *dst, int64_t n, hipStream_t s);

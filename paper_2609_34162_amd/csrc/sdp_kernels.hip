@@ -71,27 +71,55 @@ __device__ __forceinline__ float mean1(const uint16_t *const *g, int64_t i) {
     return mean_of<R>(s);
 }
 
-__device__ __forceinline__ double wave_sum(double x) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
-    return x;
+// Double-double accumulation.  S is the sum of the squares of FP32 values,
+// each exact in FP64; it is carried as an unevaluated pair hi + lo (about
+// 106 significant bits), so its final rounding to FP64 is that of the exact
+// sum except when the exact sum lies within ~1e-28 of an FP64 rounding
+// boundary.  two_sum is Knuth's error-free addition.
+__device__ __forceinline__ void dd_add(double &hi, double &lo, double x) {
+    const double s = hi + x;
+    const double bb = s - hi;
+    const double e = (hi - (s - bb)) + (x - bb);
+    hi = s;
+    lo += e;
 }
 
-// Sum of one double per thread over the block, in a fixed order: lanes by
-// a fixed butterfly inside each wave, then waves in index order.
-template <int THREADS>
-__device__ __forceinline__ double block_sum(double x) {
-    __shared__ double ws[THREADS / 64];
-    x = wave_sum(x);
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    if (lane == 0) ws[wave] = x;
-    __syncthreads();
-    double t = 0.0;
-    if (threadIdx.x == 0) {
+__device__ __forceinline__ void dd_merge(double &hi, double &lo, double bhi, double blo) {
+    const double s = hi + bhi;
+    const double bb = s - hi;
+    double e = (hi - (s - bb)) + (bhi - bb);
+    e += lo + blo;
+    hi = s + e;           // renormalised: hi is the pair rounded to FP64
+    lo = e - (hi - s);
+}
+
+__device__ __forceinline__ void wave_merge(double &hi, double &lo) {
 #pragma unroll
-        for (int k = 0; k < THREADS / 64; ++k) t += ws[k];
+    for (int off = 32; off > 0; off >>= 1) {
+        const double oh = __shfl_xor(hi, off, 64);
+        const double ol = __shfl_xor(lo, off, 64);
+        dd_merge(hi, lo, oh, ol);
     }
-    return t;  // valid in thread 0
+}
+
+// Block sum of one pair per thread in a fixed order: a fixed butterfly inside
+// each wave, then the waves in index order.  Valid in thread 0.
+template <int THREADS>
+__device__ __forceinline__ void block_merge(double &hi, double &lo) {
+    __shared__ double ws_hi[THREADS / 64], ws_lo[THREADS / 64];
+    wave_merge(hi, lo);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0) {
+        ws_hi[wave] = hi;
+        ws_lo[wave] = lo;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        hi = ws_hi[0];
+        lo = ws_lo[0];
+#pragma unroll
+        for (int k = 1; k < THREADS / 64; ++k) dd_merge(hi, lo, ws_hi[k], ws_lo[k]);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -116,7 +144,7 @@ __global__ __launch_bounds__(kNormThreads) void k_norm_partials(NormArgs a) {
     const int64_t n = a.n;
     const int64_t full_groups = n / kVec;
     const int64_t tile0 = (int64_t)blockIdx.x * kGroupsPerTile;
-    double acc = 0.0;
+    double hi = 0.0, lo = 0.0;
     for (int it = 0; it < kIters; ++it) {
         uint4 raw[kUnroll][R];
         bool ok[kUnroll];
@@ -133,7 +161,7 @@ __global__ __launch_bounds__(kNormThreads) void k_norm_partials(NormArgs a) {
             float g[kVec];
             mean8<R>(raw[u], g);
 #pragma unroll
-            for (int e = 0; e < kVec; ++e) acc += (double)g[e] * (double)g[e];
+            for (int e = 0; e < kVec; ++e) dd_add(hi, lo, (double)g[e] * (double)g[e]);
             if constexpr (WRITE_GBAR) {
                 const int64_t e0 = (tile0 + (int64_t)(it * kUnroll + u) * kNormThreads + threadIdx.x) * kVec;
                 float4 *o = reinterpret_cast<float4 *>(a.gbar_out + e0);
@@ -146,25 +174,30 @@ __global__ __launch_bounds__(kNormThreads) void k_norm_partials(NormArgs a) {
     if (threadIdx.x == 0 && tail0 < n && tail0 / kTile == (int64_t)blockIdx.x) {
         for (int64_t i = tail0; i < n; ++i) {
             float g = mean1<R>(a.g, i);
-            acc += (double)g * (double)g;
+            dd_add(hi, lo, (double)g * (double)g);
             if constexpr (WRITE_GBAR) a.gbar_out[i] = g;
         }
     }
-    double t = block_sum<kNormThreads>(acc);
-    if (threadIdx.x == 0) a.partials[blockIdx.x] = t;
+    block_merge<kNormThreads>(hi, lo);
+    if (threadIdx.x == 0) {
+        a.partials[2 * blockIdx.x] = hi;
+        a.partials[2 * blockIdx.x + 1] = lo;
+    }
 }
 
-// One block: fixed-order sum of all tile partials, then the norm, the clip
-// coefficient and the non-finite flag.
+// One block: fixed-order sum of all tile partials (pairs), then the norm, the
+// clip coefficient and the non-finite flag.
 __global__ __launch_bounds__(kFinalizeThreads) void k_norm_finalize(
     const double *__restrict__ partials, int64_t n_partials, double max_grad_norm,
     NormState *__restrict__ ns) {
-    double acc = 0.0;
-    for (int64_t i = threadIdx.x; i < n_partials; i += kFinalizeThreads) acc += partials[i];
-    double S = block_sum<kFinalizeThreads>(acc);
+    double hi = 0.0, lo = 0.0;
+    for (int64_t i = threadIdx.x; i < n_partials; i += kFinalizeThreads)
+        dd_merge(hi, lo, partials[2 * i], partials[2 * i + 1]);
+    block_merge<kFinalizeThreads>(hi, lo);
     if (threadIdx.x == 0) {
-        double norm = sqrt(S);
-        int bad = !isfinite(S);
+        const double S = hi;
+        const double norm = sqrt(S);
+        const int bad = !isfinite(S);
         double c = 1.0;
         if (max_grad_norm > 0.0 && !bad) {
             c = max_grad_norm / (norm + 1e-6);

@@ -247,7 +247,8 @@ int ensure_partials(sdp_ctx *ctx, int64_t n) {
     ctx->partials = nullptr;
     ctx->partials_cap = 0;
     int64_t cap = std::max<int64_t>(n, 4096);
-    if (hipMalloc(&ctx->partials, (size_t)cap * sizeof(double)) != hipSuccess) {
+    // each tile partial is a double-double pair
+    if (hipMalloc(&ctx->partials, (size_t)cap * 2 * sizeof(double)) != hipSuccess) {
         (void)hipGetLastError();
         ctx->partials = nullptr;
         return fail(SDP_ERR_OUT_OF_MEMORY, "cannot allocate %lld norm partials", (long long)cap);
@@ -412,7 +413,7 @@ int read_norm(sdp_ctx *ctx, hipStream_t s, NormState *out) {
 int device_norm(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R, const Plan &plan, bool store_gbar,
                 double max_grad_norm, hipStream_t s) {
     for (int32_t k = 0; k < n_segs; ++k)
-        SDP_TRY(norm_launch(ctx, R, segs[k].grads, segs[k].numel, ctx->partials + plan.tile_base[k],
+        SDP_TRY(norm_launch(ctx, R, segs[k].grads, segs[k].numel, ctx->partials + 2 * plan.tile_base[k],
                             store_gbar ? ctx->gbar + plan.gbar_base[k] : nullptr, s));
     return finalize_launch(ctx, plan.tiles, max_grad_norm, s);
 }
@@ -472,7 +473,7 @@ int stream_norm_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int
         HIP_TRY(hipStreamWaitEvent(ctx->s_comp, ctx->h2d_done[sl], 0));
         const uint16_t *gp[SDP_MAX_RANKS];
         for (int32_t r = 0; r < R; ++r) gp[r] = slot.g[r];
-        SDP_TRY(norm_launch(ctx, R, gp, c.len, ctx->partials + plan.tile_base[c.seg] + c.off / SDP_NORM_TILE,
+        SDP_TRY(norm_launch(ctx, R, gp, c.len, ctx->partials + 2 * (plan.tile_base[c.seg] + c.off / SDP_NORM_TILE),
                             store_gbar ? ctx->gbar + plan.gbar_base[c.seg] + c.off : nullptr, ctx->s_comp));
         SDP_TRY(poison(ctx, sl));
         HIP_TRY(hipEventRecord(ctx->slot_free[sl], ctx->s_comp));

@@ -257,8 +257,18 @@ def sdp_last_error() -> str:
     return _lib.sdp_last_error().decode()
 
 
+class _Region:
+    """A byte range of a HostBuffer exposed to numpy; keeps the buffer alive."""
+
+    def __init__(self, owner: "HostBuffer", ptr: int, nbytes: int):
+        self.owner = owner
+        self.__array_interface__ = {"data": (ptr, False), "shape": (nbytes,), "typestr": "|u1", "version": 3}
+
+
 class HostBuffer:
-    """Pinned host memory from sdp_host_alloc, viewable as numpy arrays."""
+    """Pinned host memory from sdp_host_alloc, viewable as numpy arrays.
+    The memory is freed by close() or when neither the buffer nor any view
+    of it is referenced any more."""
 
     def __init__(self, nbytes: int):
         self.nbytes = nbytes
@@ -267,9 +277,9 @@ class HostBuffer:
     def view(self, dtype, count: int, offset: int = 0):
         import numpy as np
         dt = np.dtype(dtype)
-        assert offset + count * dt.itemsize <= self.nbytes
-        buf = (ctypes.c_char * (count * dt.itemsize)).from_address(self.ptr + offset)
-        return np.frombuffer(buf, dtype=dt, count=count)
+        if offset < 0 or offset + count * dt.itemsize > self.nbytes:
+            raise ValueError("view outside the buffer")
+        return np.asarray(_Region(self, self.ptr + offset, count * dt.itemsize)).view(dt)
 
     def close(self):
         if self.ptr:

@@ -1,5 +1,8 @@
 """Helpers for the GPU parity tests: device states in torch tensors, pinned
 host states, and the parity criteria against the oracle."""
+import ctypes
+import os
+import subprocess
 import sys
 import time
 
@@ -121,8 +124,7 @@ class HostState:
                             [x.copy() for x in self.v], [x.copy() for x in self.pb])
 
     def close(self):
-        for b in self.bufs:
-            b.close()
+        """Views keep their buffers alive; dropping the list frees the rest."""
         self.bufs = []
 
 
@@ -134,36 +136,75 @@ NORM_RTOL = 1e-6     # gradient norm
 BF16_MISMATCH = 1e-4  # fraction of BF16 params that may differ from bf16(oracle master)
 
 
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_PC_LIB = os.path.join(_HERE, "libparity_check.so")
+_pc = None
+
+
+def build_parity_check(force=True):
+    if force or not os.path.exists(_PC_LIB):
+        tmp = _PC_LIB + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-o", tmp,
+                               os.path.join(_HERE, "parity_check.c"), "-lm"])
+        os.replace(tmp, _PC_LIB)
+    return _PC_LIB
+
+
+def pc():
+    global _pc
+    if _pc is None:
+        if not os.path.exists(_PC_LIB):
+            build_parity_check(force=False)
+        L = ctypes.CDLL(_PC_LIB)
+        vp, i64 = ctypes.c_void_p, ctypes.c_int64
+        L.pc_compare_f32.restype = None
+        L.pc_compare_f32.argtypes = [vp, vp, i64] + [vp] * 5
+        L.pc_compare_bf16.restype = None
+        L.pc_compare_bf16.argtypes = [vp, vp, i64, vp, vp, vp]
+        L.pc_equal.restype = ctypes.c_int
+        L.pc_equal.argtypes = [vp, vp, i64]
+        _pc = L
+    return _pc
+
+
 def check_f32(got, ref, name):
-    got = np.asarray(got, np.float32)
-    ref = np.asarray(ref, np.float32)
+    """Strict per-element relative error (an oracle zero needs a GPU zero)."""
+    got = np.ascontiguousarray(got, np.float32)
+    ref = np.ascontiguousarray(ref, np.float32)
     assert got.shape == ref.shape
-    g = got.astype(np.float64)
-    r = ref.astype(np.float64)
-    zero = r == 0
-    assert np.all(g[zero] == 0), f"{name}: oracle value is 0 but the GPU's is not"
-    nz = ~zero
-    rel = np.abs(g[nz] - r[nz]) / np.abs(r[nz]) if nz.any() else np.zeros(1)
-    worst = float(rel.max()) if rel.size else 0.0
-    assert np.all(np.isfinite(g)) == np.all(np.isfinite(r)), f"{name}: finiteness differs"
-    assert worst <= RTOL, f"{name}: max relative error {worst:.3e} > {RTOL}"
-    return worst, float(np.mean(got.view(np.uint32) == ref.view(np.uint32)))
+    worst = ctypes.c_double()
+    wi, zm, fm, be = (ctypes.c_int64() for _ in range(4))
+    pc().pc_compare_f32(got.ctypes.data, ref.ctypes.data, got.size, ctypes.byref(worst), ctypes.byref(wi),
+                        ctypes.byref(zm), ctypes.byref(fm), ctypes.byref(be))
+    assert fm.value == 0, f"{name}: finiteness differs on {fm.value} elements"
+    assert zm.value == 0, f"{name}: oracle value is 0 but the GPU's is not on {zm.value} elements"
+    assert worst.value <= RTOL, (f"{name}: max relative error {worst.value:.3e} > {RTOL} at {wi.value} "
+                                 f"(gpu {got[wi.value]!r}, oracle {ref[wi.value]!r})")
+    return worst.value, be.value / max(got.size, 1)
 
 
-def check_bf16(gpu_pb, gpu_master, ref_master):
-    gpu_pb = np.asarray(gpu_pb, np.uint16)
+def check_bf16(gpu_pb, gpu_master, ref_pb):
+    """ref_pb: the oracle's BF16 params, i.e. bf16(oracle master)."""
+    gpu_pb = np.ascontiguousarray(gpu_pb, np.uint16)
     own = oracle.bf16(gpu_master)
-    assert np.array_equal(gpu_pb, own), "param_bf16 != bf16(GPU master)"
-    ref = oracle.bf16(ref_master)
-    diff = gpu_pb != ref
-    frac = float(diff.mean())
+    assert arrays_equal(gpu_pb, own), "param_bf16 != bf16(GPU master)"
+    ref = np.ascontiguousarray(ref_pb, np.uint16)
+    d, sg, far = (ctypes.c_int64() for _ in range(3))
+    pc().pc_compare_bf16(gpu_pb.ctypes.data, ref.ctypes.data, gpu_pb.size, ctypes.byref(d), ctypes.byref(sg),
+                         ctypes.byref(far))
+    assert sg.value == 0, "BF16 sign differs"
+    assert far.value == 0, "BF16 differs by more than 1 ulp"
+    frac = d.value / max(gpu_pb.size, 1)
     assert frac <= BF16_MISMATCH, f"BF16 params differ from bf16(oracle master) on {frac:.2e} of elements"
-    if diff.any():
-        a = gpu_pb[diff].astype(np.int32)
-        b = ref[diff].astype(np.int32)
-        assert np.all((a >> 15) == (b >> 15)), "BF16 sign differs"
-        assert np.all(np.abs((a & 0x7fff) - (b & 0x7fff)) <= 1), "BF16 differs by more than 1 ulp"
     return frac
+
+
+def arrays_equal(a, b) -> bool:
+    a = np.ascontiguousarray(a)
+    b = np.ascontiguousarray(b)
+    if a.nbytes != b.nbytes:
+        return False
+    return bool(pc().pc_equal(a.ctypes.data, b.ctypes.data, a.nbytes))
 
 
 def check_norm(got, ref):
@@ -176,7 +217,7 @@ def check_state(gpu_host: oracle.State, ref: oracle.State):
         stats[f"master{s}"] = check_f32(gpu_host.master[s], ref.master[s], f"seg{s}.master")
         stats[f"exp_avg{s}"] = check_f32(gpu_host.exp_avg[s], ref.exp_avg[s], f"seg{s}.exp_avg")
         stats[f"exp_avg_sq{s}"] = check_f32(gpu_host.exp_avg_sq[s], ref.exp_avg_sq[s], f"seg{s}.exp_avg_sq")
-        stats[f"bf16_{s}"] = check_bf16(gpu_host.param_bf16[s], gpu_host.master[s], ref.master[s])
+        stats[f"bf16_{s}"] = check_bf16(gpu_host.param_bf16[s], gpu_host.master[s], ref.param_bf16[s])
     return stats
 
 
@@ -184,7 +225,7 @@ def states_equal(a: oracle.State, b: oracle.State) -> bool:
     for x, y in ((a.master, b.master), (a.exp_avg, b.exp_avg), (a.exp_avg_sq, b.exp_avg_sq),
                  (a.param_bf16, b.param_bf16)):
         for s in range(len(x)):
-            if not np.array_equal(np.asarray(x[s]).view(np.uint8), np.asarray(y[s]).view(np.uint8)):
+            if not arrays_equal(x[s], y[s]):
                 return False
     return True
 

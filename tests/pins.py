@@ -131,6 +131,41 @@ def pin_norm_constant(lib):
     assert oracle.grad_norm([a, b], lib=lib) == 5.0
 
 
+def pin_exact_sum_vs_fsum(lib):
+    """The norm's sum is the exactly rounded sum: compare with math.fsum
+    (a correctly rounded library summation) on values of widely spread
+    magnitude, where any rounding inside the sum would show."""
+    import math
+    rng = np.random.default_rng(8)
+    for trial in range(6):
+        n = int(rng.integers(1, 20000))
+        x = (rng.normal(0, 1, n) * np.exp2(rng.integers(-140, 126, n).astype(np.float64))).astype(np.float32)
+        x = x[np.isfinite(x)]
+        want = math.fsum(float(v) * float(v) for v in x)
+        assert oracle.sum_squares(x, lib=lib) == want, trial
+
+
+def pin_exact_sum_ties_and_carries(lib):
+    import math
+    cases = [
+        [1.0, 2.0 ** -27, 2.0 ** -27],                 # 1 + 2^-53: a tie, stays 1
+        [1.0, 2.0 ** -27, 2.0 ** -27, 2.0 ** -100],    # just above the tie: rounds up
+        [1.0 + 2.0 ** -23, 2.0 ** -27, 2.0 ** -27],    # tie next to an odd significand
+        [2.0 ** 63] * 4096 + [2.0 ** -60] * 3,         # long carry chains, tiny tail
+        [2.0 ** -149] * 1000 + [3.0],                  # subnormal squares
+        [1e-20, 1e20, -1e20, 3e-15],
+    ]
+    for k, c in enumerate(cases):
+        x = np.array(c, np.float32)
+        want = math.fsum(float(v) * float(v) for v in x)
+        assert oracle.sum_squares(x, lib=lib) == want, (k, oracle.sum_squares(x, lib=lib), want)
+    # the norm itself: sqrt of that exact sum, over two segments and ranks
+    gs = [rand_grads(3000, 3, seed=31, outlier_p=0.05), rand_grads(77, 3, seed=32)]
+    means = np.concatenate([oracle.mean_grads(g, lib=lib) for g in gs])
+    want = math.sqrt(math.fsum(float(v) * float(v) for v in means))
+    assert oracle.grad_norm(gs, lib=lib) == want
+
+
 def pin_norm_vs_torch(lib):
     segs = [rand_grads(n, 3, seed=n, outlier_p=0.01) for n in (1, 1000, 4097, 70000)]
     got = oracle.grad_norm(segs, lib=lib)

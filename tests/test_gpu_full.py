@@ -1,0 +1,195 @@
+"""GPU parity at the full workload sizes, in the launch configuration bench.py
+times: one Qwen3-8B layer (192,946,176 params, R = 4, 10 steps) and one
+Qwen2.5-72B layer (877,674,496 params, R = 8, 3 steps) in device mode, and one
+Qwen3-14B layer (330,311,680 params, R = 4, 5 steps) in streamed mode.
+
+Every element of every output is compared with the oracle at every step,
+teacher-forced (the oracle steps from the GPU's state before the step) and,
+where stated, also free-running (the oracle carries its own state from step
+one).  Criteria as in test_gpu_parity.py.  The full Qwen3-14B model in
+streamed mode (14.8B params, 266 GB of pinned host state) is in
+test_gpu_full_model.py.
+"""
+import time
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_util import (DevState, HostState, check_norm, check_state, log, need_gpu, states_equal, torch)
+
+pytestmark = [pytest.mark.gpu, pytest.mark.big]
+
+
+@pytest.fixture(scope="module")
+def sdp():
+    return need_gpu()
+
+
+class Pinned:
+    """Reusable pinned host arrays."""
+
+    def __init__(self, sdp):
+        self.sdp = sdp
+        self.bufs = []
+
+    def array(self, dtype, n):
+        b = self.sdp.HostBuffer(max(16, n * np.dtype(dtype).itemsize))
+        self.bufs.append(b)
+        return b.view(dtype, n)
+
+    def state(self, sizes):
+        st = oracle.State([np.zeros(0, np.float32) for _ in sizes])
+        st.master = [self.array(np.float32, n) for n in sizes]
+        st.exp_avg = [self.array(np.float32, n) for n in sizes]
+        st.exp_avg_sq = [self.array(np.float32, n) for n in sizes]
+        st.param_bf16 = [self.array(np.uint16, n) for n in sizes]
+        return st
+
+    def close(self):
+        """Views keep their buffers alive; dropping the list frees the rest."""
+        self.bufs = []
+
+
+def copy_state(dst: oracle.State, src: oracle.State):
+    for a, b in ((dst.master, src.master), (dst.exp_avg, src.exp_avg), (dst.exp_avg_sq, src.exp_avg_sq),
+                 (dst.param_bf16, src.param_bf16)):
+        for s in range(len(a)):
+            np.copyto(a[s], b[s])
+
+
+def dev_to_host(dst: oracle.State, dev: DevState):
+    torch.cuda.synchronize()
+    for s in range(len(dev.p)):
+        torch.from_numpy(dst.master[s]).copy_(dev.p[s])
+        torch.from_numpy(dst.exp_avg[s]).copy_(dev.m[s])
+        torch.from_numpy(dst.exp_avg_sq[s]).copy_(dev.v[s])
+        torch.from_numpy(dst.param_bf16[s].view(np.int16)).copy_(dev.pb[s])
+
+
+def gen_grads(w, step, out):
+    for s in range(len(w.segments)):
+        for r in range(w.ranks):
+            synth.grad_bf16(w, s, step, r, out=out[s][r])
+
+
+def run_device_workload(sdp, cid, free_running):
+    w = synth.workload(cid)
+    sizes = [s.numel for s in w.segments]
+    log(f"full device workload {w.name}: N={w.numel} R={w.ranks} steps={w.steps}")
+    t0 = time.time()
+    pin = Pinned(sdp)
+    try:
+        masters = [synth.master(w, s) for s in range(len(sizes))]
+        dev = DevState(masters, w.ranks)
+        grads = [[pin.array(np.uint16, n) for _ in range(w.ranks)] for n in sizes]
+        before, after = pin.state(sizes), pin.state(sizes)
+        forced = oracle.State([np.zeros(n, np.float32) for n in sizes])
+        ref = oracle.State(masters) if free_running else None
+        del masters
+        ctx = sdp.sdp_ctx_create(0, 0, w.ranks, 0)
+        try:
+            for t in range(1, w.steps + 1):
+                gen_grads(w, t, grads)
+                dev.set_grads(grads)
+                dev_to_host(before, dev)
+                norm = sdp.sdp_agg_adam_step(ctx, dev.segments(sdp), sdp.make_params(**w.hparams(t)), w.chunk,
+                                             torch.cuda.current_stream().cuda_stream, want_norm=True)
+                dev_to_host(after, dev)
+                copy_state(forced, before)
+                rc, fnorm = oracle.step(forced, grads, oracle.hparams(**w.hparams(t)))
+                assert rc == oracle.ORC_OK
+                check_norm(norm, fnorm)
+                assert norm > w.max_grad_norm      # these workloads clip every step
+                stats = check_state(after, forced)
+                if ref is not None:
+                    oracle.step(ref, grads, oracle.hparams(**w.hparams(t)))
+                    stats_free = check_state(after, ref)
+                else:
+                    stats_free = None
+                log(f"  step {t}: norm {norm:.9g} (oracle {fnorm:.9g}) forced {stats['master0']}"
+                    f" free {stats_free['master0'] if stats_free else '-'}  {time.time() - t0:.0f}s")
+        finally:
+            sdp.sdp_ctx_destroy(ctx)
+    finally:
+        pin.close()
+
+
+@pytest.mark.timeout(400)
+def test_qwen3_8b_layer_device_full(sdp):
+    run_device_workload(sdp, 1, free_running=True)
+
+
+@pytest.mark.timeout(400)
+def test_qwen25_72b_layer_device_full(sdp):
+    run_device_workload(sdp, 4, free_running=False)
+
+
+@pytest.mark.timeout(400)
+def test_qwen3_14b_layer_streamed_full(sdp):
+    w = synth.workload(2)
+    n = w.numel
+    log(f"full streamed workload {w.name}: N={n} R={w.ranks} chunk={w.chunk} steps={w.steps}")
+    t0 = time.time()
+    master = synth.master(w, 0)
+    host = HostState(sdp, [master], w.ranks)
+    ctx = sdp.sdp_ctx_create(0, w.chunk, w.ranks, 0)
+    pin = Pinned(sdp)
+    try:
+        before = pin.state([n])
+        forced = oracle.State([np.zeros(n, np.float32)])
+        ref = oracle.State([master])
+        del master
+        for t in range(1, w.steps + 1):
+            gen_grads(w, t, host.g)
+            for a, b in ((before.master, host.p), (before.exp_avg, host.m), (before.exp_avg_sq, host.v),
+                         (before.param_bf16, host.pb)):
+                np.copyto(a[0], b[0])
+            norm = sdp.sdp_stream_step(ctx, host.segments(), sdp.make_params(**w.hparams(t)), w.chunk)
+            after = oracle.State.__new__(oracle.State)
+            after.master, after.exp_avg, after.exp_avg_sq, after.param_bf16 = host.p, host.m, host.v, host.pb
+            copy_state(forced, before)
+            rc, fnorm = oracle.step(forced, host.g, oracle.hparams(**w.hparams(t)))
+            assert rc == oracle.ORC_OK
+            check_norm(norm, fnorm)
+            stats = check_state(after, forced)
+            oracle.step(ref, host.g, oracle.hparams(**w.hparams(t)))
+            stats_free = check_state(after, ref)
+            log(f"  step {t}: norm {norm:.9g} (oracle {fnorm:.9g}) forced {stats['master0']} "
+                f"free {stats_free['master0']}  {time.time() - t0:.0f}s")
+    finally:
+        sdp.sdp_ctx_destroy(ctx)
+        host.close()
+        pin.close()
+
+
+@pytest.mark.timeout(300)
+def test_qwen3_14b_layer_device_equals_streamed(sdp):
+    """The same Qwen3-14B layer in both modes gives the same bits."""
+    w = synth.workload(2)
+    n = w.numel
+    master = synth.master(w, 0)
+    host = HostState(sdp, [master], w.ranks)
+    dev = DevState([master], w.ranks)
+    ctx = sdp.sdp_ctx_create(0, w.chunk, w.ranks, 0)
+    pin = Pinned(sdp)
+    try:
+        got = pin.state([n])
+        for t in (1, 2):
+            gen_grads(w, t, host.g)
+            dev.set_grads(host.g)
+            hs = sdp.make_params(**w.hparams(t))
+            dn = sdp.sdp_agg_adam_step(ctx, dev.segments(sdp), hs, w.chunk, torch.cuda.current_stream().cuda_stream,
+                                       want_norm=True)
+            sn = sdp.sdp_stream_step(ctx, host.segments(), hs, w.chunk)
+            assert dn == sn
+            dev_to_host(got, dev)
+            hstate = oracle.State.__new__(oracle.State)
+            hstate.master, hstate.exp_avg, hstate.exp_avg_sq, hstate.param_bf16 = host.p, host.m, host.v, host.pb
+            assert states_equal(got, hstate), f"device and streamed modes differ at step {t}"
+            log(f"  step {t}: device == streamed, norm {dn:.9g}")
+    finally:
+        sdp.sdp_ctx_destroy(ctx)
+        host.close()
+        pin.close()

@@ -212,6 +212,30 @@ def test_grad_norm_modes_agree(sdp, ctx):
     assert dn == hn
 
 
+def test_norm_equals_exactly_rounded_sum(sdp, ctx):
+    """The GPU's double-double norm equals the oracle's exactly rounded one,
+    bit for bit, in both modes, on gradients of widely spread magnitude."""
+    rng = np.random.default_rng(123)
+    for trial in range(12):
+        R = int(rng.integers(1, 9))
+        sizes = [int(rng.integers(1, 3 * TILE)) for _ in range(int(rng.integers(1, 4)))]
+        grads = []
+        for n in sizes:
+            gs = []
+            for r in range(R):
+                x = rng.normal(0, 1, n) * np.exp2(rng.integers(-60, 60, n).astype(np.float64))
+                gs.append(synth.to_bf16_bits(x.astype(np.float32)))
+            grads.append(gs)
+        want = oracle.grad_norm(grads)
+        dev = DevState([np.zeros(n, np.float32) for n in sizes], R)
+        dev.set_grads(grads)
+        got = sdp.sdp_grad_norm(ctx, dev.segments(sdp), True, 0, stream())
+        host = HostState(sdp, [np.zeros(n, np.float32) for n in sizes], R)
+        host.set_grads(grads)
+        got_s = sdp.sdp_grad_norm(ctx, host.segments(), False, TILE)
+        assert got == want and got_s == want, (trial, got, got_s, want)
+
+
 @pytest.mark.parametrize("mode", ["device", "streamed"])
 @pytest.mark.parametrize("bad", [np.nan, np.inf])
 def test_nonfinite_gradient_leaves_states_unchanged(sdp, ctx, mode, bad):

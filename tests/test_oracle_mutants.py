@@ -31,11 +31,18 @@ MUTATIONS = {
                         "s += (double)orc_f32_from_bf16(grads[0][i]);"),
     "mean_fp32_sum": ("double s = 0.0;\n    for (int32_t r = 0; r < R; ++r)\n        s += (double)orc_f32_from_bf16(grads[r][i]);",
                       "float s = 0.0f;\n    for (int32_t r = 0; r < R; ++r)\n        s += orc_f32_from_bf16(grads[r][i]);"),
-    "norm_no_sqrt": ("return sqrt(S);", "return S;"),
+    "norm_no_sqrt": ("    return sqrt(acc_round(&total));", "    return acc_round(&total);"),
     "norm_first_segment_only": ("for (int32_t s = 0; s < n_segs; ++s) {\n        const uint16_t *const *g = segs[s].grads;",
                                 "for (int32_t s = 0; s < 1; ++s) {\n        const uint16_t *const *g = segs[s].grads;"),
-    "norm_block_skips_last": ("            for (int64_t k = 0; k < len; ++k) {\n                double gb",
-                              "            for (int64_t k = 0; k + 1 < len; ++k) {\n                double gb"),
+    "norm_skips_last_element": ("            for (int64_t i = 0; i < n; ++i) {\n                double gb",
+                                "            for (int64_t i = 0; i < n - 1; ++i) {\n                double gb"),
+    "acc_no_carry": ("        v = a->limb[k] < old; /* carry */", "        v = 0;"),
+    "acc_round_no_sticky": ("(acc_any_below(a, lsb - 1) || (mant & 1u))", "(mant & 1u)"),
+    "acc_round_truncates": ("        ++mant; /* may become 2^53, still exact */", "        (void)0;"),
+    "acc_high_part_dropped": ("        acc_add_at(a, k + 1, m >> (64 - s));", "        (void)0;"),
+    "acc_implicit_bit_missing": ("        m |= 1ull << 52;", "        (void)0;"),
+    "acc_merge_without_carry": ("    for (int k = 0; k < ACC_LIMBS; ++k)\n        acc_add_at(a, k, b->limb[k]);",
+                                "    for (int k = 0; k < ACC_LIMBS; ++k)\n        a->limb[k] += b->limb[k];"),
     "clip_uncapped": ("return c < 1.0 ? c : 1.0;", "return c;"),
     "clip_no_guard": ("max_grad_norm / (norm + 1e-6)", "max_grad_norm / norm"),
     "clip_applied_to_square": ("(double)g_bar * c, hp,", "(double)g_bar * c * c, hp,"),
@@ -49,6 +56,7 @@ MUTATIONS = {
 
 # cheap pins first so that most mutants are rejected quickly
 ORDER = ["pin_bf16_special_values", "pin_mean_closed_forms", "pin_norm_constant",
+         "pin_exact_sum_ties_and_carries", "pin_exact_sum_vs_fsum",
          "pin_clip_coef", "pin_first_step_sign", "pin_zero_gradient", "pin_sign_descent",
          "pin_lr_zero", "pin_identical_ranks", "pin_clip_noop", "pin_nonfinite",
          "pin_param_is_bf16_of_master", "pin_mean_vs_numpy", "pin_norm_vs_torch",
