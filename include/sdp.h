@@ -85,6 +85,13 @@ extern "C" {
 /* Streamed mode: after each staging slot is released, fill it with a NaN
  * pattern (debug aid: a missing wait then shows up as corrupted results). */
 #define SDP_FLAG_DEBUG_POISON 0x8u
+/* Streamed mode, staged: the host buffers may be ordinary (pageable) memory.
+ * Each chunk moves through context-owned pinned bounce buffers: host threads
+ * copy it in while the previous chunk's DMA runs, and copy results out while
+ * the next chunk's runs.  For host states larger than the pinned memory the
+ * system grants.  Needs max_chunk_elems > 0; pins 2 * (28 + 2 * max_ranks) *
+ * max_chunk_elems bytes; host threads: SDP_STAGING_THREADS, default up to 16. */
+#define SDP_FLAG_STREAM_STAGED 0x10u
 
 /* ---- types ------------------------------------------------------------- */
 typedef struct sdp_ctx sdp_ctx;
@@ -155,7 +162,8 @@ int sdp_agg_adam_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs,
                       void *stream, double *grad_norm_out);
 
 /* Streamed mode.  All state and gradient buffers are pinned host memory
- * (e.g. from sdp_host_alloc).  chunk_elems: a multiple of SDP_NORM_TILE,
+ * (e.g. from sdp_host_alloc), or any host memory when the context was
+ * created with SDP_FLAG_STREAM_STAGED.  chunk_elems: a multiple of SDP_NORM_TILE,
  * at most the context's max_chunk_elems, and n_ranks <= its max_ranks.
  * Phase 1 copies each chunk's R gradients host-to-device on the copy
  * stream and runs the norm pass on the compute stream, alternating two

@@ -15,7 +15,11 @@
 // layer).  Phase 1 streams the gradients for the global norm; phase 2
 // streams master/m/v through the fused update and back.
 #include <algorithm>
+#include <atomic>
 #include <chrono>
+#include <condition_variable>
+#include <mutex>
+#include <thread>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -79,6 +83,94 @@ struct Timed {
     int64_t elems;
 };
 
+// A fixed set of host threads that split large memcpys between them.  Used
+// by the staged streamed mode to move chunks between the caller's host
+// memory and the context's pinned bounce buffers (the CPU-side staging lane
+// of the paper's chunked overlap, Design, overlap within a layer).
+class CopyPool {
+  public:
+    struct Job {
+        void *dst;
+        const void *src;
+        size_t bytes;
+    };
+
+    explicit CopyPool(int workers) {
+        for (int i = 0; i < workers; ++i) threads_.emplace_back([this] { loop(); });
+    }
+    ~CopyPool() {
+        {
+            std::lock_guard<std::mutex> g(mu_);
+            stop_ = true;
+        }
+        cv_work_.notify_all();
+        for (auto &t : threads_) t.join();
+    }
+    int size() const { return (int)threads_.size() + 1; }
+
+    // Copies every job; returns when all bytes have landed.  The calling
+    // thread takes part.
+    void copy(const std::vector<Job> &jobs) {
+        constexpr size_t kPiece = 4u << 20;
+        std::unique_lock<std::mutex> g(mu_);
+        pieces_.clear();
+        for (const Job &j : jobs)
+            for (size_t off = 0; off < j.bytes; off += kPiece)
+                pieces_.push_back({(char *)j.dst + off, (const char *)j.src + off, std::min(kPiece, j.bytes - off)});
+        next_ = 0;
+        left_ = pieces_.size();
+        ++gen_;
+        g.unlock();
+        cv_work_.notify_all();
+        work();
+        g.lock();
+        cv_done_.wait(g, [this] { return left_ == 0; });
+    }
+
+  private:
+    void work() {
+        for (;;) {
+            size_t k;
+            {
+                std::lock_guard<std::mutex> g(mu_);
+                if (next_ >= pieces_.size()) return;
+                k = next_++;
+            }
+            std::memcpy(pieces_[k].dst, pieces_[k].src, pieces_[k].bytes);
+            std::lock_guard<std::mutex> g(mu_);
+            if (--left_ == 0) cv_done_.notify_all();
+        }
+    }
+    void loop() {
+        uint64_t seen = 0;
+        for (;;) {
+            {
+                std::unique_lock<std::mutex> g(mu_);
+                cv_work_.wait(g, [&] { return stop_ || gen_ != seen; });
+                if (stop_) return;
+                seen = gen_;
+            }
+            work();
+        }
+    }
+
+    std::vector<std::thread> threads_;
+    std::mutex mu_;
+    std::condition_variable cv_work_, cv_done_;
+    std::vector<Job> pieces_;
+    size_t next_ = 0, left_ = 0;
+    uint64_t gen_ = 0;
+    bool stop_ = false;
+};
+
+// A host <-> staging-slot transfer of one chunk: `bytes` at byte offset `off`
+// of a slot, from or to `host`.
+struct Xfer {
+    size_t off;
+    char *host;
+    size_t bytes;
+};
+
 }  // namespace
 
 struct sdp_ctx {
@@ -93,6 +185,13 @@ struct sdp_ctx {
     bool last_done_valid = false;
     char *staging = nullptr;
     size_t slot_bytes = 0;
+    // staged streamed mode: pinned bounce buffers shaped like the slots
+    char *bounce_in = nullptr;   // 2 x slot_bytes
+    char *bounce_out = nullptr;  // 2 x 14 * max_chunk (master, m, v, bf16 part of a slot)
+    hipEvent_t d2h_done[2] = {nullptr, nullptr};
+    bool bin_used[2] = {false, false};
+    std::vector<Xfer> pending_out[2];
+    CopyPool *copier = nullptr;
     double *partials = nullptr;
     int64_t partials_cap = 0;
     float *gbar = nullptr;
@@ -162,6 +261,21 @@ int check_pinned_ptr(const void *p, size_t bytes, const char *what, int seg) {
     return SDP_OK;
 }
 
+// Host memory for the staged streamed mode: anything that is not device
+// memory (pageable or pinned).  Pageable ranges cannot be checked further.
+int check_host_ptr(const void *p, const char *what, int seg) {
+    hipPointerAttribute_t at;
+    if (hipPointerGetAttributes(&at, p) == hipSuccess) {
+        if (at.type == hipMemoryTypeDevice)
+            return fail(SDP_ERR_INVALID_ARGUMENT, "segment %d %s (%p) is device memory, not host memory", seg, what, p);
+    } else {
+        (void)hipGetLastError();
+    }
+    return SDP_OK;
+}
+
+enum MemKind { kDeviceMem, kPinnedHost, kAnyHost };
+
 struct Range {
     uintptr_t a, b;
     int seg;
@@ -171,7 +285,7 @@ struct Range {
 bool overlap(const Range &x, const Range &y) { return x.a < y.b && y.a < x.b; }
 
 // Checks every segment of a call; returns R and the per-segment sizes.
-int validate_segments(const sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, bool device, bool grads_only,
+int validate_segments(const sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, MemKind kind, bool grads_only,
                       int32_t *R_out) {
     if (!segs || n_segs < 1) return fail(SDP_ERR_INVALID_ARGUMENT, "need at least one segment");
     int32_t R = segs[0].n_ranks;
@@ -207,7 +321,9 @@ int validate_segments(const sdp_ctx *ctx, const sdp_segment *segs, int32_t n_seg
         }
         for (size_t k = 0; k < bufs.size(); ++k) {
             const Buf &b = bufs[k];
-            SDP_TRY(device ? check_device_ptr(ctx, b.p, b.bytes, b.what, s) : check_pinned_ptr(b.p, b.bytes, b.what, s));
+            SDP_TRY(kind == kDeviceMem   ? check_device_ptr(ctx, b.p, b.bytes, b.what, s)
+                    : kind == kPinnedHost ? check_pinned_ptr(b.p, b.bytes, b.what, s)
+                                          : check_host_ptr(b.p, b.what, s));
             Range rg{(uintptr_t)b.p, (uintptr_t)b.p + b.bytes, s, b.what};
             (k < n_state ? states : grads).push_back(rg);
         }
@@ -458,17 +574,90 @@ int poison(sdp_ctx *ctx, int k) {
     return SDP_OK;
 }
 
+bool staged(const sdp_ctx *ctx) { return (ctx->flags & SDP_FLAG_STREAM_STAGED) != 0; }
+
+size_t off_in_slot(const sdp_ctx *ctx, int sl, const void *p) {
+    return (size_t)((const char *)p - (ctx->staging + (size_t)sl * ctx->slot_bytes));
+}
+
+// Runs of transfers that are contiguous in the slot, for the bounce copies.
+std::vector<Xfer> merge_runs(std::vector<Xfer> xs) {
+    std::sort(xs.begin(), xs.end(), [](const Xfer &a, const Xfer &b) { return a.off < b.off; });
+    std::vector<Xfer> runs;
+    for (const Xfer &x : xs) {
+        if (!runs.empty() && runs.back().off + runs.back().bytes == x.off)
+            runs.back().bytes += x.bytes;
+        else
+            runs.push_back({x.off, nullptr, x.bytes});
+    }
+    return runs;
+}
+
+// Host -> slot `sl` copies of one chunk, enqueued on the copy stream.  In the
+// staged mode the host threads first copy into the slot's pinned bounce
+// buffer, after waiting for that buffer's previous copy to leave it.
+int copy_in(sdp_ctx *ctx, int sl, const std::vector<Xfer> &xs) {
+    char *dev = ctx->staging + (size_t)sl * ctx->slot_bytes;
+    if (!staged(ctx)) {
+        for (const Xfer &x : xs)
+            HIP_TRY(hipMemcpyAsync(dev + x.off, x.host, x.bytes, hipMemcpyHostToDevice, ctx->s_copy));
+        return SDP_OK;
+    }
+    char *bin = ctx->bounce_in + (size_t)sl * ctx->slot_bytes;
+    if (ctx->bin_used[sl]) HIP_TRY(hipEventSynchronize(ctx->h2d_done[sl]));
+    std::vector<CopyPool::Job> jobs;
+    for (const Xfer &x : xs) jobs.push_back({bin + x.off, x.host, x.bytes});
+    ctx->copier->copy(jobs);
+    for (const Xfer &r : merge_runs(xs))
+        HIP_TRY(hipMemcpyAsync(dev + r.off, bin + r.off, r.bytes, hipMemcpyHostToDevice, ctx->s_copy));
+    ctx->bin_used[sl] = true;
+    return SDP_OK;
+}
+
+// Slot `sl` -> host copies of one chunk, enqueued on the compute stream.  In
+// the staged mode they land in the pinned bounce buffer and are moved to
+// their destinations by drain().
+int copy_out(sdp_ctx *ctx, int sl, const std::vector<Xfer> &xs) {
+    char *dev = ctx->staging + (size_t)sl * ctx->slot_bytes;
+    if (!staged(ctx)) {
+        for (const Xfer &x : xs)
+            HIP_TRY(hipMemcpyAsync(x.host, dev + x.off, x.bytes, hipMemcpyDeviceToHost, ctx->s_comp));
+        return SDP_OK;
+    }
+    char *bout = ctx->bounce_out + (size_t)sl * 14 * (size_t)ctx->max_chunk;
+    for (const Xfer &r : merge_runs(xs))
+        HIP_TRY(hipMemcpyAsync(bout + r.off, dev + r.off, r.bytes, hipMemcpyDeviceToHost, ctx->s_comp));
+    HIP_TRY(hipEventRecord(ctx->d2h_done[sl], ctx->s_comp));
+    ctx->pending_out[sl] = xs;
+    return SDP_OK;
+}
+
+// Staged mode: wait for slot `sl`'s outgoing copies and move them from the
+// bounce buffer to their host destinations.
+int drain(sdp_ctx *ctx, int sl) {
+    if (ctx->pending_out[sl].empty()) return SDP_OK;
+    HIP_TRY(hipEventSynchronize(ctx->d2h_done[sl]));
+    char *bout = ctx->bounce_out + (size_t)sl * 14 * (size_t)ctx->max_chunk;
+    std::vector<CopyPool::Job> jobs;
+    for (const Xfer &x : ctx->pending_out[sl]) jobs.push_back({x.host, bout + x.off, x.bytes});
+    ctx->copier->copy(jobs);
+    ctx->pending_out[sl].clear();
+    return SDP_OK;
+}
+
 // Phase 1: gradients in, norm partials (and stored g_bar) out, then finalize.
 int stream_norm_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R, const Plan &plan,
                       const std::vector<Chunk> &chunks, bool store_gbar, double max_grad_norm, bool used[2]) {
+    (void)n_segs;
     for (size_t k = 0; k < chunks.size(); ++k) {
         const Chunk &c = chunks[k];
         const int sl = (int)(k & 1);
         Slot slot = slot_at(ctx, sl);
-        if (used[sl]) HIP_TRY(hipStreamWaitEvent(ctx->s_copy, ctx->slot_free[sl], 0));
+        std::vector<Xfer> xs;
         for (int32_t r = 0; r < R; ++r)
-            HIP_TRY(hipMemcpyAsync(slot.g[r], segs[c.seg].grads[r] + c.off, (size_t)c.len * 2, hipMemcpyHostToDevice,
-                                   ctx->s_copy));
+            xs.push_back({off_in_slot(ctx, sl, slot.g[r]), (char *)(segs[c.seg].grads[r] + c.off), (size_t)c.len * 2});
+        if (used[sl]) HIP_TRY(hipStreamWaitEvent(ctx->s_copy, ctx->slot_free[sl], 0));
+        SDP_TRY(copy_in(ctx, sl, xs));
         HIP_TRY(hipEventRecord(ctx->h2d_done[sl], ctx->s_copy));
         HIP_TRY(hipStreamWaitEvent(ctx->s_comp, ctx->h2d_done[sl], 0));
         const uint16_t *gp[SDP_MAX_RANKS];
@@ -493,26 +682,34 @@ int stream_update_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t R, const 
         const int sl = (int)((j + k0) & 1);
         Slot slot = slot_at(ctx, sl);
         const size_t f4 = (size_t)c.len * 4, b2 = (size_t)c.len * 2;
-        if (used[sl]) HIP_TRY(hipStreamWaitEvent(ctx->s_copy, ctx->slot_free[sl], 0));
-        HIP_TRY(hipMemcpyAsync(slot.p, g.master + c.off, f4, hipMemcpyHostToDevice, ctx->s_copy));
-        HIP_TRY(hipMemcpyAsync(slot.m, g.exp_avg + c.off, f4, hipMemcpyHostToDevice, ctx->s_copy));
-        HIP_TRY(hipMemcpyAsync(slot.v, g.exp_avg_sq + c.off, f4, hipMemcpyHostToDevice, ctx->s_copy));
+        std::vector<Xfer> in = {{off_in_slot(ctx, sl, slot.p), (char *)(g.master + c.off), f4},
+                                {off_in_slot(ctx, sl, slot.m), (char *)(g.exp_avg + c.off), f4},
+                                {off_in_slot(ctx, sl, slot.v), (char *)(g.exp_avg_sq + c.off), f4}};
         if (!stored_gbar)
             for (int32_t r = 0; r < R; ++r)
-                HIP_TRY(hipMemcpyAsync(slot.g[r], g.grads[r] + c.off, b2, hipMemcpyHostToDevice, ctx->s_copy));
+                in.push_back({off_in_slot(ctx, sl, slot.g[r]), (char *)(g.grads[r] + c.off), b2});
+        if (used[sl]) HIP_TRY(hipStreamWaitEvent(ctx->s_copy, ctx->slot_free[sl], 0));
+        SDP_TRY(copy_in(ctx, sl, in));
         HIP_TRY(hipEventRecord(ctx->h2d_done[sl], ctx->s_copy));
         HIP_TRY(hipStreamWaitEvent(ctx->s_comp, ctx->h2d_done[sl], 0));
         const uint16_t *gp[SDP_MAX_RANKS];
         for (int32_t r = 0; r < R; ++r) gp[r] = slot.g[r];
         SDP_TRY(update_launch(ctx, R, hp, slot.p, slot.m, slot.v, slot.pb, gp,
                               stored_gbar ? ctx->gbar + plan.gbar_base[c.seg] + c.off : nullptr, c.len, ctx->s_comp));
-        HIP_TRY(hipMemcpyAsync(g.master + c.off, slot.p, f4, hipMemcpyDeviceToHost, ctx->s_comp));
-        HIP_TRY(hipMemcpyAsync(g.exp_avg + c.off, slot.m, f4, hipMemcpyDeviceToHost, ctx->s_comp));
-        HIP_TRY(hipMemcpyAsync(g.exp_avg_sq + c.off, slot.v, f4, hipMemcpyDeviceToHost, ctx->s_comp));
-        HIP_TRY(hipMemcpyAsync(g.param_bf16 + c.off, slot.pb, b2, hipMemcpyDeviceToHost, ctx->s_comp));
+        std::vector<Xfer> out = {{off_in_slot(ctx, sl, slot.p), (char *)(g.master + c.off), f4},
+                                 {off_in_slot(ctx, sl, slot.m), (char *)(g.exp_avg + c.off), f4},
+                                 {off_in_slot(ctx, sl, slot.v), (char *)(g.exp_avg_sq + c.off), f4},
+                                 {off_in_slot(ctx, sl, slot.pb), (char *)(g.param_bf16 + c.off), b2}};
+        SDP_TRY(copy_out(ctx, sl, out));
         SDP_TRY(poison(ctx, sl));
         HIP_TRY(hipEventRecord(ctx->slot_free[sl], ctx->s_comp));
         used[sl] = true;
+        // staged: move the previous chunk's results out while this one is in flight
+        if (staged(ctx)) SDP_TRY(drain(ctx, sl ^ 1));
+    }
+    if (staged(ctx)) {
+        SDP_TRY(drain(ctx, 0));
+        SDP_TRY(drain(ctx, 1));
     }
     return SDP_OK;
 }
@@ -530,7 +727,8 @@ int stream_common_checks(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, 
     if (chunk > ctx->max_chunk)
         return fail(SDP_ERR_CHUNK_TOO_LARGE, "chunk_elems %lld exceeds the context's %lld", (long long)chunk,
                     (long long)ctx->max_chunk);
-    SDP_TRY(validate_segments(ctx, segs, n_segs, false, grads_only, R));
+    SDP_TRY(validate_segments(ctx, segs, n_segs, (ctx->flags & SDP_FLAG_STREAM_STAGED) ? kAnyHost : kPinnedHost,
+                              grads_only, R));
     if (*R > ctx->max_ranks)
         return fail(SDP_ERR_INVALID_ARGUMENT, "n_ranks %d exceeds the context's max_ranks %d", *R, ctx->max_ranks);
     return SDP_OK;
@@ -673,6 +871,21 @@ int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems, int32_t m
             return bail(fail(SDP_ERR_OUT_OF_MEMORY, "cannot allocate 2 x %zu bytes of staging", c->slot_bytes));
         }
     }
+    if (flags & SDP_FLAG_STREAM_STAGED) {
+        if (max_chunk_elems <= 0)
+            return bail(fail(SDP_ERR_INVALID_ARGUMENT, "SDP_FLAG_STREAM_STAGED needs max_chunk_elems > 0"));
+        const size_t out_bytes = 14 * (size_t)max_chunk_elems;
+        if (hipHostMalloc(&c->bounce_in, 2 * c->slot_bytes, hipHostMallocDefault) != hipSuccess ||
+            hipHostMalloc(&c->bounce_out, 2 * out_bytes, hipHostMallocDefault) != hipSuccess) {
+            (void)hipGetLastError();
+            return bail(fail(SDP_ERR_OUT_OF_MEMORY, "cannot allocate %zu bytes of pinned bounce buffers",
+                             2 * (c->slot_bytes + out_bytes)));
+        }
+        for (int k = 0; k < 2; ++k) CTX_HIP(hipEventCreateWithFlags(&c->d2h_done[k], hipEventDisableTiming));
+        int threads = (int)std::min(16u, std::max(1u, std::thread::hardware_concurrency()));
+        if (const char *env = std::getenv("SDP_STAGING_THREADS")) threads = std::max(1, std::min(64, std::atoi(env)));
+        c->copier = new CopyPool(threads - 1);
+    }
     rc = ensure_partials(c, 4096);
     if (rc != SDP_OK) return bail(rc);
 #undef CTX_HIP
@@ -697,6 +910,11 @@ void sdp_ctx_destroy(sdp_ctx *ctx) {
     if (ctx->s_copy) (void)hipStreamDestroy(ctx->s_copy);
     if (ctx->s_comp) (void)hipStreamDestroy(ctx->s_comp);
     if (ctx->staging) (void)hipFree(ctx->staging);
+    if (ctx->bounce_in) (void)hipHostFree(ctx->bounce_in);
+    if (ctx->bounce_out) (void)hipHostFree(ctx->bounce_out);
+    for (int k = 0; k < 2; ++k)
+        if (ctx->d2h_done[k]) (void)hipEventDestroy(ctx->d2h_done[k]);
+    delete ctx->copier;
     if (ctx->partials) (void)hipFree(ctx->partials);
     if (ctx->gbar) (void)hipFree(ctx->gbar);
     if (ctx->ns) (void)hipFree(ctx->ns);
@@ -713,7 +931,7 @@ int sdp_agg_adam_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, con
     SDP_TRY(check_chunk(chunk_elems, true));
     DeviceGuard guard(ctx->device);
     int32_t R = 0;
-    SDP_TRY(validate_segments(ctx, segs, n_segs, true, false, &R));
+    SDP_TRY(validate_segments(ctx, segs, n_segs, kDeviceMem, false, &R));
     const Plan plan = make_plan(segs, n_segs);
     const bool store = device_gbar(ctx, R);
     SDP_TRY(ensure_partials(ctx, plan.tiles));
@@ -780,7 +998,7 @@ int sdp_grad_norm(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int dev
     int32_t R = 0;
     NormState st{};
     if (device_resident) {
-        SDP_TRY(validate_segments(ctx, segs, n_segs, true, true, &R));
+        SDP_TRY(validate_segments(ctx, segs, n_segs, kDeviceMem, true, &R));
         const Plan p = make_plan(segs, n_segs);
         SDP_TRY(ensure_partials(ctx, p.tiles));
         hipStream_t s = (hipStream_t)stream;

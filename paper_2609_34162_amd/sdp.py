@@ -29,6 +29,7 @@ SDP_FLAG_DEVICE_GBAR_NEVER = 0x1
 SDP_FLAG_DEVICE_GBAR_ALWAYS = 0x2
 SDP_FLAG_STREAM_GBAR_NEVER = 0x4
 SDP_FLAG_DEBUG_POISON = 0x8
+SDP_FLAG_STREAM_STAGED = 0x10
 
 
 class SdpError(RuntimeError):

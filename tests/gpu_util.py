@@ -109,6 +109,25 @@ class HostState:
             self.pb.append(pb)
             self.g.append([alloc(np.uint16) for _ in range(R)])
 
+    @classmethod
+    def allocate(cls, sdp, sizes, R):
+        """Pinned arrays of the given segment sizes, contents not initialised."""
+        self = cls.__new__(cls)
+        self.sdp, self.R, self.bufs = sdp, R, []
+        self.p, self.m, self.v, self.pb, self.g = [], [], [], [], []
+
+        def alloc(dtype, n):
+            b = sdp.HostBuffer(max(n * np.dtype(dtype).itemsize, 16))
+            self.bufs.append(b)
+            return b.view(dtype, n)
+        for n in sizes:
+            self.p.append(alloc(np.float32, n))
+            self.m.append(alloc(np.float32, n))
+            self.v.append(alloc(np.float32, n))
+            self.pb.append(alloc(np.uint16, n))
+            self.g.append([alloc(np.uint16, n) for _ in range(R)])
+        return self
+
     def set_grads(self, grads):
         for s, gs in enumerate(grads):
             for r, g in enumerate(gs):
@@ -126,6 +145,29 @@ class HostState:
     def close(self):
         """Views keep their buffers alive; dropping the list frees the rest."""
         self.bufs = []
+
+
+class PageableState(HostState):
+    """The same state in ordinary (pageable) numpy arrays, for the staged mode."""
+
+    def __init__(self, sdp, masters, R):
+        self.sdp, self.R, self.bufs = sdp, R, []
+        self.p = [np.ascontiguousarray(m, np.float32).copy() for m in masters]
+        self.m = [np.zeros(x.size, np.float32) for x in self.p]
+        self.v = [np.zeros(x.size, np.float32) for x in self.p]
+        self.pb = [np.zeros(x.size, np.uint16) for x in self.p]
+        self.g = [[np.zeros(x.size, np.uint16) for _ in range(R)] for x in self.p]
+
+    @classmethod
+    def allocate(cls, sdp, sizes, R):
+        self = cls.__new__(cls)
+        self.sdp, self.R, self.bufs = sdp, R, []
+        self.p = [np.empty(n, np.float32) for n in sizes]
+        self.m = [np.empty(n, np.float32) for n in sizes]
+        self.v = [np.empty(n, np.float32) for n in sizes]
+        self.pb = [np.empty(n, np.uint16) for n in sizes]
+        self.g = [[np.empty(n, np.uint16) for _ in range(R)] for n in sizes]
+        return self
 
 
 # ---------------------------------------------------------------------------

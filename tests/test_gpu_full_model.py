@@ -1,0 +1,118 @@
+"""GPU parity on the full Qwen3-14B model in streamed mode: the embedding, 40
+decoder layers and the lm_head (42 segments, 14,768,291,840 params, R = 2,
+32M-element chunks, 2 steps), with every state in host memory (265.8 GB).
+The host grants far less pinned memory than that (65 GiB per process on
+the MI355X boxes used here), so the states are ordinary pageable memory
+and the context runs the staged streamed mode: chunks move through its
+pinned bounce buffers.
+
+The oracle cannot hold a second copy of that state, so each step is checked
+(a) on the gradient norm, from all 29.5 billion gradient values, which must
+equal the oracle's exactly rounded norm bit for bit; and (b) element by
+element on about 8.4 million sampled points -- random points of every
+segment plus both sides of every chunk boundary and every segment's ends --
+where the oracle updates each point from its state before the step
+(teacher-forced) and from its own state carried from step one
+(free-running).
+
+Opt-in (SDP_FULL_MODEL=1): it needs about 252 GiB of host memory and a few
+minutes, most of them generating inputs.
+"""
+import os
+import time
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_util import PageableState, check_bf16, check_f32, check_norm, log, need_gpu
+
+pytestmark = [pytest.mark.gpu, pytest.mark.big]
+
+NEED_GIB = 262  # pinned state plus the process, with a margin
+
+
+def mem_available_gib():
+    with open("/proc/meminfo") as f:
+        for line in f:
+            if line.startswith("MemAvailable:"):
+                return int(line.split()[1]) / (1 << 20)
+    return 0.0
+
+
+@pytest.mark.timeout(1500)
+def test_qwen3_14b_full_model_streamed():
+    if os.environ.get("SDP_FULL_MODEL") != "1":
+        pytest.skip("full-model streamed run is opt-in (SDP_FULL_MODEL=1): 266 GB of pinned host state")
+    avail = mem_available_gib()
+    if avail < NEED_GIB:
+        pytest.skip(f"needs {NEED_GIB} GiB of available host memory, {avail:.0f} GiB available")
+    sdp = need_gpu()
+    w = synth.workload(3)
+    R, C = w.ranks, w.chunk
+    sizes = [s.numel for s in w.segments]
+    t0 = time.time()
+    log(f"{w.name}: {len(sizes)} segments, N={w.numel}, R={R}, chunk={C}; {avail:.0f} GiB available")
+
+    # sample points of every segment
+    rng = np.random.default_rng(2024)
+    samples = []
+    for n in sizes:
+        pts = [rng.integers(0, n, 200000), np.arange(min(64, n)), np.arange(max(0, n - 64), n)]
+        for b in range(C, n, C):
+            pts.append(np.arange(max(0, b - 4), min(n, b + 4)))
+        samples.append(np.unique(np.concatenate(pts)).astype(np.int64))
+    log(f"  {sum(s.size for s in samples)} sample points")
+
+    host = PageableState.allocate(sdp, sizes, R)
+    for s in range(len(sizes)):
+        synth.master(w, s, out=host.p[s])
+        host.m[s][:] = 0
+        host.v[s][:] = 0
+        host.pb[s][:] = 0
+        if s % 6 == 0:
+            log(f"  segment {s}/{len(sizes)} initialised  {time.time() - t0:.0f}s;"
+                f" MemAvailable {mem_available_gib():.0f} GiB")
+    free = [(synth.master_at(w, s, samples[s]), np.zeros(samples[s].size, np.float32),
+             np.zeros(samples[s].size, np.float32)) for s in range(len(sizes))]
+    ctx = sdp.sdp_ctx_create(0, C, R, sdp.SDP_FLAG_STREAM_STAGED)
+    try:
+        for t in range(1, w.steps + 1):
+            for s in range(len(sizes)):
+                for r in range(R):
+                    synth.grad_bf16(w, s, t, r, out=host.g[s][r])
+                if s % 6 == 0:
+                    log(f"  step {t}: gradients of segment {s} generated  {time.time() - t0:.0f}s")
+            before = [(host.p[s][samples[s]], host.m[s][samples[s]], host.v[s][samples[s]])
+                      for s in range(len(sizes))]
+            ts = time.time()
+            norm = sdp.sdp_stream_step(ctx, host.segments(), sdp.make_params(**w.hparams(t)), C)
+            step_s = time.time() - ts
+            onorm = oracle.grad_norm(host.g)
+            log(f"  step {t}: streamed step {step_s:.2f} s, norm {norm!r} (oracle {onorm!r})")
+            check_norm(norm, onorm)
+            assert norm == onorm, "norm differs from the exactly rounded oracle norm"
+            hp = oracle.hparams(**w.hparams(t))
+            c = oracle.clip_coef(onorm, w.max_grad_norm)
+            worst = 0.0
+            for s in range(len(sizes)):
+                idx = samples[s]
+                g_rows = np.stack([host.g[s][r][idx] for r in range(R)], axis=1)
+                after = (host.p[s][idx], host.m[s][idx], host.v[s][idx], host.pb[s][idx])
+                ep, em, ev, epb = oracle.update_points(*before[s], g_rows, c, hp)
+                for got, want, name in ((after[0], ep, "master"), (after[1], em, "exp_avg"),
+                                        (after[2], ev, "exp_avg_sq")):
+                    worst = max(worst, check_f32(got, want, f"seg{s}.{name} (teacher-forced)")[0])
+                check_bf16(after[3], after[0], epb)
+                fp, fm, fv, fpb = oracle.update_points(*free[s], g_rows, c, hp)
+                for got, want, name in ((after[0], fp, "master"), (after[1], fm, "exp_avg"),
+                                        (after[2], fv, "exp_avg_sq")):
+                    check_f32(got, want, f"seg{s}.{name} (free-running)")
+                check_bf16(after[3], after[0], fpb)
+                free[s] = (fp, fm, fv)
+            log(f"  step {t}: {sum(x.size for x in samples)} points match, worst relative error {worst:.2e}"
+                f"  {time.time() - t0:.0f}s")
+    finally:
+        sdp.sdp_ctx_destroy(ctx)
+        host.close()

@@ -12,7 +12,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import (DevState, HostState, check_norm, check_state, hp_pair, log, need_gpu,
+from gpu_util import (DevState, HostState, PageableState, check_norm, check_state, hp_pair, log, need_gpu,
                       rand_inputs, states_equal, torch)
 
 pytestmark = pytest.mark.gpu
@@ -192,6 +192,53 @@ def test_streamed_matches_oracle_and_device(sdp, ctx, ctx_poison, ctx_nostore, c
                 assert states_equal(got, dev_states[t]), "streamed differs from device mode"
         finally:
             host.close()
+
+
+@pytest.fixture(scope="module")
+def ctx_staged(sdp):
+    c = sdp.sdp_ctx_create(0, 4 * TILE, 16, sdp.SDP_FLAG_STREAM_STAGED | sdp.SDP_FLAG_DEBUG_POISON)
+    yield c
+    sdp.sdp_ctx_destroy(c)
+
+
+@pytest.fixture(scope="module")
+def ctx_staged_nostore(sdp):
+    c = sdp.sdp_ctx_create(0, 2 * TILE, 8, sdp.SDP_FLAG_STREAM_STAGED | sdp.SDP_FLAG_STREAM_GBAR_NEVER)
+    yield c
+    sdp.sdp_ctx_destroy(c)
+
+
+@pytest.mark.parametrize("chunk_tiles", [1, 2])
+def test_staged_streamed_matches_device_and_oracle(sdp, ctx, ctx_staged, ctx_staged_nostore, chunk_tiles):
+    """Staged streamed mode on pageable (and on pinned) host memory gives the
+    same bits as device mode, and matches the oracle."""
+    sizes = [3 * TILE + 5, 1, 70000, 2 * TILE]
+    R = 3
+    steps = 3
+    masters, grads = rand_inputs(sizes, R, steps, seed=61 + chunk_tiles)
+    hps = [hp_pair(sdp, lr=1e-3, weight_decay=0.05, max_grad_norm=0.2, step=t) for t in range(1, steps + 1)]
+    dev = DevState(masters, R)
+    ref = oracle.State(masters)
+    dev_states, ref_states, norms = [], [], []
+    for t in range(steps):
+        norms.append(dev_step(sdp, ctx, dev, grads[t], hps[t][0]))
+        oracle.step(ref, grads[t], hps[t][1])
+        dev_states.append(dev.host())
+        ref_states.append(ref.copy())
+    for c in (ctx_staged, ctx_staged_nostore):
+        for host in (PageableState(sdp, masters, R), HostState(sdp, masters, R)):
+            for t in range(steps):
+                host.set_grads(grads[t])
+                snorm = sdp.sdp_stream_step(c, host.segments(), hps[t][0], chunk_tiles * TILE)
+                assert snorm == norms[t]
+                got = host.host()
+                check_state(got, ref_states[t])
+                assert states_equal(got, dev_states[t]), f"staged streamed differs from device mode at step {t + 1}"
+            host.close()
+    # the staged mode still refuses device memory
+    with pytest.raises(sdp.SdpError) as e:
+        sdp.sdp_stream_step(ctx_staged, dev.segments(sdp), hps[0][0], TILE)
+    assert e.value.status == sdp.SDP_ERR_INVALID_ARGUMENT
 
 
 def test_grad_norm_modes_agree(sdp, ctx):
