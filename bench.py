@@ -12,6 +12,10 @@ JSON line also carries:
   streamed      -- one Qwen3-14B layer (330,311,680 parameters, R = 4) in
                    pinned host memory, streamed in 32M-element chunks, against
                    the pinned link bandwidth measured in the same run;
+  device_r8     -- one Qwen2.5-72B layer (877,674,496 parameters, R = 8) in
+                   device mode, where the norm pass stores the mean gradient;
+  staged_pageable (inside streamed) -- the streamed step again with the
+                   states in pageable memory, through the staged mode;
   cpu_baseline  -- the CPU oracle on the same layer, on this host's cores.
 Inputs are generated before the timed region and stay resident; the same
 gradient buffers are reused by every timed step.
@@ -52,8 +56,9 @@ def measured_traffic(algorithmic_bytes):
     return rec.get("hbm_bytes_per_launch")
 
 
-def device_leg(args, torch, np, synth, sdp):
-    w = synth.workload(1)
+def device_leg(args, torch, np, synth, sdp, cid, steps, warmup, copy_probe):
+    """Times `steps` device-mode steps of workload `cid` after `warmup` ones."""
+    w = synth.workload(cid)
     N, R = w.numel, w.ranks
     log(f"device leg: {w.name} N={N} R={R}; generating inputs")
     dev = torch.device("cuda:0")
@@ -76,55 +81,65 @@ def device_leg(args, torch, np, synth, sdp):
     def step(t):
         sdp.sdp_agg_adam_step(ctx, segs, sdp.make_params(**w.hparams(t)), w.chunk, sh)
 
-    log(f"device leg: {args.warmup} warmup + {args.steps} timed steps")
-    for t in range(1, args.warmup + 1):
+    log(f"device leg: {warmup} warmup + {steps} timed steps")
+    for t in range(1, warmup + 1):
         step(t)
     torch.cuda.synchronize()
     sdp.sdp_ctx_set_timing(ctx, True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for t in range(args.warmup + 1, args.warmup + args.steps + 1):
+    for t in range(warmup + 1, warmup + steps + 1):
         step(t)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     kt = sdp.sdp_ctx_get_timing(ctx)
     sdp.sdp_ctx_set_timing(ctx, False)
     norm, clip, bad = sdp.sdp_ctx_last_norm(ctx)
-    assert not bad and clip < 1.0, (norm, clip)  # this workload clips every step
+    assert not bad and clip < 1.0, (norm, clip)  # these workloads clip every step
 
-    step_bytes, _ = sdp.sdp_bytes_per_elem(False, R, 0)      # 26 + 4R
-    upd_bytes_per_elem = 2 * R + 12 + 14                      # update kernel: reads 2R+12, writes 14
+    step_bytes, _ = sdp.sdp_bytes_per_elem(False, R, 0)
+    stored = R > 4                                   # the library's default policy
+    upd_bytes_per_elem = (4 if stored else 2 * R) + 12 + 14
+    norm_bytes_per_elem = 2 * R + (4 if stored else 0)
     upd_s = kt.update_ms / kt.update_launches / 1e3
     norm_s = kt.norm_ms / kt.norm_launches / 1e3
-    achieved = upd_bytes_per_elem * N / upd_s / 1e9
     res = dict(
-        N=N, R=R, elapsed=elapsed, ms_per_step=elapsed / args.steps * 1e3,
-        params_per_s=N * args.steps / elapsed,
-        step_hbm_gbs=step_bytes * N * args.steps / elapsed / 1e9,
+        workload=w.name, N=N, R=R, chunk=w.chunk, steps=steps, elapsed=elapsed,
+        ms_per_step=elapsed / steps * 1e3, params_per_s=N * steps / elapsed,
+        step_bytes_per_elem=step_bytes, step_hbm_gbs=step_bytes * N * steps / elapsed / 1e9,
         update_ms=upd_s * 1e3, norm_ms=norm_s * 1e3,
         finalize_ms=kt.finalize_ms / max(kt.finalize_launches, 1),
-        update_gbs=achieved, update_bytes=upd_bytes_per_elem * N,
-        norm_gbs=2 * R * N / norm_s / 1e9, grad_norm=norm, clip=clip,
-        workload=w.name, chunk=w.chunk,
+        update_gbs=upd_bytes_per_elem * N / upd_s / 1e9, update_bytes=upd_bytes_per_elem * N,
+        norm_gbs=norm_bytes_per_elem * N / norm_s / 1e9, grad_norm=norm, clip=clip,
     )
-    # HBM copy ceiling with the same access width (2 x 2 GiB buffers)
-    nbytes = 2 << 30
-    a = torch.empty(nbytes, dtype=torch.uint8, device=dev)
-    b = torch.empty(nbytes, dtype=torch.uint8, device=dev)
-    a.fill_(1)
-    for _ in range(2):
-        sdp.sdp_probe_copy(ctx, b.data_ptr(), a.data_ptr(), nbytes, sh)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    reps = 10
-    for _ in range(reps):
-        sdp.sdp_probe_copy(ctx, b.data_ptr(), a.data_ptr(), nbytes, sh)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    res["copy_gbs"] = 2 * nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
-    del a, b
+    if copy_probe:
+        # HBM copy ceiling with the same access width (2 x 2 GiB buffers)
+        nbytes = 2 << 30
+        a = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        b = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        a.fill_(1)
+        for _ in range(2):
+            sdp.sdp_probe_copy(ctx, b.data_ptr(), a.data_ptr(), nbytes, sh)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        reps = 10
+        for _ in range(reps):
+            sdp.sdp_probe_copy(ctx, b.data_ptr(), a.data_ptr(), nbytes, sh)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        res["copy_gbs"] = 2 * nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+        del a, b
     sdp.sdp_ctx_destroy(ctx)
+    del p, m, v, pb, g
+    torch.cuda.empty_cache()
     return res, master, host_grads, w
+
+
+def brief(res):
+    """The device-leg figures reported for a non-headline workload."""
+    return {k: res[k] for k in ("workload", "N", "R", "chunk", "steps", "ms_per_step", "params_per_s",
+                                "step_bytes_per_elem", "step_hbm_gbs", "update_ms", "update_gbs", "norm_ms",
+                                "norm_gbs")} | {"step_hbm_frac": res["step_hbm_gbs"] / HBM_PEAK_GBS}
 
 
 def cpu_leg(args, np, oracle, master, host_grads, w):
@@ -173,9 +188,9 @@ def stream_leg(args, torch, np, synth, sdp):
                           [x.ctypes.data for x in g], N)])
     ctx = sdp.sdp_ctx_create(0, C, R, 0)
     # Pinned link bandwidth with the engine's copy path and its largest copy
-    # (one chunk of one FP32 state array).  The first copies on a fresh pair
-    # of streams do not overlap, so the probe is warmed first; the best of
-    # three runs is kept, which makes the bound below the tightest one.
+    # (one chunk of one FP32 state array).  How much the two directions
+    # overlap varies from run to run (57 to 97 GB/s together), so the best
+    # of ten runs is kept: the bound below is then the tightest one.
     probe_bytes, copy_bytes = 1 << 30, 4 * C
     ha, hb = pinned(np.uint8, probe_bytes), pinned(np.uint8, probe_bytes)
     ha[:] = 1
@@ -184,25 +199,40 @@ def stream_leg(args, torch, np, synth, sdp):
     probe = lambda reps: sdp.sdp_probe_link(ctx, ha.ctypes.data, hb.ctypes.data, da.data_ptr(),  # noqa: E731
                                             db.data_ptr(), probe_bytes, copy_bytes, reps)
     probe(2)
-    runs = [probe(2) for _ in range(3)]
+    runs = [probe(2) for _ in range(10)]
     link = [max(r[k] for r in runs) for k in range(3)]
     del da, db
     log(f"streamed leg: link h2d {link[0]:.1f} d2h {link[1]:.1f} both {link[2]:.1f} GB/s")
-    sdp.sdp_stream_step(ctx, segs, sdp.make_params(**w.hparams(1)), C)  # warmup
-    t0 = time.perf_counter()
-    for t in range(2, args.stream_steps + 2):
-        sdp.sdp_stream_step(ctx, segs, sdp.make_params(**w.hparams(t)), C)
-    el = (time.perf_counter() - t0) / args.stream_steps
+    def timed(c, sg):
+        sdp.sdp_stream_step(c, sg, sdp.make_params(**w.hparams(1)), C)  # warmup
+        t0 = time.perf_counter()
+        for t in range(2, args.stream_steps + 2):
+            sdp.sdp_stream_step(c, sg, sdp.make_params(**w.hparams(t)), C)
+        return (time.perf_counter() - t0) / args.stream_steps
+
+    el = timed(ctx, segs)
     h2d_b, d2h_b = sdp.sdp_bytes_per_elem(True, R, 0)
     t_link = (2 * R * N / (link[0] * 1e9)
               + max(12 * N / (link[0] * 1e9), 14 * N / (link[1] * 1e9), 26 * N / (link[2] * 1e9)))
     sdp.sdp_ctx_destroy(ctx)
+    out = dict(workload=w.name, params=N, ranks=R, chunk_elems=C, ms_per_step=el * 1e3,
+               params_per_s=N / el, h2d_gbs=h2d_b * N / el / 1e9, d2h_gbs=d2h_b * N / el / 1e9,
+               link_gbs={"h2d": link[0], "d2h": link[1], "bidir": link[2]},
+               t_link_ms=t_link * 1e3, frac_of_link_bound=t_link / el)
+    if not args.no_extra:
+        # the same step with the states in pageable memory, through the staged mode
+        log("streamed leg: staged mode on pageable copies of the same state")
+        pg = [np.array(x) for x in (p, m, v, pb)] + [np.array(x) for x in g]
+        sseg = sdp.Segments([(pg[0].ctypes.data, pg[1].ctypes.data, pg[2].ctypes.data, pg[3].ctypes.data,
+                              [x.ctypes.data for x in pg[4:]], N)])
+        sctx = sdp.sdp_ctx_create(0, C, R, sdp.SDP_FLAG_STREAM_STAGED)
+        sel = timed(sctx, sseg)
+        sdp.sdp_ctx_destroy(sctx)
+        out["staged_pageable"] = dict(ms_per_step=sel * 1e3, params_per_s=N / sel, frac_of_link_bound=t_link / sel)
+        del pg
     for hbuf in bufs:
         hbuf.close()
-    return dict(workload=w.name, params=N, ranks=R, chunk_elems=C, ms_per_step=el * 1e3,
-                params_per_s=N / el, h2d_gbs=h2d_b * N / el / 1e9, d2h_gbs=d2h_b * N / el / 1e9,
-                link_gbs={"h2d": link[0], "d2h": link[1], "bidir": link[2]},
-                t_link_ms=t_link * 1e3, frac_of_link_bound=t_link / el)
+    return out
 
 
 def main():
@@ -214,6 +244,8 @@ def main():
     ap.add_argument("--no-stream", action="store_true", help="skip the streamed-mode leg")
     ap.add_argument("--stream-steps", type=int, default=3)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the Qwen2.5-72B layer (R = 8) device leg and the staged streamed run")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -232,9 +264,13 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     torch.cuda.set_device(0)
-    dres, master, host_grads, w = device_leg(args, torch, np, synth, sdp)
+    dres, master, host_grads, w = device_leg(args, torch, np, synth, sdp, 1, args.steps, args.warmup, True)
     cpu = None if args.no_cpu else cpu_leg(args, np, oracle, master, host_grads, w)
     del master, host_grads
+    r8 = None
+    if not args.no_extra:
+        r8_res, _, _, _ = device_leg(args, torch, np, synth, sdp, 4, 10, 2, False)
+        r8 = brief(r8_res)
     streamed = None if args.no_stream else stream_leg(args, torch, np, synth, sdp)
 
     traffic = measured_traffic(dres["update_bytes"])
@@ -266,6 +302,7 @@ def main():
         "hbm_copy_gbs": dres["copy_gbs"],
         "grad_norm_last_step": dres["grad_norm"],
         "streamed": streamed,
+        "device_r8": r8,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
