@@ -16,6 +16,9 @@ JSON line also carries:
                    device mode, where the norm pass stores the mean gradient;
   staged_pageable (inside streamed) -- the streamed step again with the
                    states in pageable memory, through the staged mode;
+  delivery (inside streamed) -- BF16 copies of the layer's FP32 master
+                   delivered into a device window, rounded on the host or on
+                   the GPU, from pinned and pageable memory;
   cpu_baseline  -- the CPU oracle on the same layer, on this host's cores.
 Inputs are generated before the timed region and stay resident; the same
 gradient buffers are reused by every timed step.
@@ -229,7 +232,24 @@ def stream_leg(args, torch, np, synth, sdp):
         sel = timed(sctx, sseg)
         sdp.sdp_ctx_destroy(sctx)
         out["staged_pageable"] = dict(ms_per_step=sel * 1e3, params_per_s=N / sel, frac_of_link_bound=t_link / sel)
-        del pg
+        # parameter delivery of the updated master as BF16 into a device window
+        log("streamed leg: parameter delivery")
+        window = torch.empty(N, dtype=torch.int16, device="cuda")
+        dctx = sdp.sdp_ctx_create(0, C, R, 0)
+        deliv = {}
+        for mname, mode in (("host_cast", sdp.SDP_DELIVER_HOST_CAST), ("device_cast", sdp.SDP_DELIVER_DEVICE_CAST)):
+            for sname, src in (("pinned", p), ("pageable", pg[0])):
+                sdp.sdp_deliver_params(dctx, src.ctypes.data, window.data_ptr(), N, C, mode)
+                t0 = time.perf_counter()
+                for _ in range(3):
+                    sdp.sdp_deliver_params(dctx, src.ctypes.data, window.data_ptr(), N, C, mode)
+                el_d = (time.perf_counter() - t0) / 3
+                link_bytes = (2 if mode == sdp.SDP_DELIVER_HOST_CAST else 4) * N
+                deliv[f"{mname}_{sname}"] = dict(ms=el_d * 1e3, params_per_s=N / el_d, bf16_gbs=2 * N / el_d / 1e9,
+                                                 link_gbs=link_bytes / el_d / 1e9)
+        sdp.sdp_ctx_destroy(dctx)
+        out["delivery"] = deliv
+        del pg, window
     for hbuf in bufs:
         hbuf.close()
     return out

@@ -195,6 +195,31 @@ int sdp_ctx_last_norm(sdp_ctx *ctx, double *norm, double *clip_coef, int *nonfin
  * its sign and top payload bits and gets the quiet bit. */
 int sdp_cast_bf16(sdp_ctx *ctx, const float *src, uint16_t *dst, int64_t n, void *stream);
 
+/* ---- parameter delivery ------------------------------------------------ */
+
+/* How sdp_deliver_params makes the BF16 copy. */
+#define SDP_DELIVER_HOST_CAST 0   /* host threads round to BF16 into pinned bounce buffers; BF16 crosses the link */
+#define SDP_DELIVER_DEVICE_CAST 1 /* the FP32 chunk crosses the link and the GPU rounds it */
+
+/* Parameter delivery for the next forward pass: dev_bf16[i] = bf16_rne(
+ * host_master[i]) for n elements, chunk by chunk, double-buffered.  The paper
+ * keeps only the FP32 master on the host and casts each chunk to BF16 while
+ * the DMA moves the previous one (Design, overlap within a layer); that is
+ * SDP_DELIVER_HOST_CAST.  host_master: any host memory (pinned memory is
+ * copied directly in SDP_DELIVER_DEVICE_CAST); dev_bf16: device memory of
+ * ctx's GPU.  chunk_elems as for sdp_stream_step.  Blocks until the last
+ * chunk has landed, so a forward pass started after the call sees the
+ * updated weights (the per-layer version gate).  The first call creates
+ * the context's host threads and pinned bounce buffers if it has none. */
+int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf16, int64_t n,
+                       int64_t chunk_elems, int mode);
+
+/* The BF16 rounding of the host delivery lane on its own: dst[i] =
+ * bf16_rne(src[i]) for n elements of host memory.  ctx may be NULL (runs on
+ * the calling thread, no GPU needed) or a context whose host threads share
+ * the work. */
+int sdp_cast_bf16_host(sdp_ctx *ctx, const float *src, uint16_t *dst, int64_t n);
+
 /* ---- planning (host only, no GPU needed) --------------------------------- */
 
 /* Chunks and norm tiles of a call: n_chunks = sum over segments of

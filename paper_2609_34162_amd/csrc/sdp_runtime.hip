@@ -87,12 +87,30 @@ struct Timed {
 // by the staged streamed mode to move chunks between the caller's host
 // memory and the context's pinned bounce buffers (the CPU-side staging lane
 // of the paper's chunked overlap, Design, overlap within a layer).
+// Round FP32 values to BF16, nearest even, on the host (the parameter
+// delivery lane).  NaN keeps its sign and top payload bits and gets the quiet
+// bit; infinities are kept; overflow of the largest values rounds to
+// infinity.  Plain integer code that the compiler vectorises.
+void cast_bf16_host(const float *src, uint16_t *dst, size_t n) {
+    for (size_t i = 0; i < n; ++i) {
+        uint32_t x;
+        std::memcpy(&x, src + i, sizeof x);
+        const uint32_t r = ((x & 0x7fffffffu) > 0x7f800000u) ? ((x >> 16) | 0x0040u)
+                                                             : ((x + 0x7fffu + ((x >> 16) & 1u)) >> 16);
+        dst[i] = (uint16_t)r;
+    }
+}
+
 class CopyPool {
   public:
+    // kind kCopy: memcpy `bytes`; kind kCastBf16: round `bytes` FP32 values
+    // at src to BF16 at dst (the count is in elements).
+    enum Kind { kCopy = 0, kCastBf16 = 1 };
     struct Job {
         void *dst;
         const void *src;
         size_t bytes;
+        int kind = kCopy;
     };
 
     explicit CopyPool(int workers) {
@@ -114,9 +132,17 @@ class CopyPool {
         constexpr size_t kPiece = 4u << 20;
         std::unique_lock<std::mutex> g(mu_);
         pieces_.clear();
-        for (const Job &j : jobs)
-            for (size_t off = 0; off < j.bytes; off += kPiece)
-                pieces_.push_back({(char *)j.dst + off, (const char *)j.src + off, std::min(kPiece, j.bytes - off)});
+        constexpr size_t kCastPiece = 1u << 20;  // elements
+        for (const Job &j : jobs) {
+            if (j.kind == kCastBf16) {
+                for (size_t off = 0; off < j.bytes; off += kCastPiece)
+                    pieces_.push_back({(uint16_t *)j.dst + off, (const float *)j.src + off,
+                                       std::min(kCastPiece, j.bytes - off), kCastBf16});
+            } else {
+                for (size_t off = 0; off < j.bytes; off += kPiece)
+                    pieces_.push_back({(char *)j.dst + off, (const char *)j.src + off, std::min(kPiece, j.bytes - off)});
+            }
+        }
         next_ = 0;
         left_ = pieces_.size();
         ++gen_;
@@ -136,7 +162,11 @@ class CopyPool {
                 if (next_ >= pieces_.size()) return;
                 k = next_++;
             }
-            std::memcpy(pieces_[k].dst, pieces_[k].src, pieces_[k].bytes);
+            const Job &pc = pieces_[k];
+            if (pc.kind == kCastBf16)
+                cast_bf16_host((const float *)pc.src, (uint16_t *)pc.dst, pc.bytes);
+            else
+                std::memcpy(pc.dst, pc.src, pc.bytes);
             std::lock_guard<std::mutex> g(mu_);
             if (--left_ == 0) cv_done_.notify_all();
         }
@@ -714,6 +744,34 @@ int stream_update_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t R, const 
     return SDP_OK;
 }
 
+// The host threads and pinned bounce buffers, created on first use by a
+// context that was not created for the staged mode.
+int ensure_host_staging(sdp_ctx *ctx) {
+    if (!ctx->copier) {
+        int threads = (int)std::min(16u, std::max(1u, std::thread::hardware_concurrency()));
+        if (const char *env = std::getenv("SDP_STAGING_THREADS")) threads = std::max(1, std::min(64, std::atoi(env)));
+        ctx->copier = new CopyPool(threads - 1);
+    }
+    if (!ctx->bounce_in) {
+        if (hipHostMalloc(&ctx->bounce_in, 2 * ctx->slot_bytes, hipHostMallocDefault) != hipSuccess) {
+            (void)hipGetLastError();
+            ctx->bounce_in = nullptr;
+            return fail(SDP_ERR_OUT_OF_MEMORY, "cannot allocate %zu bytes of pinned bounce buffers", 2 * ctx->slot_bytes);
+        }
+        ctx->bin_used[0] = ctx->bin_used[1] = false;
+    }
+    return SDP_OK;
+}
+
+bool is_pinned_host(const void *p) {
+    hipPointerAttribute_t at;
+    if (hipPointerGetAttributes(&at, p) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    return at.type == hipMemoryTypeHost;
+}
+
 int sync_streams(sdp_ctx *ctx) {
     HIP_TRY(hipStreamSynchronize(ctx->s_copy));
     HIP_TRY(hipStreamSynchronize(ctx->s_comp));
@@ -1050,6 +1108,91 @@ int sdp_cast_bf16(sdp_ctx *ctx, const float *src, uint16_t *dst, int64_t n, void
     if (a0 < b1 && b0 < a1) return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_cast_bf16: src and dst overlap");
     HIP_TRY(sdp::launch_cast_bf16(src, dst, n, (hipStream_t)stream));
     return SDP_OK;
+}
+
+int sdp_cast_bf16_host(sdp_ctx *ctx, const float *src, uint16_t *dst, int64_t n) {
+    t_err.clear();
+    if (!src || !dst || n < 1) return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_cast_bf16_host: bad argument");
+    if (ctx && ctx->copier)
+        ctx->copier->copy({{dst, src, (size_t)n, CopyPool::kCastBf16}});
+    else
+        cast_bf16_host(src, dst, (size_t)n);
+    return SDP_OK;
+}
+
+int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf16, int64_t n, int64_t chunk_elems,
+                       int mode) {
+    t_err.clear();
+    if (!ctx || !host_master || !dev_bf16 || n < 1)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_deliver_params: bad argument");
+    if (mode != SDP_DELIVER_HOST_CAST && mode != SDP_DELIVER_DEVICE_CAST)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_deliver_params: unknown mode %d", mode);
+    if (!ctx->staging) return fail(SDP_ERR_CHUNK_TOO_LARGE, "context was created without streamed-mode staging");
+    SDP_TRY(check_chunk(chunk_elems, false));
+    if (chunk_elems > ctx->max_chunk)
+        return fail(SDP_ERR_CHUNK_TOO_LARGE, "chunk_elems %lld exceeds the context's %lld", (long long)chunk_elems,
+                    (long long)ctx->max_chunk);
+    if (!aligned(host_master) || !aligned(dev_bf16))
+        return fail(SDP_ERR_ALIGNMENT, "sdp_deliver_params: pointers must be %d-byte aligned", SDP_ALIGN);
+    DeviceGuard guard(ctx->device);
+    SDP_TRY(check_host_ptr(host_master, "host_master", 0));
+    SDP_TRY(check_device_ptr(ctx, dev_bf16, (size_t)n * 2, "dev_bf16", 0));
+    const bool pinned = is_pinned_host(host_master);
+    if (mode == SDP_DELIVER_HOST_CAST || !pinned) SDP_TRY(ensure_host_staging(ctx));
+    SDP_TRY(order_after_last(ctx, ctx->s_copy));
+    SDP_TRY(order_after_last(ctx, ctx->s_comp));
+    bool used[2] = {false, false};
+    int rc = SDP_OK;
+    size_t k = 0;
+    for (int64_t off = 0; off < n && rc == SDP_OK; off += chunk_elems, ++k) {
+        const int sl = (int)(k & 1);
+        const int64_t len = std::min(chunk_elems, n - off);
+        char *bin = ctx->bounce_in + (size_t)sl * ctx->slot_bytes;
+        if (mode == SDP_DELIVER_HOST_CAST) {
+            // host threads round chunk k while the DMA still moves chunk k-1
+            if (ctx->bin_used[sl] && hipEventSynchronize(ctx->h2d_done[sl]) != hipSuccess) {
+                rc = fail(SDP_ERR_HIP, "sdp_deliver_params: event wait failed");
+                break;
+            }
+            ctx->copier->copy({{bin, host_master + off, (size_t)len, CopyPool::kCastBf16}});
+            if (hipMemcpyAsync(dev_bf16 + off, bin, (size_t)len * 2, hipMemcpyHostToDevice, ctx->s_copy) != hipSuccess ||
+                hipEventRecord(ctx->h2d_done[sl], ctx->s_copy) != hipSuccess)
+                rc = fail(SDP_ERR_HIP, "sdp_deliver_params: copy enqueue failed");
+            ctx->bin_used[sl] = true;
+        } else {
+            Slot slot = slot_at(ctx, sl);
+            std::vector<Xfer> xs = {{off_in_slot(ctx, sl, slot.p), (char *)(host_master + off), (size_t)len * 4}};
+            if (used[sl] && hipStreamWaitEvent(ctx->s_copy, ctx->slot_free[sl], 0) != hipSuccess) {
+                rc = fail(SDP_ERR_HIP, "sdp_deliver_params: stream wait failed");
+                break;
+            }
+            if (pinned) {
+                if (hipMemcpyAsync(slot.p, host_master + off, (size_t)len * 4, hipMemcpyHostToDevice, ctx->s_copy) !=
+                    hipSuccess)
+                    rc = fail(SDP_ERR_HIP, "sdp_deliver_params: copy enqueue failed");
+            } else {
+                if (ctx->bin_used[sl] && hipEventSynchronize(ctx->h2d_done[sl]) != hipSuccess) {
+                    rc = fail(SDP_ERR_HIP, "sdp_deliver_params: event wait failed");
+                    break;
+                }
+                ctx->copier->copy({{bin, host_master + off, (size_t)len * 4}});
+                if (hipMemcpyAsync(slot.p, bin, (size_t)len * 4, hipMemcpyHostToDevice, ctx->s_copy) != hipSuccess)
+                    rc = fail(SDP_ERR_HIP, "sdp_deliver_params: copy enqueue failed");
+                ctx->bin_used[sl] = true;
+            }
+            if (rc != SDP_OK) break;
+            if (hipEventRecord(ctx->h2d_done[sl], ctx->s_copy) != hipSuccess ||
+                hipStreamWaitEvent(ctx->s_comp, ctx->h2d_done[sl], 0) != hipSuccess ||
+                sdp::launch_cast_bf16(slot.p, dev_bf16 + off, len, ctx->s_comp) != hipSuccess ||
+                hipEventRecord(ctx->slot_free[sl], ctx->s_comp) != hipSuccess)
+                rc = fail(SDP_ERR_HIP, "sdp_deliver_params: enqueue failed");
+            used[sl] = true;
+        }
+    }
+    const int rc2 = sync_streams(ctx);
+    if (rc != SDP_OK) return rc;
+    if (rc2 != SDP_OK) return rc2;
+    return mark_done(ctx, ctx->s_comp);
 }
 
 int sdp_ctx_set_timing(sdp_ctx *ctx, int enable) {

@@ -30,6 +30,8 @@ SDP_FLAG_DEVICE_GBAR_ALWAYS = 0x2
 SDP_FLAG_STREAM_GBAR_NEVER = 0x4
 SDP_FLAG_DEBUG_POISON = 0x8
 SDP_FLAG_STREAM_STAGED = 0x10
+SDP_DELIVER_HOST_CAST = 0
+SDP_DELIVER_DEVICE_CAST = 1
 
 
 class SdpError(RuntimeError):
@@ -79,6 +81,8 @@ def _load():
         "sdp_grad_norm": (ctypes.c_int, [vp, vp, i32, ctypes.c_int, i64, vp, P(dbl)]),
         "sdp_ctx_last_norm": (ctypes.c_int, [vp, P(dbl), P(dbl), P(ctypes.c_int)]),
         "sdp_cast_bf16": (ctypes.c_int, [vp, vp, vp, i64, vp]),
+        "sdp_deliver_params": (ctypes.c_int, [vp, vp, vp, i64, i64, ctypes.c_int]),
+        "sdp_cast_bf16_host": (ctypes.c_int, [vp, vp, vp, i64]),
         "sdp_plan": (ctypes.c_int, [vp, i32, i64, P(i64), P(i64)]),
         "sdp_bytes_per_elem": (ctypes.c_int, [ctypes.c_int, i32, ctypes.c_uint32, P(dbl), P(dbl)]),
         "sdp_ctx_set_timing": (ctypes.c_int, [vp, ctypes.c_int]),
@@ -202,6 +206,15 @@ def sdp_ctx_last_norm(ctx) -> Tuple[float, float, bool]:
 
 def sdp_cast_bf16(ctx, src: int, dst: int, n: int, stream=None) -> None:
     _check(_lib.sdp_cast_bf16(ctx, src, dst, n, _stream(stream)))
+
+
+def sdp_deliver_params(ctx, host_master: int, dev_bf16: int, n: int, chunk_elems: int,
+                       mode: int = SDP_DELIVER_HOST_CAST) -> None:
+    _check(_lib.sdp_deliver_params(ctx, host_master, dev_bf16, n, chunk_elems, mode))
+
+
+def sdp_cast_bf16_host(ctx, src: int, dst: int, n: int) -> None:
+    _check(_lib.sdp_cast_bf16_host(ctx, src, dst, n))
 
 
 def sdp_plan(numels: Sequence[int], chunk_elems: int) -> Tuple[int, int]:

@@ -241,6 +241,26 @@ def test_staged_streamed_matches_device_and_oracle(sdp, ctx, ctx_staged, ctx_sta
     assert e.value.status == sdp.SDP_ERR_INVALID_ARGUMENT
 
 
+@pytest.mark.parametrize("mode", ["host_cast", "device_cast"])
+def test_deliver_params(sdp, ctx, mode):
+    """Parameter delivery: the device BF16 window equals bf16(host master),
+    for pinned and pageable masters, ragged sizes and both chunkings."""
+    m = sdp.SDP_DELIVER_HOST_CAST if mode == "host_cast" else sdp.SDP_DELIVER_DEVICE_CAST
+    rng = np.random.default_rng(77)
+    for n in (1, 7, TILE + 3, 3 * TILE + 5, 1 << 20):
+        x = (rng.normal(0, 0.02, n) * np.exp2(rng.integers(-20, 20, n))).astype(np.float32)
+        x[:min(n, 3)] = [np.nan, np.inf, -0.0][:min(n, 3)]
+        want = oracle.bf16(x)
+        hb = sdp.HostBuffer(max(16, 4 * n))
+        pinned = hb.view(np.float32, n)
+        pinned[:] = x
+        for src in (x, pinned):
+            for chunk in (TILE, 2 * TILE):
+                out = torch.full((n,), 0x5555, dtype=torch.int16, device="cuda")
+                sdp.sdp_deliver_params(ctx, src.ctypes.data, out.data_ptr(), n, chunk, m)
+                assert np.array_equal(out.cpu().numpy().view(np.uint16), want), (n, chunk, src is pinned)
+
+
 def test_grad_norm_modes_agree(sdp, ctx):
     sizes = [TILE * 2 + 1, 513]
     R = 5
