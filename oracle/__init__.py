@@ -65,6 +65,11 @@ def _declare(L):
     L.orc_adamw_f64.argtypes = [i64, vp, vp, vp, vp, ctypes.POINTER(HParams), vp, vp, vp]
     L.orc_step.restype = ctypes.c_int
     L.orc_step.argtypes = [vp, i32, i32, ctypes.POINTER(HParams), ctypes.POINTER(dbl)]
+    L.orc_step_fmt.restype = ctypes.c_int
+    L.orc_step_fmt.argtypes = [vp, i32, i32, ctypes.POINTER(HParams), i32, ctypes.POINTER(dbl)]
+    L.orc_update_points_fmt.restype = None
+    L.orc_update_points_fmt.argtypes = [i64, vp, vp, vp, vp, i32, dbl,
+                                        ctypes.POINTER(HParams), i32, vp, vp, vp, vp]
     L.orc_update_points.restype = None
     L.orc_update_points.argtypes = [i64, vp, vp, vp, vp, i32, dbl,
                                     ctypes.POINTER(HParams), vp, vp, vp, vp]
@@ -133,13 +138,14 @@ def _segments(state: State, grads):
     return segs, R, keep
 
 
-def step(state: State, grads, hp: HParams, lib=None):
-    """One oracle step in place.  Returns (status, norm)."""
+def step(state: State, grads, hp: HParams, lib=None, gbar_bf16=False):
+    """One oracle step in place.  Returns (status, norm).  gbar_bf16: the
+    update consumes the mean gradient rounded to BF16 (the norm does not)."""
     L = lib or load()
     segs, R, keep = _segments(state, grads)
     norm = ctypes.c_double(0.0)
-    rc = L.orc_step(ctypes.cast(segs, ctypes.c_void_p), len(state.master), R,
-                    ctypes.byref(hp), ctypes.byref(norm))
+    rc = L.orc_step_fmt(ctypes.cast(segs, ctypes.c_void_p), len(state.master), R,
+                        ctypes.byref(hp), int(bool(gbar_bf16)), ctypes.byref(norm))
     del keep
     return rc, norm.value
 
@@ -196,7 +202,7 @@ def adamw_f64(p, m, v, g, hp: HParams, lib=None):
     return po, mo, vo
 
 
-def update_points(p, m, v, g_rows, clip_c: float, hp: HParams, lib=None):
+def update_points(p, m, v, g_rows, clip_c: float, hp: HParams, lib=None, gbar_bf16=False):
     """Update independent points; g_rows has shape (n, R) of uint16."""
     L = lib or load()
     p = np.ascontiguousarray(p, np.float32)
@@ -206,9 +212,9 @@ def update_points(p, m, v, g_rows, clip_c: float, hp: HParams, lib=None):
     n, R = g_rows.shape
     po, mo, vo = (np.empty(n, np.float32) for _ in range(3))
     pb = np.empty(n, np.uint16)
-    L.orc_update_points(n, p.ctypes.data, m.ctypes.data, v.ctypes.data,
-                        g_rows.ctypes.data, R, clip_c, ctypes.byref(hp),
-                        po.ctypes.data, mo.ctypes.data, vo.ctypes.data, pb.ctypes.data)
+    L.orc_update_points_fmt(n, p.ctypes.data, m.ctypes.data, v.ctypes.data,
+                            g_rows.ctypes.data, R, clip_c, ctypes.byref(hp), int(bool(gbar_bf16)),
+                            po.ctypes.data, mo.ctypes.data, vo.ctypes.data, pb.ctypes.data)
     return po, mo, vo, pb
 
 

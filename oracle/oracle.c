@@ -29,6 +29,11 @@
  *   5. master = fp32(p'), exp_avg = fp32(m'), exp_avg_sq = fp32(v'),
  *      param_bf16 = bf16(master) -- BF16 compute weights for the next
  *      dispatch (training states table; Design, overlap within a layer).
+ * Variant for a mean gradient returned to the host in BF16 (the paper's
+ * GPU-reduction route hands one BF16 gradient to the host update; Design,
+ * gradient return, and the per-layer reduce -> D2H -> Adam chain): step 4
+ * then takes g = bf16(g_bar[i]) * c, while steps 2 and 3 still use the FP32
+ * g_bar, so the clip decision does not depend on the transport format.
  * fp32() is the C conversion from double (round to nearest, ties to even);
  * bf16() is round to nearest even on the 8-bit significand, written below
  * from that definition.
@@ -329,10 +334,23 @@ static void update_one(float *p, float *m, float *v, uint16_t *pb, float g_bar,
     *pb = orc_bf16_from_f32(*p);
 }
 
+/* The gradient step 4 consumes: g_bar, or g_bar rounded to BF16. */
+static float update_gradient(float g_bar, int gbar_bf16)
+{
+    return gbar_bf16 ? orc_f32_from_bf16(orc_bf16_from_f32(g_bar)) : g_bar;
+}
+
 /* One full optimizer step over all segments; states are updated in place.
  * Returns ORC_NONFINITE (states untouched) when the norm is not finite. */
 int orc_step(orc_segment *segs, int32_t n_segs, int32_t R, const orc_hparams *hp,
              double *norm_out)
+{
+    return orc_step_fmt(segs, n_segs, R, hp, 0, norm_out);
+}
+
+/* orc_step with the update fed bf16(g_bar) when gbar_bf16 is non-zero. */
+int orc_step_fmt(orc_segment *segs, int32_t n_segs, int32_t R, const orc_hparams *hp,
+                 int gbar_bf16, double *norm_out)
 {
     if (R < 1 || n_segs < 0 || hp->step < 1)
         return ORC_INVALID;
@@ -349,8 +367,9 @@ int orc_step(orc_segment *segs, int32_t n_segs, int32_t R, const orc_hparams *hp
 #pragma omp parallel for schedule(static)
         for (int64_t i = 0; i < sg->numel; ++i)
             update_one(&sg->master[i], &sg->exp_avg[i], &sg->exp_avg_sq[i],
-                       &sg->param_bf16[i], orc_mean_grad(sg->grads, R, i), c,
-                       hp, bc1, bc2);
+                       &sg->param_bf16[i],
+                       update_gradient(orc_mean_grad(sg->grads, R, i), gbar_bf16),
+                       c, hp, bc1, bc2);
     }
     return ORC_OK;
 }
@@ -363,6 +382,16 @@ void orc_update_points(int64_t n, const float *p, const float *m, const float *v
                        const orc_hparams *hp, float *p_out, float *m_out,
                        float *v_out, uint16_t *pb_out)
 {
+    orc_update_points_fmt(n, p, m, v, g_rows, R, clip_coef, hp, 0,
+                          p_out, m_out, v_out, pb_out);
+}
+
+/* orc_update_points with the update fed bf16(g_bar) when gbar_bf16 is set. */
+void orc_update_points_fmt(int64_t n, const float *p, const float *m, const float *v,
+                           const uint16_t *g_rows, int32_t R, double clip_coef,
+                           const orc_hparams *hp, int gbar_bf16, float *p_out,
+                           float *m_out, float *v_out, uint16_t *pb_out)
+{
     double bc1, bc2;
     bias_corrections(hp, &bc1, &bc2);
     if (R < 1 || R > ORC_MAX_RANKS)
@@ -371,7 +400,7 @@ void orc_update_points(int64_t n, const float *p, const float *m, const float *v
         const uint16_t *rows[ORC_MAX_RANKS];
         for (int32_t r = 0; r < R; ++r)
             rows[r] = &g_rows[k * R + r];
-        float g_bar = orc_mean_grad(rows, R, 0);
+        float g_bar = update_gradient(orc_mean_grad(rows, R, 0), gbar_bf16);
         p_out[k] = p[k];
         m_out[k] = m[k];
         v_out[k] = v[k];

@@ -53,11 +53,18 @@ void orc_adamw_f64(int64_t n, const double *p, const double *m, const double *v,
 
 int orc_step(orc_segment *segs, int32_t n_segs, int32_t R, const orc_hparams *hp,
              double *norm_out);
+/* gbar_bf16 != 0: the update consumes bf16(g_bar); the norm still uses g_bar. */
+int orc_step_fmt(orc_segment *segs, int32_t n_segs, int32_t R, const orc_hparams *hp,
+                 int gbar_bf16, double *norm_out);
 
 void orc_update_points(int64_t n, const float *p, const float *m, const float *v,
                        const uint16_t *g_rows, int32_t R, double clip_coef,
                        const orc_hparams *hp, float *p_out, float *m_out,
                        float *v_out, uint16_t *pb_out);
+void orc_update_points_fmt(int64_t n, const float *p, const float *m, const float *v,
+                           const uint16_t *g_rows, int32_t R, double clip_coef,
+                           const orc_hparams *hp, int gbar_bf16, float *p_out,
+                           float *m_out, float *v_out, uint16_t *pb_out);
 
 int orc_num_threads(void);
 

@@ -350,6 +350,67 @@ def pin_param_is_bf16_of_master(lib):
 
 
 # ---------------------------------------------------------------------------
+# Variant: the update fed the mean gradient rounded to BF16
+
+def _bf16_route_case(n, seed):
+    """Rank gradients whose FP32 mean lies exactly on, below or above a BF16
+    midpoint, and the BF16 value that round-to-nearest-even must give.  A is a
+    random finite BF16 value away from its binade's top, so A+1 and A+2 (the
+    next BF16 values away from zero) share its exponent."""
+    rng = np.random.default_rng(seed)
+    sign = rng.integers(0, 2, n).astype(np.uint16) << 15
+    expo = rng.integers(0x70, 0x7c, n).astype(np.uint16) << 7   # |a| in [2^-15, 2^-3)
+    mant = rng.integers(0, 0x7d, n).astype(np.uint16)
+    A = sign | expo | mant
+    kind = np.arange(n) % 3
+    g = [A.copy(), A.copy(), A.copy(), A.copy()]
+    # kind 0: mean a + u/2 (two ranks at A, two at A+1): tie, even bits win
+    # kind 1: mean a + u/4 (one rank at A+1): rounds down to A
+    # kind 2: mean a + 3u/4 (three ranks at A+1): rounds up to A+1
+    for r in range(4):
+        up = (kind == 0) & (r >= 2) | (kind == 1) & (r == 3) | (kind == 2) & (r >= 1)
+        g[r][up] += 1
+    want = np.where(kind == 0, np.where(A % 2 == 0, A, A + 1),
+                    np.where(kind == 1, A, A + 1)).astype(np.uint16)
+    return g, want
+
+
+def pin_bf16_gradient_route(lib):
+    # R = 1: the mean is a BF16 value already, so rounding it changes nothing
+    n = 3000
+    master = rand_master(n, seed=31)
+    g1 = rand_grads(n, 1, seed=31, outlier_p=0.01)
+    hp = oracle.hparams(step=2, max_grad_norm=0.05)
+    a = oracle.State([master])
+    b = oracle.State([master])
+    ra, na = oracle.step(a, [g1], hp, lib=lib)
+    rb, nb = oracle.step(b, [g1], hp, lib=lib, gbar_bf16=True)
+    assert ra == rb == 0 and na == nb
+    for x, y in ((a.master, b.master), (a.exp_avg, b.exp_avg), (a.exp_avg_sq, b.exp_avg_sq),
+                 (a.param_bf16, b.param_bf16)):
+        assert np.array_equal(x[0], y[0])
+    # R = 4 with the mean on, below and above BF16 midpoints: without
+    # clipping the step equals the step on the single rounded gradient
+    g4, want = _bf16_route_case(n, seed=32)
+    hp0 = oracle.hparams(step=1, max_grad_norm=0.0)
+    c = oracle.State([master])
+    d = oracle.State([master])
+    _, nc = oracle.step(c, [g4], hp0, lib=lib, gbar_bf16=True)
+    _, nd = oracle.step(d, [[want]], hp0, lib=lib)
+    for x, y in ((c.master, d.master), (c.exp_avg, d.exp_avg), (c.exp_avg_sq, d.exp_avg_sq),
+                 (c.param_bf16, d.param_bf16)):
+        assert np.array_equal(x[0], y[0])
+    # the norm (and so the clip decision) comes from the unrounded FP32 mean
+    exact = np.float64(np.sum(np.square(oracle.mean_grads(g4, lib=lib).astype(np.float64))))
+    assert abs(nc - np.sqrt(exact)) <= 1e-12 * nc and nc != nd
+    # the sampled-point entry takes the same rounding
+    po, mo, vo, pb = oracle.update_points(master, np.zeros(n, np.float32), np.zeros(n, np.float32),
+                                          np.stack(g4, axis=1), 1.0, hp0, lib=lib, gbar_bf16=True)
+    assert np.array_equal(po, d.master[0]) and np.array_equal(vo, d.exp_avg_sq[0])
+    assert np.array_equal(pb, d.param_bf16[0])
+
+
+# ---------------------------------------------------------------------------
 # The whole step against torch (library special case, brute force sizes)
 
 def torch_step(masters, ms, vs, grads, hp):

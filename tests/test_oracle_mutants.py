@@ -51,6 +51,13 @@ MUTATIONS = {
     "bf16_truncates": ("if (dlo < dhi)\n        pick = lo;", "if (1)\n        pick = lo;"),
     "bf16_nan_not_quiet": ("return (uint16_t)((u >> 16) | 0x0040u);", "return (uint16_t)(u >> 16);"),
     "bf16_no_overflow_to_inf": ("ldexp(1.0, 128)", "ldexp(1.0, 200)"),
+    "route_gbar_not_rounded": ("return gbar_bf16 ? orc_f32_from_bf16(orc_bf16_from_f32(g_bar)) : g_bar;",
+                               "return g_bar;"),
+    "route_gbar_truncated": ("return gbar_bf16 ? orc_f32_from_bf16(orc_bf16_from_f32(g_bar)) : g_bar;",
+                             "uint32_t u_;\n    memcpy(&u_, &g_bar, 4);\n"
+                             "    return gbar_bf16 ? orc_f32_from_bf16((uint16_t)(u_ >> 16)) : g_bar;"),
+    "route_points_not_rounded": ("float g_bar = update_gradient(orc_mean_grad(rows, R, 0), gbar_bf16);",
+                                 "float g_bar = orc_mean_grad(rows, R, 0);"),
     "param_from_unrounded": ("*pb = orc_bf16_from_f32(*p);", "*pb = orc_bf16_from_f32((float)(po + 1e-9));"),
 }
 
@@ -60,7 +67,8 @@ ORDER = ["pin_bf16_special_values", "pin_mean_closed_forms", "pin_norm_constant"
          "pin_clip_coef", "pin_first_step_sign", "pin_zero_gradient", "pin_sign_descent",
          "pin_lr_zero", "pin_identical_ranks", "pin_clip_noop", "pin_nonfinite",
          "pin_param_is_bf16_of_master", "pin_mean_vs_numpy", "pin_norm_vs_torch",
-         "pin_adamw_f64_vs_torch", "pin_bf16_random_vs_torch", "pin_step_vs_torch",
+         "pin_adamw_f64_vs_torch", "pin_bf16_random_vs_torch", "pin_bf16_gradient_route",
+         "pin_step_vs_torch",
          "pin_brute_force"]
 
 
