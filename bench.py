@@ -19,6 +19,10 @@ JSON line also carries:
   delivery (inside streamed) -- BF16 copies of the layer's FP32 master
                    delivered into a device window, rounded on the host or on
                    the GPU, from pinned and pageable memory;
+  host_route    -- the paper's own datapath for the same Qwen3-14B layer:
+                   gradients in HBM, states in pageable host memory, the mean
+                   gradient copied down (FP32 or BF16) and AdamW on this
+                   host's cores, with the host AdamW's core scaling;
   cpu_baseline  -- the CPU oracle on the same layer, on this host's cores.
 Inputs are generated before the timed region and stay resident; the same
 gradient buffers are reused by every timed step.
@@ -255,6 +259,92 @@ def stream_leg(args, torch, np, synth, sdp):
     return out
 
 
+def host_route_leg(args, torch, np, synth, sdp):
+    """The paper's own datapath on one GPU: the rank gradients in HBM, the
+    states in pageable host memory, the GPU's norm pass and mean gradient,
+    chunked copies to the host, and AdamW on this host's cores."""
+    w = synth.workload(2)
+    N, R, C = w.numel, w.ranks, w.chunk
+    log(f"host route leg: {w.name} N={N} R={R} chunk={C}")
+    p = synth.master(w, 0)
+    m = np.zeros(N, np.float32)
+    v = np.zeros(N, np.float32)
+    pb = np.zeros(N, np.uint16)
+    g = []
+    tmp = np.empty(N, np.uint16)
+    for r in range(R):
+        synth.grad_bf16(w, 0, 1, r, out=tmp)
+        g.append(torch.from_numpy(tmp.view(np.int16)).to("cuda"))
+    torch.cuda.synchronize()
+    del tmp
+    segs = sdp.Segments([(p.ctypes.data, m.ctypes.data, v.ctypes.data, pb.ctypes.data,
+                          [x.data_ptr() for x in g], N)])
+    ctx = sdp.sdp_ctx_create(0, C, R, 0)
+    threads = sdp.sdp_ctx_host_threads(ctx)
+    # host memory ceiling of the same threads: a copy of 1 GiB
+    src = np.ones(1 << 28, np.float32)
+    dst = np.empty_like(src)
+    sdp.sdp_probe_host_copy(ctx, dst.ctypes.data, src.ctypes.data, src.nbytes, 1)
+    host_copy = max(sdp.sdp_probe_host_copy(ctx, dst.ctypes.data, src.ctypes.data, src.nbytes, 2) for _ in range(3))
+    del src, dst
+    # D2H alone, pinned, with the route's copy size
+    ha, hb = sdp.HostBuffer(4 * C), sdp.HostBuffer(4 * C)
+    da = torch.empty(4 * C, dtype=torch.uint8, device="cuda")
+    db = torch.empty(4 * C, dtype=torch.uint8, device="cuda")
+    d2h = max(sdp.sdp_probe_link(ctx, ha.ptr, hb.ptr, da.data_ptr(), db.data_ptr(), 4 * C, 4 * C, 4)[1]
+              for _ in range(3))
+    del da, db
+    ha.close()
+    hb.close()
+    log(f"host route leg: {threads} host threads, host copy {host_copy:.1f} GB/s, d2h {d2h:.1f} GB/s")
+    out = dict(workload=w.name, params=N, ranks=R, chunk_elems=C, host_threads=threads,
+               host_copy_gbs=host_copy, d2h_gbs_probe=d2h, states="pageable host memory",
+               grads="device memory")
+    for name, fmt, gsz in (("f32", sdp.SDP_GBAR_F32, 4), ("bf16", sdp.SDP_GBAR_BF16, 2)):
+        sdp.sdp_host_update_step(ctx, segs, sdp.make_params(**w.hparams(1)), C, fmt)  # warmup
+        sdp.sdp_ctx_set_timing(ctx, 1)
+        t0 = time.perf_counter()
+        for t in range(2, args.stream_steps + 2):
+            sdp.sdp_host_update_step(ctx, segs, sdp.make_params(**w.hparams(t)), C, fmt)
+        el = (time.perf_counter() - t0) / args.stream_steps
+        kt = sdp.sdp_ctx_get_timing(ctx)
+        sdp.sdp_ctx_set_timing(ctx, 0)
+        k = args.stream_steps
+        host_bytes = (26 + gsz) * N  # p, m, v read and written, g_bar read, BF16 params written
+        adam_s = kt.host_adam_ms / k / 1e3
+        bound = max(host_bytes / (host_copy * 1e9), gsz * N / (d2h * 1e9))
+        out[name] = dict(ms_per_step=el * 1e3, params_per_s=N / el, d2h_bytes_per_param=gsz,
+                         gpu_norm_ms=(kt.norm_ms + kt.finalize_ms) / k, gbar_kernel_ms=kt.gbar_ms / k,
+                         host_adam_ms=kt.host_adam_ms / k, host_wait_ms=kt.host_wait_ms / k,
+                         host_adam_gbs=host_bytes / adam_s / 1e9, host_adam_params_per_s=N / adam_s,
+                         bound_ms=bound * 1e3, frac_of_bound=bound / el)
+        log(f"host route leg {name}: {el * 1e3:.1f} ms/step, host AdamW {kt.host_adam_ms / k:.1f} ms "
+            f"({host_bytes / adam_s / 1e9:.1f} GB/s), waits {kt.host_wait_ms / k:.1f} ms")
+    # core scaling of the host AdamW alone on the same layer (the paper's
+    # CPU Adam scaling microbenchmark)
+    gb = np.full(N, 1e-3, np.float32)
+    hp = sdp.make_params(**w.hparams(3))
+    scaling = []
+    for t in (1, 2, 4, 8, 12, 16):
+        if t > max(threads, 16):
+            break
+        sdp.sdp_ctx_set_host_threads(ctx, t)
+        call = lambda: sdp.sdp_host_adamw(ctx, p.ctypes.data, m.ctypes.data, v.ctypes.data,  # noqa: E731
+                                          pb.ctypes.data, gb.ctypes.data, sdp.SDP_GBAR_F32, N, 1.0, hp)
+        call()
+        reps = 2 if t < 4 else 4
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            call()
+        el = (time.perf_counter() - t0) / reps
+        scaling.append(dict(threads=t, params_per_s=N / el, gbs=30 * N / el / 1e9))
+        log(f"host AdamW {t:2d} threads: {N / el / 1e9:.2f} G params/s, {30 * N / el / 1e9:.1f} GB/s")
+    out["adamw_core_scaling"] = scaling
+    sdp.sdp_ctx_destroy(ctx)
+    del g
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -292,6 +382,7 @@ def main():
         r8_res, _, _, _ = device_leg(args, torch, np, synth, sdp, 4, 10, 2, False)
         r8 = brief(r8_res)
     streamed = None if args.no_stream else stream_leg(args, torch, np, synth, sdp)
+    route = None if args.no_stream else host_route_leg(args, torch, np, synth, sdp)
 
     traffic = measured_traffic(dres["update_bytes"])
     out = {
@@ -322,6 +413,7 @@ def main():
         "hbm_copy_gbs": dres["copy_gbs"],
         "grad_norm_last_step": dres["grad_norm"],
         "streamed": streamed,
+        "host_route": route,
         "device_r8": r8,
         "cpu_baseline": cpu,
     }

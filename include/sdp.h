@@ -13,7 +13,8 @@
  * The paper runs that update on host CPUs.  This library runs it on the GPU,
  * either on states in device memory (sdp_agg_adam_step) or on states in
  * pinned host memory streamed through the GPU in double-buffered chunks
- * (sdp_stream_step).
+ * (sdp_stream_step); and, as the paper does, on host cores fed by the
+ * GPU-averaged gradient (sdp_host_update_step).
  *
  * Conventions for every call:
  *  - Return value: SDP_OK (0) or a negative SDP_ERR_* status.  A failing call
@@ -128,6 +129,12 @@ typedef struct {
     double update_ms;     /* fused aggregate + clip + AdamW + BF16 kernel */
     int64_t norm_launches, finalize_launches, update_launches;
     int64_t update_elems; /* elements processed by the timed update launches */
+    /* host-update route (sdp_host_update_step) */
+    double gbar_ms;       /* mean-gradient kernel (HIP events) */
+    int64_t gbar_launches;
+    double host_adam_ms;  /* host threads running AdamW (host clock) */
+    double host_wait_ms;  /* host waiting for a chunk's g_bar copy to land (host clock) */
+    int64_t host_adam_elems;
 } sdp_kernel_times;
 
 /* ---- context ----------------------------------------------------------- */
@@ -176,6 +183,52 @@ int sdp_agg_adam_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs,
 int sdp_stream_step(sdp_ctx *ctx, const sdp_segment *host_segs, int32_t n_segs,
                     const sdp_adamw_params *hp, int64_t chunk_elems,
                     double *grad_norm_out);
+
+/* Gradient formats of the host-update route: the mean gradient crosses the
+ * link as FP32 (4 B/element) or rounded to BF16 (2 B/element). */
+#define SDP_GBAR_F32 0
+#define SDP_GBAR_BF16 1
+
+/* Host-update route: the paper's own datapath on one GPU (Design, gradient
+ * return by GPU reduction; cross-rank pipelining, the per-layer chain of
+ * reduction, chunked D2H and host Adam).  The R rank gradients are device
+ * memory of ctx's GPU; master/exp_avg/exp_avg_sq/param_bf16 are host memory
+ * (pinned or pageable; the host threads touch them, no DMA does).
+ * Phase 1 runs the norm pass and finalize over the device gradients and
+ * reads the norm back.  Phase 2 walks the chunks: the GPU writes the chunk's
+ * mean gradient into a device staging slot, the copy stream moves it into a
+ * pinned bounce buffer, and the context's host threads run AdamW on the
+ * previous chunk meanwhile (double-buffered).  gbar_format SDP_GBAR_BF16
+ * rounds the mean gradient to BF16 before the copy, as the paper returns
+ * one BF16 gradient; the update then uses bf16(g_bar) * c, while the norm
+ * and c still come from the FP32 mean.  SDP_GBAR_F32 gives the same results
+ * as the other modes, up to FP64 rounding.  chunk_elems as for
+ * sdp_stream_step (the context needs staging).  Blocks until every state is
+ * written; returns SDP_ERR_NONFINITE (states unchanged) for a non-finite
+ * norm.  grad_norm_out may be NULL.  Host threads: sdp_ctx_set_host_threads,
+ * else SDP_STAGING_THREADS, else up to 16. */
+int sdp_host_update_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs,
+                         const sdp_adamw_params *hp, int64_t chunk_elems, int gbar_format,
+                         double *grad_norm_out);
+
+/* The host AdamW lane of the route on its own, for n elements of host memory:
+ * master/exp_avg/exp_avg_sq updated in place and param_bf16 written from
+ * gbar (FP32 or BF16 per gbar_format) and the clip coefficient clip_coef
+ * (finite, >= 0), with the per-element arithmetic of the fused update (FP64,
+ * no fused multiply-add, one rounding to FP32).  AVX-512 where the CPU has
+ * it (SDP_HOST_SIMD=0 forces the scalar path; both give the same bits).
+ * ctx may be NULL: the calling thread does the work and no GPU is needed;
+ * else the context's host threads share it.  Buffers 16-byte aligned and
+ * pairwise disjoint. */
+int sdp_host_adamw(sdp_ctx *ctx, float *master, float *exp_avg, float *exp_avg_sq,
+                   uint16_t *param_bf16, const void *gbar, int gbar_format, int64_t n,
+                   double clip_coef, const sdp_adamw_params *hp);
+
+/* Host threads of a context (the calling thread counts as one): they run the
+ * staged mode's bounce copies, the host BF16 cast and the host AdamW.
+ * threads in 1..256; replaces the context's thread pool. */
+int sdp_ctx_set_host_threads(sdp_ctx *ctx, int32_t threads);
+int sdp_ctx_host_threads(sdp_ctx *ctx, int32_t *threads_out);
 
 /* The global norm of the mean gradient alone (the first pass and finalize of
  * either mode; device_resident selects device or pinned-host buffers; only
@@ -256,6 +309,14 @@ int sdp_probe_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, void
  * `bytes`.  Blocks. */
 int sdp_probe_link(sdp_ctx *ctx, void *host_a, void *host_b, void *dev_a, void *dev_b,
                    int64_t bytes, int64_t chunk_bytes, int32_t reps, double *gbs_out);
+
+/* Host memory bandwidth of the context's host threads: `bytes` copied from
+ * src to dst (host memory, disjoint) `reps` times in 4 MiB pieces over the
+ * threads; gbs_out = bytes read plus bytes written per second / 1e9.  The
+ * ceiling of the host lanes (bounce copies, host cast, host AdamW).  Blocks;
+ * no GPU work. */
+int sdp_probe_host_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, int32_t reps,
+                        double *gbs_out);
 
 /* Pinned host memory of exactly `bytes` (hipHostMalloc), for streamed-mode
  * states; free with sdp_host_free. */

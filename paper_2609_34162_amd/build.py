@@ -2,12 +2,18 @@
 import os
 import subprocess
 import sys
+import tempfile
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB_PATH = os.path.join(HERE, "libsdp.so")
 SOURCES = [os.path.join(HERE, "csrc", f) for f in ("sdp_runtime.hip", "sdp_kernels.hip")]
+# host-only lanes, built with the host compiler: no fused multiply-add, so the
+# FP64 update rounds every product and sum as written
+HOST_SOURCES = [os.path.join(HERE, "csrc", "sdp_host_adamw.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+HOSTCXX = os.environ.get("SDP_HOSTCXX", "/opt/rocm/llvm/bin/clang++")
+HOST_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off", "-fno-math-errno", "-Wall"]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     # no packed FP32 instructions in device code
@@ -18,11 +24,20 @@ FLAGS = [
 
 def build(verbose: bool = False) -> str:
     tmp = LIB_PATH + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-I", os.path.join(ROOT, "include"), "-I", os.path.join(HERE, "csrc"),
-           "-o", tmp, *SOURCES]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.check_call(cmd)
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", os.path.join(HERE, "csrc")]
+    with tempfile.TemporaryDirectory() as d:
+        objs = []
+        for src in HOST_SOURCES:
+            obj = os.path.join(d, os.path.basename(src) + ".o")
+            cmd = [HOSTCXX, *HOST_FLAGS, *inc, "-c", src, "-o", obj]
+            if verbose:
+                print(" ".join(cmd), flush=True)
+            subprocess.check_call(cmd)
+            objs.append(obj)
+        cmd = [HIPCC, *FLAGS, *inc, "-o", tmp, *SOURCES, "-x", "none", *objs]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        subprocess.check_call(cmd)
     os.replace(tmp, LIB_PATH)
     return LIB_PATH
 

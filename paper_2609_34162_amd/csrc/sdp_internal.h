@@ -48,6 +48,16 @@ struct UpdateArgs {
     double eps;
 };
 
+// One launch of the mean-gradient kernel of the host-update route: g_bar of
+// `n` elements from the R BF16 buffers, written to `out` as FP32 or, when
+// bf16 is set, rounded to BF16.
+struct GbarArgs {
+    const uint16_t *g[SDP_MAX_RANKS];
+    int64_t n;
+    void *out;
+    int bf16;
+};
+
 constexpr int kTile = SDP_NORM_TILE;
 constexpr int kNormThreads = 256;
 constexpr int kFinalizeThreads = 1024;
@@ -58,6 +68,7 @@ hipError_t launch_norm_partials(int R, const NormArgs &a, hipStream_t s);
 hipError_t launch_norm_finalize(const double *partials /* pairs */, int64_t n_partials,
                                 double max_grad_norm, NormState *ns, hipStream_t s);
 hipError_t launch_update(int R, const UpdateArgs &a, int max_blocks, hipStream_t s);
+hipError_t launch_gbar_out(int R, const GbarArgs &a, hipStream_t s);
 hipError_t launch_cast_bf16(const float *src, uint16_t *dst, int64_t n, hipStream_t s);
 hipError_t launch_copy16(void *dst, const void *src, int64_t n16, int max_blocks, hipStream_t s);
 hipError_t launch_fill_u32(void *dst, int64_t n_words, uint32_t value, hipStream_t s);

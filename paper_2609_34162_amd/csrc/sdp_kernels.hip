@@ -316,6 +316,45 @@ __global__ __launch_bounds__(kUpdateThreads) void k_update(UpdateArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Mean gradient for the host-update route: g_bar of a chunk, FP32 or rounded
+// to BF16, written to a staging slot that the copy engine then moves to host
+// memory.  The rank gradients are read once and not reused (non-temporal).
+
+template <int R, bool BF16>
+__global__ __launch_bounds__(256) void k_gbar_out(GbarArgs a) {
+    const int64_t n = a.n;
+    const int64_t groups = n / kVec;
+    const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    for (int64_t q = gid; q < groups; q += stride) {
+        uint4 raw[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) raw[r] = load_stream(a.g[r] + q * kVec);
+        float g[kVec];
+        mean8<R>(raw, g);
+        if constexpr (BF16) {
+            uint4 b;
+            b.x = pack_bf16(g[0], g[1]);
+            b.y = pack_bf16(g[2], g[3]);
+            b.z = pack_bf16(g[4], g[5]);
+            b.w = pack_bf16(g[6], g[7]);
+            reinterpret_cast<uint4 *>(a.out)[q] = b;
+        } else {
+            float4 *o = reinterpret_cast<float4 *>(a.out) + 2 * q;
+            o[0] = make_float4(g[0], g[1], g[2], g[3]);
+            o[1] = make_float4(g[4], g[5], g[6], g[7]);
+        }
+    }
+    if (gid == 0) {
+        for (int64_t i = groups * kVec; i < n; ++i) {
+            const float g = mean1<R>(a.g, i);
+            if constexpr (BF16) reinterpret_cast<uint16_t *>(a.out)[i] = (uint16_t)bf16_rne(g);
+            else reinterpret_cast<float *>(a.out)[i] = g;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Small helpers.
 
 __global__ __launch_bounds__(256) void k_cast_bf16(const float *__restrict__ src,
@@ -374,6 +413,15 @@ hipError_t update_r(const UpdateArgs &a, int64_t blocks, hipStream_t s) {
     return hipGetLastError();
 }
 
+template <int R>
+hipError_t gbar_r(const GbarArgs &a, int64_t blocks, hipStream_t s) {
+    if (a.bf16)
+        hipLaunchKernelGGL((k_gbar_out<R, true>), dim3((uint32_t)blocks), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL((k_gbar_out<R, false>), dim3((uint32_t)blocks), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 #define SDP_FOR_EACH_R(X) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15) X(16)
@@ -400,6 +448,18 @@ hipError_t launch_update(int R, const UpdateArgs &a, int max_blocks, hipStream_t
     if (max_blocks > 0 && blocks > max_blocks) blocks = max_blocks;
     switch (R) {
 #define CASE(r) case r: return update_r<r>(a, blocks, s);
+        SDP_FOR_EACH_R(CASE)
+#undef CASE
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_gbar_out(int R, const GbarArgs &a, hipStream_t s) {
+    int64_t blocks = cdiv(a.n / kVec, 256);
+    if (blocks < 1) blocks = 1;
+    if (blocks > 65536) blocks = 65536;
+    switch (R) {
+#define CASE(r) case r: return gbar_r<r>(a, blocks, s);
         SDP_FOR_EACH_R(CASE)
 #undef CASE
         default: return hipErrorInvalidValue;

@@ -25,9 +25,11 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <functional>
 #include <string>
 #include <vector>
 
+#include "sdp_host.h"
 #include "sdp_internal.h"
 
 using sdp::NormState;
@@ -75,7 +77,7 @@ struct DeviceGuard {
     }
 };
 
-enum TimedKind { kNorm = 0, kFinalize = 1, kUpdate = 2 };
+enum TimedKind { kNorm = 0, kFinalize = 1, kUpdate = 2, kGbar = 3 };
 
 struct Timed {
     int kind;
@@ -101,22 +103,16 @@ void cast_bf16_host(const float *src, uint16_t *dst, size_t n) {
     }
 }
 
-class CopyPool {
+// A fixed set of host threads for the host lanes of the streamed engine:
+// copies between the caller's memory and pinned bounce buffers, the BF16
+// rounding of parameter delivery and the host AdamW route.  run(n, fn)
+// calls fn(i) for every i in [0, n) across the workers and the caller.
+class HostPool {
   public:
-    // kind kCopy: memcpy `bytes`; kind kCastBf16: round `bytes` FP32 values
-    // at src to BF16 at dst (the count is in elements).
-    enum Kind { kCopy = 0, kCastBf16 = 1 };
-    struct Job {
-        void *dst;
-        const void *src;
-        size_t bytes;
-        int kind = kCopy;
-    };
-
-    explicit CopyPool(int workers) {
+    explicit HostPool(int workers) {
         for (int i = 0; i < workers; ++i) threads_.emplace_back([this] { loop(); });
     }
-    ~CopyPool() {
+    ~HostPool() {
         {
             std::lock_guard<std::mutex> g(mu_);
             stop_ = true;
@@ -126,47 +122,33 @@ class CopyPool {
     }
     int size() const { return (int)threads_.size() + 1; }
 
-    // Copies every job; returns when all bytes have landed.  The calling
-    // thread takes part.
-    void copy(const std::vector<Job> &jobs) {
-        constexpr size_t kPiece = 4u << 20;
+    void run(size_t n, const std::function<void(size_t)> &fn) {
         std::unique_lock<std::mutex> g(mu_);
-        pieces_.clear();
-        constexpr size_t kCastPiece = 1u << 20;  // elements
-        for (const Job &j : jobs) {
-            if (j.kind == kCastBf16) {
-                for (size_t off = 0; off < j.bytes; off += kCastPiece)
-                    pieces_.push_back({(uint16_t *)j.dst + off, (const float *)j.src + off,
-                                       std::min(kCastPiece, j.bytes - off), kCastBf16});
-            } else {
-                for (size_t off = 0; off < j.bytes; off += kPiece)
-                    pieces_.push_back({(char *)j.dst + off, (const char *)j.src + off, std::min(kPiece, j.bytes - off)});
-            }
-        }
+        fn_ = &fn;
+        n_ = n;
         next_ = 0;
-        left_ = pieces_.size();
+        left_ = n;
         ++gen_;
         g.unlock();
         cv_work_.notify_all();
         work();
         g.lock();
         cv_done_.wait(g, [this] { return left_ == 0; });
+        fn_ = nullptr;
     }
 
   private:
     void work() {
         for (;;) {
             size_t k;
+            const std::function<void(size_t)> *fn;
             {
                 std::lock_guard<std::mutex> g(mu_);
-                if (next_ >= pieces_.size()) return;
+                if (next_ >= n_) return;
                 k = next_++;
+                fn = fn_;
             }
-            const Job &pc = pieces_[k];
-            if (pc.kind == kCastBf16)
-                cast_bf16_host((const float *)pc.src, (uint16_t *)pc.dst, pc.bytes);
-            else
-                std::memcpy(pc.dst, pc.src, pc.bytes);
+            (*fn)(k);
             std::lock_guard<std::mutex> g(mu_);
             if (--left_ == 0) cv_done_.notify_all();
         }
@@ -187,11 +169,44 @@ class CopyPool {
     std::vector<std::thread> threads_;
     std::mutex mu_;
     std::condition_variable cv_work_, cv_done_;
-    std::vector<Job> pieces_;
-    size_t next_ = 0, left_ = 0;
+    const std::function<void(size_t)> *fn_ = nullptr;
+    size_t n_ = 0, next_ = 0, left_ = 0;
     uint64_t gen_ = 0;
     bool stop_ = false;
 };
+
+// Copies (kind kCopy: `bytes`) and BF16 roundings (kind kCastBf16: `bytes`
+// FP32 values at src into BF16 at dst), split into pieces over the pool.
+struct Job {
+    enum Kind { kCopy = 0, kCastBf16 = 1 };
+    void *dst;
+    const void *src;
+    size_t bytes;
+    int kind = kCopy;
+};
+
+void pool_jobs(HostPool *pool, const std::vector<Job> &jobs) {
+    constexpr size_t kPiece = 4u << 20;      // bytes per copy piece
+    constexpr size_t kCastPiece = 1u << 20;  // elements per rounding piece
+    std::vector<Job> pieces;
+    for (const Job &j : jobs) {
+        if (j.kind == Job::kCastBf16) {
+            for (size_t off = 0; off < j.bytes; off += kCastPiece)
+                pieces.push_back({(uint16_t *)j.dst + off, (const float *)j.src + off,
+                                  std::min(kCastPiece, j.bytes - off), Job::kCastBf16});
+        } else {
+            for (size_t off = 0; off < j.bytes; off += kPiece)
+                pieces.push_back({(char *)j.dst + off, (const char *)j.src + off, std::min(kPiece, j.bytes - off)});
+        }
+    }
+    pool->run(pieces.size(), [&](size_t k) {
+        const Job &pc = pieces[k];
+        if (pc.kind == Job::kCastBf16)
+            cast_bf16_host((const float *)pc.src, (uint16_t *)pc.dst, pc.bytes);
+        else
+            std::memcpy(pc.dst, pc.src, pc.bytes);
+    });
+}
 
 // A host <-> staging-slot transfer of one chunk: `bytes` at byte offset `off`
 // of a slot, from or to `host`.
@@ -221,7 +236,7 @@ struct sdp_ctx {
     hipEvent_t d2h_done[2] = {nullptr, nullptr};
     bool bin_used[2] = {false, false};
     std::vector<Xfer> pending_out[2];
-    CopyPool *copier = nullptr;
+    HostPool *copier = nullptr;
     double *partials = nullptr;
     int64_t partials_cap = 0;
     float *gbar = nullptr;
@@ -231,6 +246,9 @@ struct sdp_ctx {
     int update_max_blocks = 0;     // 0: one 8-element group per lane
     bool timing = false;
     std::vector<Timed> timed;
+    // host lanes of the host-update route, timed on the host clock
+    double host_adam_ms = 0.0, host_wait_ms = 0.0;
+    int64_t host_adam_elems = 0;
     std::vector<hipEvent_t> pool;
 };
 
@@ -315,8 +333,8 @@ struct Range {
 bool overlap(const Range &x, const Range &y) { return x.a < y.b && y.a < x.b; }
 
 // Checks every segment of a call; returns R and the per-segment sizes.
-int validate_segments(const sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, MemKind kind, bool grads_only,
-                      int32_t *R_out) {
+int validate_segments(const sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, MemKind state_kind,
+                      MemKind grad_kind, bool grads_only, int32_t *R_out) {
     if (!segs || n_segs < 1) return fail(SDP_ERR_INVALID_ARGUMENT, "need at least one segment");
     int32_t R = segs[0].n_ranks;
     if (R < 1 || R > SDP_MAX_RANKS)
@@ -351,6 +369,7 @@ int validate_segments(const sdp_ctx *ctx, const sdp_segment *segs, int32_t n_seg
         }
         for (size_t k = 0; k < bufs.size(); ++k) {
             const Buf &b = bufs[k];
+            const MemKind kind = k < n_state ? state_kind : grad_kind;
             SDP_TRY(kind == kDeviceMem   ? check_device_ptr(ctx, b.p, b.bytes, b.what, s)
                     : kind == kPinnedHost ? check_pinned_ptr(b.p, b.bytes, b.what, s)
                                           : check_host_ptr(b.p, b.what, s));
@@ -635,9 +654,9 @@ int copy_in(sdp_ctx *ctx, int sl, const std::vector<Xfer> &xs) {
     }
     char *bin = ctx->bounce_in + (size_t)sl * ctx->slot_bytes;
     if (ctx->bin_used[sl]) HIP_TRY(hipEventSynchronize(ctx->h2d_done[sl]));
-    std::vector<CopyPool::Job> jobs;
+    std::vector<Job> jobs;
     for (const Xfer &x : xs) jobs.push_back({bin + x.off, x.host, x.bytes});
-    ctx->copier->copy(jobs);
+    pool_jobs(ctx->copier, jobs);
     for (const Xfer &r : merge_runs(xs))
         HIP_TRY(hipMemcpyAsync(dev + r.off, bin + r.off, r.bytes, hipMemcpyHostToDevice, ctx->s_copy));
     ctx->bin_used[sl] = true;
@@ -668,9 +687,9 @@ int drain(sdp_ctx *ctx, int sl) {
     if (ctx->pending_out[sl].empty()) return SDP_OK;
     HIP_TRY(hipEventSynchronize(ctx->d2h_done[sl]));
     char *bout = ctx->bounce_out + (size_t)sl * 14 * (size_t)ctx->max_chunk;
-    std::vector<CopyPool::Job> jobs;
+    std::vector<Job> jobs;
     for (const Xfer &x : ctx->pending_out[sl]) jobs.push_back({x.host, bout + x.off, x.bytes});
-    ctx->copier->copy(jobs);
+    pool_jobs(ctx->copier, jobs);
     ctx->pending_out[sl].clear();
     return SDP_OK;
 }
@@ -744,14 +763,18 @@ int stream_update_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t R, const 
     return SDP_OK;
 }
 
+// Host threads of a context: SDP_STAGING_THREADS, else the hardware
+// threads, at most 16 (the calling thread counts as one of them).
+int default_host_threads() {
+    int threads = (int)std::min(16u, std::max(1u, std::thread::hardware_concurrency()));
+    if (const char *env = std::getenv("SDP_STAGING_THREADS")) threads = std::max(1, std::min(256, std::atoi(env)));
+    return threads;
+}
+
 // The host threads and pinned bounce buffers, created on first use by a
 // context that was not created for the staged mode.
 int ensure_host_staging(sdp_ctx *ctx) {
-    if (!ctx->copier) {
-        int threads = (int)std::min(16u, std::max(1u, std::thread::hardware_concurrency()));
-        if (const char *env = std::getenv("SDP_STAGING_THREADS")) threads = std::max(1, std::min(64, std::atoi(env)));
-        ctx->copier = new CopyPool(threads - 1);
-    }
+    if (!ctx->copier) ctx->copier = new HostPool(default_host_threads() - 1);
     if (!ctx->bounce_in) {
         if (hipHostMalloc(&ctx->bounce_in, 2 * ctx->slot_bytes, hipHostMallocDefault) != hipSuccess) {
             (void)hipGetLastError();
@@ -759,6 +782,122 @@ int ensure_host_staging(sdp_ctx *ctx) {
             return fail(SDP_ERR_OUT_OF_MEMORY, "cannot allocate %zu bytes of pinned bounce buffers", 2 * ctx->slot_bytes);
         }
         ctx->bin_used[0] = ctx->bin_used[1] = false;
+    }
+    return SDP_OK;
+}
+
+// ---- host-update route -------------------------------------------------------
+
+sdp_host::AdamConsts host_consts(const sdp_adamw_params *hp, double clip) {
+    sdp::UpdateArgs u{};
+    fill_consts(hp, u);
+    sdp_host::AdamConsts k;
+    k.c = clip;
+    k.lr_wd = u.lr_wd;
+    k.beta1 = u.beta1;
+    k.one_minus_beta1 = u.one_minus_beta1;
+    k.beta2 = u.beta2;
+    k.one_minus_beta2 = u.one_minus_beta2;
+    k.step_size = u.step_size;
+    k.inv_bc2 = u.inv_bc2;
+    k.eps = u.eps;
+    return k;
+}
+
+// Instruction set of the host update: the CPU's best unless SDP_HOST_SIMD=0.
+int host_simd() {
+    if (const char *env = std::getenv("SDP_HOST_SIMD"))
+        if (std::atoi(env) == 0) return sdp_host::kScalar;
+    return sdp_host::simd_best();
+}
+
+// Host AdamW over n elements, in 32,768-element pieces over the pool's
+// threads (on the calling thread alone when pool is NULL).
+void host_adamw(HostPool *pool, const sdp_host::AdamArgs &a, const sdp_host::AdamConsts &k, int64_t n) {
+    constexpr int64_t kPiece = 32768;
+    const int simd = host_simd();
+    const size_t pieces = (size_t)cdiv(n, kPiece);
+    auto body = [&](size_t j) {
+        const int64_t i0 = (int64_t)j * kPiece;
+        sdp_host::adamw_range(a, k, i0, std::min(n, i0 + kPiece), simd);
+    };
+    if (pool)
+        pool->run(pieces, body);
+    else
+        for (size_t j = 0; j < pieces; ++j) body(j);
+}
+
+using Clock = std::chrono::steady_clock;
+
+double ms_between(Clock::time_point a, Clock::time_point b) {
+    return std::chrono::duration<double, std::milli>(b - a).count();
+}
+
+// The host-update route over validated segments (grads in device memory,
+// states in host memory).  Phase 1: the norm pass over the device gradients
+// and the finalize; the norm state comes back to the host.  Phase 2, chunk
+// by chunk: the GPU writes g_bar of chunk j (FP32 or BF16) into device slot
+// j%2 on the compute stream, the copy stream moves it into pinned host buffer
+// j%2, and the host threads update chunk j-1 from the other buffer meanwhile.
+int host_route(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R, const Plan &plan,
+               const sdp_adamw_params *hp, int64_t C, bool bf16, double *grad_norm_out) {
+    hipStream_t sc = ctx->s_comp, sy = ctx->s_copy;
+    SDP_TRY(device_norm(ctx, segs, n_segs, R, plan, false, hp->max_grad_norm, sc));
+    NormState st{};
+    SDP_TRY(read_norm(ctx, sc, &st));
+    if (grad_norm_out) *grad_norm_out = st.norm;
+    if (st.nonfinite) return fail(SDP_ERR_NONFINITE, "gradient norm is not finite (%g); nothing was updated", st.norm);
+    const sdp_host::AdamConsts k = host_consts(hp, st.clip);
+    const std::vector<Chunk> chunks = make_chunks(segs, n_segs, C);
+    const size_t esz = bf16 ? 2 : 4;
+    bool used[2] = {false, false};
+    auto issue = [&](size_t j) -> int {
+        const Chunk &c = chunks[j];
+        const int sl = (int)(j & 1);
+        char *dev = ctx->staging + (size_t)sl * ctx->slot_bytes;
+        char *host = ctx->bounce_in + (size_t)sl * ctx->slot_bytes;
+        // the slot's previous copy to the host has read it
+        if (used[sl]) HIP_TRY(hipStreamWaitEvent(sc, ctx->slot_free[sl], 0));
+        sdp::GbarArgs a{};
+        for (int32_t r = 0; r < R; ++r) a.g[r] = segs[c.seg].grads[r] + c.off;
+        a.n = c.len;
+        a.out = dev;
+        a.bf16 = bf16 ? 1 : 0;
+        hipEvent_t t0 = timed_begin(ctx, sc);
+        HIP_TRY(sdp::launch_gbar_out(R, a, sc));
+        timed_end(ctx, sc, t0, kGbar, c.len);
+        // h2d_done doubles as "g_bar of this slot is written" here
+        HIP_TRY(hipEventRecord(ctx->h2d_done[sl], sc));
+        HIP_TRY(hipStreamWaitEvent(sy, ctx->h2d_done[sl], 0));
+        HIP_TRY(hipMemcpyAsync(host, dev, (size_t)c.len * esz, hipMemcpyDeviceToHost, sy));
+        HIP_TRY(hipEventRecord(ctx->slot_free[sl], sy));  // in the host buffer; the slot is free
+        used[sl] = true;
+        return SDP_OK;
+    };
+    if (!chunks.empty()) SDP_TRY(issue(0));
+    for (size_t j = 0; j < chunks.size(); ++j) {
+        // the next chunk's kernel and copy run while the host updates this one
+        if (j + 1 < chunks.size()) SDP_TRY(issue(j + 1));
+        const int sl = (int)(j & 1);
+        const Clock::time_point t0 = Clock::now();
+        HIP_TRY(hipEventSynchronize(ctx->slot_free[sl]));
+        const Clock::time_point t1 = Clock::now();
+        const Chunk &c = chunks[j];
+        const sdp_segment &g = segs[c.seg];
+        sdp_host::AdamArgs a;
+        a.p = g.master + c.off;
+        a.m = g.exp_avg + c.off;
+        a.v = g.exp_avg_sq + c.off;
+        a.pb = g.param_bf16 + c.off;
+        a.gbar = ctx->bounce_in + (size_t)sl * ctx->slot_bytes;
+        a.gbar_bf16 = bf16 ? 1 : 0;
+        host_adamw(ctx->copier, a, k, c.len);
+        if (ctx->timing) {
+            const Clock::time_point t2 = Clock::now();
+            ctx->host_wait_ms += ms_between(t0, t1);
+            ctx->host_adam_ms += ms_between(t1, t2);
+            ctx->host_adam_elems += c.len;
+        }
     }
     return SDP_OK;
 }
@@ -785,8 +924,8 @@ int stream_common_checks(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, 
     if (chunk > ctx->max_chunk)
         return fail(SDP_ERR_CHUNK_TOO_LARGE, "chunk_elems %lld exceeds the context's %lld", (long long)chunk,
                     (long long)ctx->max_chunk);
-    SDP_TRY(validate_segments(ctx, segs, n_segs, (ctx->flags & SDP_FLAG_STREAM_STAGED) ? kAnyHost : kPinnedHost,
-                              grads_only, R));
+    const MemKind host_kind = (ctx->flags & SDP_FLAG_STREAM_STAGED) ? kAnyHost : kPinnedHost;
+    SDP_TRY(validate_segments(ctx, segs, n_segs, host_kind, host_kind, grads_only, R));
     if (*R > ctx->max_ranks)
         return fail(SDP_ERR_INVALID_ARGUMENT, "n_ranks %d exceeds the context's max_ranks %d", *R, ctx->max_ranks);
     return SDP_OK;
@@ -940,9 +1079,7 @@ int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems, int32_t m
                              2 * (c->slot_bytes + out_bytes)));
         }
         for (int k = 0; k < 2; ++k) CTX_HIP(hipEventCreateWithFlags(&c->d2h_done[k], hipEventDisableTiming));
-        int threads = (int)std::min(16u, std::max(1u, std::thread::hardware_concurrency()));
-        if (const char *env = std::getenv("SDP_STAGING_THREADS")) threads = std::max(1, std::min(64, std::atoi(env)));
-        c->copier = new CopyPool(threads - 1);
+        c->copier = new HostPool(default_host_threads() - 1);
     }
     rc = ensure_partials(c, 4096);
     if (rc != SDP_OK) return bail(rc);
@@ -989,7 +1126,7 @@ int sdp_agg_adam_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, con
     SDP_TRY(check_chunk(chunk_elems, true));
     DeviceGuard guard(ctx->device);
     int32_t R = 0;
-    SDP_TRY(validate_segments(ctx, segs, n_segs, kDeviceMem, false, &R));
+    SDP_TRY(validate_segments(ctx, segs, n_segs, kDeviceMem, kDeviceMem, false, &R));
     const Plan plan = make_plan(segs, n_segs);
     const bool store = device_gbar(ctx, R);
     SDP_TRY(ensure_partials(ctx, plan.tiles));
@@ -1056,7 +1193,7 @@ int sdp_grad_norm(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int dev
     int32_t R = 0;
     NormState st{};
     if (device_resident) {
-        SDP_TRY(validate_segments(ctx, segs, n_segs, kDeviceMem, true, &R));
+        SDP_TRY(validate_segments(ctx, segs, n_segs, kDeviceMem, kDeviceMem, true, &R));
         const Plan p = make_plan(segs, n_segs);
         SDP_TRY(ensure_partials(ctx, p.tiles));
         hipStream_t s = (hipStream_t)stream;
@@ -1114,7 +1251,7 @@ int sdp_cast_bf16_host(sdp_ctx *ctx, const float *src, uint16_t *dst, int64_t n)
     t_err.clear();
     if (!src || !dst || n < 1) return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_cast_bf16_host: bad argument");
     if (ctx && ctx->copier)
-        ctx->copier->copy({{dst, src, (size_t)n, CopyPool::kCastBf16}});
+        pool_jobs(ctx->copier, {{dst, src, (size_t)n, Job::kCastBf16}});
     else
         cast_bf16_host(src, dst, (size_t)n);
     return SDP_OK;
@@ -1154,7 +1291,7 @@ int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf1
                 rc = fail(SDP_ERR_HIP, "sdp_deliver_params: event wait failed");
                 break;
             }
-            ctx->copier->copy({{bin, host_master + off, (size_t)len, CopyPool::kCastBf16}});
+            pool_jobs(ctx->copier, {{bin, host_master + off, (size_t)len, Job::kCastBf16}});
             if (hipMemcpyAsync(dev_bf16 + off, bin, (size_t)len * 2, hipMemcpyHostToDevice, ctx->s_copy) != hipSuccess ||
                 hipEventRecord(ctx->h2d_done[sl], ctx->s_copy) != hipSuccess)
                 rc = fail(SDP_ERR_HIP, "sdp_deliver_params: copy enqueue failed");
@@ -1175,7 +1312,7 @@ int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf1
                     rc = fail(SDP_ERR_HIP, "sdp_deliver_params: event wait failed");
                     break;
                 }
-                ctx->copier->copy({{bin, host_master + off, (size_t)len * 4}});
+                pool_jobs(ctx->copier, {{bin, host_master + off, (size_t)len * 4}});
                 if (hipMemcpyAsync(slot.p, bin, (size_t)len * 4, hipMemcpyHostToDevice, ctx->s_copy) != hipSuccess)
                     rc = fail(SDP_ERR_HIP, "sdp_deliver_params: copy enqueue failed");
                 ctx->bin_used[sl] = true;
@@ -1195,6 +1332,106 @@ int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf1
     return mark_done(ctx, ctx->s_comp);
 }
 
+int sdp_host_update_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, const sdp_adamw_params *hp,
+                         int64_t chunk_elems, int gbar_format, double *grad_norm_out) {
+    t_err.clear();
+    if (!ctx) return fail(SDP_ERR_INVALID_ARGUMENT, "context is NULL");
+    SDP_TRY(check_hparams(hp));
+    if (gbar_format != SDP_GBAR_F32 && gbar_format != SDP_GBAR_BF16)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_host_update_step: unknown gradient format %d", gbar_format);
+    if (!ctx->staging) return fail(SDP_ERR_CHUNK_TOO_LARGE, "context was created without streamed-mode staging");
+    SDP_TRY(check_chunk(chunk_elems, false));
+    if (chunk_elems > ctx->max_chunk)
+        return fail(SDP_ERR_CHUNK_TOO_LARGE, "chunk_elems %lld exceeds the context's %lld", (long long)chunk_elems,
+                    (long long)ctx->max_chunk);
+    DeviceGuard guard(ctx->device);
+    int32_t R = 0;
+    SDP_TRY(validate_segments(ctx, segs, n_segs, kAnyHost, kDeviceMem, false, &R));
+    const Plan plan = make_plan(segs, n_segs);
+    SDP_TRY(ensure_partials(ctx, plan.tiles));
+    SDP_TRY(ensure_host_staging(ctx));
+    SDP_TRY(order_after_last(ctx, ctx->s_comp));
+    SDP_TRY(order_after_last(ctx, ctx->s_copy));
+    const int rc = host_route(ctx, segs, n_segs, R, plan, hp, chunk_elems, gbar_format == SDP_GBAR_BF16,
+                              grad_norm_out);
+    // nothing of this call may still read the caller's gradients on return
+    const std::string err = t_err;
+    const int rc2 = sync_streams(ctx);
+    if (rc != SDP_OK) {
+        t_err = err;
+        return rc;
+    }
+    if (rc2 != SDP_OK) return rc2;
+    return mark_done(ctx, ctx->s_comp);
+}
+
+int sdp_host_adamw(sdp_ctx *ctx, float *master, float *exp_avg, float *exp_avg_sq, uint16_t *param_bf16,
+                   const void *gbar, int gbar_format, int64_t n, double clip_coef, const sdp_adamw_params *hp) {
+    t_err.clear();
+    if (!master || !exp_avg || !exp_avg_sq || !param_bf16 || !gbar || n < 1)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_host_adamw: NULL buffer or n < 1");
+    if (gbar_format != SDP_GBAR_F32 && gbar_format != SDP_GBAR_BF16)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_host_adamw: unknown gradient format %d", gbar_format);
+    if (!std::isfinite(clip_coef) || clip_coef < 0.0)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_host_adamw: clip_coef must be finite and >= 0");
+    SDP_TRY(check_hparams(hp));
+    const size_t gb = (size_t)n * (gbar_format == SDP_GBAR_BF16 ? 2 : 4);
+    const Range rs[5] = {{(uintptr_t)master, (uintptr_t)master + (size_t)n * 4, 0, "master"},
+                         {(uintptr_t)exp_avg, (uintptr_t)exp_avg + (size_t)n * 4, 0, "exp_avg"},
+                         {(uintptr_t)exp_avg_sq, (uintptr_t)exp_avg_sq + (size_t)n * 4, 0, "exp_avg_sq"},
+                         {(uintptr_t)param_bf16, (uintptr_t)param_bf16 + (size_t)n * 2, 0, "param_bf16"},
+                         {(uintptr_t)gbar, (uintptr_t)gbar + gb, 0, "gbar"}};
+    for (int x = 0; x < 5; ++x) {
+        if (rs[x].a % SDP_ALIGN != 0)
+            return fail(SDP_ERR_ALIGNMENT, "sdp_host_adamw: %s is not %d-byte aligned", rs[x].what, SDP_ALIGN);
+        for (int y = 0; y < x; ++y)
+            if (overlap(rs[x], rs[y]))
+                return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_host_adamw: %s overlaps %s", rs[x].what, rs[y].what);
+    }
+    if (ctx && !ctx->copier) ctx->copier = new HostPool(default_host_threads() - 1);
+    sdp_host::AdamArgs a;
+    a.p = master;
+    a.m = exp_avg;
+    a.v = exp_avg_sq;
+    a.pb = param_bf16;
+    a.gbar = gbar;
+    a.gbar_bf16 = gbar_format == SDP_GBAR_BF16 ? 1 : 0;
+    host_adamw(ctx ? ctx->copier : nullptr, a, host_consts(hp, clip_coef), n);
+    return SDP_OK;
+}
+
+int sdp_probe_host_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, int32_t reps, double *gbs_out) {
+    t_err.clear();
+    if (!ctx || !dst || !src || bytes < 1 || reps < 1 || !gbs_out)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_probe_host_copy: bad argument");
+    const uintptr_t a = (uintptr_t)dst, b = (uintptr_t)src;
+    if (a < b + (size_t)bytes && b < a + (size_t)bytes)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_probe_host_copy: dst and src overlap");
+    if (!ctx->copier) ctx->copier = new HostPool(default_host_threads() - 1);
+    const Clock::time_point t0 = Clock::now();
+    for (int32_t r = 0; r < reps; ++r) pool_jobs(ctx->copier, {{dst, src, (size_t)bytes}});
+    const double s = ms_between(t0, Clock::now()) / 1e3;
+    *gbs_out = 2.0 * (double)bytes * reps / s / 1e9;
+    return SDP_OK;
+}
+
+int sdp_ctx_set_host_threads(sdp_ctx *ctx, int32_t threads) {
+    t_err.clear();
+    if (!ctx) return fail(SDP_ERR_INVALID_ARGUMENT, "context is NULL");
+    if (threads < 1 || threads > 256)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "host threads must be in 1..256 (got %d)", threads);
+    delete ctx->copier;
+    ctx->copier = new HostPool(threads - 1);
+    return SDP_OK;
+}
+
+int sdp_ctx_host_threads(sdp_ctx *ctx, int32_t *threads_out) {
+    t_err.clear();
+    if (!ctx || !threads_out) return fail(SDP_ERR_INVALID_ARGUMENT, "context or out is NULL");
+    *threads_out = ctx->copier ? ctx->copier->size() : default_host_threads();
+    return SDP_OK;
+}
+
 int sdp_ctx_set_timing(sdp_ctx *ctx, int enable) {
     t_err.clear();
     if (!ctx) return fail(SDP_ERR_INVALID_ARGUMENT, "context is NULL");
@@ -1206,6 +1443,8 @@ int sdp_ctx_set_timing(sdp_ctx *ctx, int enable) {
             ctx->pool.push_back(t.b);
         }
         ctx->timed.clear();
+        ctx->host_adam_ms = ctx->host_wait_ms = 0.0;
+        ctx->host_adam_elems = 0;
     }
     ctx->timing = enable != 0;
     return SDP_OK;
@@ -1226,12 +1465,18 @@ int sdp_ctx_get_timing(sdp_ctx *ctx, sdp_kernel_times *out) {
         } else if (t.kind == kFinalize) {
             r.finalize_ms += ms;
             r.finalize_launches++;
+        } else if (t.kind == kGbar) {
+            r.gbar_ms += ms;
+            r.gbar_launches++;
         } else {
             r.update_ms += ms;
             r.update_launches++;
             r.update_elems += t.elems;
         }
     }
+    r.host_adam_ms = ctx->host_adam_ms;
+    r.host_wait_ms = ctx->host_wait_ms;
+    r.host_adam_elems = ctx->host_adam_elems;
     *out = r;
     return SDP_OK;
 }

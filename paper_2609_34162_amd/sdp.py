@@ -32,6 +32,8 @@ SDP_FLAG_DEBUG_POISON = 0x8
 SDP_FLAG_STREAM_STAGED = 0x10
 SDP_DELIVER_HOST_CAST = 0
 SDP_DELIVER_DEVICE_CAST = 1
+SDP_GBAR_F32 = 0
+SDP_GBAR_BF16 = 1
 
 
 class SdpError(RuntimeError):
@@ -64,7 +66,9 @@ class sdp_kernel_times(ctypes.Structure):
     _fields_ = [("norm_ms", ctypes.c_double), ("finalize_ms", ctypes.c_double),
                 ("update_ms", ctypes.c_double), ("norm_launches", ctypes.c_int64),
                 ("finalize_launches", ctypes.c_int64), ("update_launches", ctypes.c_int64),
-                ("update_elems", ctypes.c_int64)]
+                ("update_elems", ctypes.c_int64), ("gbar_ms", ctypes.c_double),
+                ("gbar_launches", ctypes.c_int64), ("host_adam_ms", ctypes.c_double),
+                ("host_wait_ms", ctypes.c_double), ("host_adam_elems", ctypes.c_int64)]
 
 
 def _load():
@@ -83,6 +87,12 @@ def _load():
         "sdp_cast_bf16": (ctypes.c_int, [vp, vp, vp, i64, vp]),
         "sdp_deliver_params": (ctypes.c_int, [vp, vp, vp, i64, i64, ctypes.c_int]),
         "sdp_cast_bf16_host": (ctypes.c_int, [vp, vp, vp, i64]),
+        "sdp_host_update_step": (ctypes.c_int, [vp, vp, i32, P(sdp_adamw_params), i64, ctypes.c_int, P(dbl)]),
+        "sdp_host_adamw": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, ctypes.c_int, i64, dbl,
+                                           P(sdp_adamw_params)]),
+        "sdp_ctx_set_host_threads": (ctypes.c_int, [vp, i32]),
+        "sdp_probe_host_copy": (ctypes.c_int, [vp, vp, vp, i64, i32, P(dbl)]),
+        "sdp_ctx_host_threads": (ctypes.c_int, [vp, P(i32)]),
         "sdp_plan": (ctypes.c_int, [vp, i32, i64, P(i64), P(i64)]),
         "sdp_bytes_per_elem": (ctypes.c_int, [ctypes.c_int, i32, ctypes.c_uint32, P(dbl), P(dbl)]),
         "sdp_ctx_set_timing": (ctypes.c_int, [vp, ctypes.c_int]),
@@ -215,6 +225,37 @@ def sdp_deliver_params(ctx, host_master: int, dev_bf16: int, n: int, chunk_elems
 
 def sdp_cast_bf16_host(ctx, src: int, dst: int, n: int) -> None:
     _check(_lib.sdp_cast_bf16_host(ctx, src, dst, n))
+
+
+def sdp_host_update_step(ctx, segs: Segments, hp: sdp_adamw_params, chunk_elems: int,
+                         gbar_format: int = SDP_GBAR_F32) -> float:
+    norm = ctypes.c_double(float("nan"))
+    rc = _lib.sdp_host_update_step(ctx, segs.ptr, segs.n, ctypes.byref(hp), chunk_elems, gbar_format,
+                                   ctypes.byref(norm))
+    _check(rc, norm.value)
+    return norm.value
+
+
+def sdp_host_adamw(ctx, master: int, exp_avg: int, exp_avg_sq: int, param_bf16: int, gbar: int,
+                   gbar_format: int, n: int, clip_coef: float, hp: sdp_adamw_params) -> None:
+    _check(_lib.sdp_host_adamw(ctx, master, exp_avg, exp_avg_sq, param_bf16, gbar, gbar_format, n,
+                               clip_coef, ctypes.byref(hp)))
+
+
+def sdp_probe_host_copy(ctx, dst: int, src: int, nbytes: int, reps: int) -> float:
+    g = ctypes.c_double()
+    _check(_lib.sdp_probe_host_copy(ctx, dst, src, nbytes, reps, ctypes.byref(g)))
+    return g.value
+
+
+def sdp_ctx_set_host_threads(ctx, threads: int) -> None:
+    _check(_lib.sdp_ctx_set_host_threads(ctx, threads))
+
+
+def sdp_ctx_host_threads(ctx) -> int:
+    t = ctypes.c_int32()
+    _check(_lib.sdp_ctx_host_threads(ctx, ctypes.byref(t)))
+    return t.value
 
 
 def sdp_plan(numels: Sequence[int], chunk_elems: int) -> Tuple[int, int]:

@@ -1,7 +1,9 @@
 """GPU parity at the full workload sizes, in the launch configuration bench.py
 times: one Qwen3-8B layer (192,946,176 params, R = 4, 10 steps) and one
 Qwen2.5-72B layer (877,674,496 params, R = 8, 3 steps) in device mode, and one
-Qwen3-14B layer (330,311,680 params, R = 4, 5 steps) in streamed mode.
+Qwen3-14B layer (330,311,680 params, R = 4, 5 steps) in streamed mode and on
+the host-update route (FP32 mean gradient, 5 steps; BF16 mean gradient, 3
+steps; pageable host states, gradients in device memory).
 
 Every element of every output is compared with the oracle at every step,
 teacher-forced (the oracle steps from the GPU's state before the step) and,
@@ -17,7 +19,8 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import (DevState, HostState, check_norm, check_state, log, need_gpu, states_equal, torch)
+from gpu_util import (DevState, HostState, PageableState, check_norm, check_state, log, need_gpu, states_equal,
+                      torch)
 
 pytestmark = [pytest.mark.gpu, pytest.mark.big]
 
@@ -189,6 +192,57 @@ def test_qwen3_14b_layer_device_equals_streamed(sdp):
             hstate.master, hstate.exp_avg, hstate.exp_avg_sq, hstate.param_bf16 = host.p, host.m, host.v, host.pb
             assert states_equal(got, hstate), f"device and streamed modes differ at step {t}"
             log(f"  step {t}: device == streamed, norm {dn:.9g}")
+    finally:
+        sdp.sdp_ctx_destroy(ctx)
+        host.close()
+        pin.close()
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("fmt", ["f32", "bf16"])
+def test_qwen3_14b_layer_host_route_full(sdp, fmt):
+    w = synth.workload(2)
+    n, R = w.numel, w.ranks
+    steps = w.steps if fmt == "f32" else 3
+    bf = fmt == "bf16"
+    log(f"full host route {w.name} fmt={fmt}: N={n} R={R} chunk={w.chunk} steps={steps}")
+    t0 = time.time()
+    master = synth.master(w, 0)
+    host = PageableState(sdp, [master], R)
+    devg = [torch.empty(n, dtype=torch.int16, device="cuda") for _ in range(R)]
+    ctx = sdp.sdp_ctx_create(0, w.chunk, R, 0)
+    pin = Pinned(sdp)
+    try:
+        before = pin.state([n])
+        forced = oracle.State([np.zeros(n, np.float32)])
+        ref = oracle.State([master])
+        del master
+        segs = sdp.Segments([(host.p[0].ctypes.data, host.m[0].ctypes.data, host.v[0].ctypes.data,
+                              host.pb[0].ctypes.data, [g.data_ptr() for g in devg], n)])
+        for t in range(1, steps + 1):
+            gen_grads(w, t, host.g)
+            for r in range(R):
+                devg[r].copy_(torch.from_numpy(host.g[0][r].view(np.int16)))
+            torch.cuda.synchronize()
+            for a, b in ((before.master, host.p), (before.exp_avg, host.m), (before.exp_avg_sq, host.v),
+                         (before.param_bf16, host.pb)):
+                np.copyto(a[0], b[0])
+            ts = time.time()
+            norm = sdp.sdp_host_update_step(ctx, segs, sdp.make_params(**w.hparams(t)), w.chunk,
+                                            sdp.SDP_GBAR_BF16 if bf else sdp.SDP_GBAR_F32)
+            step_s = time.time() - ts
+            after = oracle.State.__new__(oracle.State)
+            after.master, after.exp_avg, after.exp_avg_sq, after.param_bf16 = host.p, host.m, host.v, host.pb
+            copy_state(forced, before)
+            rc, fnorm = oracle.step(forced, host.g, oracle.hparams(**w.hparams(t)), gbar_bf16=bf)
+            assert rc == oracle.ORC_OK
+            check_norm(norm, fnorm)
+            assert norm == fnorm
+            stats = check_state(after, forced)
+            oracle.step(ref, host.g, oracle.hparams(**w.hparams(t)), gbar_bf16=bf)
+            stats_free = check_state(after, ref)
+            log(f"  step {t}: route {step_s:.3f} s, norm {norm:.9g} forced {stats['master0']} "
+                f"free {stats_free['master0']}  {time.time() - t0:.0f}s")
     finally:
         sdp.sdp_ctx_destroy(ctx)
         host.close()

@@ -1,0 +1,196 @@
+"""GPU parity of the host-update route (sdp_host_update_step): the R rank
+gradients in device memory, the states in host memory (pageable or pinned),
+the GPU's norm pass and mean-gradient kernel, chunked copies to the host and
+the host threads' AdamW, against the oracle -- with the FP32 mean gradient
+(the oracle's plain step) and with the mean gradient rounded to BF16 (the
+oracle's BF16-gradient variant).  Criteria as in test_gpu_parity.py.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_util import (DevState, HostState, PageableState, check_norm, check_state, hp_pair, log, need_gpu,
+                      rand_inputs, states_equal, to_dev_u16, torch)
+
+pytestmark = pytest.mark.gpu
+
+TILE = 65536
+
+
+@pytest.fixture(scope="module")
+def sdp():
+    return need_gpu()
+
+
+@pytest.fixture(scope="module")
+def ctx(sdp):
+    c = sdp.sdp_ctx_create(0, 4 * TILE, 16, 0)
+    yield c
+    sdp.sdp_ctx_destroy(c)
+
+
+class RouteState:
+    """Host states (pageable numpy arrays, or pinned buffers) and the rank
+    gradients on the GPU."""
+
+    def __init__(self, sdp, masters, R, pinned=False):
+        self.host = HostState(sdp, masters, R) if pinned else PageableState(sdp, masters, R)
+        self.g = [[torch.zeros(m.size, dtype=torch.int16, device="cuda") for _ in range(R)] for m in masters]
+
+    def set_grads(self, grads):
+        for s, gs in enumerate(grads):
+            for r, g in enumerate(gs):
+                self.g[s][r].copy_(to_dev_u16(g))
+        torch.cuda.synchronize()
+
+    def segments(self, sdp):
+        h = self.host
+        return sdp.Segments([(h.p[s].ctypes.data, h.m[s].ctypes.data, h.v[s].ctypes.data, h.pb[s].ctypes.data,
+                              [g.data_ptr() for g in self.g[s]], h.p[s].size) for s in range(len(h.p))])
+
+    def state(self):
+        return self.host.host()
+
+    def close(self):
+        self.host.close()
+
+
+def fmt_of(sdp, name):
+    return sdp.SDP_GBAR_BF16 if name == "bf16" else sdp.SDP_GBAR_F32
+
+
+@pytest.mark.parametrize("fmt", ["f32", "bf16"])
+@pytest.mark.parametrize("chunk_tiles", [1, 3])
+@pytest.mark.parametrize("pinned", [False, True])
+def test_host_route_matches_oracle(sdp, ctx, fmt, chunk_tiles, pinned):
+    sizes = [3 * TILE + 5, 1, 70000, 2 * TILE]
+    R = 3
+    steps = 3
+    masters, grads = rand_inputs(sizes, R, steps, seed=61 + chunk_tiles)
+    log(f"host route fmt={fmt} chunk={chunk_tiles} tiles pinned={pinned}")
+    st = RouteState(sdp, masters, R, pinned=pinned)
+    ref = oracle.State(masters)
+    try:
+        for t in range(1, steps + 1):
+            hs, ho = hp_pair(sdp, lr=1e-3, weight_decay=0.05, max_grad_norm=0.2, step=t)
+            st.set_grads(grads[t - 1])
+            norm = sdp.sdp_host_update_step(ctx, st.segments(sdp), hs, chunk_tiles * TILE, fmt_of(sdp, fmt))
+            _, onorm = oracle.step(ref, grads[t - 1], ho, gbar_bf16=(fmt == "bf16"))
+            check_norm(norm, onorm)
+            assert norm == onorm, "the norm is the exactly rounded one in every mode"
+            check_state(st.state(), ref)
+    finally:
+        st.close()
+
+
+@pytest.mark.parametrize("R", [1, 2, 4, 8, 16])
+def test_host_route_ranks_against_device_mode(sdp, ctx, R):
+    """FP32 route and device mode: same norm bits, both within the criteria
+    of the oracle."""
+    sizes = [2 * TILE + 17]
+    masters, grads = rand_inputs(sizes, R, 2, seed=70 + R)
+    st = RouteState(sdp, masters, R)
+    dev = DevState(masters, R)
+    ref = oracle.State(masters)
+    try:
+        for t in (1, 2):
+            hs, ho = hp_pair(sdp, lr=2e-3, weight_decay=0.01, max_grad_norm=0.1, step=t)
+            st.set_grads(grads[t - 1])
+            dev.set_grads(grads[t - 1])
+            hn = sdp.sdp_host_update_step(ctx, st.segments(sdp), hs, TILE, sdp.SDP_GBAR_F32)
+            dn = sdp.sdp_agg_adam_step(ctx, dev.segments(sdp), hs, 0, torch.cuda.current_stream().cuda_stream,
+                                       want_norm=True)
+            torch.cuda.synchronize()
+            oracle.step(ref, grads[t - 1], ho)
+            assert hn == dn
+            check_state(st.state(), ref)
+            check_state(dev.host(), ref)
+    finally:
+        st.close()
+
+
+def test_host_route_threads_and_simd_give_same_bits(sdp, ctx):
+    sizes = [3 * TILE + 3, 999]
+    R = 4
+    masters, grads = rand_inputs(sizes, R, 1, seed=81)
+    hs = sdp.make_params(lr=1e-3, weight_decay=0.1, max_grad_norm=0.5, step=1)
+    outs = []
+    saved = sdp.sdp_ctx_host_threads(ctx)
+    try:
+        for threads, simd in ((1, None), (5, None), (16, None), (3, "0")):
+            sdp.sdp_ctx_set_host_threads(ctx, threads)
+            assert sdp.sdp_ctx_host_threads(ctx) == threads
+            if simd is not None:
+                os.environ["SDP_HOST_SIMD"] = simd
+            st = RouteState(sdp, masters, R)
+            try:
+                st.set_grads(grads[0])
+                sdp.sdp_host_update_step(ctx, st.segments(sdp), hs, 2 * TILE, sdp.SDP_GBAR_BF16)
+                outs.append(st.state())
+            finally:
+                st.close()
+                os.environ.pop("SDP_HOST_SIMD", None)
+    finally:
+        sdp.sdp_ctx_set_host_threads(ctx, saved)
+    for o in outs[1:]:
+        assert states_equal(outs[0], o)
+
+
+@pytest.mark.parametrize("bad", [np.nan, np.inf])
+def test_host_route_nonfinite_leaves_states_unchanged(sdp, ctx, bad):
+    sizes = [TILE + 9]
+    R = 2
+    masters, grads = rand_inputs(sizes, R, 1, seed=91)
+    g = [[x.copy() for x in grads[0][0]]]
+    g[0][1][4321] = synth.to_bf16_bits(np.array([bad], np.float32))[0]
+    st = RouteState(sdp, masters, R)
+    try:
+        st.host.pb[0][:] = 7
+        st.set_grads(g)
+        before = st.state()
+        with pytest.raises(sdp.SdpNonFinite) as e:
+            sdp.sdp_host_update_step(ctx, st.segments(sdp), sdp.make_params(step=1), TILE, sdp.SDP_GBAR_F32)
+        assert not np.isfinite(e.value.norm)
+        assert states_equal(before, st.state())
+    finally:
+        st.close()
+
+
+def test_host_route_argument_errors(sdp, ctx):
+    n, R = 4096, 2
+    masters, grads = rand_inputs([n], R, 1, seed=95)
+    st = RouteState(sdp, masters, R)
+    dev = DevState(masters, R)
+    L = sdp._lib
+    hs = sdp.make_params(step=1)
+    try:
+        st.set_grads(grads[0])
+        dev.set_grads(grads[0])
+        before = st.state()
+        good = st.segments(sdp)
+
+        def call(segs=good, chunk=TILE, fmt=sdp.SDP_GBAR_F32, c=ctx):
+            return L.sdp_host_update_step(c, segs.ptr, segs.n, hs, chunk, fmt, None)
+
+        assert call(fmt=5) == sdp.SDP_ERR_INVALID_ARGUMENT
+        assert call(chunk=TILE + 1) == sdp.SDP_ERR_INVALID_ARGUMENT
+        assert call(chunk=8 * TILE) == sdp.SDP_ERR_CHUNK_TOO_LARGE
+        # states in device memory are refused
+        assert call(segs=dev.segments(sdp)) == sdp.SDP_ERR_INVALID_ARGUMENT
+        assert "device memory" in sdp.sdp_last_error()
+        # gradients in host memory are refused
+        h = st.host
+        host_grads = sdp.Segments([(h.p[0].ctypes.data, h.m[0].ctypes.data, h.v[0].ctypes.data,
+                                    h.pb[0].ctypes.data, [g.ctypes.data for g in h.g[0]], n)])
+        assert call(segs=host_grads) == sdp.SDP_ERR_NOT_DEVICE_MEMORY
+        nostage = sdp.sdp_ctx_create(0, 0, 4, 0)
+        try:
+            assert call(c=nostage) == sdp.SDP_ERR_CHUNK_TOO_LARGE
+        finally:
+            sdp.sdp_ctx_destroy(nostage)
+        assert states_equal(before, st.state())
+    finally:
+        st.close()
