@@ -19,6 +19,10 @@ JSON line also carries:
   delivery (inside streamed) -- BF16 copies of the layer's FP32 master
                    delivered into a device window, rounded on the host or on
                    the GPU, from pinned and pageable memory;
+  chunk_sweep (inside streamed and host_route) -- measured step time at
+                   chunk sizes of 4-128 MiB per FP32 array beside the
+                   library's step-time model fed with rates measured in
+                   the same run, and the chunk each would pick;
   host_route    -- the paper's own datapath for the same Qwen3-14B layer:
                    gradients in HBM, states in pageable host memory, the mean
                    gradient copied down (FP32 or BF16) and AdamW on this
@@ -167,7 +171,77 @@ def cpu_leg(args, np, oracle, master, host_grads, w):
                        f"({w.numel} params, R={w.ranks}), {el:.1f} s")
 
 
-def stream_leg(args, torch, np, synth, sdp):
+SWEEP_CHUNKS = [1 << 20, 1 << 21, 1 << 22, 1 << 23, 1 << 24, 1 << 25]  # 4-128 MiB per FP32 state array
+
+
+def measure_rates(args, torch, np, sdp, ctx, link, dres):
+    """The step-time model's inputs, each measured on this machine: link rates
+    (passed in), the per-command copy cost, the kernels' HBM rates and the
+    launch cost from the device leg, the norm read-back round trip, the host
+    threads' copy bandwidth and their per-hand-off cost."""
+    big, small = 256 << 20, 1 << 20
+    ha, hb = sdp.HostBuffer(big), sdp.HostBuffer(big)
+    da = torch.empty(big, dtype=torch.uint8, device="cuda")
+    db = torch.empty(big, dtype=torch.uint8, device="cuda")
+    per = {}
+    for cb in (small, 64 << 20):
+        gbs = max(sdp.sdp_probe_link(ctx, ha.ptr, hb.ptr, da.data_ptr(), db.data_ptr(), big, cb, 2)[0]
+                  for _ in range(3))
+        per[cb] = (big / (gbs * 1e9), big // cb)
+    copy_cmd_us = max(0.0, (per[small][0] - per[64 << 20][0]) / (per[small][1] - per[64 << 20][1]) * 1e6)
+    del da, db
+    ha.close()
+    hb.close()
+    sdp.sdp_ctx_last_norm(ctx)
+    t0 = time.perf_counter()
+    for _ in range(200):
+        sdp.sdp_ctx_last_norm(ctx)
+    sync_us = (time.perf_counter() - t0) / 200 * 1e6
+    src = np.ones(1 << 28, np.float32)
+    dst = np.empty_like(src)
+    sdp.sdp_probe_host_copy(ctx, dst.ctypes.data, src.ctypes.data, src.nbytes, 1)
+    host_gbs = max(sdp.sdp_probe_host_copy(ctx, dst.ctypes.data, src.ctypes.data, src.nbytes, 2) for _ in range(3))
+    del src, dst
+    # hand-off cost: an 8-element host update through the context's threads
+    x = [np.zeros(64, np.float32) for _ in range(4)]
+    pbuf = np.zeros(64, np.uint16)
+    hp = sdp.make_params(step=1)
+    call = lambda: sdp.sdp_host_adamw(ctx, x[0].ctypes.data, x[1].ctypes.data, x[2].ctypes.data,  # noqa: E731
+                                      pbuf.ctypes.data, x[3].ctypes.data, sdp.SDP_GBAR_F32, 8, 1.0, hp)
+    call()
+    t0 = time.perf_counter()
+    for _ in range(500):
+        call()
+    host_task_us = (time.perf_counter() - t0) / 500 * 1e6
+    kern_ms = dres["update_ms"] + dres["norm_ms"] + dres["finalize_ms"]
+    launch_us = max(0.0, (dres["ms_per_step"] - kern_ms) / 3 * 1e3)
+    vals = dict(h2d_gbs=link[0], d2h_gbs=link[1], both_gbs=link[2], copy_cmd_us=copy_cmd_us,
+                norm_gbs=dres["norm_gbs"], update_gbs=dres["update_gbs"], launch_us=launch_us, sync_us=sync_us,
+                host_gbs=host_gbs, host_task_us=host_task_us)
+    log("model rates: " + ", ".join(f"{k} {v:.1f}" for k, v in vals.items()))
+    return sdp.make_rates(**vals), vals
+
+
+def chunk_sweep(sdp, schedule, numels, R, rates, run_at):
+    """Measured step time at each chunk size beside the model's prediction,
+    and the chunk each would pick."""
+    rows = []
+    for c in SWEEP_CHUNKS:
+        pr = sdp.sdp_predict_step(schedule, numels, R, c, 0, rates)
+        ms = run_at(c)
+        rows.append(dict(chunk_elems=c, measured_ms=ms, predicted_ms=pr.predicted_ms, bound_ms=pr.bound_ms))
+        log(f"  chunk {c >> 20:3d}M: measured {ms:.2f} ms, predicted {pr.predicted_ms:.2f} ms, "
+            f"bound {pr.bound_ms:.2f} ms")
+    best_pred, _ = sdp.sdp_tune_chunk(schedule, numels, R, 0, rates, SWEEP_CHUNKS)
+    best_meas = min(rows, key=lambda r: r["measured_ms"])
+    at_pick = next(r["measured_ms"] for r in rows if r["chunk_elems"] == best_pred)
+    err = [abs(r["predicted_ms"] - r["measured_ms"]) / r["measured_ms"] for r in rows]
+    return dict(rows=rows, model_pick=best_pred, measured_best=best_meas["chunk_elems"],
+                measured_at_model_pick_ms=at_pick, measured_best_ms=best_meas["measured_ms"],
+                mean_abs_rel_error=sum(err) / len(err), max_abs_rel_error=max(err))
+
+
+def stream_leg(args, torch, np, synth, sdp, dres):
     w = synth.workload(2)
     N, R, C = w.numel, w.ranks, w.chunk
     log(f"streamed leg: {w.name} N={N} R={R} chunk={C}; pinning {N * (14 + 2 * R) / 1e9:.2f} GB")
@@ -218,6 +292,7 @@ def stream_leg(args, torch, np, synth, sdp):
         return (time.perf_counter() - t0) / args.stream_steps
 
     el = timed(ctx, segs)
+    rates, rate_vals = measure_rates(args, torch, np, sdp, ctx, link, dres)
     h2d_b, d2h_b = sdp.sdp_bytes_per_elem(True, R, 0)
     t_link = (2 * R * N / (link[0] * 1e9)
               + max(12 * N / (link[0] * 1e9), 14 * N / (link[1] * 1e9), 26 * N / (link[2] * 1e9)))
@@ -225,8 +300,22 @@ def stream_leg(args, torch, np, synth, sdp):
     out = dict(workload=w.name, params=N, ranks=R, chunk_elems=C, ms_per_step=el * 1e3,
                params_per_s=N / el, h2d_gbs=h2d_b * N / el / 1e9, d2h_gbs=d2h_b * N / el / 1e9,
                link_gbs={"h2d": link[0], "d2h": link[1], "bidir": link[2]},
-               t_link_ms=t_link * 1e3, frac_of_link_bound=t_link / el)
+               t_link_ms=t_link * 1e3, frac_of_link_bound=t_link / el, model_rates=rate_vals,
+               predicted_ms=sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, C, 0, rates).predicted_ms)
     if not args.no_extra:
+        log("streamed leg: chunk sweep")
+
+        def run_at(c):
+            cctx = sdp.sdp_ctx_create(0, c, R, 0)
+            try:
+                sdp.sdp_stream_step(cctx, segs, sdp.make_params(**w.hparams(1)), c)
+                t0 = time.perf_counter()
+                for t in (2, 3):
+                    sdp.sdp_stream_step(cctx, segs, sdp.make_params(**w.hparams(t)), c)
+                return (time.perf_counter() - t0) / 2 * 1e3
+            finally:
+                sdp.sdp_ctx_destroy(cctx)
+        out["chunk_sweep"] = chunk_sweep(sdp, sdp.SDP_SCHED_STREAMED, [N], R, rates, run_at)
         # the same step with the states in pageable memory, through the staged mode
         log("streamed leg: staged mode on pageable copies of the same state")
         pg = [np.array(x) for x in (p, m, v, pb)] + [np.array(x) for x in g]
@@ -256,10 +345,10 @@ def stream_leg(args, torch, np, synth, sdp):
         del pg, window
     for hbuf in bufs:
         hbuf.close()
-    return out
+    return out, rates
 
 
-def host_route_leg(args, torch, np, synth, sdp):
+def host_route_leg(args, torch, np, synth, sdp, rates):
     """The paper's own datapath on one GPU: the rank gradients in HBM, the
     states in pageable host memory, the GPU's norm pass and mean gradient,
     chunked copies to the host, and AdamW on this host's cores."""
@@ -318,8 +407,21 @@ def host_route_leg(args, torch, np, synth, sdp):
                          host_adam_ms=kt.host_adam_ms / k, host_wait_ms=kt.host_wait_ms / k,
                          host_adam_gbs=host_bytes / adam_s / 1e9, host_adam_params_per_s=N / adam_s,
                          bound_ms=bound * 1e3, frac_of_bound=bound / el)
+        sched = sdp.SDP_SCHED_HOST_ROUTE_BF16 if fmt == sdp.SDP_GBAR_BF16 else sdp.SDP_SCHED_HOST_ROUTE_F32
+        if rates is not None:
+            out[name]["predicted_ms"] = sdp.sdp_predict_step(sched, [N], R, C, 0, rates).predicted_ms
         log(f"host route leg {name}: {el * 1e3:.1f} ms/step, host AdamW {kt.host_adam_ms / k:.1f} ms "
             f"({host_bytes / adam_s / 1e9:.1f} GB/s), waits {kt.host_wait_ms / k:.1f} ms")
+        if rates is not None and not args.no_extra:
+            log(f"host route leg {name}: chunk sweep")
+
+            def run_at(c, fmt=fmt):
+                sdp.sdp_host_update_step(ctx, segs, sdp.make_params(**w.hparams(1)), c, fmt)
+                t0 = time.perf_counter()
+                for t in (2, 3, 4):
+                    sdp.sdp_host_update_step(ctx, segs, sdp.make_params(**w.hparams(t)), c, fmt)
+                return (time.perf_counter() - t0) / 3 * 1e3
+            out[name]["chunk_sweep"] = chunk_sweep(sdp, sched, [N], R, rates, run_at)
     # core scaling of the host AdamW alone on the same layer (the paper's
     # CPU Adam scaling microbenchmark)
     gb = np.full(N, 1e-3, np.float32)
@@ -381,8 +483,8 @@ def main():
     if not args.no_extra:
         r8_res, _, _, _ = device_leg(args, torch, np, synth, sdp, 4, 10, 2, False)
         r8 = brief(r8_res)
-    streamed = None if args.no_stream else stream_leg(args, torch, np, synth, sdp)
-    route = None if args.no_stream else host_route_leg(args, torch, np, synth, sdp)
+    streamed, rates = (None, None) if args.no_stream else stream_leg(args, torch, np, synth, sdp, dres)
+    route = None if args.no_stream else host_route_leg(args, torch, np, synth, sdp, rates)
 
     traffic = measured_traffic(dres["update_bytes"])
     out = {

@@ -273,6 +273,61 @@ int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf1
  * the work. */
 int sdp_cast_bf16_host(sdp_ctx *ctx, const float *src, uint16_t *dst, int64_t n);
 
+/* ---- step-time model (host only, no GPU needed) --------------------------- */
+
+/* Measured rates that the model takes (each from the library's probes or
+ * kernel timing on the machine to be predicted). */
+typedef struct {
+    double h2d_gbs, d2h_gbs; /* pinned host link, each direction alone (GB/s) */
+    double both_gbs;         /* the same, both directions at once (sum of the two) */
+    double copy_cmd_us;      /* fixed cost of one copy command */
+    double norm_gbs;         /* norm pass and mean-gradient kernel, HBM GB/s */
+    double update_gbs;       /* fused update kernel, HBM GB/s */
+    double launch_us;        /* fixed cost of one kernel */
+    double sync_us;          /* host round trip of the norm read-back */
+    double host_gbs;         /* host threads' memory bandwidth (bytes read + written) */
+    double host_task_us;     /* fixed cost of one hand-off to the host threads */
+} sdp_rates;
+
+/* What the model predicts for one call. */
+typedef struct {
+    double predicted_ms; /* finish time of the modelled schedule */
+    double bound_ms;     /* resource lower bound: the largest of the five below */
+    double h2d_ms, d2h_ms; /* link bytes of each direction / its rate alone */
+    double link_ms;      /* all link bytes / the bidirectional rate */
+    double gpu_ms;       /* sum of the kernels' modelled times */
+    double host_ms;      /* sum of the host-thread tasks' modelled times */
+    int64_t n_chunks;
+} sdp_prediction;
+
+/* Schedules the model covers. */
+#define SDP_SCHED_STREAMED 0        /* sdp_stream_step, pinned host states */
+#define SDP_SCHED_STREAMED_STAGED 1 /* sdp_stream_step with SDP_FLAG_STREAM_STAGED */
+#define SDP_SCHED_HOST_ROUTE_F32 2  /* sdp_host_update_step, SDP_GBAR_F32 */
+#define SDP_SCHED_HOST_ROUTE_BF16 3 /* sdp_host_update_step, SDP_GBAR_BF16 */
+
+/* Step time of one call on segments of the given sizes, R ranks, chunk_elems
+ * and context flags (only the g_bar policy of streamed mode matters).  The
+ * paper's step-time model (Design, step-time model) pairs a resource lower
+ * bound, max_j W_j / beta_j, with a dependency recurrence f(v) = d_v +
+ * max(a_v, f(u) over predecessors u), whose edges are data dependences,
+ * stream order and buffer release.  The model builds that graph for the
+ * library's own issue order -- each copy, kernel and host-thread task on its
+ * stream, each event wait as an edge -- and evaluates it; copies share the
+ * link by a fluid model (a direction alone moves at its own rate, both
+ * directions together at the bidirectional rate, split in proportion). */
+int sdp_predict_step(int schedule, const int64_t *numels, int32_t n_segs, int32_t n_ranks,
+                     int64_t chunk_elems, uint32_t flags, const sdp_rates *rates,
+                     sdp_prediction *out);
+
+/* Chunk tuning (the paper's AutoPolicy tunes chunk sizes; Design, automatic
+ * policy): the candidate (each a positive multiple of SDP_NORM_TILE) with the
+ * smallest predicted step time, the first one on a tie; predicted_ms_out, if
+ * not NULL, receives every candidate's prediction. */
+int sdp_tune_chunk(int schedule, const int64_t *numels, int32_t n_segs, int32_t n_ranks,
+                   uint32_t flags, const sdp_rates *rates, const int64_t *candidates,
+                   int32_t n_candidates, int64_t *best_out, double *predicted_ms_out);
+
 /* ---- planning (host only, no GPU needed) --------------------------------- */
 
 /* Chunks and norm tiles of a call: n_chunks = sum over segments of

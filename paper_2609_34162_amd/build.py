@@ -10,7 +10,7 @@ LIB_PATH = os.path.join(HERE, "libsdp.so")
 SOURCES = [os.path.join(HERE, "csrc", f) for f in ("sdp_runtime.hip", "sdp_kernels.hip")]
 # host-only lanes, built with the host compiler: no fused multiply-add, so the
 # FP64 update rounds every product and sum as written
-HOST_SOURCES = [os.path.join(HERE, "csrc", "sdp_host_adamw.cpp")]
+HOST_SOURCES = [os.path.join(HERE, "csrc", f) for f in ("sdp_host_adamw.cpp", "sdp_schedule.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 HOSTCXX = os.environ.get("SDP_HOSTCXX", "/opt/rocm/llvm/bin/clang++")
 HOST_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off", "-fno-math-errno", "-Wall"]

@@ -26,10 +26,12 @@
 #include <cstdlib>
 #include <cstring>
 #include <functional>
+#include <limits>
 #include <string>
 #include <vector>
 
 #include "sdp_host.h"
+#include "sdp_schedule.h"
 #include "sdp_internal.h"
 
 using sdp::NormState;
@@ -988,6 +990,86 @@ int sdp_bytes_per_elem(int streamed, int32_t n_ranks, uint32_t flags, double *hb
         // 12 + (2R or 4) and writes 14
         *hbm_or_h2d = cache ? 2.0 * R + 4.0 + 4.0 + 12.0 + 14.0 : 2.0 * R + 2.0 * R + 12.0 + 14.0;
         *d2h = 0.0;
+    }
+    return SDP_OK;
+}
+
+namespace {
+
+int check_model_args(int schedule, const int64_t *numels, int32_t n_segs, int32_t n_ranks, const sdp_rates *r,
+                     std::vector<int64_t> *sizes) {
+    if (schedule < SDP_SCHED_STREAMED || schedule > SDP_SCHED_HOST_ROUTE_BF16)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "unknown schedule %d", schedule);
+    if (!numels || n_segs < 1 || !r) return fail(SDP_ERR_INVALID_ARGUMENT, "NULL argument or no segments");
+    if (n_ranks < 1 || n_ranks > SDP_MAX_RANKS)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "n_ranks must be in 1..%d", SDP_MAX_RANKS);
+    const double pos[] = {r->h2d_gbs, r->d2h_gbs, r->both_gbs, r->norm_gbs, r->update_gbs, r->host_gbs};
+    const double nonneg[] = {r->copy_cmd_us, r->launch_us, r->sync_us, r->host_task_us};
+    for (double x : pos)
+        if (!(std::isfinite(x) && x > 0.0)) return fail(SDP_ERR_INVALID_ARGUMENT, "rates must be finite and > 0");
+    for (double x : nonneg)
+        if (!(std::isfinite(x) && x >= 0.0))
+            return fail(SDP_ERR_INVALID_ARGUMENT, "fixed costs must be finite and >= 0");
+    sizes->assign(numels, numels + n_segs);
+    for (int32_t s = 0; s < n_segs; ++s)
+        if (numels[s] < 1) return fail(SDP_ERR_INVALID_ARGUMENT, "segment %d has numel < 1", s);
+    return SDP_OK;
+}
+
+sdp_sched::Rates to_rates(const sdp_rates *r) {
+    return sdp_sched::Rates{r->h2d_gbs,  r->d2h_gbs,    r->both_gbs,  r->copy_cmd_us, r->norm_gbs,
+                            r->update_gbs, r->launch_us, r->sync_us, r->host_gbs,    r->host_task_us};
+}
+
+int model_chunk_ok(const std::vector<int64_t> &sizes, int64_t chunk) {
+    SDP_TRY(check_chunk(chunk, false));
+    int64_t n = 0;
+    for (int64_t x : sizes) n += cdiv(x, chunk);
+    if (n > (int64_t)1 << 22) return fail(SDP_ERR_INVALID_ARGUMENT, "%lld chunks: too many to model", (long long)n);
+    return SDP_OK;
+}
+
+}  // namespace
+
+int sdp_predict_step(int schedule, const int64_t *numels, int32_t n_segs, int32_t n_ranks, int64_t chunk_elems,
+                     uint32_t flags, const sdp_rates *rates, sdp_prediction *out) {
+    t_err.clear();
+    std::vector<int64_t> sizes;
+    SDP_TRY(check_model_args(schedule, numels, n_segs, n_ranks, rates, &sizes));
+    if (!out) return fail(SDP_ERR_INVALID_ARGUMENT, "out is NULL");
+    SDP_TRY(model_chunk_ok(sizes, chunk_elems));
+    const sdp_sched::Prediction p = sdp_sched::predict(schedule, sizes, n_ranks, chunk_elems,
+                                                       !(flags & SDP_FLAG_STREAM_GBAR_NEVER), to_rates(rates));
+    out->predicted_ms = p.predicted_ms;
+    out->bound_ms = p.bound_ms;
+    out->h2d_ms = p.h2d_ms;
+    out->d2h_ms = p.d2h_ms;
+    out->link_ms = p.link_ms;
+    out->gpu_ms = p.gpu_ms;
+    out->host_ms = p.host_ms;
+    out->n_chunks = p.n_chunks;
+    return SDP_OK;
+}
+
+int sdp_tune_chunk(int schedule, const int64_t *numels, int32_t n_segs, int32_t n_ranks, uint32_t flags,
+                   const sdp_rates *rates, const int64_t *candidates, int32_t n_candidates, int64_t *best_out,
+                   double *predicted_ms_out) {
+    t_err.clear();
+    std::vector<int64_t> sizes;
+    SDP_TRY(check_model_args(schedule, numels, n_segs, n_ranks, rates, &sizes));
+    if (!candidates || n_candidates < 1 || !best_out)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_tune_chunk: no candidates or best_out is NULL");
+    for (int32_t k = 0; k < n_candidates; ++k) SDP_TRY(model_chunk_ok(sizes, candidates[k]));
+    double best = std::numeric_limits<double>::infinity();
+    for (int32_t k = 0; k < n_candidates; ++k) {
+        const double ms = sdp_sched::predict(schedule, sizes, n_ranks, candidates[k],
+                                             !(flags & SDP_FLAG_STREAM_GBAR_NEVER), to_rates(rates))
+                              .predicted_ms;
+        if (predicted_ms_out) predicted_ms_out[k] = ms;
+        if (ms < best) {
+            best = ms;
+            *best_out = candidates[k];
+        }
     }
     return SDP_OK;
 }

@@ -1,0 +1,265 @@
+// Step-time model of the chunked schedules; see sdp_schedule.h.
+//
+// The graph mirrors the runtime's issue order:
+//  - streamed mode, phase 1: per chunk k (slot k mod 2) the R gradient
+//    copies on the copy stream, after the slot's previous norm kernel
+//    (slot_free); the norm kernel on the compute stream after the copies
+//    (h2d_done); then the finalize and the host's read-back of the norm;
+//  - phase 2: per chunk, the state copies in after the slot's previous
+//    outgoing copy, the update kernel, and the outgoing copies on the
+//    compute stream, all issued after the read-back;
+//  - staged variant: host-thread copies into the pinned bounce buffer before
+//    each incoming copy (after that buffer's previous copy left it) and out
+//    of it after each outgoing copy, in the host thread's own order;
+//  - host-update route: the norm pass and read-back, then per chunk the
+//    mean-gradient kernel (after the slot's previous outgoing copy, and
+//    issued by the host after it finished the update of chunk j-2), its copy
+//    to the host on the copy stream, and the host update after the copy.
+#include "sdp_schedule.h"
+
+#include <algorithm>
+#include <cmath>
+#include <limits>
+
+namespace sdp_sched {
+namespace {
+
+enum Stream { kCopyS = 0, kCompS = 1, kHostS = 2, kStreams = 3 };
+enum Kind { kFixed = 0, kH2D = 1, kD2H = 2 };
+
+struct Node {
+    int stream = 0, kind = kFixed;
+    double dur_us = 0.0;  // kFixed
+    double bytes = 0.0;   // copies
+    int cmds = 0;         // copies: commands, each paying the fixed command cost
+    std::vector<int> preds;
+    int state = 0;  // 0 waiting, 1 command latency, 2 running / transferring, 3 done
+    double t_end = 0.0, lat_end = 0.0, remaining = 0.0;
+};
+
+struct Graph {
+    std::vector<Node> nodes;
+    std::vector<int> fifo[kStreams];
+    double h2d_bytes = 0.0, d2h_bytes = 0.0, gpu_us = 0.0, host_us = 0.0;
+
+    int add(int stream, int kind, double dur_us, double bytes, int cmds, std::initializer_list<int> preds) {
+        Node n;
+        n.stream = stream;
+        n.kind = kind;
+        n.dur_us = dur_us;
+        n.bytes = bytes;
+        n.cmds = cmds;
+        for (int u : preds)
+            if (u >= 0) n.preds.push_back(u);
+        nodes.push_back(n);
+        const int id = (int)nodes.size() - 1;
+        fifo[stream].push_back(id);
+        if (kind == kH2D) h2d_bytes += bytes;
+        if (kind == kD2H) d2h_bytes += bytes;
+        if (kind == kFixed && stream == kCompS) gpu_us += dur_us;
+        if (kind == kFixed && stream == kHostS) host_us += dur_us;
+        return id;
+    }
+};
+
+// Finish time (us) of the graph: each stream runs its nodes in order, a node
+// starts once its stream is free and its predecessors are done, and copies
+// share the link as described in the header.
+double evaluate(Graph &g, const Rates &r) {
+    const size_t total = g.nodes.size();
+    size_t head[kStreams] = {0, 0, 0};
+    int cur[kStreams] = {-1, -1, -1};
+    size_t done = 0;
+    double t = 0.0;
+    const double h2d = r.h2d_gbs * 1e3, d2h = r.d2h_gbs * 1e3, both = r.both_gbs * 1e3;  // bytes per us
+    const double inf = std::numeric_limits<double>::infinity();
+    while (done < total) {
+        for (int s = 0; s < kStreams; ++s) {
+            if (cur[s] >= 0 || head[s] >= g.fifo[s].size()) continue;
+            const int id = g.fifo[s][head[s]];
+            Node &v = g.nodes[id];
+            bool ready = true;
+            for (int u : v.preds)
+                if (g.nodes[u].state != 3) {
+                    ready = false;
+                    break;
+                }
+            if (!ready) continue;
+            cur[s] = id;
+            if (v.kind == kFixed) {
+                v.state = 2;
+                v.t_end = t + v.dur_us;
+            } else {
+                v.state = 1;
+                v.lat_end = t + v.cmds * r.copy_cmd_us;
+                v.remaining = v.bytes;
+            }
+        }
+        int nh = 0, nd = 0;
+        for (int s = 0; s < kStreams; ++s) {
+            if (cur[s] < 0) continue;
+            const Node &v = g.nodes[cur[s]];
+            if (v.state == 2 && v.kind == kH2D) ++nh;
+            if (v.state == 2 && v.kind == kD2H) ++nd;
+        }
+        double rh = 0.0, rd = 0.0;
+        if (nh && nd) {
+            rh = std::min(h2d, both * h2d / (h2d + d2h));
+            rd = std::min(d2h, both - rh);
+        } else if (nh) {
+            rh = h2d;
+        } else if (nd) {
+            rd = d2h;
+        }
+        auto rate = [&](const Node &v) { return v.kind == kH2D ? rh / nh : rd / nd; };
+        double next = inf;
+        int first = -1;
+        for (int s = 0; s < kStreams; ++s) {
+            if (cur[s] < 0) continue;
+            const Node &v = g.nodes[cur[s]];
+            double e;
+            if (v.state == 1) e = v.lat_end;
+            else if (v.kind == kFixed) e = v.t_end;
+            else e = t + v.remaining / rate(v);
+            if (e < next) {
+                next = e;
+                first = s;
+            }
+        }
+        if (first < 0) return std::numeric_limits<double>::quiet_NaN();  // nothing can run: not a valid schedule
+        const double dt = next - t;
+        for (int s = 0; s < kStreams; ++s) {
+            if (cur[s] < 0) continue;
+            Node &v = g.nodes[cur[s]];
+            if (v.state == 2 && v.kind != kFixed) v.remaining -= rate(v) * dt;
+        }
+        {
+            Node &v = g.nodes[cur[first]];
+            if (v.state == 2 && v.kind != kFixed) v.remaining = 0.0;
+        }
+        t = next;
+        for (int s = 0; s < kStreams; ++s) {
+            if (cur[s] < 0) continue;
+            Node &v = g.nodes[cur[s]];
+            if (v.state == 1 && v.lat_end <= t) v.state = 2;
+            bool fin = false;
+            if (v.state == 2) {
+                if (v.kind == kFixed) fin = v.t_end <= t;
+                else fin = v.remaining <= 1e-9 * std::max(1.0, v.bytes);
+            }
+            if (fin) {
+                v.state = 3;
+                v.t_end = t;
+                cur[s] = -1;
+                ++head[s];
+                ++done;
+            }
+        }
+    }
+    return t;
+}
+
+struct Chunk {
+    int64_t len;
+    bool full;  // len == chunk: the slot's arrays are back to back, so copies merge into one run
+};
+
+std::vector<Chunk> chunks_of(const std::vector<int64_t> &numels, int64_t C) {
+    std::vector<Chunk> out;
+    for (int64_t n : numels)
+        for (int64_t off = 0; off < n; off += C) {
+            const int64_t len = std::min(C, n - off);
+            out.push_back({len, len == C});
+        }
+    return out;
+}
+
+double kernel_us(double bytes, double gbs, const Rates &r) { return bytes / (gbs * 1e3) + r.launch_us; }
+double host_us(double bytes, const Rates &r) { return bytes / (r.host_gbs * 1e3) + r.host_task_us; }
+
+void build_streamed(Graph &g, const std::vector<int64_t> &numels, int R, int64_t C, bool store, bool staged,
+                    const Rates &r) {
+    const std::vector<Chunk> ch = chunks_of(numels, C);
+    int slot_free[2] = {-1, -1}, bin_h2d[2] = {-1, -1};
+    for (size_t k = 0; k < ch.size(); ++k) {
+        const int sl = (int)(k & 1);
+        const double len = (double)ch[k].len;
+        int hin = -1;
+        if (staged) hin = g.add(kHostS, kFixed, host_us(2.0 * 2 * R * len, r), 0, 0, {bin_h2d[sl]});
+        const int cmds = (staged && ch[k].full) ? 1 : R;
+        const int h2d = g.add(kCopyS, kH2D, 0, 2.0 * R * len, cmds, {slot_free[sl], hin});
+        const int norm = g.add(kCompS, kFixed, kernel_us((2.0 * R + (store ? 4.0 : 0.0)) * len, r.norm_gbs, r), 0, 0,
+                               {h2d});
+        slot_free[sl] = norm;
+        bin_h2d[sl] = h2d;
+    }
+    const int fin = g.add(kCompS, kFixed, r.launch_us, 0, 0, {});
+    const int rb = g.add(kHostS, kFixed, r.sync_us, 0, 0, {fin});
+    const size_t k0 = ch.size();
+    int d2h_slot[2] = {-1, -1};
+    int prev_d2h = -1;
+    double prev_len = 0.0;
+    const double in_bpe = 12.0 + (store ? 0.0 : 2.0 * R);
+    for (size_t j = 0; j < ch.size(); ++j) {
+        const int sl = (int)((j + k0) & 1);
+        const double len = (double)ch[j].len;
+        int hin = -1;
+        if (staged) hin = g.add(kHostS, kFixed, host_us(2.0 * in_bpe * len, r), 0, 0, {rb, bin_h2d[sl]});
+        const int in_cmds = (staged && ch[j].full) ? 1 : 3 + (store ? 0 : R);
+        const int h2d = g.add(kCopyS, kH2D, 0, in_bpe * len, in_cmds, {rb, hin, d2h_slot[sl]});
+        const int upd = g.add(kCompS, kFixed, kernel_us((26.0 + (store ? 4.0 : 2.0 * R)) * len, r.update_gbs, r), 0,
+                              0, {h2d, rb});
+        const int out_cmds = (staged && ch[j].full) ? 1 : 4;
+        const int d2h = g.add(kCompS, kD2H, 0, 14.0 * len, out_cmds, {upd, hin});
+        if (staged && prev_d2h >= 0) g.add(kHostS, kFixed, host_us(2.0 * 14.0 * prev_len, r), 0, 0, {prev_d2h});
+        bin_h2d[sl] = h2d;
+        d2h_slot[sl] = d2h;
+        prev_d2h = d2h;
+        prev_len = len;
+    }
+    if (staged && prev_d2h >= 0) g.add(kHostS, kFixed, host_us(2.0 * 14.0 * prev_len, r), 0, 0, {prev_d2h});
+}
+
+void build_host_route(Graph &g, const std::vector<int64_t> &numels, int R, int64_t C, bool bf16, const Rates &r) {
+    for (int64_t n : numels) g.add(kCompS, kFixed, kernel_us(2.0 * R * (double)n, r.norm_gbs, r), 0, 0, {});
+    const int fin = g.add(kCompS, kFixed, r.launch_us, 0, 0, {});
+    const int rb = g.add(kHostS, kFixed, r.sync_us, 0, 0, {fin});
+    const std::vector<Chunk> ch = chunks_of(numels, C);
+    const double esz = bf16 ? 2.0 : 4.0;
+    std::vector<int> d2h(ch.size(), -1), adam(ch.size(), -1);
+    auto issue = [&](size_t j, int host_pred) {
+        const double len = (double)ch[j].len;
+        const int slot_pred = j >= 2 ? d2h[j - 2] : -1;
+        const int gk = g.add(kCompS, kFixed, kernel_us((2.0 * R + esz) * len, r.norm_gbs, r), 0, 0,
+                             {rb, host_pred, slot_pred});
+        d2h[j] = g.add(kCopyS, kD2H, 0, esz * len, 1, {gk});
+    };
+    if (!ch.empty()) issue(0, -1);
+    for (size_t j = 0; j < ch.size(); ++j) {
+        if (j + 1 < ch.size()) issue(j + 1, j >= 1 ? adam[j - 1] : -1);
+        adam[j] = g.add(kHostS, kFixed, host_us((26.0 + esz) * (double)ch[j].len, r), 0, 0, {d2h[j]});
+    }
+}
+
+}  // namespace
+
+Prediction predict(int schedule, const std::vector<int64_t> &numels, int R, int64_t chunk, bool store_gbar,
+                   const Rates &r) {
+    Graph g;
+    if (schedule == kStreamed || schedule == kStreamedStaged)
+        build_streamed(g, numels, R, chunk, store_gbar, schedule == kStreamedStaged, r);
+    else
+        build_host_route(g, numels, R, chunk, schedule == kHostRouteBf16, r);
+    Prediction p{};
+    for (int64_t n : numels) p.n_chunks += (n + chunk - 1) / chunk;
+    p.h2d_ms = g.h2d_bytes / (r.h2d_gbs * 1e9) * 1e3;
+    p.d2h_ms = g.d2h_bytes / (r.d2h_gbs * 1e9) * 1e3;
+    p.link_ms = (g.h2d_bytes + g.d2h_bytes) / (r.both_gbs * 1e9) * 1e3;
+    p.gpu_ms = g.gpu_us / 1e3;
+    p.host_ms = g.host_us / 1e3;
+    p.bound_ms = std::max({p.h2d_ms, p.d2h_ms, p.link_ms, p.gpu_ms, p.host_ms});
+    p.predicted_ms = evaluate(g, r) / 1e3;
+    return p;
+}
+
+}  // namespace sdp_sched

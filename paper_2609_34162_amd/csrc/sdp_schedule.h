@@ -1,0 +1,50 @@
+// Step-time model of the library's chunked schedules (streamed mode, its
+// staged variant, the host-update route).  Plain C++, host only; compiled by
+// the host compiler.  Not installed; not part of the ABI.
+//
+// The paper predicts a step from two quantities (Design, step-time model):
+// a resource-demand lower bound, max over resources j of W_j / beta_j, and a
+// dependency recurrence f(v) = d_v + max({a_v} and f(u) over the
+// predecessors u of v), whose predecessors are data and version dependences,
+// stream order and buffer release.  This model builds that graph for one
+// call of the library, node for node as the runtime issues its work:
+// copies, kernels and host-thread tasks on their streams, with the events
+// the runtime records and waits on as the cross-stream edges.  Copy
+// durations come from a fluid model of the host link: a copy moves at its
+// direction's rate while it is alone on the link, and at its share of the
+// bidirectional rate while the other direction is busy.  With no copy in
+// both directions at once, the evaluation is exactly the recurrence.
+#pragma once
+
+#include <stdint.h>
+
+#include <vector>
+
+namespace sdp_sched {
+
+struct Rates {
+    double h2d_gbs, d2h_gbs, both_gbs;  // link: each direction alone; both at once (sum)
+    double copy_cmd_us;                 // fixed cost of one copy command
+    double norm_gbs;                    // norm pass and mean-gradient kernel (HBM bytes / s / 1e9)
+    double update_gbs;                  // fused update kernel
+    double launch_us;                   // fixed cost of one kernel
+    double sync_us;                     // host round trip of the norm read-back
+    double host_gbs;                    // host threads' memory bandwidth
+    double host_task_us;                // fixed cost of one hand-off to the host threads
+};
+
+enum Schedule { kStreamed = 0, kStreamedStaged = 1, kHostRouteF32 = 2, kHostRouteBf16 = 3 };
+
+struct Prediction {
+    double predicted_ms;
+    double bound_ms;
+    double h2d_ms, d2h_ms, link_ms, gpu_ms, host_ms;
+    int64_t n_chunks;
+};
+
+// store_gbar: streamed mode keeps the mean gradient in device memory
+// between its passes (the default) instead of streaming the gradients twice.
+Prediction predict(int schedule, const std::vector<int64_t> &numels, int R, int64_t chunk, bool store_gbar,
+                   const Rates &r);
+
+}  // namespace sdp_sched

@@ -34,6 +34,10 @@ SDP_DELIVER_HOST_CAST = 0
 SDP_DELIVER_DEVICE_CAST = 1
 SDP_GBAR_F32 = 0
 SDP_GBAR_BF16 = 1
+SDP_SCHED_STREAMED = 0
+SDP_SCHED_STREAMED_STAGED = 1
+SDP_SCHED_HOST_ROUTE_F32 = 2
+SDP_SCHED_HOST_ROUTE_BF16 = 3
 
 
 class SdpError(RuntimeError):
@@ -71,6 +75,16 @@ class sdp_kernel_times(ctypes.Structure):
                 ("host_wait_ms", ctypes.c_double), ("host_adam_elems", ctypes.c_int64)]
 
 
+class sdp_rates(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_double) for n in ("h2d_gbs", "d2h_gbs", "both_gbs", "copy_cmd_us", "norm_gbs",
+                                              "update_gbs", "launch_us", "sync_us", "host_gbs", "host_task_us")]
+
+
+class sdp_prediction(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_double) for n in ("predicted_ms", "bound_ms", "h2d_ms", "d2h_ms", "link_ms",
+                                              "gpu_ms", "host_ms")] + [("n_chunks", ctypes.c_int64)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
@@ -91,6 +105,10 @@ def _load():
         "sdp_host_adamw": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, ctypes.c_int, i64, dbl,
                                            P(sdp_adamw_params)]),
         "sdp_ctx_set_host_threads": (ctypes.c_int, [vp, i32]),
+        "sdp_predict_step": (ctypes.c_int, [ctypes.c_int, vp, i32, i32, i64, ctypes.c_uint32, P(sdp_rates),
+                                            P(sdp_prediction)]),
+        "sdp_tune_chunk": (ctypes.c_int, [ctypes.c_int, vp, i32, i32, ctypes.c_uint32, P(sdp_rates), vp, i32,
+                                          P(i64), P(dbl)]),
         "sdp_probe_host_copy": (ctypes.c_int, [vp, vp, vp, i64, i32, P(dbl)]),
         "sdp_ctx_host_threads": (ctypes.c_int, [vp, P(i32)]),
         "sdp_plan": (ctypes.c_int, [vp, i32, i64, P(i64), P(i64)]),
@@ -256,6 +274,36 @@ def sdp_ctx_host_threads(ctx) -> int:
     t = ctypes.c_int32()
     _check(_lib.sdp_ctx_host_threads(ctx, ctypes.byref(t)))
     return t.value
+
+
+def make_rates(**kw) -> sdp_rates:
+    r = sdp_rates()
+    for k, v in kw.items():
+        if not hasattr(r, k):
+            raise TypeError(f"unknown rate {k}")
+        setattr(r, k, float(v))
+    return r
+
+
+def sdp_predict_step(schedule: int, numels: Sequence[int], n_ranks: int, chunk_elems: int, flags: int,
+                     rates: sdp_rates) -> sdp_prediction:
+    arr = (ctypes.c_int64 * len(numels))(*numels)
+    out = sdp_prediction()
+    _check(_lib.sdp_predict_step(schedule, ctypes.cast(arr, ctypes.c_void_p), len(numels), n_ranks, chunk_elems,
+                                 flags, ctypes.byref(rates), ctypes.byref(out)))
+    return out
+
+
+def sdp_tune_chunk(schedule: int, numels: Sequence[int], n_ranks: int, flags: int, rates: sdp_rates,
+                   candidates: Sequence[int]) -> Tuple[int, List[float]]:
+    arr = (ctypes.c_int64 * len(numels))(*numels)
+    cand = (ctypes.c_int64 * len(candidates))(*candidates)
+    ms = (ctypes.c_double * len(candidates))()
+    best = ctypes.c_int64()
+    _check(_lib.sdp_tune_chunk(schedule, ctypes.cast(arr, ctypes.c_void_p), len(numels), n_ranks, flags,
+                               ctypes.byref(rates), ctypes.cast(cand, ctypes.c_void_p), len(candidates),
+                               ctypes.byref(best), ms))
+    return best.value, list(ms)
 
 
 def sdp_plan(numels: Sequence[int], chunk_elems: int) -> Tuple[int, int]:

@@ -1,0 +1,164 @@
+"""The step-time model (sdp_predict_step, sdp_tune_chunk) against closed
+forms of its dependency recurrence and its resource bound.  Host code only:
+runs without a GPU."""
+import math
+
+import numpy as np
+import pytest
+
+TILE = 65536
+
+
+@pytest.fixture(scope="module")
+def sdp():
+    from paper_2609_34162_amd import sdp as mod
+    return mod
+
+
+def rates(sdp, **kw):
+    base = dict(h2d_gbs=50.0, d2h_gbs=40.0, both_gbs=90.0, copy_cmd_us=0.0, norm_gbs=5000.0, update_gbs=4000.0,
+                launch_us=0.0, sync_us=0.0, host_gbs=300.0, host_task_us=0.0)
+    base.update(kw)
+    return sdp.make_rates(**base)
+
+
+def us(nbytes, gbs):
+    return nbytes / (gbs * 1e3)
+
+
+def test_streamed_single_chunk_is_the_serial_sum(sdp):
+    """One chunk: nothing can overlap, so the recurrence is the sum of every
+    node's duration, command costs included."""
+    N, R = 3 * TILE + 5, 3
+    r = dict(copy_cmd_us=7.0, launch_us=3.0, sync_us=11.0)
+    rt = rates(sdp, **r)
+    got = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, 4 * TILE, 0, rt)
+    want = (R * 7.0 + us(2 * R * N, 50.0)            # gradients in
+            + us((2 * R + 4) * N, 5000.0) + 3.0      # norm pass, storing g_bar
+            + 3.0 + 11.0                             # finalize, read-back
+            + 3 * 7.0 + us(12 * N, 50.0)             # states in
+            + us(30 * N, 4000.0) + 3.0               # update from stored g_bar
+            + 4 * 7.0 + us(14 * N, 40.0))            # results out
+    assert math.isclose(got.predicted_ms, want / 1e3, rel_tol=1e-12)
+    assert got.n_chunks == 1
+    # without stored g_bar the gradients cross twice and the update reads them
+    got2 = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, 4 * TILE, sdp.SDP_FLAG_STREAM_GBAR_NEVER, rt)
+    want2 = (want - us(4 * N, 5000.0) + R * 7.0 + us(2 * R * N, 50.0) - us(30 * N, 4000.0)
+             + us((26 + 2 * R) * N, 4000.0))
+    assert math.isclose(got2.predicted_ms, want2 / 1e3, rel_tol=1e-12)
+
+
+def test_host_route_two_segments_closed_form(sdp):
+    sizes, R = [TILE + 1, 2 * TILE], 4
+    rt = rates(sdp, copy_cmd_us=5.0, launch_us=2.0, sync_us=13.0, host_task_us=17.0)
+    for sched, esz in ((sdp.SDP_SCHED_HOST_ROUTE_F32, 4), (sdp.SDP_SCHED_HOST_ROUTE_BF16, 2)):
+        got = sdp.sdp_predict_step(sched, sizes, R, 4 * TILE, 0, rt)
+        want = sum(us(2 * R * n, 5000.0) + 2.0 for n in sizes) + 2.0 + 13.0
+        # two chunks (one per segment): kernel and copy of the second overlap
+        # the host update of the first
+        g = [us((2 * R + esz) * n, 5000.0) + 2.0 for n in sizes]
+        c = [5.0 + us(esz * n, 40.0) for n in sizes]
+        h = [us((26 + esz) * n, 300.0) + 17.0 for n in sizes]
+        t_c0 = want + g[0] + c[0]
+        t_h0 = t_c0 + h[0]
+        t_c1 = max(want + g[0] + g[1], t_c0) + c[1]
+        total = max(t_h0, t_c1) + h[1]
+        assert math.isclose(got.predicted_ms, total / 1e3, rel_tol=1e-12), sched
+
+
+def test_two_chunk_phase_two_recurrence(sdp):
+    """Two chunks without link contention (both_gbs = h2d + d2h): phase two is
+    the recurrence with fixed durations: in_0, then upd_0 and out_0 on the
+    compute stream while in_1 runs on the copy stream, then upd_1, out_1."""
+    N, R = 2 * TILE, 2
+    rt = rates(sdp, both_gbs=90.0, launch_us=1.0)
+    got = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, TILE, 0, rt).predicted_ms * 1e3
+    L = TILE
+    g_in = us(2 * R * L, 50.0)
+    norm = us((2 * R + 4) * L, 5000.0) + 1.0
+    # phase one: copies back to back, each norm after its copy
+    n0 = g_in + norm
+    n1 = max(2 * g_in, n0) + norm
+    t1 = n1 + 1.0  # finalize; read-back costs nothing here
+    a = us(12 * L, 50.0)
+    u = us(30 * L, 4000.0) + 1.0
+    d = us(14 * L, 40.0)
+    # in_1 and out_0 overlap but both_gbs = h2d + d2h, so neither slows down
+    t2 = max(2 * a, a + u + d) + u + d
+    assert math.isclose(got, t1 + t2, rel_tol=1e-12)
+
+
+def test_link_contention_slows_overlapping_copies(sdp):
+    N, R = 8 * TILE, 2
+    free = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, TILE, 0, rates(sdp, both_gbs=90.0))
+    shared = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, TILE, 0, rates(sdp, both_gbs=60.0))
+    assert shared.predicted_ms > free.predicted_ms
+    # never slower than running every copy and kernel one after another
+    serial = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, 8 * TILE, 0, rates(sdp, both_gbs=60.0))
+    assert shared.predicted_ms <= serial.predicted_ms * (1 + 1e-12) + 1e-9
+    assert shared.link_ms > free.link_ms
+
+
+def test_bound_never_exceeds_prediction(sdp):
+    rng = np.random.default_rng(3)
+    for trial in range(200):
+        sizes = [int(x) for x in rng.integers(1, 40 * TILE, int(rng.integers(1, 4)))]
+        R = int(rng.integers(1, 17))
+        chunk = TILE * int(rng.integers(1, 9))
+        h2d, d2h = rng.uniform(5, 80, 2)
+        rt = rates(sdp, h2d_gbs=h2d, d2h_gbs=d2h, both_gbs=rng.uniform(max(h2d, d2h), h2d + d2h),
+                   copy_cmd_us=rng.uniform(0, 30), norm_gbs=rng.uniform(100, 8000),
+                   update_gbs=rng.uniform(100, 8000), launch_us=rng.uniform(0, 10), sync_us=rng.uniform(0, 50),
+                   host_gbs=rng.uniform(10, 500), host_task_us=rng.uniform(0, 50))
+        sched = int(rng.integers(0, 4))
+        flags = sdp.SDP_FLAG_STREAM_GBAR_NEVER if rng.random() < 0.3 else 0
+        p = sdp.sdp_predict_step(sched, sizes, R, chunk, flags, rt)
+        assert p.bound_ms == max(p.h2d_ms, p.d2h_ms, p.link_ms, p.gpu_ms, p.host_ms)
+        assert p.bound_ms <= p.predicted_ms * (1 + 1e-9), (trial, sched, p.bound_ms, p.predicted_ms)
+        assert p.n_chunks == sum(-(-n // chunk) for n in sizes)
+
+
+def test_staged_equals_plain_when_host_lanes_are_free(sdp):
+    N, R = 10 * TILE + 3, 4
+    rt = rates(sdp, host_gbs=1e9, host_task_us=0.0)
+    a = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, 2 * TILE, 0, rt)
+    b = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED_STAGED, [N], R, 2 * TILE, 0, rt)
+    assert math.isclose(a.predicted_ms, b.predicted_ms, rel_tol=1e-6)
+    slow = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED_STAGED, [N], R, 2 * TILE, 0, rates(sdp, host_gbs=20.0))
+    assert slow.predicted_ms > a.predicted_ms
+
+
+def test_tune_chunk_is_the_argmin(sdp):
+    sizes, R = [300 * TILE], 4
+    cands = [TILE * k for k in (1, 2, 4, 8, 16, 32, 64)]
+    for kw, expect_largest in ((dict(copy_cmd_us=2000.0), True), (dict(norm_gbs=20.0, update_gbs=20.0), False)):
+        rt = rates(sdp, **kw)
+        best, ms = sdp.sdp_tune_chunk(sdp.SDP_SCHED_STREAMED, sizes, R, 0, rt, cands)
+        direct = [sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, sizes, R, c, 0, rt).predicted_ms for c in cands]
+        assert ms == direct
+        assert best == cands[int(np.argmin(direct))]
+        if expect_largest:
+            assert best == cands[-1]          # per-command costs dominate: fewest chunks
+        else:
+            assert best < cands[-1]           # slow kernels: pipelining pays
+
+
+def test_model_argument_errors(sdp):
+    L = sdp._lib
+    rt = rates(sdp)
+    out = sdp.sdp_prediction()
+    import ctypes
+    arr = (ctypes.c_int64 * 1)(TILE)
+    assert L.sdp_predict_step(9, arr, 1, 2, TILE, 0, rt, out) == sdp.SDP_ERR_INVALID_ARGUMENT
+    assert L.sdp_predict_step(0, arr, 1, 0, TILE, 0, rt, out) == sdp.SDP_ERR_INVALID_ARGUMENT
+    assert L.sdp_predict_step(0, arr, 1, 2, TILE + 1, 0, rt, out) == sdp.SDP_ERR_INVALID_ARGUMENT
+    assert L.sdp_predict_step(0, None, 1, 2, TILE, 0, rt, out) == sdp.SDP_ERR_INVALID_ARGUMENT
+    assert L.sdp_predict_step(0, arr, 1, 2, TILE, 0, rates(sdp, h2d_gbs=0.0), out) == sdp.SDP_ERR_INVALID_ARGUMENT
+    assert L.sdp_predict_step(0, arr, 1, 2, TILE, 0, rates(sdp, sync_us=float("nan")), out) == \
+        sdp.SDP_ERR_INVALID_ARGUMENT
+    big = (ctypes.c_int64 * 1)(TILE << 23)
+    assert L.sdp_predict_step(0, big, 1, 2, TILE, 0, rt, out) == sdp.SDP_ERR_INVALID_ARGUMENT
+    assert "too many" in sdp.sdp_last_error()
+    best = ctypes.c_int64()
+    cands = (ctypes.c_int64 * 2)(TILE, 5)
+    assert L.sdp_tune_chunk(0, arr, 1, 2, 0, rt, cands, 2, ctypes.byref(best), None) == sdp.SDP_ERR_INVALID_ARGUMENT
