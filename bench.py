@@ -178,7 +178,8 @@ def measure_rates(args, torch, np, sdp, ctx, link, dres):
     """The step-time model's inputs, each measured on this machine: link rates
     (passed in), the per-command copy cost, the kernels' HBM rates and the
     launch cost from the device leg, the norm read-back round trip, the host
-    threads' copy bandwidth and their per-hand-off cost."""
+    threads' copy bandwidth, their per-hand-off cost and the host AdamW
+    lane's rate alone."""
     big, small = 256 << 20, 1 << 20
     ha, hb = sdp.HostBuffer(big), sdp.HostBuffer(big)
     da = torch.empty(big, dtype=torch.uint8, device="cuda")
@@ -213,11 +214,24 @@ def measure_rates(args, torch, np, sdp, ctx, link, dres):
     for _ in range(500):
         call()
     host_task_us = (time.perf_counter() - t0) / 500 * 1e6
+    # the host AdamW lane alone on 64M elements (FP32 mean gradient: 30 B per element)
+    n = 1 << 26
+    st = [np.full(n, 1e-2, np.float32) for _ in range(4)]
+    pb = np.zeros(n, np.uint16)
+    hp3 = sdp.make_params(step=3)
+    lane = lambda: sdp.sdp_host_adamw(ctx, st[0].ctypes.data, st[1].ctypes.data, st[2].ctypes.data,  # noqa: E731
+                                      pb.ctypes.data, st[3].ctypes.data, sdp.SDP_GBAR_F32, n, 1.0, hp3)
+    lane()
+    t0 = time.perf_counter()
+    for _ in range(4):
+        lane()
+    host_adam_gbs = 30 * n * 4 / (time.perf_counter() - t0) / 1e9
+    del st, pb
     kern_ms = dres["update_ms"] + dres["norm_ms"] + dres["finalize_ms"]
     launch_us = max(0.0, (dres["ms_per_step"] - kern_ms) / 3 * 1e3)
     vals = dict(h2d_gbs=link[0], d2h_gbs=link[1], both_gbs=link[2], copy_cmd_us=copy_cmd_us,
                 norm_gbs=dres["norm_gbs"], update_gbs=dres["update_gbs"], launch_us=launch_us, sync_us=sync_us,
-                host_gbs=host_gbs, host_task_us=host_task_us)
+                host_gbs=host_gbs, host_task_us=host_task_us, host_adam_gbs=host_adam_gbs)
     log("model rates: " + ", ".join(f"{k} {v:.1f}" for k, v in vals.items()))
     return sdp.make_rates(**vals), vals
 

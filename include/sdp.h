@@ -285,18 +285,20 @@ typedef struct {
     double update_gbs;       /* fused update kernel, HBM GB/s */
     double launch_us;        /* fixed cost of one kernel */
     double sync_us;          /* host round trip of the norm read-back */
-    double host_gbs;         /* host threads' memory bandwidth (bytes read + written) */
+    double host_gbs;         /* host memory bandwidth of the host threads' copies (read + written) */
     double host_task_us;     /* fixed cost of one hand-off to the host threads */
+    double host_adam_gbs;    /* the host AdamW lane alone (bytes read + written) */
 } sdp_rates;
 
 /* What the model predicts for one call. */
 typedef struct {
     double predicted_ms; /* finish time of the modelled schedule */
-    double bound_ms;     /* resource lower bound: the largest of the five below */
+    double bound_ms;     /* resource lower bound: the largest of the six below */
     double h2d_ms, d2h_ms; /* link bytes of each direction / its rate alone */
     double link_ms;      /* all link bytes / the bidirectional rate */
     double gpu_ms;       /* sum of the kernels' modelled times */
-    double host_ms;      /* sum of the host-thread tasks' modelled times */
+    double host_ms;      /* sum of the host-thread tasks' times, each alone */
+    double dram_ms;      /* host-task bytes plus every DMA byte / host_gbs */
     int64_t n_chunks;
 } sdp_prediction;
 
@@ -315,7 +317,9 @@ typedef struct {
  * library's own issue order -- each copy, kernel and host-thread task on its
  * stream, each event wait as an edge -- and evaluates it; copies share the
  * link by a fluid model (a direction alone moves at its own rate, both
- * directions together at the bidirectional rate, split in proportion). */
+ * directions together at the bidirectional rate, split in proportion), and
+ * host-thread tasks share host memory with the DMA (a task moves at most
+ * host_gbs minus the copies' current rate, and at most its own rate). */
 int sdp_predict_step(int schedule, const int64_t *numels, int32_t n_segs, int32_t n_ranks,
                      int64_t chunk_elems, uint32_t flags, const sdp_rates *rates,
                      sdp_prediction *out);

@@ -1003,7 +1003,8 @@ int check_model_args(int schedule, const int64_t *numels, int32_t n_segs, int32_
     if (!numels || n_segs < 1 || !r) return fail(SDP_ERR_INVALID_ARGUMENT, "NULL argument or no segments");
     if (n_ranks < 1 || n_ranks > SDP_MAX_RANKS)
         return fail(SDP_ERR_INVALID_ARGUMENT, "n_ranks must be in 1..%d", SDP_MAX_RANKS);
-    const double pos[] = {r->h2d_gbs, r->d2h_gbs, r->both_gbs, r->norm_gbs, r->update_gbs, r->host_gbs};
+    const double pos[] = {r->h2d_gbs,    r->d2h_gbs,  r->both_gbs,     r->norm_gbs,
+                          r->update_gbs, r->host_gbs, r->host_adam_gbs};
     const double nonneg[] = {r->copy_cmd_us, r->launch_us, r->sync_us, r->host_task_us};
     for (double x : pos)
         if (!(std::isfinite(x) && x > 0.0)) return fail(SDP_ERR_INVALID_ARGUMENT, "rates must be finite and > 0");
@@ -1017,8 +1018,9 @@ int check_model_args(int schedule, const int64_t *numels, int32_t n_segs, int32_
 }
 
 sdp_sched::Rates to_rates(const sdp_rates *r) {
-    return sdp_sched::Rates{r->h2d_gbs,  r->d2h_gbs,    r->both_gbs,  r->copy_cmd_us, r->norm_gbs,
-                            r->update_gbs, r->launch_us, r->sync_us, r->host_gbs,    r->host_task_us};
+    return sdp_sched::Rates{r->h2d_gbs,   r->d2h_gbs,  r->both_gbs, r->copy_cmd_us,  r->norm_gbs,
+                            r->update_gbs, r->launch_us, r->sync_us,  r->host_gbs,     r->host_task_us,
+                            r->host_adam_gbs};
 }
 
 int model_chunk_ok(const std::vector<int64_t> &sizes, int64_t chunk) {
@@ -1047,6 +1049,7 @@ int sdp_predict_step(int schedule, const int64_t *numels, int32_t n_segs, int32_
     out->link_ms = p.link_ms;
     out->gpu_ms = p.gpu_ms;
     out->host_ms = p.host_ms;
+    out->dram_ms = p.dram_ms;
     out->n_chunks = p.n_chunks;
     return SDP_OK;
 }

@@ -25,12 +25,13 @@ namespace sdp_sched {
 namespace {
 
 enum Stream { kCopyS = 0, kCompS = 1, kHostS = 2, kStreams = 3 };
-enum Kind { kFixed = 0, kH2D = 1, kD2H = 2 };
+enum Kind { kFixed = 0, kH2D = 1, kD2H = 2, kHostWork = 3 };
 
 struct Node {
     int stream = 0, kind = kFixed;
-    double dur_us = 0.0;  // kFixed
-    double bytes = 0.0;   // copies
+    double dur_us = 0.0;  // kFixed; kHostWork: the fixed hand-off cost before its bytes
+    double bytes = 0.0;   // copies and host work
+    double peak = 0.0;    // kHostWork: its own rate alone (bytes per us)
     int cmds = 0;         // copies: commands, each paying the fixed command cost
     std::vector<int> preds;
     int state = 0;  // 0 waiting, 1 command latency, 2 running / transferring, 3 done
@@ -40,7 +41,7 @@ struct Node {
 struct Graph {
     std::vector<Node> nodes;
     std::vector<int> fifo[kStreams];
-    double h2d_bytes = 0.0, d2h_bytes = 0.0, gpu_us = 0.0, host_us = 0.0;
+    double h2d_bytes = 0.0, d2h_bytes = 0.0, gpu_us = 0.0, host_us = 0.0, host_bytes = 0.0;
 
     int add(int stream, int kind, double dur_us, double bytes, int cmds, std::initializer_list<int> preds) {
         Node n;
@@ -58,6 +59,15 @@ struct Graph {
         if (kind == kD2H) d2h_bytes += bytes;
         if (kind == kFixed && stream == kCompS) gpu_us += dur_us;
         if (kind == kFixed && stream == kHostS) host_us += dur_us;
+        return id;
+    }
+
+    // A host-thread task: a hand-off cost, then `bytes` at up to `gbs`.
+    int host(double bytes, double gbs, double task_us, std::initializer_list<int> preds) {
+        const int id = add(kHostS, kHostWork, task_us, bytes, 0, preds);
+        nodes[id].peak = gbs * 1e3;
+        host_us += task_us + bytes / (gbs * 1e3);
+        host_bytes += bytes;
         return id;
     }
 };
@@ -91,16 +101,17 @@ double evaluate(Graph &g, const Rates &r) {
                 v.t_end = t + v.dur_us;
             } else {
                 v.state = 1;
-                v.lat_end = t + v.cmds * r.copy_cmd_us;
+                v.lat_end = t + (v.kind == kHostWork ? v.dur_us : v.cmds * r.copy_cmd_us);
                 v.remaining = v.bytes;
             }
         }
-        int nh = 0, nd = 0;
+        int nh = 0, nd = 0, nw = 0;
         for (int s = 0; s < kStreams; ++s) {
             if (cur[s] < 0) continue;
             const Node &v = g.nodes[cur[s]];
             if (v.state == 2 && v.kind == kH2D) ++nh;
             if (v.state == 2 && v.kind == kD2H) ++nd;
+            if (v.state == 2 && v.kind == kHostWork) ++nw;
         }
         double rh = 0.0, rd = 0.0;
         if (nh && nd) {
@@ -111,7 +122,20 @@ double evaluate(Graph &g, const Rates &r) {
         } else if (nd) {
             rd = d2h;
         }
-        auto rate = [&](const Node &v) { return v.kind == kH2D ? rh / nh : rd / nd; };
+        // every DMA byte passes through host memory; the host threads get
+        // what the copies leave of it
+        const double dram = r.host_gbs * 1e3;
+        if (rh + rd > dram) {
+            const double f = dram / (rh + rd);
+            rh *= f;
+            rd *= f;
+        }
+        const double left = std::max(0.0, dram - rh - rd);
+        auto rate = [&](const Node &v) {
+            if (v.kind == kH2D) return rh / nh;
+            if (v.kind == kD2H) return rd / nd;
+            return std::min(v.peak, left / nw);
+        };
         double next = inf;
         int first = -1;
         for (int s = 0; s < kStreams; ++s) {
@@ -175,7 +199,6 @@ std::vector<Chunk> chunks_of(const std::vector<int64_t> &numels, int64_t C) {
 }
 
 double kernel_us(double bytes, double gbs, const Rates &r) { return bytes / (gbs * 1e3) + r.launch_us; }
-double host_us(double bytes, const Rates &r) { return bytes / (r.host_gbs * 1e3) + r.host_task_us; }
 
 void build_streamed(Graph &g, const std::vector<int64_t> &numels, int R, int64_t C, bool store, bool staged,
                     const Rates &r) {
@@ -185,7 +208,7 @@ void build_streamed(Graph &g, const std::vector<int64_t> &numels, int R, int64_t
         const int sl = (int)(k & 1);
         const double len = (double)ch[k].len;
         int hin = -1;
-        if (staged) hin = g.add(kHostS, kFixed, host_us(2.0 * 2 * R * len, r), 0, 0, {bin_h2d[sl]});
+        if (staged) hin = g.host(2.0 * 2 * R * len, r.host_gbs, r.host_task_us, {bin_h2d[sl]});
         const int cmds = (staged && ch[k].full) ? 1 : R;
         const int h2d = g.add(kCopyS, kH2D, 0, 2.0 * R * len, cmds, {slot_free[sl], hin});
         const int norm = g.add(kCompS, kFixed, kernel_us((2.0 * R + (store ? 4.0 : 0.0)) * len, r.norm_gbs, r), 0, 0,
@@ -204,20 +227,20 @@ void build_streamed(Graph &g, const std::vector<int64_t> &numels, int R, int64_t
         const int sl = (int)((j + k0) & 1);
         const double len = (double)ch[j].len;
         int hin = -1;
-        if (staged) hin = g.add(kHostS, kFixed, host_us(2.0 * in_bpe * len, r), 0, 0, {rb, bin_h2d[sl]});
+        if (staged) hin = g.host(2.0 * in_bpe * len, r.host_gbs, r.host_task_us, {rb, bin_h2d[sl]});
         const int in_cmds = (staged && ch[j].full) ? 1 : 3 + (store ? 0 : R);
         const int h2d = g.add(kCopyS, kH2D, 0, in_bpe * len, in_cmds, {rb, hin, d2h_slot[sl]});
         const int upd = g.add(kCompS, kFixed, kernel_us((26.0 + (store ? 4.0 : 2.0 * R)) * len, r.update_gbs, r), 0,
                               0, {h2d, rb});
         const int out_cmds = (staged && ch[j].full) ? 1 : 4;
         const int d2h = g.add(kCompS, kD2H, 0, 14.0 * len, out_cmds, {upd, hin});
-        if (staged && prev_d2h >= 0) g.add(kHostS, kFixed, host_us(2.0 * 14.0 * prev_len, r), 0, 0, {prev_d2h});
+        if (staged && prev_d2h >= 0) g.host(2.0 * 14.0 * prev_len, r.host_gbs, r.host_task_us, {prev_d2h});
         bin_h2d[sl] = h2d;
         d2h_slot[sl] = d2h;
         prev_d2h = d2h;
         prev_len = len;
     }
-    if (staged && prev_d2h >= 0) g.add(kHostS, kFixed, host_us(2.0 * 14.0 * prev_len, r), 0, 0, {prev_d2h});
+    if (staged && prev_d2h >= 0) g.host(2.0 * 14.0 * prev_len, r.host_gbs, r.host_task_us, {prev_d2h});
 }
 
 void build_host_route(Graph &g, const std::vector<int64_t> &numels, int R, int64_t C, bool bf16, const Rates &r) {
@@ -237,7 +260,7 @@ void build_host_route(Graph &g, const std::vector<int64_t> &numels, int R, int64
     if (!ch.empty()) issue(0, -1);
     for (size_t j = 0; j < ch.size(); ++j) {
         if (j + 1 < ch.size()) issue(j + 1, j >= 1 ? adam[j - 1] : -1);
-        adam[j] = g.add(kHostS, kFixed, host_us((26.0 + esz) * (double)ch[j].len, r), 0, 0, {d2h[j]});
+        adam[j] = g.host((26.0 + esz) * (double)ch[j].len, r.host_adam_gbs, r.host_task_us, {d2h[j]});
     }
 }
 
@@ -257,7 +280,9 @@ Prediction predict(int schedule, const std::vector<int64_t> &numels, int R, int6
     p.link_ms = (g.h2d_bytes + g.d2h_bytes) / (r.both_gbs * 1e9) * 1e3;
     p.gpu_ms = g.gpu_us / 1e3;
     p.host_ms = g.host_us / 1e3;
-    p.bound_ms = std::max({p.h2d_ms, p.d2h_ms, p.link_ms, p.gpu_ms, p.host_ms});
+    // host memory carries the host tasks' bytes and every DMA byte
+    p.dram_ms = (g.host_bytes + g.h2d_bytes + g.d2h_bytes) / (r.host_gbs * 1e9) * 1e3;
+    p.bound_ms = std::max({p.h2d_ms, p.d2h_ms, p.link_ms, p.gpu_ms, p.host_ms, p.dram_ms});
     p.predicted_ms = evaluate(g, r) / 1e3;
     return p;
 }

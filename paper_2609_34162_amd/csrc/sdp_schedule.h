@@ -12,8 +12,13 @@
 // the runtime records and waits on as the cross-stream edges.  Copy
 // durations come from a fluid model of the host link: a copy moves at its
 // direction's rate while it is alone on the link, and at its share of the
-// bidirectional rate while the other direction is busy.  With no copy in
-// both directions at once, the evaluation is exactly the recurrence.
+// bidirectional rate while the other direction is busy.  Host-thread tasks
+// share host memory with the DMA: every byte a copy moves is read from or
+// written to host memory, so the copies together move at most host_gbs, and
+// while they run at a combined rate r a host task moves at most
+// (host_gbs - r), and never more than its own peak.  With
+// no overlap of copies in both directions and no copy beside a host task,
+// the evaluation is exactly the recurrence with fixed durations.
 #pragma once
 
 #include <stdint.h>
@@ -29,8 +34,9 @@ struct Rates {
     double update_gbs;                  // fused update kernel
     double launch_us;                   // fixed cost of one kernel
     double sync_us;                     // host round trip of the norm read-back
-    double host_gbs;                    // host threads' memory bandwidth
+    double host_gbs;                    // host memory bandwidth of the host threads' copies
     double host_task_us;                // fixed cost of one hand-off to the host threads
+    double host_adam_gbs;               // host AdamW lane alone (bytes read + written)
 };
 
 enum Schedule { kStreamed = 0, kStreamedStaged = 1, kHostRouteF32 = 2, kHostRouteBf16 = 3 };
@@ -38,7 +44,7 @@ enum Schedule { kStreamed = 0, kStreamedStaged = 1, kHostRouteF32 = 2, kHostRout
 struct Prediction {
     double predicted_ms;
     double bound_ms;
-    double h2d_ms, d2h_ms, link_ms, gpu_ms, host_ms;
+    double h2d_ms, d2h_ms, link_ms, gpu_ms, host_ms, dram_ms;
     int64_t n_chunks;
 };
 

@@ -77,12 +77,13 @@ class sdp_kernel_times(ctypes.Structure):
 
 class sdp_rates(ctypes.Structure):
     _fields_ = [(n, ctypes.c_double) for n in ("h2d_gbs", "d2h_gbs", "both_gbs", "copy_cmd_us", "norm_gbs",
-                                              "update_gbs", "launch_us", "sync_us", "host_gbs", "host_task_us")]
+                                              "update_gbs", "launch_us", "sync_us", "host_gbs", "host_task_us",
+                                              "host_adam_gbs")]
 
 
 class sdp_prediction(ctypes.Structure):
     _fields_ = [(n, ctypes.c_double) for n in ("predicted_ms", "bound_ms", "h2d_ms", "d2h_ms", "link_ms",
-                                              "gpu_ms", "host_ms")] + [("n_chunks", ctypes.c_int64)]
+                                              "gpu_ms", "host_ms", "dram_ms")] + [("n_chunks", ctypes.c_int64)]
 
 
 def _load():

@@ -3,7 +3,9 @@ times: one Qwen3-8B layer (192,946,176 params, R = 4, 10 steps) and one
 Qwen2.5-72B layer (877,674,496 params, R = 8, 3 steps) in device mode, and one
 Qwen3-14B layer (330,311,680 params, R = 4, 5 steps) in streamed mode and on
 the host-update route (FP32 mean gradient, 5 steps; BF16 mean gradient, 3
-steps; pageable host states, gradients in device memory).
+steps; pageable host states, gradients in device memory), and one segment
+of 2^31 + 4099 elements in device mode and on the host-update route
+(sampled points, exact norm).
 
 Every element of every output is compared with the oracle at every step,
 teacher-forced (the oracle steps from the GPU's state before the step) and,
@@ -19,8 +21,8 @@ import pytest
 
 import oracle
 import synth
-from gpu_util import (DevState, HostState, PageableState, check_norm, check_state, log, need_gpu, states_equal,
-                      torch)
+from gpu_util import (DevState, HostState, PageableState, check_bf16, check_f32, check_norm, check_state, log,
+                      need_gpu, states_equal, torch)
 
 pytestmark = [pytest.mark.gpu, pytest.mark.big]
 
@@ -247,3 +249,73 @@ def test_qwen3_14b_layer_host_route_full(sdp, fmt):
         sdp.sdp_ctx_destroy(ctx)
         host.close()
         pin.close()
+
+
+@pytest.mark.timeout(900)
+def test_segment_beyond_int32_elements(sdp):
+    """One segment of 2^31 + 4099 elements (R = 2), in device mode and then on
+    the host-update route (BF16 mean gradient): 64-bit indexing in every
+    kernel and copy offset.  The norm over the 2^32 + 8198 gradient values
+    must equal the oracle's exactly rounded norm bit for bit; about 200,000
+    sampled points (random, both ends and both sides of 2^31) are checked
+    element by element against the oracle's update of the same points."""
+    N, R = (1 << 31) + 4099, 2
+    log(f"segment of {N} elements, R = {R}")
+    t0 = time.time()
+    master = synth.normal_f32(synth.seed(4242, 1), N, 0.02)
+    grads = []
+    tmp = np.empty(1 << 26, np.float32)
+    for r in range(R):
+        g = np.empty(N, np.uint16)
+        s = synth.seed(4242, 2, r)
+        for a in range(0, N, tmp.size):
+            b = min(a + tmp.size, N)
+            synth.normal_f32(s, b - a, 1e-3, start=a, outlier_p=0.01, outlier_scale=100.0, out=tmp[:b - a])
+            synth.to_bf16_bits(tmp[:b - a], out=g[a:b])
+        grads.append(g)
+    log(f"  inputs generated  {time.time() - t0:.0f}s")
+    rng = np.random.default_rng(77)
+    idx = np.unique(np.concatenate([rng.integers(0, N, 200000), np.arange(64), np.arange(N - 64, N),
+                                    np.arange((1 << 31) - 64, (1 << 31) + 64)])).astype(np.int64)
+    g_rows = np.stack([g[idx] for g in grads], axis=1)
+    hp_kw = dict(lr=1e-3, weight_decay=0.01, max_grad_norm=1.0, step=1)
+    onorm = oracle.grad_norm([grads])
+    c = oracle.clip_coef(onorm, hp_kw["max_grad_norm"])
+    log(f"  oracle norm {onorm!r}, clip {c!r}  {time.time() - t0:.0f}s")
+    zeros = np.zeros(idx.size, np.float32)
+
+    dev = DevState([master], R)
+    dev.set_grads([grads])
+    ctx = sdp.sdp_ctx_create(0, 1 << 25, R, 0)
+    try:
+        norm = sdp.sdp_agg_adam_step(ctx, dev.segments(sdp), sdp.make_params(**hp_kw), 0,
+                                     torch.cuda.current_stream().cuda_stream, want_norm=True)
+        torch.cuda.synchronize()
+        assert norm == onorm, (norm, onorm)
+        it = torch.from_numpy(idx).to("cuda")
+        got = [dev.p[0][it].cpu().numpy(), dev.m[0][it].cpu().numpy(), dev.v[0][it].cpu().numpy(),
+               dev.pb[0][it].cpu().numpy().view(np.uint16)]
+        want = oracle.update_points(master[idx], zeros, zeros, g_rows, c, oracle.hparams(**hp_kw))
+        for a, b, name in zip(got[:3], want[:3], ("master", "exp_avg", "exp_avg_sq")):
+            check_f32(a, b, f"device {name}")
+        check_bf16(got[3], got[0], want[3])
+        log(f"  device mode: norm equal, {idx.size} points match  {time.time() - t0:.0f}s")
+        del dev.p, dev.m, dev.v, dev.pb
+        torch.cuda.empty_cache()
+
+        host_p = master.copy()
+        host_m = np.zeros(N, np.float32)
+        host_v = np.zeros(N, np.float32)
+        host_pb = np.zeros(N, np.uint16)
+        segs = sdp.Segments([(host_p.ctypes.data, host_m.ctypes.data, host_v.ctypes.data, host_pb.ctypes.data,
+                              [g.data_ptr() for g in dev.g[0]], N)])
+        rnorm = sdp.sdp_host_update_step(ctx, segs, sdp.make_params(**hp_kw), 1 << 25, sdp.SDP_GBAR_BF16)
+        assert rnorm == onorm
+        want = oracle.update_points(master[idx], zeros, zeros, g_rows, c, oracle.hparams(**hp_kw), gbar_bf16=True)
+        for a, b, name in zip((host_p[idx], host_m[idx], host_v[idx]), want[:3],
+                              ("master", "exp_avg", "exp_avg_sq")):
+            check_f32(a, b, f"host route {name}")
+        check_bf16(host_pb[idx], host_p[idx], want[3])
+        log(f"  host route: norm equal, {idx.size} points match  {time.time() - t0:.0f}s")
+    finally:
+        sdp.sdp_ctx_destroy(ctx)

@@ -16,8 +16,9 @@ def sdp():
 
 
 def rates(sdp, **kw):
+    # host memory so fast that the DMA never slows a host task, unless a test says otherwise
     base = dict(h2d_gbs=50.0, d2h_gbs=40.0, both_gbs=90.0, copy_cmd_us=0.0, norm_gbs=5000.0, update_gbs=4000.0,
-                launch_us=0.0, sync_us=0.0, host_gbs=300.0, host_task_us=0.0)
+                launch_us=0.0, sync_us=0.0, host_gbs=1e7, host_task_us=0.0, host_adam_gbs=300.0)
     base.update(kw)
     return sdp.make_rates(**base)
 
@@ -109,13 +110,37 @@ def test_bound_never_exceeds_prediction(sdp):
         rt = rates(sdp, h2d_gbs=h2d, d2h_gbs=d2h, both_gbs=rng.uniform(max(h2d, d2h), h2d + d2h),
                    copy_cmd_us=rng.uniform(0, 30), norm_gbs=rng.uniform(100, 8000),
                    update_gbs=rng.uniform(100, 8000), launch_us=rng.uniform(0, 10), sync_us=rng.uniform(0, 50),
-                   host_gbs=rng.uniform(10, 500), host_task_us=rng.uniform(0, 50))
+                   host_gbs=rng.uniform(10, 500), host_task_us=rng.uniform(0, 50),
+                   host_adam_gbs=rng.uniform(10, 500))
         sched = int(rng.integers(0, 4))
         flags = sdp.SDP_FLAG_STREAM_GBAR_NEVER if rng.random() < 0.3 else 0
         p = sdp.sdp_predict_step(sched, sizes, R, chunk, flags, rt)
-        assert p.bound_ms == max(p.h2d_ms, p.d2h_ms, p.link_ms, p.gpu_ms, p.host_ms)
+        assert p.bound_ms == max(p.h2d_ms, p.d2h_ms, p.link_ms, p.gpu_ms, p.host_ms, p.dram_ms)
         assert p.bound_ms <= p.predicted_ms * (1 + 1e-9), (trial, sched, p.bound_ms, p.predicted_ms)
         assert p.n_chunks == sum(-(-n // chunk) for n in sizes)
+
+
+def test_host_update_shares_host_memory_with_the_copy(sdp):
+    """Host route, two equal chunks: the update of chunk 0 starts with the
+    copy of chunk 1 and runs at min(its own rate, host_gbs - copy rate) until
+    that copy ends, then at its own rate."""
+    L, R = 4 * TILE, 2
+    A, B = 300.0, 320.0   # the AdamW lane's own rate; host memory bandwidth
+    rt = rates(sdp, host_gbs=B, host_adam_gbs=A, norm_gbs=1e9)
+    esz = 2
+    got = sdp.sdp_predict_step(sdp.SDP_SCHED_HOST_ROUTE_BF16, [2 * L], R, L, 0, rt).predicted_ms * 1e3
+    start = us(2 * R * 2 * L, 1e9) + us((2 * R + esz) * L, 1e9)   # norm pass, first mean-gradient kernel
+    c = us(esz * L, 40.0)                     # one copy, alone on the link
+    W = (26 + esz) * L                        # host bytes of one chunk's update
+    # the second kernel ran long ago (its rate is huge), so copy 1 starts with update 0
+    slow = min(A, B - 40.0) * 1e3             # bytes per us while copy 1 runs
+    done_during = slow * c
+    assert done_during < W
+    u0 = c + (W - done_during) / (A * 1e3)
+    want = start + c + u0 + W / (A * 1e3)     # update 1 follows update 0 with the link idle
+    assert math.isclose(got, want, rel_tol=1e-9), (got, want)
+    p = sdp.sdp_predict_step(sdp.SDP_SCHED_HOST_ROUTE_BF16, [2 * L], R, L, 0, rt)
+    assert math.isclose(p.dram_ms, (2 * W + 2 * esz * L) / (B * 1e9) * 1e3, rel_tol=1e-12)
 
 
 def test_staged_equals_plain_when_host_lanes_are_free(sdp):
