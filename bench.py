@@ -415,7 +415,8 @@ def host_route_leg(args, torch, np, synth, sdp, rates):
         k = args.stream_steps
         host_bytes = (26 + gsz) * N  # p, m, v read and written, g_bar read, BF16 params written
         adam_s = kt.host_adam_ms / k / 1e3
-        bound = max(host_bytes / (host_copy * 1e9), gsz * N / (d2h * 1e9))
+        # host memory carries the host lane's bytes and the copies' bytes
+        bound = max((host_bytes + gsz * N) / (host_copy * 1e9), gsz * N / (d2h * 1e9))
         out[name] = dict(ms_per_step=el * 1e3, params_per_s=N / el, d2h_bytes_per_param=gsz,
                          gpu_norm_ms=(kt.norm_ms + kt.finalize_ms) / k, gbar_kernel_ms=kt.gbar_ms / k,
                          host_adam_ms=kt.host_adam_ms / k, host_wait_ms=kt.host_wait_ms / k,

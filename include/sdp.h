@@ -195,10 +195,12 @@ int sdp_stream_step(sdp_ctx *ctx, const sdp_segment *host_segs, int32_t n_segs,
  * memory of ctx's GPU; master/exp_avg/exp_avg_sq/param_bf16 are host memory
  * (pinned or pageable; the host threads touch them, no DMA does).
  * Phase 1 runs the norm pass and finalize over the device gradients and
- * reads the norm back.  Phase 2 walks the chunks: the GPU writes the chunk's
- * mean gradient into a device staging slot, the copy stream moves it into a
- * pinned bounce buffer, and the context's host threads run AdamW on the
- * previous chunk meanwhile (double-buffered).  gbar_format SDP_GBAR_BF16
+ * reads the norm back.  Phase 2 walks the chunks, the first one split into
+ * a ramp of n/16, n/16, n/8, n/4 and n/2 elements when n/16 is at least
+ * SDP_NORM_TILE: the GPU writes the piece's mean gradient into a device
+ * staging slot, the copy stream moves it into a pinned bounce buffer, and
+ * the context's host threads run AdamW on the previous piece meanwhile
+ * (double-buffered).  gbar_format SDP_GBAR_BF16
  * rounds the mean gradient to BF16 before the copy, as the paper returns
  * one BF16 gradient; the update then uses bf16(g_bar) * c, while the norm
  * and c still come from the FP32 mean.  SDP_GBAR_F32 gives the same results

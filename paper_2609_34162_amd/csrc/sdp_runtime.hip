@@ -837,10 +837,11 @@ double ms_between(Clock::time_point a, Clock::time_point b) {
 
 // The host-update route over validated segments (grads in device memory,
 // states in host memory).  Phase 1: the norm pass over the device gradients
-// and the finalize; the norm state comes back to the host.  Phase 2, chunk
-// by chunk: the GPU writes g_bar of chunk j (FP32 or BF16) into device slot
+// and the finalize; the norm state comes back to the host.  Phase 2, piece
+// by piece: the GPU writes g_bar of piece j (FP32 or BF16) into device slot
 // j%2 on the compute stream, the copy stream moves it into pinned host buffer
-// j%2, and the host threads update chunk j-1 from the other buffer meanwhile.
+// j%2, and the host threads update piece j-1 from the other buffer meanwhile.
+// The pieces are the chunks, the first one split into a ramp.
 int host_route(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R, const Plan &plan,
                const sdp_adamw_params *hp, int64_t C, bool bf16, double *grad_norm_out) {
     hipStream_t sc = ctx->s_comp, sy = ctx->s_copy;
@@ -850,7 +851,22 @@ int host_route(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R,
     if (grad_norm_out) *grad_norm_out = st.norm;
     if (st.nonfinite) return fail(SDP_ERR_NONFINITE, "gradient norm is not finite (%g); nothing was updated", st.norm);
     const sdp_host::AdamConsts k = host_consts(hp, st.clip);
-    const std::vector<Chunk> chunks = make_chunks(segs, n_segs, C);
+    // the chunks, the first one split into a ramp of short pieces so that the
+    // host threads start after a short first copy
+    std::vector<Chunk> chunks;
+    {
+        const std::vector<Chunk> whole = make_chunks(segs, n_segs, C);
+        std::vector<int64_t> lens;
+        for (const Chunk &c : whole) lens.push_back(c.len);
+        const std::vector<int64_t> pieces = sdp_sched::route_pieces(lens);
+        const size_t head = pieces.size() - (whole.size() - 1);
+        int64_t off = 0;
+        for (size_t j = 0; j < head; ++j) {
+            chunks.push_back({whole[0].seg, whole[0].off + off, pieces[j]});
+            off += pieces[j];
+        }
+        chunks.insert(chunks.end(), whole.begin() + 1, whole.end());
+    }
     const size_t esz = bf16 ? 2 : 4;
     bool used[2] = {false, false};
     auto issue = [&](size_t j) -> int {

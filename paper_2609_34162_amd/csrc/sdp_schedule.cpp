@@ -11,10 +11,11 @@
 //  - staged variant: host-thread copies into the pinned bounce buffer before
 //    each incoming copy (after that buffer's previous copy left it) and out
 //    of it after each outgoing copy, in the host thread's own order;
-//  - host-update route: the norm pass and read-back, then per chunk the
-//    mean-gradient kernel (after the slot's previous outgoing copy, and
-//    issued by the host after it finished the update of chunk j-2), its copy
-//    to the host on the copy stream, and the host update after the copy.
+//  - host-update route: the norm pass and read-back, then per piece (the
+//    chunks, the first one split into a ramp) the mean-gradient kernel
+//    (after the slot's previous outgoing copy, and issued by the host after
+//    it finished the update of piece j-2), its copy to the host on the copy
+//    stream, and the host update after the copy.
 #include "sdp_schedule.h"
 
 #include <algorithm>
@@ -200,6 +201,32 @@ std::vector<Chunk> chunks_of(const std::vector<int64_t> &numels, int64_t C) {
 
 double kernel_us(double bytes, double gbs, const Rates &r) { return bytes / (gbs * 1e3) + r.launch_us; }
 
+}  // namespace
+
+std::vector<int64_t> route_pieces(const std::vector<int64_t> &chunk_lens) {
+    std::vector<int64_t> out;
+    if (chunk_lens.empty()) return out;
+    const int64_t first = chunk_lens[0];
+    int64_t piece = first / 16 / kRampAlign * kRampAlign;
+    if (piece < kRampAlign) {
+        out = chunk_lens;
+        return out;
+    }
+    int64_t done = 0;
+    out.push_back(piece);
+    done += piece;
+    while (done < first) {
+        const int64_t len = std::min(piece, first - done);
+        out.push_back(len);
+        done += len;
+        piece *= 2;
+    }
+    out.insert(out.end(), chunk_lens.begin() + 1, chunk_lens.end());
+    return out;
+}
+
+namespace {
+
 void build_streamed(Graph &g, const std::vector<int64_t> &numels, int R, int64_t C, bool store, bool staged,
                     const Rates &r) {
     const std::vector<Chunk> ch = chunks_of(numels, C);
@@ -247,7 +274,13 @@ void build_host_route(Graph &g, const std::vector<int64_t> &numels, int R, int64
     for (int64_t n : numels) g.add(kCompS, kFixed, kernel_us(2.0 * R * (double)n, r.norm_gbs, r), 0, 0, {});
     const int fin = g.add(kCompS, kFixed, r.launch_us, 0, 0, {});
     const int rb = g.add(kHostS, kFixed, r.sync_us, 0, 0, {fin});
-    const std::vector<Chunk> ch = chunks_of(numels, C);
+    std::vector<Chunk> ch;
+    {
+        std::vector<int64_t> lens;
+        for (int64_t n : numels)
+            for (int64_t off = 0; off < n; off += C) lens.push_back(std::min(C, n - off));
+        for (int64_t len : route_pieces(lens)) ch.push_back({len, false});
+    }
     const double esz = bf16 ? 2.0 : 4.0;
     std::vector<int> d2h(ch.size(), -1), adam(ch.size(), -1);
     auto issue = [&](size_t j, int host_pred) {

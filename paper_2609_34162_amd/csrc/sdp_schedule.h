@@ -48,6 +48,14 @@ struct Prediction {
     int64_t n_chunks;
 };
 
+// The host-update route's pieces: the call's chunks in order, with the
+// first one split into a ramp of n/16, n/16, n/8, n/4, n/2 elements (each a
+// multiple of kRampAlign; left whole when n/16 is smaller), so that the host
+// threads start after a short first copy and each later copy hides behind
+// the update of the piece before it.
+constexpr int64_t kRampAlign = 65536;
+std::vector<int64_t> route_pieces(const std::vector<int64_t> &chunk_lens);
+
 // store_gbar: streamed mode keeps the mean gradient in device memory
 // between its passes (the default) instead of streaming the gradients twice.
 Prediction predict(int schedule, const std::vector<int64_t> &numels, int R, int64_t chunk, bool store_gbar,

@@ -1,10 +1,12 @@
-"""GPU parity on the full Qwen3-14B model in streamed mode: the embedding, 40
-decoder layers and the lm_head (42 segments, 14,768,291,840 params, R = 2,
-32M-element chunks, 2 steps), with every state in host memory (265.8 GB).
-The host grants far less pinned memory than that (65 GiB per process on
-the MI355X boxes used here), so the states are ordinary pageable memory
-and the context runs the staged streamed mode: chunks move through its
-pinned bounce buffers.
+"""GPU parity on the full Qwen3-14B model: the embedding, 40 decoder layers
+and the lm_head (42 segments, 14,768,291,840 params, R = 2, 32M-element
+chunks, 2 steps), with every state in host memory (206.8 GB of states, plus
+59 GB of gradients).  The host grants far less pinned memory than that
+(65 GiB per process on the MI355X boxes used here), so the states are
+ordinary pageable memory.  Two runs: the staged streamed mode, whose chunks
+move through the context's pinned bounce buffers, and the host-update route
+with the BF16 mean gradient, whose gradients sit in device memory (59 GB of
+HBM) while host threads update the states in place.
 
 The oracle cannot hold a second copy of that state, so each step is checked
 (a) on the gradient norm, from all 29.5 billion gradient values, which must
@@ -30,7 +32,7 @@ from gpu_util import PageableState, check_bf16, check_f32, check_norm, log, need
 
 pytestmark = [pytest.mark.gpu, pytest.mark.big]
 
-NEED_GIB = 262  # pinned state plus the process, with a margin
+NEED_GIB = 262  # host state plus the process, with a margin
 
 
 def mem_available_gib():
@@ -41,19 +43,22 @@ def mem_available_gib():
     return 0.0
 
 
-@pytest.mark.timeout(1500)
-def test_qwen3_14b_full_model_streamed():
+def run_full_model(route):
+    """route False: staged streamed mode; True: host-update route with the BF16
+    mean gradient (gradients copied to device memory first)."""
     if os.environ.get("SDP_FULL_MODEL") != "1":
-        pytest.skip("full-model streamed run is opt-in (SDP_FULL_MODEL=1): 266 GB of pinned host state")
+        pytest.skip("full-model runs are opt-in (SDP_FULL_MODEL=1): 266 GB of host state")
     avail = mem_available_gib()
     if avail < NEED_GIB:
         pytest.skip(f"needs {NEED_GIB} GiB of available host memory, {avail:.0f} GiB available")
     sdp = need_gpu()
+    import torch
     w = synth.workload(3)
     R, C = w.ranks, w.chunk
     sizes = [s.numel for s in w.segments]
     t0 = time.time()
-    log(f"{w.name}: {len(sizes)} segments, N={w.numel}, R={R}, chunk={C}; {avail:.0f} GiB available")
+    log(f"{w.name} ({'host route, BF16 g_bar' if route else 'staged streamed'}): {len(sizes)} segments, "
+        f"N={w.numel}, R={R}, chunk={C}; {avail:.0f} GiB available")
 
     # sample points of every segment
     rng = np.random.default_rng(2024)
@@ -76,21 +81,36 @@ def test_qwen3_14b_full_model_streamed():
                 f" MemAvailable {mem_available_gib():.0f} GiB")
     free = [(synth.master_at(w, s, samples[s]), np.zeros(samples[s].size, np.float32),
              np.zeros(samples[s].size, np.float32)) for s in range(len(sizes))]
-    ctx = sdp.sdp_ctx_create(0, C, R, sdp.SDP_FLAG_STREAM_STAGED)
+    devg = [[torch.empty(n, dtype=torch.int16, device="cuda") for _ in range(R)] for n in sizes] if route else None
+    ctx = sdp.sdp_ctx_create(0, C, R, 0 if route else sdp.SDP_FLAG_STREAM_STAGED)
     try:
+        if route:
+            segs = sdp.Segments([(host.p[s].ctypes.data, host.m[s].ctypes.data, host.v[s].ctypes.data,
+                                  host.pb[s].ctypes.data, [g.data_ptr() for g in devg[s]], sizes[s])
+                                 for s in range(len(sizes))])
+        else:
+            segs = host.segments()
         for t in range(1, w.steps + 1):
             for s in range(len(sizes)):
                 for r in range(R):
                     synth.grad_bf16(w, s, t, r, out=host.g[s][r])
+                    if route:
+                        devg[s][r].copy_(torch.from_numpy(host.g[s][r].view(np.int16)))
                 if s % 6 == 0:
                     log(f"  step {t}: gradients of segment {s} generated  {time.time() - t0:.0f}s")
+            if route:
+                torch.cuda.synchronize()
             before = [(host.p[s][samples[s]], host.m[s][samples[s]], host.v[s][samples[s]])
                       for s in range(len(sizes))]
             ts = time.time()
-            norm = sdp.sdp_stream_step(ctx, host.segments(), sdp.make_params(**w.hparams(t)), C)
+            if route:
+                norm = sdp.sdp_host_update_step(ctx, segs, sdp.make_params(**w.hparams(t)), C, sdp.SDP_GBAR_BF16)
+            else:
+                norm = sdp.sdp_stream_step(ctx, segs, sdp.make_params(**w.hparams(t)), C)
             step_s = time.time() - ts
             onorm = oracle.grad_norm(host.g)
-            log(f"  step {t}: streamed step {step_s:.2f} s, norm {norm!r} (oracle {onorm!r})")
+            log(f"  step {t}: {'host route' if route else 'streamed'} step {step_s:.2f} s, norm {norm!r}"
+                f" (oracle {onorm!r})")
             check_norm(norm, onorm)
             assert norm == onorm, "norm differs from the exactly rounded oracle norm"
             hp = oracle.hparams(**w.hparams(t))
@@ -100,12 +120,12 @@ def test_qwen3_14b_full_model_streamed():
                 idx = samples[s]
                 g_rows = np.stack([host.g[s][r][idx] for r in range(R)], axis=1)
                 after = (host.p[s][idx], host.m[s][idx], host.v[s][idx], host.pb[s][idx])
-                ep, em, ev, epb = oracle.update_points(*before[s], g_rows, c, hp)
+                ep, em, ev, epb = oracle.update_points(*before[s], g_rows, c, hp, gbar_bf16=route)
                 for got, want, name in ((after[0], ep, "master"), (after[1], em, "exp_avg"),
                                         (after[2], ev, "exp_avg_sq")):
                     worst = max(worst, check_f32(got, want, f"seg{s}.{name} (teacher-forced)")[0])
                 check_bf16(after[3], after[0], epb)
-                fp, fm, fv, fpb = oracle.update_points(*free[s], g_rows, c, hp)
+                fp, fm, fv, fpb = oracle.update_points(*free[s], g_rows, c, hp, gbar_bf16=route)
                 for got, want, name in ((after[0], fp, "master"), (after[1], fm, "exp_avg"),
                                         (after[2], fv, "exp_avg_sq")):
                     check_f32(got, want, f"seg{s}.{name} (free-running)")
@@ -116,3 +136,13 @@ def test_qwen3_14b_full_model_streamed():
     finally:
         sdp.sdp_ctx_destroy(ctx)
         host.close()
+
+
+@pytest.mark.timeout(1500)
+def test_qwen3_14b_full_model_streamed():
+    run_full_model(route=False)
+
+
+@pytest.mark.timeout(1500)
+def test_qwen3_14b_full_model_host_route():
+    run_full_model(route=True)

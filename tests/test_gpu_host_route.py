@@ -86,6 +86,35 @@ def test_host_route_matches_oracle(sdp, ctx, fmt, chunk_tiles, pinned):
         st.close()
 
 
+@pytest.mark.parametrize("fmt", ["f32", "bf16"])
+def test_host_route_first_chunk_ramp(sdp, fmt):
+    """A first chunk of 16 tiles runs as a ramp of 1, 1, 2, 4 and 8 tiles;
+    results still match the oracle, and equal those of a chunking too short
+    to ramp (every piece of the update is elementwise)."""
+    sizes = [20 * TILE + 3, 5000]
+    R = 2
+    masters, grads = rand_inputs(sizes, R, 2, seed=101)
+    c = sdp.sdp_ctx_create(0, 16 * TILE, R, 0)
+    a = RouteState(sdp, masters, R)
+    b = RouteState(sdp, masters, R)
+    ref = oracle.State(masters)
+    try:
+        for t in (1, 2):
+            hs, ho = hp_pair(sdp, lr=1e-3, weight_decay=0.02, max_grad_norm=0.3, step=t)
+            a.set_grads(grads[t - 1])
+            b.set_grads(grads[t - 1])
+            na = sdp.sdp_host_update_step(c, a.segments(sdp), hs, 16 * TILE, fmt_of(sdp, fmt))
+            nb = sdp.sdp_host_update_step(c, b.segments(sdp), hs, TILE, fmt_of(sdp, fmt))
+            oracle.step(ref, grads[t - 1], ho, gbar_bf16=(fmt == "bf16"))
+            assert na == nb
+            check_state(a.state(), ref)
+            assert states_equal(a.state(), b.state())
+    finally:
+        a.close()
+        b.close()
+        sdp.sdp_ctx_destroy(c)
+
+
 @pytest.mark.parametrize("R", [1, 2, 4, 8, 16])
 def test_host_route_ranks_against_device_mode(sdp, ctx, R):
     """FP32 route and device mode: same norm bits, both within the criteria
