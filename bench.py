@@ -153,7 +153,7 @@ def brief(res):
                                 "norm_gbs")} | {"step_hbm_frac": res["step_hbm_gbs"] / HBM_PEAK_GBS}
 
 
-def cpu_leg(args, np, oracle, master, host_grads, w):
+def cpu_leg(args, np, synth, oracle, master, host_grads, w):
     log("cpu leg: oracle on the same layer")
     st = oracle.State([master])
     grads = [host_grads]
@@ -166,9 +166,24 @@ def cpu_leg(args, np, oracle, master, host_grads, w):
         el = time.perf_counter() - t0
         if el >= args.cpu_seconds or steps >= 20:
             break
-    return dict(value=w.numel * steps / el, unit="params/s", cores=oracle.num_threads(), kind="oracle",
+    cores = oracle.num_threads()
+    # one thread on the 1024 x 1024 workload, for scale
+    t = synth.workload(0)
+    tm = synth.master(t, 0)
+    tg = [[synth.grad_bf16(t, 0, 1, r) for r in range(t.ranks)]]
+    ts = oracle.State([tm])
+    oracle.set_num_threads(1)
+    try:
+        t1 = time.perf_counter()
+        for k in range(t.steps):
+            oracle.step(ts, tg, oracle.hparams(**t.hparams(k + 1)))
+        one = t.numel * t.steps / (time.perf_counter() - t1)
+    finally:
+        oracle.set_num_threads(cores)
+    return dict(value=w.numel * steps / el, unit="params/s", cores=cores, kind="oracle",
                 sample=f"{steps} full oracle steps of the {w.name} workload "
-                       f"({w.numel} params, R={w.ranks}), {el:.1f} s")
+                       f"({w.numel} params, R={w.ranks}), {el:.1f} s",
+                one_thread=dict(workload=t.name, params_per_s=one, steps=t.steps))
 
 
 SWEEP_CHUNKS = [1 << 20, 1 << 21, 1 << 22, 1 << 23, 1 << 24, 1 << 25]  # 4-128 MiB per FP32 state array
@@ -492,7 +507,7 @@ def main():
         sys.exit(1)
     torch.cuda.set_device(0)
     dres, master, host_grads, w = device_leg(args, torch, np, synth, sdp, 1, args.steps, args.warmup, True)
-    cpu = None if args.no_cpu else cpu_leg(args, np, oracle, master, host_grads, w)
+    cpu = None if args.no_cpu else cpu_leg(args, np, synth, oracle, master, host_grads, w)
     del master, host_grads
     r8 = None
     if not args.no_extra:

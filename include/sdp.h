@@ -93,6 +93,9 @@ extern "C" {
  * system grants.  Needs max_chunk_elems > 0; pins 2 * (28 + 2 * max_ranks) *
  * max_chunk_elems bytes; host threads: SDP_STAGING_THREADS, default up to 16. */
 #define SDP_FLAG_STREAM_STAGED 0x10u
+/* Host threads: keep each of the context's worker threads on one CPU of the
+ * process's affinity set (the calling thread is left alone). */
+#define SDP_FLAG_HOST_PIN_THREADS 0x20u
 
 /* ---- types ------------------------------------------------------------- */
 typedef struct sdp_ctx sdp_ctx;

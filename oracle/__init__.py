@@ -75,6 +75,8 @@ def _declare(L):
                                     ctypes.POINTER(HParams), vp, vp, vp, vp]
     L.orc_num_threads.restype = ctypes.c_int
     L.orc_num_threads.argtypes = []
+    L.orc_set_num_threads.restype = None
+    L.orc_set_num_threads.argtypes = [ctypes.c_int]
     return L
 
 
@@ -220,3 +222,7 @@ def update_points(p, m, v, g_rows, clip_c: float, hp: HParams, lib=None, gbar_bf
 
 def num_threads(lib=None) -> int:
     return (lib or load()).orc_num_threads()
+
+
+def set_num_threads(n: int, lib=None) -> None:
+    (lib or load()).orc_set_num_threads(n)

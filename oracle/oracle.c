@@ -409,6 +409,17 @@ void orc_update_points_fmt(int64_t n, const float *p, const float *m, const floa
     }
 }
 
+/* Threads of the OpenMP loops from now on (n >= 1); for timing only. */
+void orc_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n >= 1)
+        omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 int orc_num_threads(void)
 {
 #ifdef _OPENMP

@@ -67,6 +67,7 @@ void orc_update_points_fmt(int64_t n, const float *p, const float *m, const floa
                            float *m_out, float *v_out, uint16_t *pb_out);
 
 int orc_num_threads(void);
+void orc_set_num_threads(int n);
 
 #ifdef __cplusplus
 }

@@ -20,6 +20,9 @@
 #include <condition_variable>
 #include <mutex>
 #include <thread>
+
+#include <pthread.h>
+#include <sched.h>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -111,8 +114,29 @@ void cast_bf16_host(const float *src, uint16_t *dst, size_t n) {
 // calls fn(i) for every i in [0, n) across the workers and the caller.
 class HostPool {
   public:
-    explicit HostPool(int workers) {
-        for (int i = 0; i < workers; ++i) threads_.emplace_back([this] { loop(); });
+    // pin: worker i stays on the (i+1)-th CPU of the process's affinity set
+    // (cyclically), leaving the first to the calling thread.
+    HostPool(int workers, bool pin) {
+        std::vector<int> cpus;
+        if (pin) {
+            cpu_set_t set;
+            CPU_ZERO(&set);
+            if (sched_getaffinity(0, sizeof set, &set) == 0)
+                for (int c = 0; c < CPU_SETSIZE; ++c)
+                    if (CPU_ISSET(c, &set)) cpus.push_back(c);
+        }
+        for (int i = 0; i < workers; ++i) {
+            const int cpu = cpus.empty() ? -1 : cpus[(size_t)(i + 1) % cpus.size()];
+            threads_.emplace_back([this, cpu] {
+                if (cpu >= 0) {
+                    cpu_set_t one;
+                    CPU_ZERO(&one);
+                    CPU_SET(cpu, &one);
+                    (void)pthread_setaffinity_np(pthread_self(), sizeof one, &one);
+                }
+                loop();
+            });
+        }
     }
     ~HostPool() {
         {
@@ -773,10 +797,14 @@ int default_host_threads() {
     return threads;
 }
 
+HostPool *new_pool(const sdp_ctx *ctx, int threads) {
+    return new HostPool(threads - 1, (ctx->flags & SDP_FLAG_HOST_PIN_THREADS) != 0);
+}
+
 // The host threads and pinned bounce buffers, created on first use by a
 // context that was not created for the staged mode.
 int ensure_host_staging(sdp_ctx *ctx) {
-    if (!ctx->copier) ctx->copier = new HostPool(default_host_threads() - 1);
+    if (!ctx->copier) ctx->copier = new_pool(ctx, default_host_threads());
     if (!ctx->bounce_in) {
         if (hipHostMalloc(&ctx->bounce_in, 2 * ctx->slot_bytes, hipHostMallocDefault) != hipSuccess) {
             (void)hipGetLastError();
@@ -1120,6 +1148,9 @@ int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems, int32_t m
     if (max_ranks < 1 || max_ranks > SDP_MAX_RANKS)
         return fail(SDP_ERR_INVALID_ARGUMENT, "max_ranks must be in 1..%d", SDP_MAX_RANKS);
     SDP_TRY(check_chunk(max_chunk_elems, true));
+    const uint32_t known = SDP_FLAG_DEVICE_GBAR_NEVER | SDP_FLAG_DEVICE_GBAR_ALWAYS | SDP_FLAG_STREAM_GBAR_NEVER |
+                           SDP_FLAG_DEBUG_POISON | SDP_FLAG_STREAM_STAGED | SDP_FLAG_HOST_PIN_THREADS;
+    if (flags & ~known) return fail(SDP_ERR_INVALID_ARGUMENT, "unknown context flags 0x%x", flags & ~known);
     if ((flags & SDP_FLAG_DEVICE_GBAR_NEVER) && (flags & SDP_FLAG_DEVICE_GBAR_ALWAYS))
         return fail(SDP_ERR_INVALID_ARGUMENT, "DEVICE_GBAR_NEVER and DEVICE_GBAR_ALWAYS are exclusive");
     int ndev = 0;
@@ -1180,7 +1211,7 @@ int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems, int32_t m
                              2 * (c->slot_bytes + out_bytes)));
         }
         for (int k = 0; k < 2; ++k) CTX_HIP(hipEventCreateWithFlags(&c->d2h_done[k], hipEventDisableTiming));
-        c->copier = new HostPool(default_host_threads() - 1);
+        c->copier = new_pool(c, default_host_threads());
     }
     rc = ensure_partials(c, 4096);
     if (rc != SDP_OK) return bail(rc);
@@ -1489,7 +1520,7 @@ int sdp_host_adamw(sdp_ctx *ctx, float *master, float *exp_avg, float *exp_avg_s
             if (overlap(rs[x], rs[y]))
                 return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_host_adamw: %s overlaps %s", rs[x].what, rs[y].what);
     }
-    if (ctx && !ctx->copier) ctx->copier = new HostPool(default_host_threads() - 1);
+    if (ctx && !ctx->copier) ctx->copier = new_pool(ctx, default_host_threads());
     sdp_host::AdamArgs a;
     a.p = master;
     a.m = exp_avg;
@@ -1508,7 +1539,7 @@ int sdp_probe_host_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes,
     const uintptr_t a = (uintptr_t)dst, b = (uintptr_t)src;
     if (a < b + (size_t)bytes && b < a + (size_t)bytes)
         return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_probe_host_copy: dst and src overlap");
-    if (!ctx->copier) ctx->copier = new HostPool(default_host_threads() - 1);
+    if (!ctx->copier) ctx->copier = new_pool(ctx, default_host_threads());
     const Clock::time_point t0 = Clock::now();
     for (int32_t r = 0; r < reps; ++r) pool_jobs(ctx->copier, {{dst, src, (size_t)bytes}});
     const double s = ms_between(t0, Clock::now()) / 1e3;
@@ -1522,7 +1553,7 @@ int sdp_ctx_set_host_threads(sdp_ctx *ctx, int32_t threads) {
     if (threads < 1 || threads > 256)
         return fail(SDP_ERR_INVALID_ARGUMENT, "host threads must be in 1..256 (got %d)", threads);
     delete ctx->copier;
-    ctx->copier = new HostPool(threads - 1);
+    ctx->copier = new_pool(ctx, threads);
     return SDP_OK;
 }
 

@@ -30,6 +30,7 @@ SDP_FLAG_DEVICE_GBAR_ALWAYS = 0x2
 SDP_FLAG_STREAM_GBAR_NEVER = 0x4
 SDP_FLAG_DEBUG_POISON = 0x8
 SDP_FLAG_STREAM_STAGED = 0x10
+SDP_FLAG_HOST_PIN_THREADS = 0x20
 SDP_DELIVER_HOST_CAST = 0
 SDP_DELIVER_DEVICE_CAST = 1
 SDP_GBAR_F32 = 0

@@ -164,6 +164,16 @@ def test_host_route_threads_and_simd_give_same_bits(sdp, ctx):
                 os.environ.pop("SDP_HOST_SIMD", None)
     finally:
         sdp.sdp_ctx_set_host_threads(ctx, saved)
+    # worker threads kept on fixed CPUs
+    pinned = sdp.sdp_ctx_create(0, 4 * TILE, R, sdp.SDP_FLAG_HOST_PIN_THREADS)
+    st = RouteState(sdp, masters, R)
+    try:
+        st.set_grads(grads[0])
+        sdp.sdp_host_update_step(pinned, st.segments(sdp), hs, 2 * TILE, sdp.SDP_GBAR_BF16)
+        outs.append(st.state())
+    finally:
+        st.close()
+        sdp.sdp_ctx_destroy(pinned)
     for o in outs[1:]:
         assert states_equal(outs[0], o)
 
