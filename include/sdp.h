@@ -201,7 +201,7 @@ int sdp_stream_step(sdp_ctx *ctx, const sdp_segment *host_segs, int32_t n_segs,
  * reads the norm back.  Phase 2 walks the chunks, the first one split into
  * a ramp of n/16, n/16, n/8, n/4 and n/2 elements when n/16 is at least
  * SDP_NORM_TILE: the GPU writes the piece's mean gradient into a device
- * staging slot, the copy stream moves it into a pinned bounce buffer, and
+ * staging slot, the copy stream moves it into a pinned stage buffer, and
  * the context's host threads run AdamW on the previous piece meanwhile
  * (double-buffered).  gbar_format SDP_GBAR_BF16
  * rounds the mean gradient to BF16 before the copy, as the paper returns
@@ -211,7 +211,8 @@ int sdp_stream_step(sdp_ctx *ctx, const sdp_segment *host_segs, int32_t n_segs,
  * sdp_stream_step (the context needs staging).  Blocks until every state is
  * written; returns SDP_ERR_NONFINITE (states unchanged) for a non-finite
  * norm.  grad_norm_out may be NULL.  Host threads: sdp_ctx_set_host_threads,
- * else SDP_STAGING_THREADS, else up to 16. */
+ * else SDP_STAGING_THREADS, else up to 16.  The first call creates them and
+ * the two pinned stage buffers if the context has none. */
 int sdp_host_update_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs,
                          const sdp_adamw_params *hp, int64_t chunk_elems, int gbar_format,
                          double *grad_norm_out);
@@ -268,7 +269,9 @@ int sdp_cast_bf16(sdp_ctx *ctx, const float *src, uint16_t *dst, int64_t n, void
  * ctx's GPU.  chunk_elems as for sdp_stream_step.  Blocks until the last
  * chunk has landed, so a forward pass started after the call sees the
  * updated weights (the per-layer version gate).  The first call creates
- * the context's host threads and pinned bounce buffers if it has none. */
+ * the context's host threads and its two pinned stage buffers (4 *
+ * max_chunk_elems bytes each, shared with sdp_host_update_step) if it has
+ * none. */
 int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf16, int64_t n,
                        int64_t chunk_elems, int mode);
 

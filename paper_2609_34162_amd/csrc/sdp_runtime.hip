@@ -261,6 +261,10 @@ struct sdp_ctx {
     char *bounce_out = nullptr;  // 2 x 14 * max_chunk (master, m, v, bf16 part of a slot)
     hipEvent_t d2h_done[2] = {nullptr, nullptr};
     bool bin_used[2] = {false, false};
+    // parameter delivery and the host-update route: two pinned buffers of
+    // 4 * max_chunk bytes each (one chunk of FP32), created on first use
+    char *stage = nullptr;
+    bool stage_used[2] = {false, false};
     std::vector<Xfer> pending_out[2];
     HostPool *copier = nullptr;
     double *partials = nullptr;
@@ -801,17 +805,20 @@ HostPool *new_pool(const sdp_ctx *ctx, int threads) {
     return new HostPool(threads - 1, (ctx->flags & SDP_FLAG_HOST_PIN_THREADS) != 0);
 }
 
-// The host threads and pinned bounce buffers, created on first use by a
-// context that was not created for the staged mode.
-int ensure_host_staging(sdp_ctx *ctx) {
+size_t stage_bytes(const sdp_ctx *ctx) { return 4 * (size_t)ctx->max_chunk; }
+
+// The host threads and the two pinned stage buffers of parameter delivery and
+// the host-update route, created on first use.
+int ensure_host_stage(sdp_ctx *ctx) {
     if (!ctx->copier) ctx->copier = new_pool(ctx, default_host_threads());
-    if (!ctx->bounce_in) {
-        if (hipHostMalloc(&ctx->bounce_in, 2 * ctx->slot_bytes, hipHostMallocDefault) != hipSuccess) {
+    if (!ctx->stage) {
+        if (hipHostMalloc(&ctx->stage, 2 * stage_bytes(ctx), hipHostMallocDefault) != hipSuccess) {
             (void)hipGetLastError();
-            ctx->bounce_in = nullptr;
-            return fail(SDP_ERR_OUT_OF_MEMORY, "cannot allocate %zu bytes of pinned bounce buffers", 2 * ctx->slot_bytes);
+            ctx->stage = nullptr;
+            return fail(SDP_ERR_OUT_OF_MEMORY, "cannot allocate %zu bytes of pinned stage buffers",
+                        2 * stage_bytes(ctx));
         }
-        ctx->bin_used[0] = ctx->bin_used[1] = false;
+        ctx->stage_used[0] = ctx->stage_used[1] = false;
     }
     return SDP_OK;
 }
@@ -901,7 +908,7 @@ int host_route(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R,
         const Chunk &c = chunks[j];
         const int sl = (int)(j & 1);
         char *dev = ctx->staging + (size_t)sl * ctx->slot_bytes;
-        char *host = ctx->bounce_in + (size_t)sl * ctx->slot_bytes;
+        char *host = ctx->stage + (size_t)sl * stage_bytes(ctx);
         // the slot's previous copy to the host has read it
         if (used[sl]) HIP_TRY(hipStreamWaitEvent(sc, ctx->slot_free[sl], 0));
         sdp::GbarArgs a{};
@@ -935,7 +942,7 @@ int host_route(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R,
         a.m = g.exp_avg + c.off;
         a.v = g.exp_avg_sq + c.off;
         a.pb = g.param_bf16 + c.off;
-        a.gbar = ctx->bounce_in + (size_t)sl * ctx->slot_bytes;
+        a.gbar = ctx->stage + (size_t)sl * stage_bytes(ctx);
         a.gbar_bf16 = bf16 ? 1 : 0;
         host_adamw(ctx->copier, a, k, c.len);
         if (ctx->timing) {
@@ -1238,6 +1245,7 @@ void sdp_ctx_destroy(sdp_ctx *ctx) {
     if (ctx->s_comp) (void)hipStreamDestroy(ctx->s_comp);
     if (ctx->staging) (void)hipFree(ctx->staging);
     if (ctx->bounce_in) (void)hipHostFree(ctx->bounce_in);
+    if (ctx->stage) (void)hipHostFree(ctx->stage);
     if (ctx->bounce_out) (void)hipHostFree(ctx->bounce_out);
     for (int k = 0; k < 2; ++k)
         if (ctx->d2h_done[k]) (void)hipEventDestroy(ctx->d2h_done[k]);
@@ -1407,7 +1415,7 @@ int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf1
     SDP_TRY(check_host_ptr(host_master, "host_master", 0));
     SDP_TRY(check_device_ptr(ctx, dev_bf16, (size_t)n * 2, "dev_bf16", 0));
     const bool pinned = is_pinned_host(host_master);
-    if (mode == SDP_DELIVER_HOST_CAST || !pinned) SDP_TRY(ensure_host_staging(ctx));
+    if (mode == SDP_DELIVER_HOST_CAST || !pinned) SDP_TRY(ensure_host_stage(ctx));
     SDP_TRY(order_after_last(ctx, ctx->s_copy));
     SDP_TRY(order_after_last(ctx, ctx->s_comp));
     bool used[2] = {false, false};
@@ -1416,10 +1424,10 @@ int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf1
     for (int64_t off = 0; off < n && rc == SDP_OK; off += chunk_elems, ++k) {
         const int sl = (int)(k & 1);
         const int64_t len = std::min(chunk_elems, n - off);
-        char *bin = ctx->bounce_in + (size_t)sl * ctx->slot_bytes;
+        char *bin = ctx->stage ? ctx->stage + (size_t)sl * stage_bytes(ctx) : nullptr;
         if (mode == SDP_DELIVER_HOST_CAST) {
             // host threads round chunk k while the DMA still moves chunk k-1
-            if (ctx->bin_used[sl] && hipEventSynchronize(ctx->h2d_done[sl]) != hipSuccess) {
+            if (ctx->stage_used[sl] && hipEventSynchronize(ctx->h2d_done[sl]) != hipSuccess) {
                 rc = fail(SDP_ERR_HIP, "sdp_deliver_params: event wait failed");
                 break;
             }
@@ -1427,7 +1435,7 @@ int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf1
             if (hipMemcpyAsync(dev_bf16 + off, bin, (size_t)len * 2, hipMemcpyHostToDevice, ctx->s_copy) != hipSuccess ||
                 hipEventRecord(ctx->h2d_done[sl], ctx->s_copy) != hipSuccess)
                 rc = fail(SDP_ERR_HIP, "sdp_deliver_params: copy enqueue failed");
-            ctx->bin_used[sl] = true;
+            ctx->stage_used[sl] = true;
         } else {
             Slot slot = slot_at(ctx, sl);
             std::vector<Xfer> xs = {{off_in_slot(ctx, sl, slot.p), (char *)(host_master + off), (size_t)len * 4}};
@@ -1440,14 +1448,14 @@ int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf1
                     hipSuccess)
                     rc = fail(SDP_ERR_HIP, "sdp_deliver_params: copy enqueue failed");
             } else {
-                if (ctx->bin_used[sl] && hipEventSynchronize(ctx->h2d_done[sl]) != hipSuccess) {
+                if (ctx->stage_used[sl] && hipEventSynchronize(ctx->h2d_done[sl]) != hipSuccess) {
                     rc = fail(SDP_ERR_HIP, "sdp_deliver_params: event wait failed");
                     break;
                 }
                 pool_jobs(ctx->copier, {{bin, host_master + off, (size_t)len * 4}});
                 if (hipMemcpyAsync(slot.p, bin, (size_t)len * 4, hipMemcpyHostToDevice, ctx->s_copy) != hipSuccess)
                     rc = fail(SDP_ERR_HIP, "sdp_deliver_params: copy enqueue failed");
-                ctx->bin_used[sl] = true;
+                ctx->stage_used[sl] = true;
             }
             if (rc != SDP_OK) break;
             if (hipEventRecord(ctx->h2d_done[sl], ctx->s_copy) != hipSuccess ||
@@ -1481,7 +1489,7 @@ int sdp_host_update_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, 
     SDP_TRY(validate_segments(ctx, segs, n_segs, kAnyHost, kDeviceMem, false, &R));
     const Plan plan = make_plan(segs, n_segs);
     SDP_TRY(ensure_partials(ctx, plan.tiles));
-    SDP_TRY(ensure_host_staging(ctx));
+    SDP_TRY(ensure_host_stage(ctx));
     SDP_TRY(order_after_last(ctx, ctx->s_comp));
     SDP_TRY(order_after_last(ctx, ctx->s_copy));
     const int rc = host_route(ctx, segs, n_segs, R, plan, hp, chunk_elems, gbar_format == SDP_GBAR_BF16,
