@@ -1,5 +1,7 @@
-// C ABI of libsdp: context, argument validation, the device-mode driver and
-// the streamed engine.  Kernels live in sdp_kernels.hip.
+// C ABI of libsdp: context, argument validation, the device-mode driver, the
+// streamed engine, parameter delivery and the host-update route.  Kernels
+// live in sdp_kernels.hip, the host AdamW lane in sdp_host_adamw.cpp and the
+// step-time model in sdp_schedule.cpp.
 //
 // Device mode (sdp_agg_adam_step): per call, one norm-partials launch per
 // segment, one finalize launch, one fused-update launch per segment, all on
@@ -14,6 +16,11 @@
 // a chunk starts as soon as its copy has landed (chunked overlap within a
 // layer).  Phase 1 streams the gradients for the global norm; phase 2
 // streams master/m/v through the fused update and back.
+//
+// Host-update route (sdp_host_update_step): the gradients stay in device
+// memory; the GPU computes the norm and, piece by piece, the mean gradient,
+// which the copy stream moves into pinned stage buffers while the host
+// threads run AdamW on the states in host memory.
 #include <algorithm>
 #include <atomic>
 #include <chrono>
@@ -90,10 +97,6 @@ struct Timed {
     int64_t elems;
 };
 
-// A fixed set of host threads that split large memcpys between them.  Used
-// by the staged streamed mode to move chunks between the caller's host
-// memory and the context's pinned bounce buffers (the CPU-side staging lane
-// of the paper's chunked overlap, Design, overlap within a layer).
 // Round FP32 values to BF16, nearest even, on the host (the parameter
 // delivery lane).  NaN keeps its sign and top payload bits and gets the quiet
 // bit; infinities are kept; overflow of the largest values rounds to
@@ -108,10 +111,12 @@ void cast_bf16_host(const float *src, uint16_t *dst, size_t n) {
     }
 }
 
-// A fixed set of host threads for the host lanes of the streamed engine:
-// copies between the caller's memory and pinned bounce buffers, the BF16
-// rounding of parameter delivery and the host AdamW route.  run(n, fn)
-// calls fn(i) for every i in [0, n) across the workers and the caller.
+// A fixed set of host threads for the host lanes: copies between the
+// caller's memory and the staged mode's pinned bounce buffers (the CPU-side
+// staging lane of the paper's chunked overlap, Design, overlap within a
+// layer), the BF16 rounding of parameter delivery and the host AdamW of the
+// host-update route.  run(n, fn) calls fn(i) for every i in [0, n) across
+// the workers and the caller.
 class HostPool {
   public:
     // pin: worker i stays on the (i+1)-th CPU of the process's affinity set

@@ -115,6 +115,30 @@ def test_host_route_first_chunk_ramp(sdp, fmt):
         sdp.sdp_ctx_destroy(c)
 
 
+def test_route_then_delivery_closes_the_loop(sdp, ctx):
+    """The paper's per-layer loop on one context: the host route updates the
+    host master, then parameter delivery writes its BF16 copy into a device
+    window for the next forward pass; the window must equal the route's own
+    BF16 params bit for bit, for both delivery modes and both steps."""
+    sizes = [3 * TILE + 11, 4097]
+    R = 2
+    masters, grads = rand_inputs(sizes, R, 2, seed=111)
+    st = RouteState(sdp, masters, R)
+    try:
+        for t in (1, 2):
+            hs, _ = hp_pair(sdp, lr=1e-3, weight_decay=0.01, max_grad_norm=0.5, step=t)
+            st.set_grads(grads[t - 1])
+            sdp.sdp_host_update_step(ctx, st.segments(sdp), hs, 2 * TILE, sdp.SDP_GBAR_BF16)
+            for s, n in enumerate(sizes):
+                for mode in (sdp.SDP_DELIVER_HOST_CAST, sdp.SDP_DELIVER_DEVICE_CAST):
+                    window = torch.full((n,), 0x5555, dtype=torch.int16, device="cuda")
+                    sdp.sdp_deliver_params(ctx, st.host.p[s].ctypes.data, window.data_ptr(), n, 2 * TILE, mode)
+                    got = window.cpu().numpy().view(np.uint16)
+                    assert np.array_equal(got, st.host.pb[s]), (t, s, mode)
+    finally:
+        st.close()
+
+
 @pytest.mark.parametrize("R", [1, 2, 4, 8, 16])
 def test_host_route_ranks_against_device_mode(sdp, ctx, R):
     """FP32 route and device mode: same norm bits, both within the criteria
