@@ -91,7 +91,9 @@ extern "C" {
  * copy it in while the previous chunk's DMA runs, and copy results out while
  * the next chunk's runs.  For host states larger than the pinned memory the
  * system grants.  Needs max_chunk_elems > 0; pins 2 * (28 + 2 * max_ranks) *
- * max_chunk_elems bytes; host threads: SDP_STAGING_THREADS, default up to 16. */
+ * max_chunk_elems bytes (two incoming bounce buffers shaped like a slot, two
+ * outgoing ones of 14 bytes per element); host threads: SDP_STAGING_THREADS,
+ * default up to 16. */
 #define SDP_FLAG_STREAM_STAGED 0x10u
 /* Host threads: keep each of the context's worker threads on one CPU of the
  * process's affinity set (the calling thread is left alone). */

@@ -239,6 +239,14 @@ void pool_jobs(HostPool *pool, const std::vector<Job> &jobs) {
     });
 }
 
+// Staged mode: outgoing bounce buffers.  Chunk j's results land in buffer
+// j % kOutBufs; the host threads move chunk j-1's out as soon as they have
+// landed, while chunk j's incoming copy runs.  Deferring that by one more
+// chunk (three buffers) lets the host copies overlap the next outgoing DMA,
+// which on the MI355X hosts measured here slowed the DMA enough to lose
+// 25% of the step.
+constexpr int kOutBufs = 2;
+
 // A host <-> staging-slot transfer of one chunk: `bytes` at byte offset `off`
 // of a slot, from or to `host`.
 struct Xfer {
@@ -263,14 +271,14 @@ struct sdp_ctx {
     size_t slot_bytes = 0;
     // staged streamed mode: pinned bounce buffers shaped like the slots
     char *bounce_in = nullptr;   // 2 x slot_bytes
-    char *bounce_out = nullptr;  // 2 x 14 * max_chunk (master, m, v, bf16 part of a slot)
-    hipEvent_t d2h_done[2] = {nullptr, nullptr};
+    char *bounce_out = nullptr;  // kOutBufs x 14 * max_chunk (master, m, v, bf16 part of a slot)
+    hipEvent_t d2h_done[kOutBufs] = {nullptr, nullptr};
     bool bin_used[2] = {false, false};
     // parameter delivery and the host-update route: two pinned buffers of
     // 4 * max_chunk bytes each (one chunk of FP32), created on first use
     char *stage = nullptr;
     bool stage_used[2] = {false, false};
-    std::vector<Xfer> pending_out[2];
+    std::vector<Xfer> pending_out[kOutBufs];
     HostPool *copier = nullptr;
     double *partials = nullptr;
     int64_t partials_cap = 0;
@@ -699,33 +707,33 @@ int copy_in(sdp_ctx *ctx, int sl, const std::vector<Xfer> &xs) {
 }
 
 // Slot `sl` -> host copies of one chunk, enqueued on the compute stream.  In
-// the staged mode they land in the pinned bounce buffer and are moved to
+// the staged mode they land in outgoing bounce buffer `bo` and are moved to
 // their destinations by drain().
-int copy_out(sdp_ctx *ctx, int sl, const std::vector<Xfer> &xs) {
+int copy_out(sdp_ctx *ctx, int sl, int bo, const std::vector<Xfer> &xs) {
     char *dev = ctx->staging + (size_t)sl * ctx->slot_bytes;
     if (!staged(ctx)) {
         for (const Xfer &x : xs)
             HIP_TRY(hipMemcpyAsync(x.host, dev + x.off, x.bytes, hipMemcpyDeviceToHost, ctx->s_comp));
         return SDP_OK;
     }
-    char *bout = ctx->bounce_out + (size_t)sl * 14 * (size_t)ctx->max_chunk;
+    char *bout = ctx->bounce_out + (size_t)bo * 14 * (size_t)ctx->max_chunk;
     for (const Xfer &r : merge_runs(xs))
         HIP_TRY(hipMemcpyAsync(bout + r.off, dev + r.off, r.bytes, hipMemcpyDeviceToHost, ctx->s_comp));
-    HIP_TRY(hipEventRecord(ctx->d2h_done[sl], ctx->s_comp));
-    ctx->pending_out[sl] = xs;
+    HIP_TRY(hipEventRecord(ctx->d2h_done[bo], ctx->s_comp));
+    ctx->pending_out[bo] = xs;
     return SDP_OK;
 }
 
-// Staged mode: wait for slot `sl`'s outgoing copies and move them from the
-// bounce buffer to their host destinations.
-int drain(sdp_ctx *ctx, int sl) {
-    if (ctx->pending_out[sl].empty()) return SDP_OK;
-    HIP_TRY(hipEventSynchronize(ctx->d2h_done[sl]));
-    char *bout = ctx->bounce_out + (size_t)sl * 14 * (size_t)ctx->max_chunk;
+// Staged mode: wait for the outgoing copies into bounce buffer `bo` and move
+// them to their host destinations.
+int drain(sdp_ctx *ctx, int bo) {
+    if (ctx->pending_out[bo].empty()) return SDP_OK;
+    HIP_TRY(hipEventSynchronize(ctx->d2h_done[bo]));
+    char *bout = ctx->bounce_out + (size_t)bo * 14 * (size_t)ctx->max_chunk;
     std::vector<Job> jobs;
-    for (const Xfer &x : ctx->pending_out[sl]) jobs.push_back({x.host, bout + x.off, x.bytes});
+    for (const Xfer &x : ctx->pending_out[bo]) jobs.push_back({x.host, bout + x.off, x.bytes});
     pool_jobs(ctx->copier, jobs);
-    ctx->pending_out[sl].clear();
+    ctx->pending_out[bo].clear();
     return SDP_OK;
 }
 
@@ -784,17 +792,15 @@ int stream_update_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t R, const 
                                  {off_in_slot(ctx, sl, slot.m), (char *)(g.exp_avg + c.off), f4},
                                  {off_in_slot(ctx, sl, slot.v), (char *)(g.exp_avg_sq + c.off), f4},
                                  {off_in_slot(ctx, sl, slot.pb), (char *)(g.param_bf16 + c.off), b2}};
-        SDP_TRY(copy_out(ctx, sl, out));
+        SDP_TRY(copy_out(ctx, sl, (int)(j % kOutBufs), out));
         SDP_TRY(poison(ctx, sl));
         HIP_TRY(hipEventRecord(ctx->slot_free[sl], ctx->s_comp));
         used[sl] = true;
-        // staged: move the previous chunk's results out while this one is in flight
-        if (staged(ctx)) SDP_TRY(drain(ctx, sl ^ 1));
+        // staged: move the previous chunk's results out while this one's
+        // incoming copy is in flight
+        if (staged(ctx) && j >= 1) SDP_TRY(drain(ctx, (int)((j - 1) % kOutBufs)));
     }
-    if (staged(ctx)) {
-        SDP_TRY(drain(ctx, 0));
-        SDP_TRY(drain(ctx, 1));
-    }
+    if (staged(ctx) && !chunks.empty()) SDP_TRY(drain(ctx, (int)((chunks.size() - 1) % kOutBufs)));
     return SDP_OK;
 }
 
@@ -1217,12 +1223,13 @@ int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems, int32_t m
             return bail(fail(SDP_ERR_INVALID_ARGUMENT, "SDP_FLAG_STREAM_STAGED needs max_chunk_elems > 0"));
         const size_t out_bytes = 14 * (size_t)max_chunk_elems;
         if (hipHostMalloc(&c->bounce_in, 2 * c->slot_bytes, hipHostMallocDefault) != hipSuccess ||
-            hipHostMalloc(&c->bounce_out, 2 * out_bytes, hipHostMallocDefault) != hipSuccess) {
+            hipHostMalloc(&c->bounce_out, kOutBufs * out_bytes, hipHostMallocDefault) != hipSuccess) {
             (void)hipGetLastError();
             return bail(fail(SDP_ERR_OUT_OF_MEMORY, "cannot allocate %zu bytes of pinned bounce buffers",
-                             2 * (c->slot_bytes + out_bytes)));
+                             2 * c->slot_bytes + kOutBufs * out_bytes));
         }
-        for (int k = 0; k < 2; ++k) CTX_HIP(hipEventCreateWithFlags(&c->d2h_done[k], hipEventDisableTiming));
+        for (int k = 0; k < kOutBufs; ++k)
+            CTX_HIP(hipEventCreateWithFlags(&c->d2h_done[k], hipEventDisableTiming));
         c->copier = new_pool(c, default_host_threads());
     }
     rc = ensure_partials(c, 4096);
@@ -1252,7 +1259,7 @@ void sdp_ctx_destroy(sdp_ctx *ctx) {
     if (ctx->bounce_in) (void)hipHostFree(ctx->bounce_in);
     if (ctx->stage) (void)hipHostFree(ctx->stage);
     if (ctx->bounce_out) (void)hipHostFree(ctx->bounce_out);
-    for (int k = 0; k < 2; ++k)
+    for (int k = 0; k < kOutBufs; ++k)
         if (ctx->d2h_done[k]) (void)hipEventDestroy(ctx->d2h_done[k]);
     delete ctx->copier;
     if (ctx->partials) (void)hipFree(ctx->partials);
@@ -1325,6 +1332,9 @@ int sdp_stream_step(sdp_ctx *ctx, const sdp_segment *host_segs, int32_t n_segs, 
     }
     rc = stream_update_phase(ctx, host_segs, R, plan, chunks, store, hp, used, chunks.size());
     int rc2 = sync_streams(ctx);
+    // after a failure, results still waiting in bounce buffers belong to this
+    // call only: never let a later call move them
+    for (auto &xs : ctx->pending_out) xs.clear();
     if (rc != SDP_OK) return rc;
     if (rc2 != SDP_OK) return rc2;
     return mark_done(ctx, ctx->s_comp);

@@ -9,8 +9,9 @@
 //    outgoing copy, the update kernel, and the outgoing copies on the
 //    compute stream, all issued after the read-back;
 //  - staged variant: host-thread copies into the pinned bounce buffer before
-//    each incoming copy (after that buffer's previous copy left it) and out
-//    of it after each outgoing copy, in the host thread's own order;
+//    each incoming copy (after that buffer's previous copy left it), and out
+//    of outgoing buffer j mod 2 once chunk j+1 is issued, in the host
+//    thread's own order;
 //  - host-update route: the norm pass and read-back, then per piece (the
 //    chunks, the first one split into a ramp) the mean-gradient kernel
 //    (after the slot's previous outgoing copy, and issued by the host after
@@ -247,9 +248,15 @@ void build_streamed(Graph &g, const std::vector<int64_t> &numels, int R, int64_t
     const int rb = g.add(kHostS, kFixed, r.sync_us, 0, 0, {fin});
     const size_t k0 = ch.size();
     int d2h_slot[2] = {-1, -1};
-    int prev_d2h = -1;
-    double prev_len = 0.0;
+    // staged: chunk j's results go to outgoing buffer j % 2 and are drained
+    // after chunk j+1 is issued
+    std::vector<int> d2h_of, drain_of;
     const double in_bpe = 12.0 + (store ? 0.0 : 2.0 * R);
+    auto drain = [&](size_t i) {
+        drain_of[i] = g.host(2.0 * 14.0 * (double)ch[i].len, r.host_gbs, r.host_task_us, {d2h_of[i]});
+    };
+    d2h_of.assign(ch.size(), -1);
+    drain_of.assign(ch.size(), -1);
     for (size_t j = 0; j < ch.size(); ++j) {
         const int sl = (int)((j + k0) & 1);
         const double len = (double)ch[j].len;
@@ -260,14 +267,13 @@ void build_streamed(Graph &g, const std::vector<int64_t> &numels, int R, int64_t
         const int upd = g.add(kCompS, kFixed, kernel_us((26.0 + (store ? 4.0 : 2.0 * R)) * len, r.update_gbs, r), 0,
                               0, {h2d, rb});
         const int out_cmds = (staged && ch[j].full) ? 1 : 4;
-        const int d2h = g.add(kCompS, kD2H, 0, 14.0 * len, out_cmds, {upd, hin});
-        if (staged && prev_d2h >= 0) g.host(2.0 * 14.0 * prev_len, r.host_gbs, r.host_task_us, {prev_d2h});
+        const int buf_free = (staged && j >= 2) ? drain_of[j - 2] : -1;
+        d2h_of[j] = g.add(kCompS, kD2H, 0, 14.0 * len, out_cmds, {upd, hin, buf_free});
+        if (staged && j >= 1) drain(j - 1);
         bin_h2d[sl] = h2d;
-        d2h_slot[sl] = d2h;
-        prev_d2h = d2h;
-        prev_len = len;
+        d2h_slot[sl] = d2h_of[j];
     }
-    if (staged && prev_d2h >= 0) g.host(2.0 * 14.0 * prev_len, r.host_gbs, r.host_task_us, {prev_d2h});
+    if (staged && !ch.empty()) drain(ch.size() - 1);
 }
 
 void build_host_route(Graph &g, const std::vector<int64_t> &numels, int R, int64_t C, bool bf16, const Rates &r) {

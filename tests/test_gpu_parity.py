@@ -241,6 +241,27 @@ def test_staged_streamed_matches_device_and_oracle(sdp, ctx, ctx_staged, ctx_sta
     assert e.value.status == sdp.SDP_ERR_INVALID_ARGUMENT
 
 
+@pytest.mark.parametrize("sizes", [[5], [TILE + 3], [TILE, 7], [2 * TILE + 1, TILE]])
+def test_staged_streamed_few_chunks(sdp, ctx, ctx_staged, sizes):
+    """One to four chunks: the staged mode's moves out of its outgoing bounce
+    buffers finish every chunk, the last one included, and equal device
+    mode."""
+    R = 2
+    masters, grads = rand_inputs(sizes, R, 2, seed=71 + len(sizes))
+    dev = DevState(masters, R)
+    host = PageableState(sdp, masters, R)
+    try:
+        for t in (1, 2):
+            hs = sdp.make_params(lr=1e-3, weight_decay=0.05, max_grad_norm=0.2, step=t)
+            dn = dev_step(sdp, ctx, dev, grads[t - 1], hs)
+            host.set_grads(grads[t - 1])
+            sn = sdp.sdp_stream_step(ctx_staged, host.segments(), hs, TILE)
+            assert sn == dn
+            assert states_equal(host.host(), dev.host()), f"step {t}"
+    finally:
+        host.close()
+
+
 @pytest.mark.parametrize("mode", ["host_cast", "device_cast"])
 def test_deliver_params(sdp, ctx, mode):
     """Parameter delivery: the device BF16 window equals bf16(host master),
