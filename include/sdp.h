@@ -57,6 +57,9 @@
 extern "C" {
 #endif
 
+/* Every entry point below is exported from libsdp.so; nothing else is. */
+#define SDP_API __attribute__((visibility("default")))
+
 /* ---- status codes ------------------------------------------------------ */
 #define SDP_OK 0
 #define SDP_ERR_INVALID_ARGUMENT (-1)  /* NULL pointer, bad size, R out of range, aliasing */
@@ -150,9 +153,9 @@ typedef struct {
  * max_ranks in 1..SDP_MAX_RANKS bounds R for streamed mode staging.  The
  * context creates two streams (default priority) and its events.  Other
  * workspace (norm partials, cached g_bar) grows on demand. */
-int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems,
+SDP_API int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems,
                    int32_t max_ranks, uint32_t flags);
-void sdp_ctx_destroy(sdp_ctx *ctx);
+SDP_API void sdp_ctx_destroy(sdp_ctx *ctx);
 
 /* ---- the update -------------------------------------------------------- */
 
@@ -169,7 +172,7 @@ void sdp_ctx_destroy(sdp_ctx *ctx);
  * grad_norm_out a non-finite norm still leaves the states unchanged, and
  * sdp_ctx_last_norm() reports it after the stream has finished.  The caller
  * keeps the buffers alive until the stream has finished the work. */
-int sdp_agg_adam_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs,
+SDP_API int sdp_agg_adam_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs,
                       const sdp_adamw_params *hp, int64_t chunk_elems,
                       void *stream, double *grad_norm_out);
 
@@ -185,7 +188,7 @@ int sdp_agg_adam_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs,
  * on the compute stream, again double-buffered.  Blocks until every copy
  * has landed.  Returns SDP_ERR_NONFINITE (states unchanged) for a
  * non-finite norm.  grad_norm_out may be NULL. */
-int sdp_stream_step(sdp_ctx *ctx, const sdp_segment *host_segs, int32_t n_segs,
+SDP_API int sdp_stream_step(sdp_ctx *ctx, const sdp_segment *host_segs, int32_t n_segs,
                     const sdp_adamw_params *hp, int64_t chunk_elems,
                     double *grad_norm_out);
 
@@ -215,7 +218,7 @@ int sdp_stream_step(sdp_ctx *ctx, const sdp_segment *host_segs, int32_t n_segs,
  * norm.  grad_norm_out may be NULL.  Host threads: sdp_ctx_set_host_threads,
  * else SDP_STAGING_THREADS, else up to 16.  The first call creates them and
  * the two pinned stage buffers if the context has none. */
-int sdp_host_update_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs,
+SDP_API int sdp_host_update_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs,
                          const sdp_adamw_params *hp, int64_t chunk_elems, int gbar_format,
                          double *grad_norm_out);
 
@@ -228,33 +231,33 @@ int sdp_host_update_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs,
  * ctx may be NULL: the calling thread does the work and no GPU is needed;
  * else the context's host threads share it.  Buffers 16-byte aligned and
  * pairwise disjoint. */
-int sdp_host_adamw(sdp_ctx *ctx, float *master, float *exp_avg, float *exp_avg_sq,
+SDP_API int sdp_host_adamw(sdp_ctx *ctx, float *master, float *exp_avg, float *exp_avg_sq,
                    uint16_t *param_bf16, const void *gbar, int gbar_format, int64_t n,
                    double clip_coef, const sdp_adamw_params *hp);
 
 /* Host threads of a context (the calling thread counts as one): they run the
  * staged mode's bounce copies, the host BF16 cast and the host AdamW.
  * threads in 1..256; replaces the context's thread pool. */
-int sdp_ctx_set_host_threads(sdp_ctx *ctx, int32_t threads);
-int sdp_ctx_host_threads(sdp_ctx *ctx, int32_t *threads_out);
+SDP_API int sdp_ctx_set_host_threads(sdp_ctx *ctx, int32_t threads);
+SDP_API int sdp_ctx_host_threads(sdp_ctx *ctx, int32_t *threads_out);
 
 /* The global norm of the mean gradient alone (the first pass and finalize of
  * either mode; device_resident selects device or pinned-host buffers; only
  * grads, n_ranks and numel of each segment are read).  Blocks; chunk_elems
  * is used in streamed mode only.  Stores the norm even if it is not finite
  * and then returns SDP_ERR_NONFINITE. */
-int sdp_grad_norm(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs,
+SDP_API int sdp_grad_norm(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs,
                   int device_resident, int64_t chunk_elems, void *stream,
                   double *norm_out);
 
 /* Norm, clip coefficient and non-finite flag of the last finished norm pass
  * on this context (waits for the context's pending work). */
-int sdp_ctx_last_norm(sdp_ctx *ctx, double *norm, double *clip_coef, int *nonfinite);
+SDP_API int sdp_ctx_last_norm(sdp_ctx *ctx, double *norm, double *clip_coef, int *nonfinite);
 
 /* The BF16 re-emit on its own: dst[i] = bf16_rne(src[i]) for n elements of
  * device memory (the same device routine the fused update uses).  NaN keeps
  * its sign and top payload bits and gets the quiet bit. */
-int sdp_cast_bf16(sdp_ctx *ctx, const float *src, uint16_t *dst, int64_t n, void *stream);
+SDP_API int sdp_cast_bf16(sdp_ctx *ctx, const float *src, uint16_t *dst, int64_t n, void *stream);
 
 /* ---- parameter delivery ------------------------------------------------ */
 
@@ -274,14 +277,14 @@ int sdp_cast_bf16(sdp_ctx *ctx, const float *src, uint16_t *dst, int64_t n, void
  * the context's host threads and its two pinned stage buffers (4 *
  * max_chunk_elems bytes each, shared with sdp_host_update_step) if it has
  * none. */
-int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf16, int64_t n,
+SDP_API int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf16, int64_t n,
                        int64_t chunk_elems, int mode);
 
 /* The BF16 rounding of the host delivery lane on its own: dst[i] =
  * bf16_rne(src[i]) for n elements of host memory.  ctx may be NULL (runs on
  * the calling thread, no GPU needed) or a context whose host threads share
  * the work. */
-int sdp_cast_bf16_host(sdp_ctx *ctx, const float *src, uint16_t *dst, int64_t n);
+SDP_API int sdp_cast_bf16_host(sdp_ctx *ctx, const float *src, uint16_t *dst, int64_t n);
 
 /* ---- step-time model (host only, no GPU needed) --------------------------- */
 
@@ -330,7 +333,7 @@ typedef struct {
  * directions together at the bidirectional rate, split in proportion), and
  * host-thread tasks share host memory with the DMA (a task moves at most
  * host_gbs minus the copies' current rate, and at most its own rate). */
-int sdp_predict_step(int schedule, const int64_t *numels, int32_t n_segs, int32_t n_ranks,
+SDP_API int sdp_predict_step(int schedule, const int64_t *numels, int32_t n_segs, int32_t n_ranks,
                      int64_t chunk_elems, uint32_t flags, const sdp_rates *rates,
                      sdp_prediction *out);
 
@@ -338,7 +341,7 @@ int sdp_predict_step(int schedule, const int64_t *numels, int32_t n_segs, int32_
  * policy): the candidate (each a positive multiple of SDP_NORM_TILE) with the
  * smallest predicted step time, the first one on a tie; predicted_ms_out, if
  * not NULL, receives every candidate's prediction. */
-int sdp_tune_chunk(int schedule, const int64_t *numels, int32_t n_segs, int32_t n_ranks,
+SDP_API int sdp_tune_chunk(int schedule, const int64_t *numels, int32_t n_segs, int32_t n_ranks,
                    uint32_t flags, const sdp_rates *rates, const int64_t *candidates,
                    int32_t n_candidates, int64_t *best_out, double *predicted_ms_out);
 
@@ -346,26 +349,26 @@ int sdp_tune_chunk(int schedule, const int64_t *numels, int32_t n_segs, int32_t 
 
 /* Chunks and norm tiles of a call: n_chunks = sum over segments of
  * ceil(numel / chunk_elems), n_tiles = sum of ceil(numel / SDP_NORM_TILE). */
-int sdp_plan(const int64_t *numels, int32_t n_segs, int64_t chunk_elems,
+SDP_API int sdp_plan(const int64_t *numels, int32_t n_segs, int64_t chunk_elems,
              int64_t *n_chunks_out, int64_t *n_tiles_out);
 
 /* Algorithmic bytes per element of one step: device mode HBM traffic, or
  * streamed mode host-link traffic per direction (h2d, d2h), for R ranks and
  * the given context flags' g_bar policy. */
-int sdp_bytes_per_elem(int streamed, int32_t n_ranks, uint32_t flags,
+SDP_API int sdp_bytes_per_elem(int streamed, int32_t n_ranks, uint32_t flags,
                        double *hbm_or_h2d, double *d2h);
 
 /* ---- measurement support ---------------------------------------------- */
 
 /* Start (enable = 1, also clears) or stop (0) per-kernel event timing. */
-int sdp_ctx_set_timing(sdp_ctx *ctx, int enable);
+SDP_API int sdp_ctx_set_timing(sdp_ctx *ctx, int enable);
 /* Sum of the recorded kernel times (waits for the recorded events). */
-int sdp_ctx_get_timing(sdp_ctx *ctx, sdp_kernel_times *out);
+SDP_API int sdp_ctx_get_timing(sdp_ctx *ctx, sdp_kernel_times *out);
 
 /* Device-to-device copy of `bytes` (a multiple of 16) with the library's
  * 16-byte-per-lane streaming pattern: the HBM ceiling and the scale for
  * hardware traffic counters. */
-int sdp_probe_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, void *stream);
+SDP_API int sdp_probe_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, void *stream);
 
 /* Pinned host link bandwidth with the streamed engine's copy path:
  * hipMemcpyAsync in chunk_bytes pieces over `bytes`, `reps` times, host to
@@ -376,7 +379,7 @@ int sdp_probe_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, void
  * [2] = H2D and D2H at once (sum of both directions).  host_a/host_b:
  * pinned host buffers, dev_a/dev_b: device buffers, each of at least
  * `bytes`.  Blocks. */
-int sdp_probe_link(sdp_ctx *ctx, void *host_a, void *host_b, void *dev_a, void *dev_b,
+SDP_API int sdp_probe_link(sdp_ctx *ctx, void *host_a, void *host_b, void *dev_a, void *dev_b,
                    int64_t bytes, int64_t chunk_bytes, int32_t reps, double *gbs_out);
 
 /* Host memory bandwidth of the context's host threads: `bytes` copied from
@@ -384,17 +387,17 @@ int sdp_probe_link(sdp_ctx *ctx, void *host_a, void *host_b, void *dev_a, void *
  * threads; gbs_out = bytes read plus bytes written per second / 1e9.  The
  * ceiling of the host lanes (bounce copies, host cast, host AdamW).  Blocks;
  * no GPU work. */
-int sdp_probe_host_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, int32_t reps,
+SDP_API int sdp_probe_host_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, int32_t reps,
                         double *gbs_out);
 
 /* Pinned host memory of exactly `bytes` (hipHostMalloc), for streamed-mode
  * states; free with sdp_host_free. */
-int sdp_host_alloc(void **out, size_t bytes);
-int sdp_host_free(void *p);
+SDP_API int sdp_host_alloc(void **out, size_t bytes);
+SDP_API int sdp_host_free(void *p);
 
 /* ---- errors ------------------------------------------------------------ */
-const char *sdp_status_string(int status);
-const char *sdp_last_error(void);
+SDP_API const char *sdp_status_string(int status);
+SDP_API const char *sdp_last_error(void);
 
 #ifdef __cplusplus
 }

@@ -7,18 +7,21 @@ import tempfile
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB_PATH = os.path.join(HERE, "libsdp.so")
-SOURCES = [os.path.join(HERE, "csrc", f) for f in ("sdp_runtime.hip", "sdp_kernels.hip")]
+SOURCES = [os.path.join(HERE, "csrc", f)
+           for f in ("sdp_runtime.hip", "sdp_stream.hip", "sdp_host_route.hip", "sdp_kernels.hip")]
 # host-only lanes, built with the host compiler: no fused multiply-add, so the
 # FP64 update rounds every product and sum as written
 HOST_SOURCES = [os.path.join(HERE, "csrc", f) for f in ("sdp_host_adamw.cpp", "sdp_schedule.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 HOSTCXX = os.environ.get("SDP_HOSTCXX", "/opt/rocm/llvm/bin/clang++")
-HOST_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off", "-fno-math-errno", "-Wall"]
+HOST_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off", "-fno-math-errno", "-Wall", "-fvisibility=hidden"]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     # no packed FP32 instructions in device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
+    # only the C ABI (SDP_API in sdp.h) is exported
+    "-fvisibility=hidden",
 ]
 
 

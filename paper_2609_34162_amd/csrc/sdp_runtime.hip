@@ -1,52 +1,17 @@
-// C ABI of libsdp: context, argument validation, the device-mode driver, the
-// streamed engine, parameter delivery and the host-update route.  Kernels
-// live in sdp_kernels.hip, the host AdamW lane in sdp_host_adamw.cpp and the
+// C ABI of libsdp, core: errors, the context, argument validation, the
+// device-mode driver, measurement support and the step-time model's entry
+// points.  The streamed engine is in sdp_stream.hip, parameter delivery and
+// the host-update route in sdp_host_route.hip, the kernels in
+// sdp_kernels.hip, the host AdamW lane in sdp_host_adamw.cpp and the
 // step-time model in sdp_schedule.cpp.
 //
 // Device mode (sdp_agg_adam_step): per call, one norm-partials launch per
 // segment, one finalize launch, one fused-update launch per segment, all on
 // the caller's stream.  The clip coefficient stays in device memory.
-//
-// Streamed mode (sdp_stream_step): states live in pinned host memory and
-// move through two device staging slots.  A copy stream carries host-to-
-// device copies; a compute stream runs the kernels and the device-to-host
-// copies.  Events h2d_done[s] and slot_free[s] order each slot's reuse: a
-// slot is refilled only after its previous consumer finished (the paper's
-// buffer-reuse rule, Design, completion and buffer reuse), and the update of
-// a chunk starts as soon as its copy has landed (chunked overlap within a
-// layer).  Phase 1 streams the gradients for the global norm; phase 2
-// streams master/m/v through the fused update and back.
-//
-// Host-update route (sdp_host_update_step): the gradients stay in device
-// memory; the GPU computes the norm and, piece by piece, the mean gradient,
-// which the copy stream moves into pinned stage buffers while the host
-// threads run AdamW on the states in host memory.
-#include <algorithm>
-#include <atomic>
-#include <chrono>
-#include <condition_variable>
-#include <mutex>
-#include <thread>
-
-#include <pthread.h>
-#include <sched.h>
-#include <cmath>
-#include <cstdarg>
-#include <cstdio>
-#include <cstdlib>
-#include <cstring>
-#include <functional>
-#include <limits>
-#include <string>
-#include <vector>
-
-#include "sdp_host.h"
+#include "sdp_rt.h"
 #include "sdp_schedule.h"
-#include "sdp_internal.h"
 
-using sdp::NormState;
-
-namespace {
+namespace sdprt {
 
 thread_local std::string t_err;
 
@@ -59,43 +24,6 @@ int fail(int status, const char *fmt, ...) {
     t_err = buf;
     return status;
 }
-
-#define HIP_TRY(expr)                                                                        \
-    do {                                                                                     \
-        hipError_t e_ = (expr);                                                              \
-        if (e_ != hipSuccess)                                                                \
-            return fail(SDP_ERR_HIP, "%s failed: %s (%s:%d)", #expr, hipGetErrorString(e_),   \
-                        __FILE__, __LINE__);                                                 \
-    } while (0)
-
-#define SDP_TRY(expr)              \
-    do {                           \
-        int rc_ = (expr);          \
-        if (rc_ != SDP_OK) return rc_; \
-    } while (0)
-
-inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
-inline int64_t round_up(int64_t a, int64_t b) { return cdiv(a, b) * b; }
-
-struct DeviceGuard {
-    int old = -1;
-    explicit DeviceGuard(int d) {
-        if (hipGetDevice(&old) != hipSuccess) old = -1;
-        if (old != d) (void)hipSetDevice(d);
-    }
-    ~DeviceGuard() {
-        int cur = -1;
-        if (old >= 0 && hipGetDevice(&cur) == hipSuccess && cur != old) (void)hipSetDevice(old);
-    }
-};
-
-enum TimedKind { kNorm = 0, kFinalize = 1, kUpdate = 2, kGbar = 3 };
-
-struct Timed {
-    int kind;
-    hipEvent_t a, b;
-    int64_t elems;
-};
 
 // Round FP32 values to BF16, nearest even, on the host (the parameter
 // delivery lane).  NaN keeps its sign and top payload bits and gets the quiet
@@ -110,111 +38,6 @@ void cast_bf16_host(const float *src, uint16_t *dst, size_t n) {
         dst[i] = (uint16_t)r;
     }
 }
-
-// A fixed set of host threads for the host lanes: copies between the
-// caller's memory and the staged mode's pinned bounce buffers (the CPU-side
-// staging lane of the paper's chunked overlap, Design, overlap within a
-// layer), the BF16 rounding of parameter delivery and the host AdamW of the
-// host-update route.  run(n, fn) calls fn(i) for every i in [0, n) across
-// the workers and the caller.
-class HostPool {
-  public:
-    // pin: worker i stays on the (i+1)-th CPU of the process's affinity set
-    // (cyclically), leaving the first to the calling thread.
-    HostPool(int workers, bool pin) {
-        std::vector<int> cpus;
-        if (pin) {
-            cpu_set_t set;
-            CPU_ZERO(&set);
-            if (sched_getaffinity(0, sizeof set, &set) == 0)
-                for (int c = 0; c < CPU_SETSIZE; ++c)
-                    if (CPU_ISSET(c, &set)) cpus.push_back(c);
-        }
-        for (int i = 0; i < workers; ++i) {
-            const int cpu = cpus.empty() ? -1 : cpus[(size_t)(i + 1) % cpus.size()];
-            threads_.emplace_back([this, cpu] {
-                if (cpu >= 0) {
-                    cpu_set_t one;
-                    CPU_ZERO(&one);
-                    CPU_SET(cpu, &one);
-                    (void)pthread_setaffinity_np(pthread_self(), sizeof one, &one);
-                }
-                loop();
-            });
-        }
-    }
-    ~HostPool() {
-        {
-            std::lock_guard<std::mutex> g(mu_);
-            stop_ = true;
-        }
-        cv_work_.notify_all();
-        for (auto &t : threads_) t.join();
-    }
-    int size() const { return (int)threads_.size() + 1; }
-
-    void run(size_t n, const std::function<void(size_t)> &fn) {
-        std::unique_lock<std::mutex> g(mu_);
-        fn_ = &fn;
-        n_ = n;
-        next_ = 0;
-        left_ = n;
-        ++gen_;
-        g.unlock();
-        cv_work_.notify_all();
-        work();
-        g.lock();
-        cv_done_.wait(g, [this] { return left_ == 0; });
-        fn_ = nullptr;
-    }
-
-  private:
-    void work() {
-        for (;;) {
-            size_t k;
-            const std::function<void(size_t)> *fn;
-            {
-                std::lock_guard<std::mutex> g(mu_);
-                if (next_ >= n_) return;
-                k = next_++;
-                fn = fn_;
-            }
-            (*fn)(k);
-            std::lock_guard<std::mutex> g(mu_);
-            if (--left_ == 0) cv_done_.notify_all();
-        }
-    }
-    void loop() {
-        uint64_t seen = 0;
-        for (;;) {
-            {
-                std::unique_lock<std::mutex> g(mu_);
-                cv_work_.wait(g, [&] { return stop_ || gen_ != seen; });
-                if (stop_) return;
-                seen = gen_;
-            }
-            work();
-        }
-    }
-
-    std::vector<std::thread> threads_;
-    std::mutex mu_;
-    std::condition_variable cv_work_, cv_done_;
-    const std::function<void(size_t)> *fn_ = nullptr;
-    size_t n_ = 0, next_ = 0, left_ = 0;
-    uint64_t gen_ = 0;
-    bool stop_ = false;
-};
-
-// Copies (kind kCopy: `bytes`) and BF16 roundings (kind kCastBf16: `bytes`
-// FP32 values at src into BF16 at dst), split into pieces over the pool.
-struct Job {
-    enum Kind { kCopy = 0, kCastBf16 = 1 };
-    void *dst;
-    const void *src;
-    size_t bytes;
-    int kind = kCopy;
-};
 
 void pool_jobs(HostPool *pool, const std::vector<Job> &jobs) {
     constexpr size_t kPiece = 4u << 20;      // bytes per copy piece
@@ -239,64 +62,6 @@ void pool_jobs(HostPool *pool, const std::vector<Job> &jobs) {
     });
 }
 
-// Staged mode: outgoing bounce buffers.  Chunk j's results land in buffer
-// j % kOutBufs; the host threads move chunk j-1's out as soon as they have
-// landed, while chunk j's incoming copy runs.  Deferring that by one more
-// chunk (three buffers) lets the host copies overlap the next outgoing DMA,
-// which on the MI355X hosts measured here slowed the DMA enough to lose
-// 25% of the step.
-constexpr int kOutBufs = 2;
-
-// A host <-> staging-slot transfer of one chunk: `bytes` at byte offset `off`
-// of a slot, from or to `host`.
-struct Xfer {
-    size_t off;
-    char *host;
-    size_t bytes;
-};
-
-}  // namespace
-
-struct sdp_ctx {
-    int device = 0;
-    int64_t max_chunk = 0;
-    int32_t max_ranks = 0;
-    uint32_t flags = 0;
-    hipStream_t s_copy = nullptr, s_comp = nullptr;
-    hipEvent_t h2d_done[2] = {nullptr, nullptr};
-    hipEvent_t slot_free[2] = {nullptr, nullptr};
-    hipEvent_t last_done = nullptr;
-    bool last_done_valid = false;
-    char *staging = nullptr;
-    size_t slot_bytes = 0;
-    // staged streamed mode: pinned bounce buffers shaped like the slots
-    char *bounce_in = nullptr;   // 2 x slot_bytes
-    char *bounce_out = nullptr;  // kOutBufs x 14 * max_chunk (master, m, v, bf16 part of a slot)
-    hipEvent_t d2h_done[kOutBufs] = {nullptr, nullptr};
-    bool bin_used[2] = {false, false};
-    // parameter delivery and the host-update route: two pinned buffers of
-    // 4 * max_chunk bytes each (one chunk of FP32), created on first use
-    char *stage = nullptr;
-    bool stage_used[2] = {false, false};
-    std::vector<Xfer> pending_out[kOutBufs];
-    HostPool *copier = nullptr;
-    double *partials = nullptr;
-    int64_t partials_cap = 0;
-    float *gbar = nullptr;
-    int64_t gbar_cap = 0;
-    NormState *ns = nullptr;       // device
-    NormState *ns_host = nullptr;  // pinned mirror for read-back
-    int update_max_blocks = 0;     // 0: one 8-element group per lane
-    bool timing = false;
-    std::vector<Timed> timed;
-    // host lanes of the host-update route, timed on the host clock
-    double host_adam_ms = 0.0, host_wait_ms = 0.0;
-    int64_t host_adam_elems = 0;
-    std::vector<hipEvent_t> pool;
-};
-
-namespace {
-
 // ---- validation ---------------------------------------------------------
 
 int check_hparams(const sdp_adamw_params *hp) {
@@ -310,8 +75,6 @@ int check_hparams(const sdp_adamw_params *hp) {
     if (hp->eps < 0.0) return fail(SDP_ERR_INVALID_ARGUMENT, "eps must be >= 0");
     return SDP_OK;
 }
-
-bool aligned(const void *p) { return ((uintptr_t)p % SDP_ALIGN) == 0; }
 
 int check_device_ptr(const sdp_ctx *ctx, const void *p, size_t bytes, const char *what, int seg) {
     hipPointerAttribute_t at;
@@ -364,16 +127,6 @@ int check_host_ptr(const void *p, const char *what, int seg) {
     }
     return SDP_OK;
 }
-
-enum MemKind { kDeviceMem, kPinnedHost, kAnyHost };
-
-struct Range {
-    uintptr_t a, b;
-    int seg;
-    const char *what;
-};
-
-bool overlap(const Range &x, const Range &y) { return x.a < y.b && y.a < x.b; }
 
 // Checks every segment of a call; returns R and the per-segment sizes.
 int validate_segments(const sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, MemKind state_kind,
@@ -480,12 +233,6 @@ int ensure_gbar(sdp_ctx *ctx, int64_t n) {
     return SDP_OK;
 }
 
-// Layout of one call: norm tiles and stored-g_bar offsets of each segment.
-struct Plan {
-    std::vector<int64_t> tile_base, gbar_base;
-    int64_t tiles = 0, gbar_elems = 0;
-};
-
 Plan make_plan(const sdp_segment *segs, int32_t n_segs) {
     Plan p;
     for (int32_t s = 0; s < n_segs; ++s) {
@@ -542,7 +289,7 @@ void timed_end(sdp_ctx *ctx, hipStream_t s, hipEvent_t a, int kind, int64_t elem
     ctx->timed.push_back({kind, a, b, elems});
 }
 
-// ---- launches shared by both modes ---------------------------------------
+// ---- launches shared by the modes ------------------------------------------
 
 int norm_launch(sdp_ctx *ctx, int32_t R, const uint16_t *const *g, int64_t n, double *partials, float *gbar_out,
                 hipStream_t s) {
@@ -616,6 +363,12 @@ int read_norm(sdp_ctx *ctx, hipStream_t s, NormState *out) {
     return SDP_OK;
 }
 
+int sync_streams(sdp_ctx *ctx) {
+    HIP_TRY(hipStreamSynchronize(ctx->s_copy));
+    HIP_TRY(hipStreamSynchronize(ctx->s_comp));
+    return SDP_OK;
+}
+
 // ---- device mode ----------------------------------------------------------
 
 int device_norm(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R, const Plan &plan, bool store_gbar,
@@ -626,13 +379,7 @@ int device_norm(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R
     return finalize_launch(ctx, plan.tiles, max_grad_norm, s);
 }
 
-// ---- streamed mode --------------------------------------------------------
-
-struct Slot {
-    float *p, *m, *v;
-    uint16_t *pb;
-    uint16_t *g[SDP_MAX_RANKS];
-};
+// ---- chunks and staging slots -------------------------------------------
 
 Slot slot_at(const sdp_ctx *ctx, int k) {
     Slot sl{};
@@ -646,11 +393,6 @@ Slot slot_at(const sdp_ctx *ctx, int k) {
     return sl;
 }
 
-struct Chunk {
-    int32_t seg;
-    int64_t off, len;
-};
-
 std::vector<Chunk> make_chunks(const sdp_segment *segs, int32_t n_segs, int64_t C) {
     std::vector<Chunk> out;
     for (int32_t s = 0; s < n_segs; ++s)
@@ -659,150 +401,25 @@ std::vector<Chunk> make_chunks(const sdp_segment *segs, int32_t n_segs, int64_t 
     return out;
 }
 
-int poison(sdp_ctx *ctx, int k) {
-    if (!(ctx->flags & SDP_FLAG_DEBUG_POISON)) return SDP_OK;
-    HIP_TRY(sdp::launch_fill_u32(ctx->staging + (size_t)k * ctx->slot_bytes, (int64_t)(ctx->slot_bytes / 4),
-                                 0xFFC0FFC0u, ctx->s_comp));
-    return SDP_OK;
-}
-
-bool staged(const sdp_ctx *ctx) { return (ctx->flags & SDP_FLAG_STREAM_STAGED) != 0; }
-
 size_t off_in_slot(const sdp_ctx *ctx, int sl, const void *p) {
     return (size_t)((const char *)p - (ctx->staging + (size_t)sl * ctx->slot_bytes));
 }
 
-// Runs of transfers that are contiguous in the slot, for the bounce copies.
-std::vector<Xfer> merge_runs(std::vector<Xfer> xs) {
-    std::sort(xs.begin(), xs.end(), [](const Xfer &a, const Xfer &b) { return a.off < b.off; });
-    std::vector<Xfer> runs;
-    for (const Xfer &x : xs) {
-        if (!runs.empty() && runs.back().off + runs.back().bytes == x.off)
-            runs.back().bytes += x.bytes;
-        else
-            runs.push_back({x.off, nullptr, x.bytes});
-    }
-    return runs;
-}
-
-// Host -> slot `sl` copies of one chunk, enqueued on the copy stream.  In the
-// staged mode the host threads first copy into the slot's pinned bounce
-// buffer, after waiting for that buffer's previous copy to leave it.
-int copy_in(sdp_ctx *ctx, int sl, const std::vector<Xfer> &xs) {
-    char *dev = ctx->staging + (size_t)sl * ctx->slot_bytes;
-    if (!staged(ctx)) {
-        for (const Xfer &x : xs)
-            HIP_TRY(hipMemcpyAsync(dev + x.off, x.host, x.bytes, hipMemcpyHostToDevice, ctx->s_copy));
-        return SDP_OK;
-    }
-    char *bin = ctx->bounce_in + (size_t)sl * ctx->slot_bytes;
-    if (ctx->bin_used[sl]) HIP_TRY(hipEventSynchronize(ctx->h2d_done[sl]));
-    std::vector<Job> jobs;
-    for (const Xfer &x : xs) jobs.push_back({bin + x.off, x.host, x.bytes});
-    pool_jobs(ctx->copier, jobs);
-    for (const Xfer &r : merge_runs(xs))
-        HIP_TRY(hipMemcpyAsync(dev + r.off, bin + r.off, r.bytes, hipMemcpyHostToDevice, ctx->s_copy));
-    ctx->bin_used[sl] = true;
+int stream_common_checks(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int64_t chunk, bool grads_only,
+                         int32_t *R) {
+    if (!ctx->staging) return fail(SDP_ERR_CHUNK_TOO_LARGE, "context was created without streamed-mode staging");
+    SDP_TRY(check_chunk(chunk, false));
+    if (chunk > ctx->max_chunk)
+        return fail(SDP_ERR_CHUNK_TOO_LARGE, "chunk_elems %lld exceeds the context's %lld", (long long)chunk,
+                    (long long)ctx->max_chunk);
+    const MemKind host_kind = (ctx->flags & SDP_FLAG_STREAM_STAGED) ? kAnyHost : kPinnedHost;
+    SDP_TRY(validate_segments(ctx, segs, n_segs, host_kind, host_kind, grads_only, R));
+    if (*R > ctx->max_ranks)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "n_ranks %d exceeds the context's max_ranks %d", *R, ctx->max_ranks);
     return SDP_OK;
 }
 
-// Slot `sl` -> host copies of one chunk, enqueued on the compute stream.  In
-// the staged mode they land in outgoing bounce buffer `bo` and are moved to
-// their destinations by drain().
-int copy_out(sdp_ctx *ctx, int sl, int bo, const std::vector<Xfer> &xs) {
-    char *dev = ctx->staging + (size_t)sl * ctx->slot_bytes;
-    if (!staged(ctx)) {
-        for (const Xfer &x : xs)
-            HIP_TRY(hipMemcpyAsync(x.host, dev + x.off, x.bytes, hipMemcpyDeviceToHost, ctx->s_comp));
-        return SDP_OK;
-    }
-    char *bout = ctx->bounce_out + (size_t)bo * 14 * (size_t)ctx->max_chunk;
-    for (const Xfer &r : merge_runs(xs))
-        HIP_TRY(hipMemcpyAsync(bout + r.off, dev + r.off, r.bytes, hipMemcpyDeviceToHost, ctx->s_comp));
-    HIP_TRY(hipEventRecord(ctx->d2h_done[bo], ctx->s_comp));
-    ctx->pending_out[bo] = xs;
-    return SDP_OK;
-}
-
-// Staged mode: wait for the outgoing copies into bounce buffer `bo` and move
-// them to their host destinations.
-int drain(sdp_ctx *ctx, int bo) {
-    if (ctx->pending_out[bo].empty()) return SDP_OK;
-    HIP_TRY(hipEventSynchronize(ctx->d2h_done[bo]));
-    char *bout = ctx->bounce_out + (size_t)bo * 14 * (size_t)ctx->max_chunk;
-    std::vector<Job> jobs;
-    for (const Xfer &x : ctx->pending_out[bo]) jobs.push_back({x.host, bout + x.off, x.bytes});
-    pool_jobs(ctx->copier, jobs);
-    ctx->pending_out[bo].clear();
-    return SDP_OK;
-}
-
-// Phase 1: gradients in, norm partials (and stored g_bar) out, then finalize.
-int stream_norm_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R, const Plan &plan,
-                      const std::vector<Chunk> &chunks, bool store_gbar, double max_grad_norm, bool used[2]) {
-    (void)n_segs;
-    for (size_t k = 0; k < chunks.size(); ++k) {
-        const Chunk &c = chunks[k];
-        const int sl = (int)(k & 1);
-        Slot slot = slot_at(ctx, sl);
-        std::vector<Xfer> xs;
-        for (int32_t r = 0; r < R; ++r)
-            xs.push_back({off_in_slot(ctx, sl, slot.g[r]), (char *)(segs[c.seg].grads[r] + c.off), (size_t)c.len * 2});
-        if (used[sl]) HIP_TRY(hipStreamWaitEvent(ctx->s_copy, ctx->slot_free[sl], 0));
-        SDP_TRY(copy_in(ctx, sl, xs));
-        HIP_TRY(hipEventRecord(ctx->h2d_done[sl], ctx->s_copy));
-        HIP_TRY(hipStreamWaitEvent(ctx->s_comp, ctx->h2d_done[sl], 0));
-        const uint16_t *gp[SDP_MAX_RANKS];
-        for (int32_t r = 0; r < R; ++r) gp[r] = slot.g[r];
-        SDP_TRY(norm_launch(ctx, R, gp, c.len, ctx->partials + 2 * (plan.tile_base[c.seg] + c.off / SDP_NORM_TILE),
-                            store_gbar ? ctx->gbar + plan.gbar_base[c.seg] + c.off : nullptr, ctx->s_comp));
-        SDP_TRY(poison(ctx, sl));
-        HIP_TRY(hipEventRecord(ctx->slot_free[sl], ctx->s_comp));
-        used[sl] = true;
-    }
-    return finalize_launch(ctx, plan.tiles, max_grad_norm, ctx->s_comp);
-}
-
-// Phase 2: master/m/v in (and the gradients again unless g_bar is stored),
-// fused update, master/m/v and BF16 parameters back out.
-int stream_update_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t R, const Plan &plan,
-                        const std::vector<Chunk> &chunks, bool stored_gbar, const sdp_adamw_params *hp, bool used[2],
-                        size_t k0) {
-    for (size_t j = 0; j < chunks.size(); ++j) {
-        const Chunk &c = chunks[j];
-        const sdp_segment &g = segs[c.seg];
-        const int sl = (int)((j + k0) & 1);
-        Slot slot = slot_at(ctx, sl);
-        const size_t f4 = (size_t)c.len * 4, b2 = (size_t)c.len * 2;
-        std::vector<Xfer> in = {{off_in_slot(ctx, sl, slot.p), (char *)(g.master + c.off), f4},
-                                {off_in_slot(ctx, sl, slot.m), (char *)(g.exp_avg + c.off), f4},
-                                {off_in_slot(ctx, sl, slot.v), (char *)(g.exp_avg_sq + c.off), f4}};
-        if (!stored_gbar)
-            for (int32_t r = 0; r < R; ++r)
-                in.push_back({off_in_slot(ctx, sl, slot.g[r]), (char *)(g.grads[r] + c.off), b2});
-        if (used[sl]) HIP_TRY(hipStreamWaitEvent(ctx->s_copy, ctx->slot_free[sl], 0));
-        SDP_TRY(copy_in(ctx, sl, in));
-        HIP_TRY(hipEventRecord(ctx->h2d_done[sl], ctx->s_copy));
-        HIP_TRY(hipStreamWaitEvent(ctx->s_comp, ctx->h2d_done[sl], 0));
-        const uint16_t *gp[SDP_MAX_RANKS];
-        for (int32_t r = 0; r < R; ++r) gp[r] = slot.g[r];
-        SDP_TRY(update_launch(ctx, R, hp, slot.p, slot.m, slot.v, slot.pb, gp,
-                              stored_gbar ? ctx->gbar + plan.gbar_base[c.seg] + c.off : nullptr, c.len, ctx->s_comp));
-        std::vector<Xfer> out = {{off_in_slot(ctx, sl, slot.p), (char *)(g.master + c.off), f4},
-                                 {off_in_slot(ctx, sl, slot.m), (char *)(g.exp_avg + c.off), f4},
-                                 {off_in_slot(ctx, sl, slot.v), (char *)(g.exp_avg_sq + c.off), f4},
-                                 {off_in_slot(ctx, sl, slot.pb), (char *)(g.param_bf16 + c.off), b2}};
-        SDP_TRY(copy_out(ctx, sl, (int)(j % kOutBufs), out));
-        SDP_TRY(poison(ctx, sl));
-        HIP_TRY(hipEventRecord(ctx->slot_free[sl], ctx->s_comp));
-        used[sl] = true;
-        // staged: move the previous chunk's results out while this one's
-        // incoming copy is in flight
-        if (staged(ctx) && j >= 1) SDP_TRY(drain(ctx, (int)((j - 1) % kOutBufs)));
-    }
-    if (staged(ctx) && !chunks.empty()) SDP_TRY(drain(ctx, (int)((chunks.size() - 1) % kOutBufs)));
-    return SDP_OK;
-}
+// ---- host threads and pinned stage buffers ------------------------------
 
 // Host threads of a context: SDP_STAGING_THREADS, else the hardware
 // threads, at most 16 (the calling thread counts as one of them).
@@ -815,8 +432,6 @@ int default_host_threads() {
 HostPool *new_pool(const sdp_ctx *ctx, int threads) {
     return new HostPool(threads - 1, (ctx->flags & SDP_FLAG_HOST_PIN_THREADS) != 0);
 }
-
-size_t stage_bytes(const sdp_ctx *ctx) { return 4 * (size_t)ctx->max_chunk; }
 
 // The host threads and the two pinned stage buffers of parameter delivery and
 // the host-update route, created on first use.
@@ -834,138 +449,6 @@ int ensure_host_stage(sdp_ctx *ctx) {
     return SDP_OK;
 }
 
-// ---- host-update route -------------------------------------------------------
-
-sdp_host::AdamConsts host_consts(const sdp_adamw_params *hp, double clip) {
-    sdp::UpdateArgs u{};
-    fill_consts(hp, u);
-    sdp_host::AdamConsts k;
-    k.c = clip;
-    k.lr_wd = u.lr_wd;
-    k.beta1 = u.beta1;
-    k.one_minus_beta1 = u.one_minus_beta1;
-    k.beta2 = u.beta2;
-    k.one_minus_beta2 = u.one_minus_beta2;
-    k.step_size = u.step_size;
-    k.inv_bc2 = u.inv_bc2;
-    k.eps = u.eps;
-    return k;
-}
-
-// Instruction set of the host update: the CPU's best unless SDP_HOST_SIMD=0.
-int host_simd() {
-    if (const char *env = std::getenv("SDP_HOST_SIMD"))
-        if (std::atoi(env) == 0) return sdp_host::kScalar;
-    return sdp_host::simd_best();
-}
-
-// Host AdamW over n elements, in 32,768-element pieces over the pool's
-// threads (on the calling thread alone when pool is NULL).
-void host_adamw(HostPool *pool, const sdp_host::AdamArgs &a, const sdp_host::AdamConsts &k, int64_t n) {
-    constexpr int64_t kPiece = 32768;
-    const int simd = host_simd();
-    const size_t pieces = (size_t)cdiv(n, kPiece);
-    auto body = [&](size_t j) {
-        const int64_t i0 = (int64_t)j * kPiece;
-        sdp_host::adamw_range(a, k, i0, std::min(n, i0 + kPiece), simd);
-    };
-    if (pool)
-        pool->run(pieces, body);
-    else
-        for (size_t j = 0; j < pieces; ++j) body(j);
-}
-
-using Clock = std::chrono::steady_clock;
-
-double ms_between(Clock::time_point a, Clock::time_point b) {
-    return std::chrono::duration<double, std::milli>(b - a).count();
-}
-
-// The host-update route over validated segments (grads in device memory,
-// states in host memory).  Phase 1: the norm pass over the device gradients
-// and the finalize; the norm state comes back to the host.  Phase 2, piece
-// by piece: the GPU writes g_bar of piece j (FP32 or BF16) into device slot
-// j%2 on the compute stream, the copy stream moves it into pinned host buffer
-// j%2, and the host threads update piece j-1 from the other buffer meanwhile.
-// The pieces are the chunks, the first one split into a ramp.
-int host_route(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R, const Plan &plan,
-               const sdp_adamw_params *hp, int64_t C, bool bf16, double *grad_norm_out) {
-    hipStream_t sc = ctx->s_comp, sy = ctx->s_copy;
-    SDP_TRY(device_norm(ctx, segs, n_segs, R, plan, false, hp->max_grad_norm, sc));
-    NormState st{};
-    SDP_TRY(read_norm(ctx, sc, &st));
-    if (grad_norm_out) *grad_norm_out = st.norm;
-    if (st.nonfinite) return fail(SDP_ERR_NONFINITE, "gradient norm is not finite (%g); nothing was updated", st.norm);
-    const sdp_host::AdamConsts k = host_consts(hp, st.clip);
-    // the chunks, the first one split into a ramp of short pieces so that the
-    // host threads start after a short first copy
-    std::vector<Chunk> chunks;
-    {
-        const std::vector<Chunk> whole = make_chunks(segs, n_segs, C);
-        std::vector<int64_t> lens;
-        for (const Chunk &c : whole) lens.push_back(c.len);
-        const std::vector<int64_t> pieces = sdp_sched::route_pieces(lens);
-        const size_t head = pieces.size() - (whole.size() - 1);
-        int64_t off = 0;
-        for (size_t j = 0; j < head; ++j) {
-            chunks.push_back({whole[0].seg, whole[0].off + off, pieces[j]});
-            off += pieces[j];
-        }
-        chunks.insert(chunks.end(), whole.begin() + 1, whole.end());
-    }
-    const size_t esz = bf16 ? 2 : 4;
-    bool used[2] = {false, false};
-    auto issue = [&](size_t j) -> int {
-        const Chunk &c = chunks[j];
-        const int sl = (int)(j & 1);
-        char *dev = ctx->staging + (size_t)sl * ctx->slot_bytes;
-        char *host = ctx->stage + (size_t)sl * stage_bytes(ctx);
-        // the slot's previous copy to the host has read it
-        if (used[sl]) HIP_TRY(hipStreamWaitEvent(sc, ctx->slot_free[sl], 0));
-        sdp::GbarArgs a{};
-        for (int32_t r = 0; r < R; ++r) a.g[r] = segs[c.seg].grads[r] + c.off;
-        a.n = c.len;
-        a.out = dev;
-        a.bf16 = bf16 ? 1 : 0;
-        hipEvent_t t0 = timed_begin(ctx, sc);
-        HIP_TRY(sdp::launch_gbar_out(R, a, sc));
-        timed_end(ctx, sc, t0, kGbar, c.len);
-        // h2d_done doubles as "g_bar of this slot is written" here
-        HIP_TRY(hipEventRecord(ctx->h2d_done[sl], sc));
-        HIP_TRY(hipStreamWaitEvent(sy, ctx->h2d_done[sl], 0));
-        HIP_TRY(hipMemcpyAsync(host, dev, (size_t)c.len * esz, hipMemcpyDeviceToHost, sy));
-        HIP_TRY(hipEventRecord(ctx->slot_free[sl], sy));  // in the host buffer; the slot is free
-        used[sl] = true;
-        return SDP_OK;
-    };
-    if (!chunks.empty()) SDP_TRY(issue(0));
-    for (size_t j = 0; j < chunks.size(); ++j) {
-        // the next chunk's kernel and copy run while the host updates this one
-        if (j + 1 < chunks.size()) SDP_TRY(issue(j + 1));
-        const int sl = (int)(j & 1);
-        const Clock::time_point t0 = Clock::now();
-        HIP_TRY(hipEventSynchronize(ctx->slot_free[sl]));
-        const Clock::time_point t1 = Clock::now();
-        const Chunk &c = chunks[j];
-        const sdp_segment &g = segs[c.seg];
-        sdp_host::AdamArgs a;
-        a.p = g.master + c.off;
-        a.m = g.exp_avg + c.off;
-        a.v = g.exp_avg_sq + c.off;
-        a.pb = g.param_bf16 + c.off;
-        a.gbar = ctx->stage + (size_t)sl * stage_bytes(ctx);
-        a.gbar_bf16 = bf16 ? 1 : 0;
-        host_adamw(ctx->copier, a, k, c.len);
-        if (ctx->timing) {
-            const Clock::time_point t2 = Clock::now();
-            ctx->host_wait_ms += ms_between(t0, t1);
-            ctx->host_adam_ms += ms_between(t1, t2);
-            ctx->host_adam_elems += c.len;
-        }
-    }
-    return SDP_OK;
-}
-
 bool is_pinned_host(const void *p) {
     hipPointerAttribute_t at;
     if (hipPointerGetAttributes(&at, p) != hipSuccess) {
@@ -975,27 +458,9 @@ bool is_pinned_host(const void *p) {
     return at.type == hipMemoryTypeHost;
 }
 
-int sync_streams(sdp_ctx *ctx) {
-    HIP_TRY(hipStreamSynchronize(ctx->s_copy));
-    HIP_TRY(hipStreamSynchronize(ctx->s_comp));
-    return SDP_OK;
-}
+}  // namespace sdprt
 
-int stream_common_checks(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int64_t chunk, bool grads_only,
-                         int32_t *R) {
-    if (!ctx->staging) return fail(SDP_ERR_CHUNK_TOO_LARGE, "context was created without streamed-mode staging");
-    SDP_TRY(check_chunk(chunk, false));
-    if (chunk > ctx->max_chunk)
-        return fail(SDP_ERR_CHUNK_TOO_LARGE, "chunk_elems %lld exceeds the context's %lld", (long long)chunk,
-                    (long long)ctx->max_chunk);
-    const MemKind host_kind = (ctx->flags & SDP_FLAG_STREAM_STAGED) ? kAnyHost : kPinnedHost;
-    SDP_TRY(validate_segments(ctx, segs, n_segs, host_kind, host_kind, grads_only, R));
-    if (*R > ctx->max_ranks)
-        return fail(SDP_ERR_INVALID_ARGUMENT, "n_ranks %d exceeds the context's max_ranks %d", *R, ctx->max_ranks);
-    return SDP_OK;
-}
-
-}  // namespace
+using namespace sdprt;
 
 // ===========================================================================
 // exported
@@ -1056,6 +521,8 @@ int sdp_bytes_per_elem(int streamed, int32_t n_ranks, uint32_t flags, double *hb
     return SDP_OK;
 }
 
+}  // extern "C"
+
 namespace {
 
 int check_model_args(int schedule, const int64_t *numels, int32_t n_segs, int32_t n_ranks, const sdp_rates *r,
@@ -1094,6 +561,8 @@ int model_chunk_ok(const std::vector<int64_t> &sizes, int64_t chunk) {
 }
 
 }  // namespace
+
+extern "C" {
 
 int sdp_predict_step(int schedule, const int64_t *numels, int32_t n_segs, int32_t n_ranks, int64_t chunk_elems,
                      uint32_t flags, const sdp_rates *rates, sdp_prediction *out) {
@@ -1301,45 +770,6 @@ int sdp_agg_adam_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, con
     return SDP_OK;
 }
 
-int sdp_stream_step(sdp_ctx *ctx, const sdp_segment *host_segs, int32_t n_segs, const sdp_adamw_params *hp,
-                    int64_t chunk_elems, double *grad_norm_out) {
-    t_err.clear();
-    if (!ctx) return fail(SDP_ERR_INVALID_ARGUMENT, "context is NULL");
-    SDP_TRY(check_hparams(hp));
-    DeviceGuard guard(ctx->device);
-    int32_t R = 0;
-    SDP_TRY(stream_common_checks(ctx, host_segs, n_segs, chunk_elems, false, &R));
-    const Plan plan = make_plan(host_segs, n_segs);
-    const bool store = !(ctx->flags & SDP_FLAG_STREAM_GBAR_NEVER);
-    SDP_TRY(ensure_partials(ctx, plan.tiles));
-    if (store) SDP_TRY(ensure_gbar(ctx, plan.gbar_elems));
-    const std::vector<Chunk> chunks = make_chunks(host_segs, n_segs, chunk_elems);
-    SDP_TRY(order_after_last(ctx, ctx->s_copy));
-    SDP_TRY(order_after_last(ctx, ctx->s_comp));
-    bool used[2] = {false, false};
-    int rc = stream_norm_phase(ctx, host_segs, n_segs, R, plan, chunks, store, hp->max_grad_norm, used);
-    NormState st{};
-    if (rc == SDP_OK) rc = read_norm(ctx, ctx->s_comp, &st);
-    if (rc != SDP_OK) {
-        (void)sync_streams(ctx);
-        return rc;
-    }
-    if (grad_norm_out) *grad_norm_out = st.norm;
-    if (st.nonfinite) {
-        SDP_TRY(sync_streams(ctx));
-        SDP_TRY(mark_done(ctx, ctx->s_comp));
-        return fail(SDP_ERR_NONFINITE, "gradient norm is not finite (%g); nothing was updated", st.norm);
-    }
-    rc = stream_update_phase(ctx, host_segs, R, plan, chunks, store, hp, used, chunks.size());
-    int rc2 = sync_streams(ctx);
-    // after a failure, results still waiting in bounce buffers belong to this
-    // call only: never let a later call move them
-    for (auto &xs : ctx->pending_out) xs.clear();
-    if (rc != SDP_OK) return rc;
-    if (rc2 != SDP_OK) return rc2;
-    return mark_done(ctx, ctx->s_comp);
-}
-
 int sdp_grad_norm(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int device_resident, int64_t chunk_elems,
                   void *stream, double *norm_out) {
     t_err.clear();
@@ -1399,191 +829,6 @@ int sdp_cast_bf16(sdp_ctx *ctx, const float *src, uint16_t *dst, int64_t n, void
     uintptr_t a0 = (uintptr_t)src, a1 = a0 + (size_t)n * 4, b0 = (uintptr_t)dst, b1 = b0 + (size_t)n * 2;
     if (a0 < b1 && b0 < a1) return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_cast_bf16: src and dst overlap");
     HIP_TRY(sdp::launch_cast_bf16(src, dst, n, (hipStream_t)stream));
-    return SDP_OK;
-}
-
-int sdp_cast_bf16_host(sdp_ctx *ctx, const float *src, uint16_t *dst, int64_t n) {
-    t_err.clear();
-    if (!src || !dst || n < 1) return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_cast_bf16_host: bad argument");
-    if (ctx && ctx->copier)
-        pool_jobs(ctx->copier, {{dst, src, (size_t)n, Job::kCastBf16}});
-    else
-        cast_bf16_host(src, dst, (size_t)n);
-    return SDP_OK;
-}
-
-int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf16, int64_t n, int64_t chunk_elems,
-                       int mode) {
-    t_err.clear();
-    if (!ctx || !host_master || !dev_bf16 || n < 1)
-        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_deliver_params: bad argument");
-    if (mode != SDP_DELIVER_HOST_CAST && mode != SDP_DELIVER_DEVICE_CAST)
-        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_deliver_params: unknown mode %d", mode);
-    if (!ctx->staging) return fail(SDP_ERR_CHUNK_TOO_LARGE, "context was created without streamed-mode staging");
-    SDP_TRY(check_chunk(chunk_elems, false));
-    if (chunk_elems > ctx->max_chunk)
-        return fail(SDP_ERR_CHUNK_TOO_LARGE, "chunk_elems %lld exceeds the context's %lld", (long long)chunk_elems,
-                    (long long)ctx->max_chunk);
-    if (!aligned(host_master) || !aligned(dev_bf16))
-        return fail(SDP_ERR_ALIGNMENT, "sdp_deliver_params: pointers must be %d-byte aligned", SDP_ALIGN);
-    DeviceGuard guard(ctx->device);
-    SDP_TRY(check_host_ptr(host_master, "host_master", 0));
-    SDP_TRY(check_device_ptr(ctx, dev_bf16, (size_t)n * 2, "dev_bf16", 0));
-    const bool pinned = is_pinned_host(host_master);
-    if (mode == SDP_DELIVER_HOST_CAST || !pinned) SDP_TRY(ensure_host_stage(ctx));
-    SDP_TRY(order_after_last(ctx, ctx->s_copy));
-    SDP_TRY(order_after_last(ctx, ctx->s_comp));
-    bool used[2] = {false, false};
-    int rc = SDP_OK;
-    size_t k = 0;
-    for (int64_t off = 0; off < n && rc == SDP_OK; off += chunk_elems, ++k) {
-        const int sl = (int)(k & 1);
-        const int64_t len = std::min(chunk_elems, n - off);
-        char *bin = ctx->stage ? ctx->stage + (size_t)sl * stage_bytes(ctx) : nullptr;
-        if (mode == SDP_DELIVER_HOST_CAST) {
-            // host threads round chunk k while the DMA still moves chunk k-1
-            if (ctx->stage_used[sl] && hipEventSynchronize(ctx->h2d_done[sl]) != hipSuccess) {
-                rc = fail(SDP_ERR_HIP, "sdp_deliver_params: event wait failed");
-                break;
-            }
-            pool_jobs(ctx->copier, {{bin, host_master + off, (size_t)len, Job::kCastBf16}});
-            if (hipMemcpyAsync(dev_bf16 + off, bin, (size_t)len * 2, hipMemcpyHostToDevice, ctx->s_copy) != hipSuccess ||
-                hipEventRecord(ctx->h2d_done[sl], ctx->s_copy) != hipSuccess)
-                rc = fail(SDP_ERR_HIP, "sdp_deliver_params: copy enqueue failed");
-            ctx->stage_used[sl] = true;
-        } else {
-            Slot slot = slot_at(ctx, sl);
-            std::vector<Xfer> xs = {{off_in_slot(ctx, sl, slot.p), (char *)(host_master + off), (size_t)len * 4}};
-            if (used[sl] && hipStreamWaitEvent(ctx->s_copy, ctx->slot_free[sl], 0) != hipSuccess) {
-                rc = fail(SDP_ERR_HIP, "sdp_deliver_params: stream wait failed");
-                break;
-            }
-            if (pinned) {
-                if (hipMemcpyAsync(slot.p, host_master + off, (size_t)len * 4, hipMemcpyHostToDevice, ctx->s_copy) !=
-                    hipSuccess)
-                    rc = fail(SDP_ERR_HIP, "sdp_deliver_params: copy enqueue failed");
-            } else {
-                if (ctx->stage_used[sl] && hipEventSynchronize(ctx->h2d_done[sl]) != hipSuccess) {
-                    rc = fail(SDP_ERR_HIP, "sdp_deliver_params: event wait failed");
-                    break;
-                }
-                pool_jobs(ctx->copier, {{bin, host_master + off, (size_t)len * 4}});
-                if (hipMemcpyAsync(slot.p, bin, (size_t)len * 4, hipMemcpyHostToDevice, ctx->s_copy) != hipSuccess)
-                    rc = fail(SDP_ERR_HIP, "sdp_deliver_params: copy enqueue failed");
-                ctx->stage_used[sl] = true;
-            }
-            if (rc != SDP_OK) break;
-            if (hipEventRecord(ctx->h2d_done[sl], ctx->s_copy) != hipSuccess ||
-                hipStreamWaitEvent(ctx->s_comp, ctx->h2d_done[sl], 0) != hipSuccess ||
-                sdp::launch_cast_bf16(slot.p, dev_bf16 + off, len, ctx->s_comp) != hipSuccess ||
-                hipEventRecord(ctx->slot_free[sl], ctx->s_comp) != hipSuccess)
-                rc = fail(SDP_ERR_HIP, "sdp_deliver_params: enqueue failed");
-            used[sl] = true;
-        }
-    }
-    const int rc2 = sync_streams(ctx);
-    if (rc != SDP_OK) return rc;
-    if (rc2 != SDP_OK) return rc2;
-    return mark_done(ctx, ctx->s_comp);
-}
-
-int sdp_host_update_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, const sdp_adamw_params *hp,
-                         int64_t chunk_elems, int gbar_format, double *grad_norm_out) {
-    t_err.clear();
-    if (!ctx) return fail(SDP_ERR_INVALID_ARGUMENT, "context is NULL");
-    SDP_TRY(check_hparams(hp));
-    if (gbar_format != SDP_GBAR_F32 && gbar_format != SDP_GBAR_BF16)
-        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_host_update_step: unknown gradient format %d", gbar_format);
-    if (!ctx->staging) return fail(SDP_ERR_CHUNK_TOO_LARGE, "context was created without streamed-mode staging");
-    SDP_TRY(check_chunk(chunk_elems, false));
-    if (chunk_elems > ctx->max_chunk)
-        return fail(SDP_ERR_CHUNK_TOO_LARGE, "chunk_elems %lld exceeds the context's %lld", (long long)chunk_elems,
-                    (long long)ctx->max_chunk);
-    DeviceGuard guard(ctx->device);
-    int32_t R = 0;
-    SDP_TRY(validate_segments(ctx, segs, n_segs, kAnyHost, kDeviceMem, false, &R));
-    const Plan plan = make_plan(segs, n_segs);
-    SDP_TRY(ensure_partials(ctx, plan.tiles));
-    SDP_TRY(ensure_host_stage(ctx));
-    SDP_TRY(order_after_last(ctx, ctx->s_comp));
-    SDP_TRY(order_after_last(ctx, ctx->s_copy));
-    const int rc = host_route(ctx, segs, n_segs, R, plan, hp, chunk_elems, gbar_format == SDP_GBAR_BF16,
-                              grad_norm_out);
-    // nothing of this call may still read the caller's gradients on return
-    const std::string err = t_err;
-    const int rc2 = sync_streams(ctx);
-    if (rc != SDP_OK) {
-        t_err = err;
-        return rc;
-    }
-    if (rc2 != SDP_OK) return rc2;
-    return mark_done(ctx, ctx->s_comp);
-}
-
-int sdp_host_adamw(sdp_ctx *ctx, float *master, float *exp_avg, float *exp_avg_sq, uint16_t *param_bf16,
-                   const void *gbar, int gbar_format, int64_t n, double clip_coef, const sdp_adamw_params *hp) {
-    t_err.clear();
-    if (!master || !exp_avg || !exp_avg_sq || !param_bf16 || !gbar || n < 1)
-        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_host_adamw: NULL buffer or n < 1");
-    if (gbar_format != SDP_GBAR_F32 && gbar_format != SDP_GBAR_BF16)
-        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_host_adamw: unknown gradient format %d", gbar_format);
-    if (!std::isfinite(clip_coef) || clip_coef < 0.0)
-        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_host_adamw: clip_coef must be finite and >= 0");
-    SDP_TRY(check_hparams(hp));
-    const size_t gb = (size_t)n * (gbar_format == SDP_GBAR_BF16 ? 2 : 4);
-    const Range rs[5] = {{(uintptr_t)master, (uintptr_t)master + (size_t)n * 4, 0, "master"},
-                         {(uintptr_t)exp_avg, (uintptr_t)exp_avg + (size_t)n * 4, 0, "exp_avg"},
-                         {(uintptr_t)exp_avg_sq, (uintptr_t)exp_avg_sq + (size_t)n * 4, 0, "exp_avg_sq"},
-                         {(uintptr_t)param_bf16, (uintptr_t)param_bf16 + (size_t)n * 2, 0, "param_bf16"},
-                         {(uintptr_t)gbar, (uintptr_t)gbar + gb, 0, "gbar"}};
-    for (int x = 0; x < 5; ++x) {
-        if (rs[x].a % SDP_ALIGN != 0)
-            return fail(SDP_ERR_ALIGNMENT, "sdp_host_adamw: %s is not %d-byte aligned", rs[x].what, SDP_ALIGN);
-        for (int y = 0; y < x; ++y)
-            if (overlap(rs[x], rs[y]))
-                return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_host_adamw: %s overlaps %s", rs[x].what, rs[y].what);
-    }
-    if (ctx && !ctx->copier) ctx->copier = new_pool(ctx, default_host_threads());
-    sdp_host::AdamArgs a;
-    a.p = master;
-    a.m = exp_avg;
-    a.v = exp_avg_sq;
-    a.pb = param_bf16;
-    a.gbar = gbar;
-    a.gbar_bf16 = gbar_format == SDP_GBAR_BF16 ? 1 : 0;
-    host_adamw(ctx ? ctx->copier : nullptr, a, host_consts(hp, clip_coef), n);
-    return SDP_OK;
-}
-
-int sdp_probe_host_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, int32_t reps, double *gbs_out) {
-    t_err.clear();
-    if (!ctx || !dst || !src || bytes < 1 || reps < 1 || !gbs_out)
-        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_probe_host_copy: bad argument");
-    const uintptr_t a = (uintptr_t)dst, b = (uintptr_t)src;
-    if (a < b + (size_t)bytes && b < a + (size_t)bytes)
-        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_probe_host_copy: dst and src overlap");
-    if (!ctx->copier) ctx->copier = new_pool(ctx, default_host_threads());
-    const Clock::time_point t0 = Clock::now();
-    for (int32_t r = 0; r < reps; ++r) pool_jobs(ctx->copier, {{dst, src, (size_t)bytes}});
-    const double s = ms_between(t0, Clock::now()) / 1e3;
-    *gbs_out = 2.0 * (double)bytes * reps / s / 1e9;
-    return SDP_OK;
-}
-
-int sdp_ctx_set_host_threads(sdp_ctx *ctx, int32_t threads) {
-    t_err.clear();
-    if (!ctx) return fail(SDP_ERR_INVALID_ARGUMENT, "context is NULL");
-    if (threads < 1 || threads > 256)
-        return fail(SDP_ERR_INVALID_ARGUMENT, "host threads must be in 1..256 (got %d)", threads);
-    delete ctx->copier;
-    ctx->copier = new_pool(ctx, threads);
-    return SDP_OK;
-}
-
-int sdp_ctx_host_threads(sdp_ctx *ctx, int32_t *threads_out) {
-    t_err.clear();
-    if (!ctx || !threads_out) return fail(SDP_ERR_INVALID_ARGUMENT, "context or out is NULL");
-    *threads_out = ctx->copier ? ctx->copier->size() : default_host_threads();
     return SDP_OK;
 }
 
@@ -1690,6 +935,21 @@ int sdp_probe_link(sdp_ctx *ctx, void *host_a, void *host_b, void *dev_a, void *
     gbs_out[1] = total / sec / 1e9;
     HIP_TRY(run(true, true, &sec));
     gbs_out[2] = 2.0 * total / sec / 1e9;
+    return SDP_OK;
+}
+
+int sdp_probe_host_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, int32_t reps, double *gbs_out) {
+    t_err.clear();
+    if (!ctx || !dst || !src || bytes < 1 || reps < 1 || !gbs_out)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_probe_host_copy: bad argument");
+    const uintptr_t a = (uintptr_t)dst, b = (uintptr_t)src;
+    if (a < b + (size_t)bytes && b < a + (size_t)bytes)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_probe_host_copy: dst and src overlap");
+    if (!ctx->copier) ctx->copier = new_pool(ctx, default_host_threads());
+    const Clock::time_point t0 = Clock::now();
+    for (int32_t r = 0; r < reps; ++r) pool_jobs(ctx->copier, {{dst, src, (size_t)bytes}});
+    const double s = ms_between(t0, Clock::now()) / 1e3;
+    *gbs_out = 2.0 * (double)bytes * reps / s / 1e9;
     return SDP_OK;
 }
 

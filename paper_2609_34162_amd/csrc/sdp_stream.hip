@@ -1,0 +1,207 @@
+// C ABI of libsdp, streamed mode (sdp_stream_step): states live in pinned
+// host memory (or, staged, in any host memory) and move through two device
+// staging slots.  A copy stream carries host-to-device copies; a compute
+// stream runs the kernels and the device-to-host copies.  Events h2d_done[s]
+// and slot_free[s] order each slot's reuse: a slot is refilled only after
+// its previous consumer finished (the paper's buffer-reuse rule, Design,
+// completion and buffer reuse), and the update of a chunk starts as soon as
+// its copy has landed (chunked overlap within a layer).  Phase 1 streams the
+// gradients for the global norm; phase 2 streams master/m/v through the
+// fused update and back.
+#include "sdp_rt.h"
+
+namespace sdprt {
+
+namespace {
+
+int poison(sdp_ctx *ctx, int k) {
+    if (!(ctx->flags & SDP_FLAG_DEBUG_POISON)) return SDP_OK;
+    HIP_TRY(sdp::launch_fill_u32(ctx->staging + (size_t)k * ctx->slot_bytes, (int64_t)(ctx->slot_bytes / 4),
+                                 0xFFC0FFC0u, ctx->s_comp));
+    return SDP_OK;
+}
+
+// Runs of transfers that are contiguous in the slot, for the bounce copies.
+std::vector<Xfer> merge_runs(std::vector<Xfer> xs) {
+    std::sort(xs.begin(), xs.end(), [](const Xfer &a, const Xfer &b) { return a.off < b.off; });
+    std::vector<Xfer> runs;
+    for (const Xfer &x : xs) {
+        if (!runs.empty() && runs.back().off + runs.back().bytes == x.off)
+            runs.back().bytes += x.bytes;
+        else
+            runs.push_back({x.off, nullptr, x.bytes});
+    }
+    return runs;
+}
+
+// Host -> slot `sl` copies of one chunk, enqueued on the copy stream.  In the
+// staged mode the host threads first copy into the slot's pinned bounce
+// buffer, after waiting for that buffer's previous copy to leave it.
+int copy_in(sdp_ctx *ctx, int sl, const std::vector<Xfer> &xs) {
+    char *dev = ctx->staging + (size_t)sl * ctx->slot_bytes;
+    if (!staged(ctx)) {
+        for (const Xfer &x : xs)
+            HIP_TRY(hipMemcpyAsync(dev + x.off, x.host, x.bytes, hipMemcpyHostToDevice, ctx->s_copy));
+        return SDP_OK;
+    }
+    char *bin = ctx->bounce_in + (size_t)sl * ctx->slot_bytes;
+    if (ctx->bin_used[sl]) HIP_TRY(hipEventSynchronize(ctx->h2d_done[sl]));
+    std::vector<Job> jobs;
+    for (const Xfer &x : xs) jobs.push_back({bin + x.off, x.host, x.bytes});
+    pool_jobs(ctx->copier, jobs);
+    for (const Xfer &r : merge_runs(xs))
+        HIP_TRY(hipMemcpyAsync(dev + r.off, bin + r.off, r.bytes, hipMemcpyHostToDevice, ctx->s_copy));
+    ctx->bin_used[sl] = true;
+    return SDP_OK;
+}
+
+// Slot `sl` -> host copies of one chunk, enqueued on the compute stream.  In
+// the staged mode they land in outgoing bounce buffer `bo` and are moved to
+// their destinations by drain().
+int copy_out(sdp_ctx *ctx, int sl, int bo, const std::vector<Xfer> &xs) {
+    char *dev = ctx->staging + (size_t)sl * ctx->slot_bytes;
+    if (!staged(ctx)) {
+        for (const Xfer &x : xs)
+            HIP_TRY(hipMemcpyAsync(x.host, dev + x.off, x.bytes, hipMemcpyDeviceToHost, ctx->s_comp));
+        return SDP_OK;
+    }
+    char *bout = ctx->bounce_out + (size_t)bo * 14 * (size_t)ctx->max_chunk;
+    for (const Xfer &r : merge_runs(xs))
+        HIP_TRY(hipMemcpyAsync(bout + r.off, dev + r.off, r.bytes, hipMemcpyDeviceToHost, ctx->s_comp));
+    HIP_TRY(hipEventRecord(ctx->d2h_done[bo], ctx->s_comp));
+    ctx->pending_out[bo] = xs;
+    return SDP_OK;
+}
+
+// Staged mode: wait for the outgoing copies into bounce buffer `bo` and move
+// them to their host destinations.
+int drain(sdp_ctx *ctx, int bo) {
+    if (ctx->pending_out[bo].empty()) return SDP_OK;
+    HIP_TRY(hipEventSynchronize(ctx->d2h_done[bo]));
+    char *bout = ctx->bounce_out + (size_t)bo * 14 * (size_t)ctx->max_chunk;
+    std::vector<Job> jobs;
+    for (const Xfer &x : ctx->pending_out[bo]) jobs.push_back({x.host, bout + x.off, x.bytes});
+    pool_jobs(ctx->copier, jobs);
+    ctx->pending_out[bo].clear();
+    return SDP_OK;
+}
+
+}  // namespace
+
+// Phase 1: gradients in, norm partials (and stored g_bar) out, then finalize.
+int stream_norm_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R, const Plan &plan,
+                      const std::vector<Chunk> &chunks, bool store_gbar, double max_grad_norm, bool used[2]) {
+    (void)n_segs;
+    for (size_t k = 0; k < chunks.size(); ++k) {
+        const Chunk &c = chunks[k];
+        const int sl = (int)(k & 1);
+        Slot slot = slot_at(ctx, sl);
+        std::vector<Xfer> xs;
+        for (int32_t r = 0; r < R; ++r)
+            xs.push_back({off_in_slot(ctx, sl, slot.g[r]), (char *)(segs[c.seg].grads[r] + c.off), (size_t)c.len * 2});
+        if (used[sl]) HIP_TRY(hipStreamWaitEvent(ctx->s_copy, ctx->slot_free[sl], 0));
+        SDP_TRY(copy_in(ctx, sl, xs));
+        HIP_TRY(hipEventRecord(ctx->h2d_done[sl], ctx->s_copy));
+        HIP_TRY(hipStreamWaitEvent(ctx->s_comp, ctx->h2d_done[sl], 0));
+        const uint16_t *gp[SDP_MAX_RANKS];
+        for (int32_t r = 0; r < R; ++r) gp[r] = slot.g[r];
+        SDP_TRY(norm_launch(ctx, R, gp, c.len, ctx->partials + 2 * (plan.tile_base[c.seg] + c.off / SDP_NORM_TILE),
+                            store_gbar ? ctx->gbar + plan.gbar_base[c.seg] + c.off : nullptr, ctx->s_comp));
+        SDP_TRY(poison(ctx, sl));
+        HIP_TRY(hipEventRecord(ctx->slot_free[sl], ctx->s_comp));
+        used[sl] = true;
+    }
+    return finalize_launch(ctx, plan.tiles, max_grad_norm, ctx->s_comp);
+}
+
+namespace {
+
+// Phase 2: master/m/v in (and the gradients again unless g_bar is stored),
+// fused update, master/m/v and BF16 parameters back out.
+int stream_update_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t R, const Plan &plan,
+                        const std::vector<Chunk> &chunks, bool stored_gbar, const sdp_adamw_params *hp, bool used[2],
+                        size_t k0) {
+    for (size_t j = 0; j < chunks.size(); ++j) {
+        const Chunk &c = chunks[j];
+        const sdp_segment &g = segs[c.seg];
+        const int sl = (int)((j + k0) & 1);
+        Slot slot = slot_at(ctx, sl);
+        const size_t f4 = (size_t)c.len * 4, b2 = (size_t)c.len * 2;
+        std::vector<Xfer> in = {{off_in_slot(ctx, sl, slot.p), (char *)(g.master + c.off), f4},
+                                {off_in_slot(ctx, sl, slot.m), (char *)(g.exp_avg + c.off), f4},
+                                {off_in_slot(ctx, sl, slot.v), (char *)(g.exp_avg_sq + c.off), f4}};
+        if (!stored_gbar)
+            for (int32_t r = 0; r < R; ++r)
+                in.push_back({off_in_slot(ctx, sl, slot.g[r]), (char *)(g.grads[r] + c.off), b2});
+        if (used[sl]) HIP_TRY(hipStreamWaitEvent(ctx->s_copy, ctx->slot_free[sl], 0));
+        SDP_TRY(copy_in(ctx, sl, in));
+        HIP_TRY(hipEventRecord(ctx->h2d_done[sl], ctx->s_copy));
+        HIP_TRY(hipStreamWaitEvent(ctx->s_comp, ctx->h2d_done[sl], 0));
+        const uint16_t *gp[SDP_MAX_RANKS];
+        for (int32_t r = 0; r < R; ++r) gp[r] = slot.g[r];
+        SDP_TRY(update_launch(ctx, R, hp, slot.p, slot.m, slot.v, slot.pb, gp,
+                              stored_gbar ? ctx->gbar + plan.gbar_base[c.seg] + c.off : nullptr, c.len, ctx->s_comp));
+        std::vector<Xfer> out = {{off_in_slot(ctx, sl, slot.p), (char *)(g.master + c.off), f4},
+                                 {off_in_slot(ctx, sl, slot.m), (char *)(g.exp_avg + c.off), f4},
+                                 {off_in_slot(ctx, sl, slot.v), (char *)(g.exp_avg_sq + c.off), f4},
+                                 {off_in_slot(ctx, sl, slot.pb), (char *)(g.param_bf16 + c.off), b2}};
+        SDP_TRY(copy_out(ctx, sl, (int)(j % kOutBufs), out));
+        SDP_TRY(poison(ctx, sl));
+        HIP_TRY(hipEventRecord(ctx->slot_free[sl], ctx->s_comp));
+        used[sl] = true;
+        // staged: move the previous chunk's results out while this one's
+        // incoming copy is in flight
+        if (staged(ctx) && j >= 1) SDP_TRY(drain(ctx, (int)((j - 1) % kOutBufs)));
+    }
+    if (staged(ctx) && !chunks.empty()) SDP_TRY(drain(ctx, (int)((chunks.size() - 1) % kOutBufs)));
+    return SDP_OK;
+}
+
+}  // namespace
+
+}  // namespace sdprt
+
+using namespace sdprt;
+
+extern "C" {
+
+int sdp_stream_step(sdp_ctx *ctx, const sdp_segment *host_segs, int32_t n_segs, const sdp_adamw_params *hp,
+                    int64_t chunk_elems, double *grad_norm_out) {
+    t_err.clear();
+    if (!ctx) return fail(SDP_ERR_INVALID_ARGUMENT, "context is NULL");
+    SDP_TRY(check_hparams(hp));
+    DeviceGuard guard(ctx->device);
+    int32_t R = 0;
+    SDP_TRY(stream_common_checks(ctx, host_segs, n_segs, chunk_elems, false, &R));
+    const Plan plan = make_plan(host_segs, n_segs);
+    const bool store = !(ctx->flags & SDP_FLAG_STREAM_GBAR_NEVER);
+    SDP_TRY(ensure_partials(ctx, plan.tiles));
+    if (store) SDP_TRY(ensure_gbar(ctx, plan.gbar_elems));
+    const std::vector<Chunk> chunks = make_chunks(host_segs, n_segs, chunk_elems);
+    SDP_TRY(order_after_last(ctx, ctx->s_copy));
+    SDP_TRY(order_after_last(ctx, ctx->s_comp));
+    bool used[2] = {false, false};
+    int rc = stream_norm_phase(ctx, host_segs, n_segs, R, plan, chunks, store, hp->max_grad_norm, used);
+    NormState st{};
+    if (rc == SDP_OK) rc = read_norm(ctx, ctx->s_comp, &st);
+    if (rc != SDP_OK) {
+        (void)sync_streams(ctx);
+        return rc;
+    }
+    if (grad_norm_out) *grad_norm_out = st.norm;
+    if (st.nonfinite) {
+        SDP_TRY(sync_streams(ctx));
+        SDP_TRY(mark_done(ctx, ctx->s_comp));
+        return fail(SDP_ERR_NONFINITE, "gradient norm is not finite (%g); nothing was updated", st.norm);
+    }
+    rc = stream_update_phase(ctx, host_segs, R, plan, chunks, store, hp, used, chunks.size());
+    int rc2 = sync_streams(ctx);
+    // after a failure, results still waiting in bounce buffers belong to this
+    // call only: never let a later call move them
+    for (auto &xs : ctx->pending_out) xs.clear();
+    if (rc != SDP_OK) return rc;
+    if (rc2 != SDP_OK) return rc2;
+    return mark_done(ctx, ctx->s_comp);
+}
+
+}  // extern "C"
