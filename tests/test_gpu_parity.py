@@ -162,6 +162,78 @@ def test_bit_exact_invariants(sdp, ctx, ctx_store, ctx_nostore):
     assert np.array_equal(got.param_bf16[0], oracle.bf16(masters[0]))
 
 
+def edge_cases():
+    """(name, masters, m, v, grads, hyperparameters) of degenerate inputs."""
+    rng = np.random.default_rng(321)
+    n = TILE + 37
+    R = 2
+    out = []
+    # all-zero gradients: norm 0, c = 1, decay only, moments scale down
+    m0 = (rng.normal(0, 1e-3, n)).astype(np.float32)
+    v0 = (rng.random(n) * 1e-6).astype(np.float32)
+    z = np.zeros(n, np.uint16)
+    out.append(("zero gradients", rng.normal(0, 0.02, n).astype(np.float32), m0, v0, [z, z],
+                dict(lr=1e-3, weight_decay=0.1, max_grad_norm=1.0, step=3)))
+    # subnormal states and gradients (BF16 has FP32's exponent range)
+    tiny = np.float32(1e-40)
+    sub = lambda k: (rng.integers(-60, 60, n) * tiny).astype(np.float32)
+    gsub = [synth.to_bf16_bits((rng.integers(-60, 60, n) * tiny).astype(np.float32)) for _ in range(R)]
+    out.append(("subnormals", sub(0), sub(1), np.abs(sub(2)), gsub,
+                dict(lr=1e-3, weight_decay=0.01, eps=1e-45, max_grad_norm=0.0, step=2)))
+    # huge gradients near the BF16 maximum: the norm is huge and c tiny
+    big = [synth.to_bf16_bits((rng.choice([-1, 1], n) * rng.uniform(1e37, 3e38, n)).astype(np.float32))
+           for _ in range(R)]
+    out.append(("huge gradients", rng.normal(0, 0.02, n).astype(np.float32), np.zeros(n, np.float32),
+                np.zeros(n, np.float32), big, dict(lr=1e-3, weight_decay=0.01, max_grad_norm=1.0, step=1)))
+    # masters on BF16 rounding ties, lr = 0 so the master stays put: the BF16
+    # output must round every tie to even
+    hi = rng.integers(0, 1 << 16, n).astype(np.uint32) & ~np.uint32(0x7f80)   # finite, not NaN/Inf
+    hi |= np.uint32(0x3c00)
+    ties = ((hi << 16) | 0x8000).view(np.float32)
+    g1 = synth.to_bf16_bits(rng.normal(0, 1e-3, n).astype(np.float32))
+    out.append(("bf16 ties", ties, np.zeros(n, np.float32), np.zeros(n, np.float32), [g1, g1],
+                dict(lr=0.0, weight_decay=0.0, max_grad_norm=1.0, step=1)))
+    return out
+
+
+@pytest.mark.parametrize("case", range(4))
+@pytest.mark.parametrize("mode", ["device", "streamed", "route"])
+def test_edge_values(sdp, ctx, case, mode):
+    name, master, m, v, grads, kw = edge_cases()[case]
+    R = len(grads)
+    log(f"edge case {name}, {mode}")
+    ref = oracle.State([master], [m], [v])
+    rc, onorm = oracle.step(ref, [grads], oracle.hparams(**kw))
+    assert rc == oracle.ORC_OK
+    hs = sdp.make_params(**kw)
+    if mode == "device":
+        dev = DevState([master], R, [m], [v])
+        norm = dev_step(sdp, ctx, dev, [grads], hs)
+        got = dev.host()
+    elif mode == "streamed":
+        host = HostState(sdp, [master], R, [m], [v])
+        try:
+            host.set_grads([grads])
+            norm = sdp.sdp_stream_step(ctx, host.segments(), hs, TILE)
+            got = host.host()
+        finally:
+            host.close()
+    else:
+        host = PageableState(sdp, [master], R)
+        host.m[0][:] = m
+        host.v[0][:] = v
+        g = [torch.from_numpy(x.view(np.int16)).to("cuda") for x in grads]
+        segs = sdp.Segments([(host.p[0].ctypes.data, host.m[0].ctypes.data, host.v[0].ctypes.data,
+                              host.pb[0].ctypes.data, [x.data_ptr() for x in g], master.size)])
+        norm = sdp.sdp_host_update_step(ctx, segs, hs, TILE, sdp.SDP_GBAR_F32)
+        got = host.host()
+    assert norm == onorm, (name, norm, onorm)
+    check_state(got, ref)
+    if name == "bf16 ties":
+        assert np.array_equal(got.master[0], master)
+        assert np.array_equal(got.param_bf16[0], oracle.bf16(master))
+
+
 @pytest.mark.parametrize("chunk_tiles", [1, 2, 4])
 def test_streamed_matches_oracle_and_device(sdp, ctx, ctx_poison, ctx_nostore, chunk_tiles):
     sizes = [3 * TILE + 5, 1, 70000]
