@@ -42,10 +42,14 @@
  *    master = fp32(p'), exp_avg = fp32(m'), exp_avg_sq = fp32(v'),
  *    param_bf16 = bf16_rne(master)
  *  The per-element update is evaluated in FP64 registers and rounded once.
+ *  The host-update route with SDP_GBAR_BF16 uses g = bf16_rne(g_bar) * c
+ *  (the norm and c still come from the FP32 g_bar).
  *  A non-finite norm leaves every state and parameter unchanged.
  *  Results do not depend on the chunk size, on the mode (device or
  *  streamed) or on run-to-run scheduling: the norm is a fixed-order tree
- *  over fixed 65,536-element tiles of each segment.
+ *  over fixed 65,536-element tiles of each segment.  The host-update route
+ *  with SDP_GBAR_F32 gives the same norm bits and, element by element, the
+ *  same FP64 expression without fused multiply-adds.
  */
 #ifndef SDP_H
 #define SDP_H
