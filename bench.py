@@ -9,6 +9,8 @@ JSON line also carries:
   roofline      -- the fused update kernel's algorithmic HBM GB/s (HIP events
                    recorded around each launch on its stream) against 8 TB/s;
   hbm_copy_gbs  -- a 16-byte-per-lane device copy, the practical ceiling;
+  update_pattern_gbs -- the fused update's own loads and stores with trivial
+                   arithmetic: the ceiling of its 20:14 read:write mix;
   streamed      -- one Qwen3-14B layer (330,311,680 parameters, R = 4) in
                    pinned host memory, streamed in 32M-element chunks, against
                    the pinned link bandwidth measured in the same run;
@@ -140,6 +142,16 @@ def device_leg(args, torch, np, synth, sdp, cid, steps, warmup, copy_probe):
         torch.cuda.synchronize()
         res["copy_gbs"] = 2 * nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
         del a, b
+        # the update's own access pattern with trivial arithmetic (overwrites
+        # the states, whose results were read above): its traffic-mix ceiling
+        for _ in range(2):
+            sdp.sdp_probe_update_pattern(ctx, segs, sh)
+        e0.record(stream)
+        for _ in range(reps):
+            sdp.sdp_probe_update_pattern(ctx, segs, sh)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        res["pattern_gbs"] = (2 * R + 26) * N * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
     sdp.sdp_ctx_destroy(ctx)
     del p, m, v, pb, g
     torch.cuda.empty_cache()
@@ -543,6 +555,8 @@ def main():
                      "kernel": "fused aggregate+clip+AdamW+BF16 update",
                      "algorithmic_bytes_per_launch": dres["update_bytes"]},
         "hbm_copy_gbs": dres["copy_gbs"],
+        "update_pattern_gbs": dres["pattern_gbs"],
+        "update_frac_of_pattern": dres["update_gbs"] / dres["pattern_gbs"],
         "grad_norm_last_step": dres["grad_norm"],
         "streamed": streamed,
         "host_route": route,

@@ -375,6 +375,14 @@ SDP_API int sdp_ctx_get_timing(sdp_ctx *ctx, sdp_kernel_times *out);
  * hardware traffic counters. */
 SDP_API int sdp_probe_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, void *stream);
 
+/* The fused update's memory access pattern with trivial arithmetic, on one
+ * device-mode segment (validated as for sdp_agg_adam_step): the same loads
+ * and stores, widths and lane mapping, FP32 adds instead of AdamW.  Its rate
+ * is the HBM ceiling of the update's own traffic mix.  Measurement only: it
+ * overwrites the segment's states and BF16 params.  Asynchronous on
+ * `stream`. */
+SDP_API int sdp_probe_update_pattern(sdp_ctx *ctx, const sdp_segment *seg, void *stream);
+
 /* Pinned host link bandwidth with the streamed engine's copy path:
  * hipMemcpyAsync in chunk_bytes pieces over `bytes`, `reps` times, host to
  * device on the context's copy stream and device to host on its compute

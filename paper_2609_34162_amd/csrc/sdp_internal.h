@@ -69,6 +69,7 @@ hipError_t launch_norm_finalize(const double *partials /* pairs */, int64_t n_pa
                                 double max_grad_norm, NormState *ns, hipStream_t s);
 hipError_t launch_update(int R, const UpdateArgs &a, int max_blocks, hipStream_t s);
 hipError_t launch_gbar_out(int R, const GbarArgs &a, hipStream_t s);
+hipError_t launch_update_pattern(int R, const UpdateArgs &a, hipStream_t s);
 hipError_t launch_cast_bf16(const float *src, uint16_t *dst, int64_t n, hipStream_t s);
 hipError_t launch_copy16(void *dst, const void *src, int64_t n16, int max_blocks, hipStream_t s);
 hipError_t launch_fill_u32(void *dst, int64_t n_words, uint32_t value, hipStream_t s);

@@ -316,6 +316,56 @@ __global__ __launch_bounds__(kUpdateThreads) void k_update(UpdateArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Measurement: the fused update's memory access pattern with trivial
+// arithmetic (integer and FP32 adds instead of the FP64 AdamW), the same
+// loads, stores, widths and lane mapping.  Its rate is the ceiling that the
+// update's own traffic mix allows on this part.  Overwrites the states.
+
+template <int R>
+__global__ __launch_bounds__(kUpdateThreads) void k_update_pattern(UpdateArgs a) {
+    float *__restrict__ P = a.p;
+    float *__restrict__ M = a.m;
+    float *__restrict__ V = a.v;
+    uint16_t *__restrict__ PB = a.pb;
+    const int64_t n = a.n;
+    const int64_t groups = n / kVec;
+    const int64_t gid = (int64_t)blockIdx.x * kUpdateThreads + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * kUpdateThreads;
+    for (int64_t q = gid; q < groups; q += stride) {
+        const int64_t e0 = q * kVec;
+        uint32_t x = 0;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const uint4 w = *reinterpret_cast<const uint4 *>(a.g[r] + e0);
+            x ^= w.x ^ w.y ^ w.z ^ w.w;
+        }
+        const float gx = __uint_as_float((x & 0x007fffffu) | 0x3f800000u);
+        float4 *p4 = reinterpret_cast<float4 *>(P + e0);
+        float4 *m4 = reinterpret_cast<float4 *>(M + e0);
+        float4 *v4 = reinterpret_cast<float4 *>(V + e0);
+        float4 pv[2] = {p4[0], p4[1]};
+        float4 mv[2] = {m4[0], m4[1]};
+        float4 vv[2] = {v4[0], v4[1]};
+        float *pf = &pv[0].x, *mf = &mv[0].x, *vf = &vv[0].x;
+#pragma unroll
+        for (int e = 0; e < kVec; ++e) {
+            pf[e] += gx;
+            mf[e] += pf[e];
+            vf[e] += mf[e];
+        }
+        p4[0] = pv[0]; p4[1] = pv[1];
+        m4[0] = mv[0]; m4[1] = mv[1];
+        v4[0] = vv[0]; v4[1] = vv[1];
+        uint4 b;
+        b.x = (__float_as_uint(pf[0]) >> 16) | (__float_as_uint(pf[1]) & 0xffff0000u);
+        b.y = (__float_as_uint(pf[2]) >> 16) | (__float_as_uint(pf[3]) & 0xffff0000u);
+        b.z = (__float_as_uint(pf[4]) >> 16) | (__float_as_uint(pf[5]) & 0xffff0000u);
+        b.w = (__float_as_uint(pf[6]) >> 16) | (__float_as_uint(pf[7]) & 0xffff0000u);
+        *reinterpret_cast<uint4 *>(PB + e0) = b;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Mean gradient for the host-update route: g_bar of a chunk, FP32 or rounded
 // to BF16, written to a staging slot that the copy engine then moves to host
 // memory.  The rank gradients are read once and not reused (non-temporal).
@@ -414,6 +464,12 @@ hipError_t update_r(const UpdateArgs &a, int64_t blocks, hipStream_t s) {
 }
 
 template <int R>
+hipError_t pattern_r(const UpdateArgs &a, int64_t blocks, hipStream_t s) {
+    hipLaunchKernelGGL((k_update_pattern<R>), dim3((uint32_t)blocks), dim3(kUpdateThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int R>
 hipError_t gbar_r(const GbarArgs &a, int64_t blocks, hipStream_t s) {
     if (a.bf16)
         hipLaunchKernelGGL((k_gbar_out<R, true>), dim3((uint32_t)blocks), dim3(256), 0, s, a);
@@ -448,6 +504,17 @@ hipError_t launch_update(int R, const UpdateArgs &a, int max_blocks, hipStream_t
     if (max_blocks > 0 && blocks > max_blocks) blocks = max_blocks;
     switch (R) {
 #define CASE(r) case r: return update_r<r>(a, blocks, s);
+        SDP_FOR_EACH_R(CASE)
+#undef CASE
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_update_pattern(int R, const UpdateArgs &a, hipStream_t s) {
+    int64_t blocks = cdiv(a.n / kVec, kUpdateThreads);
+    if (blocks < 1) blocks = 1;
+    switch (R) {
+#define CASE(r) case r: return pattern_r<r>(a, blocks, s);
         SDP_FOR_EACH_R(CASE)
 #undef CASE
         default: return hipErrorInvalidValue;

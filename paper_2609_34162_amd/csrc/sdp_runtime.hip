@@ -893,6 +893,23 @@ int sdp_probe_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, void
     return SDP_OK;
 }
 
+int sdp_probe_update_pattern(sdp_ctx *ctx, const sdp_segment *seg, void *stream) {
+    t_err.clear();
+    if (!ctx) return fail(SDP_ERR_INVALID_ARGUMENT, "context is NULL");
+    DeviceGuard guard(ctx->device);
+    int32_t R = 0;
+    SDP_TRY(validate_segments(ctx, seg, 1, kDeviceMem, kDeviceMem, false, &R));
+    sdp::UpdateArgs a{};
+    a.p = seg->master;
+    a.m = seg->exp_avg;
+    a.v = seg->exp_avg_sq;
+    a.pb = seg->param_bf16;
+    for (int32_t r = 0; r < R; ++r) a.g[r] = seg->grads[r];
+    a.n = seg->numel;
+    HIP_TRY(sdp::launch_update_pattern(R, a, (hipStream_t)stream));
+    return SDP_OK;
+}
+
 int sdp_probe_link(sdp_ctx *ctx, void *host_a, void *host_b, void *dev_a, void *dev_b, int64_t bytes,
                    int64_t chunk_bytes, int32_t reps, double *gbs_out) {
     t_err.clear();

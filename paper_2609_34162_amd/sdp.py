@@ -118,6 +118,7 @@ def _load():
         "sdp_ctx_set_timing": (ctypes.c_int, [vp, ctypes.c_int]),
         "sdp_ctx_get_timing": (ctypes.c_int, [vp, P(sdp_kernel_times)]),
         "sdp_probe_copy": (ctypes.c_int, [vp, vp, vp, i64, vp]),
+        "sdp_probe_update_pattern": (ctypes.c_int, [vp, vp, vp]),
         "sdp_probe_link": (ctypes.c_int, [vp, vp, vp, vp, vp, i64, i64, i32, P(dbl)]),
         "sdp_host_alloc": (ctypes.c_int, [P(vp), ctypes.c_size_t]),
         "sdp_host_free": (ctypes.c_int, [vp]),
@@ -334,6 +335,12 @@ def sdp_ctx_get_timing(ctx) -> sdp_kernel_times:
 
 def sdp_probe_copy(ctx, dst: int, src: int, nbytes: int, stream=None) -> None:
     _check(_lib.sdp_probe_copy(ctx, dst, src, nbytes, _stream(stream)))
+
+
+def sdp_probe_update_pattern(ctx, segs: Segments, stream=None) -> None:
+    if segs.n != 1:
+        raise ValueError("sdp_probe_update_pattern takes one segment")
+    _check(_lib.sdp_probe_update_pattern(ctx, segs.ptr, _stream(stream)))
 
 
 def sdp_probe_link(ctx, host_a: int, host_b: int, dev_a: int, dev_b: int, nbytes: int,

@@ -234,6 +234,26 @@ def test_edge_values(sdp, ctx, case, mode):
         assert np.array_equal(got.param_bf16[0], oracle.bf16(master))
 
 
+def test_update_pattern_probe(sdp, ctx):
+    """The measurement probe with the update's access pattern runs on device
+    segments (and writes its trivial results over the states) and refuses
+    host memory."""
+    n, R = 3 * TILE + 8, 4
+    masters, grads = rand_inputs([n], R, 1, seed=131)
+    dev = DevState(masters, R)
+    dev.set_grads(grads[0])
+    sdp.sdp_probe_update_pattern(ctx, dev.segments(sdp), stream())
+    torch.cuda.synchronize()
+    assert not np.array_equal(dev.host().master[0], masters[0])
+    host = HostState(sdp, masters, R)
+    try:
+        with pytest.raises(sdp.SdpError) as e:
+            sdp.sdp_probe_update_pattern(ctx, host.segments(), stream())
+        assert e.value.status == sdp.SDP_ERR_NOT_DEVICE_MEMORY
+    finally:
+        host.close()
+
+
 @pytest.mark.parametrize("chunk_tiles", [1, 2, 4])
 def test_streamed_matches_oracle_and_device(sdp, ctx, ctx_poison, ctx_nostore, chunk_tiles):
     sizes = [3 * TILE + 5, 1, 70000]
