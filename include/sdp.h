@@ -285,6 +285,21 @@ SDP_API int sdp_cast_bf16(sdp_ctx *ctx, const float *src, uint16_t *dst, int64_t
 SDP_API int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf16, int64_t n,
                        int64_t chunk_elems, int mode);
 
+/* Parameter delivery with the version gate on the GPU instead of the host:
+ * as sdp_deliver_params, but the call returns once every chunk is enqueued
+ * (in SDP_DELIVER_HOST_CAST mode, once the host threads have rounded the
+ * last chunk), and work enqueued on `consumer_stream` (a hipStream_t; NULL
+ * is the null stream) after this call waits until the last copy has landed
+ * -- the paper's gate, where dispatch of layer l at iteration t+1 waits for
+ * that layer's update from iteration t (Design, completion and buffer
+ * reuse).  The caller must keep dev_bf16 alive until then.  In
+ * SDP_DELIVER_DEVICE_CAST mode with pinned host_master the DMA reads
+ * host_master after the call returns: leave it unchanged until the gate
+ * has passed.  Later calls on the context are ordered after this one. */
+SDP_API int sdp_deliver_params_async(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf16,
+                                     int64_t n, int64_t chunk_elems, int mode,
+                                     void *consumer_stream);
+
 /* The BF16 rounding of the host delivery lane on its own: dst[i] =
  * bf16_rne(src[i]) for n elements of host memory.  ctx may be NULL (runs on
  * the calling thread, no GPU needed) or a context whose host threads share

@@ -151,9 +151,15 @@ int sdp_cast_bf16_host(sdp_ctx *ctx, const float *src, uint16_t *dst, int64_t n)
     return SDP_OK;
 }
 
-int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf16, int64_t n, int64_t chunk_elems,
-                       int mode) {
-    t_err.clear();
+}  // extern "C"
+
+namespace {
+
+// Parameter delivery; with `gate` the call returns once every chunk is
+// enqueued and `consumer` waits for the last copy on the GPU, else it
+// blocks until the copies have landed.
+int deliver(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf16, int64_t n, int64_t chunk_elems, int mode,
+            bool gate, hipStream_t consumer) {
     if (!ctx || !host_master || !dev_bf16 || n < 1)
         return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_deliver_params: bad argument");
     if (mode != SDP_DELIVER_HOST_CAST && mode != SDP_DELIVER_DEVICE_CAST)
@@ -220,10 +226,39 @@ int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf1
             used[sl] = true;
         }
     }
-    const int rc2 = sync_streams(ctx);
-    if (rc != SDP_OK) return rc;
-    if (rc2 != SDP_OK) return rc2;
-    return mark_done(ctx, ctx->s_comp);
+    if (!gate || rc != SDP_OK) {
+        const std::string err = t_err;
+        const int rc2 = sync_streams(ctx);
+        if (rc != SDP_OK) {
+            t_err = err;
+            return rc;
+        }
+        if (rc2 != SDP_OK) return rc2;
+        return mark_done(ctx, ctx->s_comp);
+    }
+    // the version gate: last_done follows this call's work on both streams,
+    // and the consumer's later work follows last_done
+    HIP_TRY(hipEventRecord(ctx->copy_done, ctx->s_copy));
+    HIP_TRY(hipStreamWaitEvent(ctx->s_comp, ctx->copy_done, 0));
+    SDP_TRY(mark_done(ctx, ctx->s_comp));
+    HIP_TRY(hipStreamWaitEvent(consumer, ctx->last_done, 0));
+    return SDP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf16, int64_t n, int64_t chunk_elems,
+                       int mode) {
+    t_err.clear();
+    return deliver(ctx, host_master, dev_bf16, n, chunk_elems, mode, false, nullptr);
+}
+
+int sdp_deliver_params_async(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf16, int64_t n,
+                             int64_t chunk_elems, int mode, void *consumer_stream) {
+    t_err.clear();
+    return deliver(ctx, host_master, dev_bf16, n, chunk_elems, mode, true, (hipStream_t)consumer_stream);
 }
 
 int sdp_host_update_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, const sdp_adamw_params *hp,

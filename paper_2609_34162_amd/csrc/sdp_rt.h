@@ -215,6 +215,7 @@ struct sdp_ctx {
     hipEvent_t h2d_done[2] = {nullptr, nullptr};
     hipEvent_t slot_free[2] = {nullptr, nullptr};
     hipEvent_t last_done = nullptr;
+    hipEvent_t copy_done = nullptr;  // copy stream's last work of a gated delivery
     bool last_done_valid = false;
     char *staging = nullptr;
     size_t slot_bytes = 0;

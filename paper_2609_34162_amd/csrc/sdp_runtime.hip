@@ -670,6 +670,7 @@ int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems, int32_t m
         CTX_HIP(hipEventCreateWithFlags(&c->slot_free[k], hipEventDisableTiming));
     }
     CTX_HIP(hipEventCreateWithFlags(&c->last_done, hipEventDisableTiming));
+    CTX_HIP(hipEventCreateWithFlags(&c->copy_done, hipEventDisableTiming));
     if (hipMalloc(&c->ns, sizeof(NormState)) != hipSuccess) {
         (void)hipGetLastError();
         return bail(fail(SDP_ERR_OUT_OF_MEMORY, "cannot allocate the norm state"));
@@ -722,6 +723,7 @@ void sdp_ctx_destroy(sdp_ctx *ctx) {
         if (ctx->slot_free[k]) (void)hipEventDestroy(ctx->slot_free[k]);
     }
     if (ctx->last_done) (void)hipEventDestroy(ctx->last_done);
+    if (ctx->copy_done) (void)hipEventDestroy(ctx->copy_done);
     if (ctx->s_copy) (void)hipStreamDestroy(ctx->s_copy);
     if (ctx->s_comp) (void)hipStreamDestroy(ctx->s_comp);
     if (ctx->staging) (void)hipFree(ctx->staging);

@@ -103,6 +103,7 @@ def _load():
         "sdp_cast_bf16": (ctypes.c_int, [vp, vp, vp, i64, vp]),
         "sdp_deliver_params": (ctypes.c_int, [vp, vp, vp, i64, i64, ctypes.c_int]),
         "sdp_cast_bf16_host": (ctypes.c_int, [vp, vp, vp, i64]),
+        "sdp_deliver_params_async": (ctypes.c_int, [vp, vp, vp, i64, i64, ctypes.c_int, vp]),
         "sdp_host_update_step": (ctypes.c_int, [vp, vp, i32, P(sdp_adamw_params), i64, ctypes.c_int, P(dbl)]),
         "sdp_host_adamw": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, ctypes.c_int, i64, dbl,
                                            P(sdp_adamw_params)]),
@@ -242,6 +243,12 @@ def sdp_cast_bf16(ctx, src: int, dst: int, n: int, stream=None) -> None:
 def sdp_deliver_params(ctx, host_master: int, dev_bf16: int, n: int, chunk_elems: int,
                        mode: int = SDP_DELIVER_HOST_CAST) -> None:
     _check(_lib.sdp_deliver_params(ctx, host_master, dev_bf16, n, chunk_elems, mode))
+
+
+def sdp_deliver_params_async(ctx, host_master: int, dev_bf16: int, n: int, chunk_elems: int,
+                             mode: int = SDP_DELIVER_HOST_CAST, consumer_stream=None) -> None:
+    _check(_lib.sdp_deliver_params_async(ctx, host_master, dev_bf16, n, chunk_elems, mode,
+                                         _stream(consumer_stream)))
 
 
 def sdp_cast_bf16_host(ctx, src: int, dst: int, n: int) -> None:

@@ -32,7 +32,7 @@ def sdp():
 
 def test_exports_every_declared_symbol(sdp):
     names = header_functions()
-    assert len(names) == 27, names
+    assert len(names) == 28, names
     lib = ctypes.CDLL(sdp.LIB_PATH)
     missing = [n for n in names if not hasattr(lib, n)]
     assert not missing, missing
@@ -110,6 +110,8 @@ def test_null_arguments_fail_before_any_gpu_call(sdp):
     assert L.sdp_host_adamw(None, None, None, None, None, None, 0, 0, 1.0, None) == sdp.SDP_ERR_INVALID_ARGUMENT
     assert L.sdp_ctx_set_host_threads(None, 4) == sdp.SDP_ERR_INVALID_ARGUMENT
     assert L.sdp_probe_host_copy(None, None, None, 16, 1, None) == sdp.SDP_ERR_INVALID_ARGUMENT
+    assert L.sdp_deliver_params(None, None, None, 1, 65536, 0) == sdp.SDP_ERR_INVALID_ARGUMENT
+    assert L.sdp_deliver_params_async(None, None, None, 1, 65536, 0, None) == sdp.SDP_ERR_INVALID_ARGUMENT
     assert L.sdp_ctx_create(None, 0, 0, 1, 0) == sdp.SDP_ERR_INVALID_ARGUMENT
     assert "NULL" in sdp.sdp_last_error()
     out = ctypes.c_void_p()

@@ -139,6 +139,57 @@ def test_route_then_delivery_closes_the_loop(sdp, ctx):
         st.close()
 
 
+@pytest.mark.parametrize("mode", ["host_cast", "device_cast"])
+@pytest.mark.parametrize("pinned", [False, True])
+def test_async_delivery_gates_the_consumer_stream(sdp, ctx, mode, pinned):
+    """Event-gated delivery: the call returns with the copies in flight, and
+    work that the caller then enqueues on its own stream sees the whole BF16
+    window; back-to-back gated deliveries, a blocking one after them and a
+    route step after them keep their order and results."""
+    m = sdp.SDP_DELIVER_HOST_CAST if mode == "host_cast" else sdp.SDP_DELIVER_DEVICE_CAST
+    sizes = [5 * TILE + 13, 3 * TILE]
+    R = 2
+    masters, grads = rand_inputs(sizes, R, 1, seed=121)
+    st = RouteState(sdp, masters, R, pinned=pinned)
+    consumer = torch.cuda.Stream()
+    try:
+        log(f"gated delivery mode={mode} pinned={pinned}")
+        wins = [torch.full((n,), 0x5555, dtype=torch.int16, device="cuda") for n in sizes]
+        outs = [torch.empty_like(w) for w in wins]
+        torch.cuda.synchronize()
+        for s, n in enumerate(sizes):
+            sdp.sdp_deliver_params_async(ctx, st.host.p[s].ctypes.data, wins[s].data_ptr(), n, TILE, m,
+                                         consumer_stream=consumer.cuda_stream)
+        with torch.cuda.stream(consumer):
+            for w, o in zip(wins, outs):
+                o.copy_(w)
+        consumer.synchronize()
+        for s in range(len(sizes)):
+            want = oracle.bf16(st.host.p[s])
+            assert np.array_equal(outs[s].cpu().numpy().view(np.uint16), want), s
+        # a route step after a gated delivery; then the loop closes with a
+        # gated delivery of the updated master and a blocking one beside it
+        hs, ho = hp_pair(sdp, lr=1e-3, weight_decay=0.01, max_grad_norm=0.5, step=1)
+        ref = oracle.State(masters)
+        sdp.sdp_deliver_params_async(ctx, st.host.p[0].ctypes.data, wins[0].data_ptr(), sizes[0], TILE, m,
+                                     consumer_stream=consumer.cuda_stream)
+        st.set_grads(grads[0])
+        sdp.sdp_host_update_step(ctx, st.segments(sdp), hs, 2 * TILE, sdp.SDP_GBAR_F32)
+        oracle.step(ref, grads[0], ho)
+        check_state(st.state(), ref)
+        sdp.sdp_deliver_params_async(ctx, st.host.p[0].ctypes.data, wins[0].data_ptr(), sizes[0], TILE, m,
+                                     consumer_stream=consumer.cuda_stream)
+        sdp.sdp_deliver_params(ctx, st.host.p[1].ctypes.data, wins[1].data_ptr(), sizes[1], TILE, m)
+        with torch.cuda.stream(consumer):
+            outs[0].copy_(wins[0])
+        consumer.synchronize()
+        assert np.array_equal(outs[0].cpu().numpy().view(np.uint16), st.host.pb[0])
+        assert np.array_equal(wins[1].cpu().numpy().view(np.uint16), st.host.pb[1])
+    finally:
+        torch.cuda.synchronize()
+        st.close()
+
+
 @pytest.mark.parametrize("R", [1, 2, 4, 8, 16])
 def test_host_route_ranks_against_device_mode(sdp, ctx, R):
     """FP32 route and device mode: same norm bits, both within the criteria

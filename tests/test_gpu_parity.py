@@ -390,6 +390,15 @@ def test_grad_norm_modes_agree(sdp, ctx):
     on = oracle.grad_norm(grads[0])
     check_norm(dn, on)
     assert dn == hn
+    # the staged context takes pageable gradients
+    staged = sdp.sdp_ctx_create(0, TILE, R, sdp.SDP_FLAG_STREAM_STAGED)
+    pg = PageableState(sdp, [np.zeros(n, np.float32) for n in sizes], R)
+    try:
+        pg.set_grads(grads[0])
+        assert sdp.sdp_grad_norm(staged, pg.segments(), False, TILE) == dn
+    finally:
+        pg.close()
+        sdp.sdp_ctx_destroy(staged)
 
 
 def test_norm_equals_exactly_rounded_sum(sdp, ctx):
