@@ -77,7 +77,7 @@ extern "C" {
 #define SDP_ERR_NONFINITE (-8)         /* gradient norm is NaN or Inf; nothing was updated */
 
 /* ---- constants --------------------------------------------------------- */
-#define SDP_NORM_TILE 65536 /* elements per norm partial; chunk sizes are multiples of it */
+#define SDP_NORM_TILE 65536 /* norm tile: the norm sums in a grid fixed per tile (eight partials each); chunk sizes are multiples of it */
 #define SDP_MAX_RANKS 16    /* largest R */
 #define SDP_ALIGN 16        /* byte alignment required of every buffer */
 

@@ -20,9 +20,11 @@ struct NormState {
 };
 
 // One launch of the norm pass: `n` elements starting at a tile boundary of
-// a segment.  Block b covers elements [b*TILE, min((b+1)*TILE, n)) and writes
-// the double-double pair partials[2b], partials[2b+1].  When gbar_out is
-// non-null it also stores g_bar there.
+// a segment.  The grid is kNormSplit blocks per tile; block b covers the
+// elements [b*kNormSpan, min((b+1)*kNormSpan, n)) (none, past the end) and
+// writes the double-double pair partials[2b], partials[2b+1], so the tile k
+// of the launch owns pairs kNormSplit*k .. kNormSplit*k + kNormSplit - 1.
+// When gbar_out is non-null it also stores g_bar there.
 struct NormArgs {
     const uint16_t *g[SDP_MAX_RANKS];
     int64_t n;
@@ -59,13 +61,15 @@ struct GbarArgs {
 };
 
 constexpr int kTile = SDP_NORM_TILE;
+constexpr int kNormSplit = 8;                    // norm blocks, and partial pairs, per tile
+constexpr int kNormSpan = kTile / kNormSplit;    // elements per norm block
 constexpr int kNormThreads = 256;
 constexpr int kFinalizeThreads = 1024;
 constexpr int kUpdateThreads = 256;
 constexpr int kVec = 8;  // elements per lane per access (16 B of BF16, 32 B of FP32)
 
 hipError_t launch_norm_partials(int R, const NormArgs &a, hipStream_t s);
-hipError_t launch_norm_finalize(const double *partials /* pairs */, int64_t n_partials,
+hipError_t launch_norm_finalize(const double *partials /* pairs */, int64_t n_pairs,
                                 double max_grad_norm, NormState *ns, hipStream_t s);
 hipError_t launch_update(int R, const UpdateArgs &a, int max_blocks, hipStream_t s);
 hipError_t launch_gbar_out(int R, const GbarArgs &a, hipStream_t s);

@@ -18,6 +18,7 @@ namespace sdp {
 namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -123,55 +124,90 @@ __device__ __forceinline__ void block_merge(double &hi, double &lo) {
 }
 
 // ---------------------------------------------------------------------------
-// Norm partials: block b sums g_bar^2 over tile b.  Lane t handles the
-// 8-element groups b*8192 + j*256 + t for j = 0..31 in increasing j, so each
-// pass of the block reads a contiguous 4 KB per rank; two passes are issued
-// before either is consumed.  The gradients are read with non-temporal loads:
-// they are not reused before the update pass, and the 256 MB last-level cache
-// cannot hold them.  The ragged tail of fewer than 8 elements is added by
-// lane 0 of its tile after the groups.  The per-lane order, the butterfly and
-// the wave order are fixed, so a tile's partial depends on its contents only.
+// Norm partials: each tile is split into kNormSplit spans of kNormSpan
+// elements, and block b sums g_bar^2 over span b of the segment (the grid is
+// kNormSplit blocks per tile, those past the end write a zero pair).  Lanes
+// read V elements per rank at a time: V = 4 (8-byte loads) for the plain
+// pass, V = 8 (16-byte loads) when g_bar is stored, so that a lane's 8 FP32
+// outputs go out as two 16-byte stores.  Lane t handles the V-element groups
+// b*S + 256*j + t (S groups per span) in increasing j, two groups issued
+// before either is consumed.  The gradients are read with non-temporal
+// loads: they are not reused before the update pass, and the 256 MB
+// last-level cache cannot hold them.  The ragged tail of fewer than V
+// elements is added by lane 0 of its span after the groups.  The per-lane
+// order, the butterfly and the wave order are fixed, so a span's partial
+// depends on its contents only.
 __device__ __forceinline__ uint4 load_stream(const uint16_t *p) {
     const u32x4 t = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
     return make_uint4(t.x, t.y, t.z, t.w);
 }
 
+template <int V>
+__device__ __forceinline__ void load_stream_v(const uint16_t *p, uint32_t (&w)[V / 2]) {
+    if constexpr (V == 8) {
+        const u32x4 t = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+        w[0] = t.x; w[1] = t.y; w[2] = t.z; w[3] = t.w;
+    } else {
+        const u32x2 t = __builtin_nontemporal_load(reinterpret_cast<const u32x2 *>(p));
+        w[0] = t.x; w[1] = t.y;
+    }
+}
+
 template <int R, bool WRITE_GBAR>
 __global__ __launch_bounds__(kNormThreads) void k_norm_partials(NormArgs a) {
-    constexpr int kGroupsPerTile = kTile / kVec;                    // 8192
+    constexpr int V = WRITE_GBAR ? 8 : 4;
+    constexpr int kGroupsPerSpan = kNormSpan / V;
     constexpr int kUnroll = 2;
-    constexpr int kIters = kGroupsPerTile / (kNormThreads * kUnroll);  // 16
+    constexpr int kIters = kGroupsPerSpan / (kNormThreads * kUnroll);
+    static_assert(kIters * kNormThreads * kUnroll == kGroupsPerSpan, "span must split evenly over the lanes");
     const int64_t n = a.n;
-    const int64_t full_groups = n / kVec;
-    const int64_t tile0 = (int64_t)blockIdx.x * kGroupsPerTile;
+    const int64_t full_groups = n / V;
+    const int64_t span0 = (int64_t)blockIdx.x * kGroupsPerSpan;
     double hi = 0.0, lo = 0.0;
     for (int it = 0; it < kIters; ++it) {
-        uint4 raw[kUnroll][R];
+        uint32_t raw[kUnroll][R][V / 2];
         bool ok[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            const int64_t q = tile0 + (int64_t)(it * kUnroll + u) * kNormThreads + threadIdx.x;
+            const int64_t q = span0 + (int64_t)(it * kUnroll + u) * kNormThreads + threadIdx.x;
             ok[u] = q < full_groups;
 #pragma unroll
-            for (int r = 0; r < R; ++r) raw[u][r] = ok[u] ? load_stream(a.g[r] + q * kVec) : make_uint4(0, 0, 0, 0);
+            for (int r = 0; r < R; ++r) {
+                if (ok[u]) {
+                    load_stream_v<V>(a.g[r] + q * V, raw[u][r]);
+                } else {
+#pragma unroll
+                    for (int w = 0; w < V / 2; ++w) raw[u][r][w] = 0;
+                }
+            }
         }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             if (!ok[u]) continue;
-            float g[kVec];
-            mean8<R>(raw[u], g);
+            float g[V];
 #pragma unroll
-            for (int e = 0; e < kVec; ++e) dd_add(hi, lo, (double)g[e] * (double)g[e]);
+            for (int w = 0; w < V / 2; ++w) {
+                double s_lo = 0.0, s_hi = 0.0;
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    s_lo += (double)bf16_lo(raw[u][r][w]);
+                    s_hi += (double)bf16_hi(raw[u][r][w]);
+                }
+                g[2 * w] = mean_of<R>(s_lo);
+                g[2 * w + 1] = mean_of<R>(s_hi);
+            }
+#pragma unroll
+            for (int e = 0; e < V; ++e) dd_add(hi, lo, (double)g[e] * (double)g[e]);
             if constexpr (WRITE_GBAR) {
-                const int64_t e0 = (tile0 + (int64_t)(it * kUnroll + u) * kNormThreads + threadIdx.x) * kVec;
+                const int64_t e0 = (span0 + (int64_t)(it * kUnroll + u) * kNormThreads + threadIdx.x) * V;
                 float4 *o = reinterpret_cast<float4 *>(a.gbar_out + e0);
                 o[0] = make_float4(g[0], g[1], g[2], g[3]);
                 o[1] = make_float4(g[4], g[5], g[6], g[7]);
             }
         }
     }
-    const int64_t tail0 = full_groups * kVec;
-    if (threadIdx.x == 0 && tail0 < n && tail0 / kTile == (int64_t)blockIdx.x) {
+    const int64_t tail0 = full_groups * V;
+    if (threadIdx.x == 0 && tail0 < n && tail0 / kNormSpan == (int64_t)blockIdx.x) {
         for (int64_t i = tail0; i < n; ++i) {
             float g = mean1<R>(a.g, i);
             dd_add(hi, lo, (double)g * (double)g);
@@ -185,14 +221,33 @@ __global__ __launch_bounds__(kNormThreads) void k_norm_partials(NormArgs a) {
     }
 }
 
-// One block: fixed-order sum of all tile partials (pairs), then the norm, the
-// clip coefficient and the non-finite flag.
+// One block: fixed-order sum of all span partials (pairs), then the norm, the
+// clip coefficient and the non-finite flag.  Thread t takes the pairs
+// t + 1024*j; pair j goes to the thread's accumulator j mod 4 (four
+// independent chains), each merged in increasing j, and the four are then
+// merged in order.  Loads are issued 16 at a time so that their latencies
+// overlap.
 __global__ __launch_bounds__(kFinalizeThreads) void k_norm_finalize(
     const double *__restrict__ partials, int64_t n_partials, double max_grad_norm,
     NormState *__restrict__ ns) {
-    double hi = 0.0, lo = 0.0;
-    for (int64_t i = threadIdx.x; i < n_partials; i += kFinalizeThreads)
-        dd_merge(hi, lo, partials[2 * i], partials[2 * i + 1]);
+    constexpr int kBatch = 16;
+    constexpr int kChains = 4;
+    const double2 *pairs = reinterpret_cast<const double2 *>(partials);
+    double chi[kChains] = {0.0, 0.0, 0.0, 0.0}, clo[kChains] = {0.0, 0.0, 0.0, 0.0};
+    for (int64_t i0 = threadIdx.x; i0 < n_partials; i0 += (int64_t)kBatch * kFinalizeThreads) {
+        double2 b[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int64_t i = i0 + (int64_t)u * kFinalizeThreads;
+            b[u] = i < n_partials ? pairs[i] : make_double2(0.0, 0.0);
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u)
+            if (i0 + (int64_t)u * kFinalizeThreads < n_partials) dd_merge(chi[u % kChains], clo[u % kChains], b[u].x, b[u].y);
+    }
+    double hi = chi[0], lo = clo[0];
+#pragma unroll
+    for (int c = 1; c < kChains; ++c) dd_merge(hi, lo, chi[c], clo[c]);
     block_merge<kFinalizeThreads>(hi, lo);
     if (threadIdx.x == 0) {
         const double S = hi;
@@ -446,7 +501,7 @@ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 template <int R>
 hipError_t norm_r(const NormArgs &a, hipStream_t s) {
-    const int64_t blocks = cdiv(a.n, kTile);
+    const int64_t blocks = cdiv(a.n, kTile) * kNormSplit;
     if (a.gbar_out)
         hipLaunchKernelGGL((k_norm_partials<R, true>), dim3((uint32_t)blocks), dim3(kNormThreads), 0, s, a);
     else

@@ -267,7 +267,8 @@ int check_chunk(int64_t chunk, bool allow_zero);
 
 // ---- workspace ----------------------------------------------------------
 
-int ensure_partials(sdp_ctx *ctx, int64_t n);
+int ensure_partials(sdp_ctx *ctx, int64_t tiles);
+double *tile_partials(sdp_ctx *ctx, int64_t tile);  // the first pair of a tile's span partials
 int ensure_gbar(sdp_ctx *ctx, int64_t n);
 // Layout of one call: norm tiles and stored-g_bar offsets of each segment.
 struct Plan {

@@ -201,14 +201,17 @@ int check_chunk(int64_t chunk, bool allow_zero) {
 
 // ---- workspace ----------------------------------------------------------
 
-int ensure_partials(sdp_ctx *ctx, int64_t n) {
+double *tile_partials(sdp_ctx *ctx, int64_t tile) { return ctx->partials + 2 * sdp::kNormSplit * tile; }
+
+int ensure_partials(sdp_ctx *ctx, int64_t tiles) {
+    const int64_t n = tiles * sdp::kNormSplit;
     if (n <= ctx->partials_cap) return SDP_OK;
     HIP_TRY(hipDeviceSynchronize());
     if (ctx->partials) HIP_TRY(hipFree(ctx->partials));
     ctx->partials = nullptr;
     ctx->partials_cap = 0;
     int64_t cap = std::max<int64_t>(n, 4096);
-    // each tile partial is a double-double pair
+    // each span partial is a double-double pair
     if (hipMalloc(&ctx->partials, (size_t)cap * 2 * sizeof(double)) != hipSuccess) {
         (void)hipGetLastError();
         ctx->partials = nullptr;
@@ -306,7 +309,7 @@ int norm_launch(sdp_ctx *ctx, int32_t R, const uint16_t *const *g, int64_t n, do
 
 int finalize_launch(sdp_ctx *ctx, int64_t tiles, double max_grad_norm, hipStream_t s) {
     hipEvent_t t0 = timed_begin(ctx, s);
-    HIP_TRY(sdp::launch_norm_finalize(ctx->partials, tiles, max_grad_norm, ctx->ns, s));
+    HIP_TRY(sdp::launch_norm_finalize(ctx->partials, tiles * sdp::kNormSplit, max_grad_norm, ctx->ns, s));
     timed_end(ctx, s, t0, kFinalize, tiles);
     return SDP_OK;
 }
@@ -374,7 +377,7 @@ int sync_streams(sdp_ctx *ctx) {
 int device_norm(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R, const Plan &plan, bool store_gbar,
                 double max_grad_norm, hipStream_t s) {
     for (int32_t k = 0; k < n_segs; ++k)
-        SDP_TRY(norm_launch(ctx, R, segs[k].grads, segs[k].numel, ctx->partials + 2 * plan.tile_base[k],
+        SDP_TRY(norm_launch(ctx, R, segs[k].grads, segs[k].numel, tile_partials(ctx, plan.tile_base[k]),
                             store_gbar ? ctx->gbar + plan.gbar_base[k] : nullptr, s));
     return finalize_launch(ctx, plan.tiles, max_grad_norm, s);
 }

@@ -105,7 +105,7 @@ int stream_norm_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int
         HIP_TRY(hipStreamWaitEvent(ctx->s_comp, ctx->h2d_done[sl], 0));
         const uint16_t *gp[SDP_MAX_RANKS];
         for (int32_t r = 0; r < R; ++r) gp[r] = slot.g[r];
-        SDP_TRY(norm_launch(ctx, R, gp, c.len, ctx->partials + 2 * (plan.tile_base[c.seg] + c.off / SDP_NORM_TILE),
+        SDP_TRY(norm_launch(ctx, R, gp, c.len, tile_partials(ctx, plan.tile_base[c.seg] + c.off / SDP_NORM_TILE),
                             store_gbar ? ctx->gbar + plan.gbar_base[c.seg] + c.off : nullptr, ctx->s_comp));
         SDP_TRY(poison(ctx, sl));
         HIP_TRY(hipEventRecord(ctx->slot_free[sl], ctx->s_comp));
