@@ -65,15 +65,21 @@ constexpr int kNormSplit = 8;                    // norm blocks, and partial pai
 constexpr int kNormSpan = kTile / kNormSplit;    // elements per norm block
 constexpr int kNormThreads = 256;
 constexpr int kFinalizeThreads = 1024;
-constexpr int kUpdateThreads = 256;
+constexpr int kUpdateThreads = 64;
+// Fused update residency: blocks of one wave, at most kUpdateBlocksPerCU of
+// them per compute unit (two waves per SIMD).  The update's mix of seven read
+// and four write streams runs faster with fewer waves in flight than the
+// registers would allow; the cap is imposed with dynamic LDS that the kernel
+// does not use (the LDS of a compute unit divided by the cap, per block).
+constexpr int kUpdateBlocksPerCU = 8;
 constexpr int kVec = 8;  // elements per lane per access (16 B of BF16, 32 B of FP32)
 
 hipError_t launch_norm_partials(int R, const NormArgs &a, hipStream_t s);
 hipError_t launch_norm_finalize(const double *partials /* pairs */, int64_t n_pairs,
                                 double max_grad_norm, NormState *ns, hipStream_t s);
-hipError_t launch_update(int R, const UpdateArgs &a, int max_blocks, hipStream_t s);
+hipError_t launch_update(int R, const UpdateArgs &a, int max_blocks, int lds_pad, hipStream_t s);
 hipError_t launch_gbar_out(int R, const GbarArgs &a, hipStream_t s);
-hipError_t launch_update_pattern(int R, const UpdateArgs &a, hipStream_t s);
+hipError_t launch_update_pattern(int R, const UpdateArgs &a, int lds_pad, hipStream_t s);
 hipError_t launch_cast_bf16(const float *src, uint16_t *dst, int64_t n, hipStream_t s);
 hipError_t launch_copy16(void *dst, const void *src, int64_t n16, int max_blocks, hipStream_t s);
 hipError_t launch_fill_u32(void *dst, int64_t n_words, uint32_t value, hipStream_t s);

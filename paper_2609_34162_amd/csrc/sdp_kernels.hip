@@ -510,17 +510,17 @@ hipError_t norm_r(const NormArgs &a, hipStream_t s) {
 }
 
 template <int R>
-hipError_t update_r(const UpdateArgs &a, int64_t blocks, hipStream_t s) {
+hipError_t update_r(const UpdateArgs &a, int64_t blocks, int lds_pad, hipStream_t s) {
     if (a.gbar)
-        hipLaunchKernelGGL((k_update<1, true>), dim3((uint32_t)blocks), dim3(kUpdateThreads), 0, s, a);
+        hipLaunchKernelGGL((k_update<1, true>), dim3((uint32_t)blocks), dim3(kUpdateThreads), lds_pad, s, a);
     else
-        hipLaunchKernelGGL((k_update<R, false>), dim3((uint32_t)blocks), dim3(kUpdateThreads), 0, s, a);
+        hipLaunchKernelGGL((k_update<R, false>), dim3((uint32_t)blocks), dim3(kUpdateThreads), lds_pad, s, a);
     return hipGetLastError();
 }
 
 template <int R>
-hipError_t pattern_r(const UpdateArgs &a, int64_t blocks, hipStream_t s) {
-    hipLaunchKernelGGL((k_update_pattern<R>), dim3((uint32_t)blocks), dim3(kUpdateThreads), 0, s, a);
+hipError_t pattern_r(const UpdateArgs &a, int64_t blocks, int lds_pad, hipStream_t s) {
+    hipLaunchKernelGGL((k_update_pattern<R>), dim3((uint32_t)blocks), dim3(kUpdateThreads), lds_pad, s, a);
     return hipGetLastError();
 }
 
@@ -553,23 +553,23 @@ hipError_t launch_norm_finalize(const double *partials, int64_t n_partials, doub
     return hipGetLastError();
 }
 
-hipError_t launch_update(int R, const UpdateArgs &a, int max_blocks, hipStream_t s) {
+hipError_t launch_update(int R, const UpdateArgs &a, int max_blocks, int lds_pad, hipStream_t s) {
     int64_t blocks = cdiv(a.n / kVec, kUpdateThreads);
     if (blocks < 1) blocks = 1;
     if (max_blocks > 0 && blocks > max_blocks) blocks = max_blocks;
     switch (R) {
-#define CASE(r) case r: return update_r<r>(a, blocks, s);
+#define CASE(r) case r: return update_r<r>(a, blocks, lds_pad, s);
         SDP_FOR_EACH_R(CASE)
 #undef CASE
         default: return hipErrorInvalidValue;
     }
 }
 
-hipError_t launch_update_pattern(int R, const UpdateArgs &a, hipStream_t s) {
+hipError_t launch_update_pattern(int R, const UpdateArgs &a, int lds_pad, hipStream_t s) {
     int64_t blocks = cdiv(a.n / kVec, kUpdateThreads);
     if (blocks < 1) blocks = 1;
     switch (R) {
-#define CASE(r) case r: return pattern_r<r>(a, blocks, s);
+#define CASE(r) case r: return pattern_r<r>(a, blocks, lds_pad, s);
         SDP_FOR_EACH_R(CASE)
 #undef CASE
         default: return hipErrorInvalidValue;

@@ -342,7 +342,7 @@ int update_launch(sdp_ctx *ctx, int32_t R, const sdp_adamw_params *hp, float *p,
     a.ns = ctx->ns;
     fill_consts(hp, a);
     hipEvent_t t0 = timed_begin(ctx, s);
-    HIP_TRY(sdp::launch_update(R, a, ctx->update_max_blocks, s));
+    HIP_TRY(sdp::launch_update(R, a, ctx->update_max_blocks, ctx->update_lds_pad, s));
     timed_end(ctx, s, t0, kUpdate, n);
     return SDP_OK;
 }
@@ -658,6 +658,23 @@ int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems, int32_t m
         sdp_ctx_destroy(c);
         return status;
     };
+    {
+        // residency cap of the fused update: the compute unit's LDS split
+        // over kUpdateBlocksPerCU blocks (SDP_UPDATE_BLOCKS_PER_CU overrides;
+        // 0 lifts the cap)
+        int per_cu = sdp::kUpdateBlocksPerCU;
+        if (const char *env = std::getenv("SDP_UPDATE_BLOCKS_PER_CU")) per_cu = std::max(0, std::atoi(env));
+        int lds_cu = 0, lds_block = 0;
+        if (hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, device) != hipSuccess ||
+            hipDeviceGetAttribute(&lds_block, hipDeviceAttributeMaxSharedMemoryPerBlock, device) != hipSuccess) {
+            (void)hipGetLastError();
+            return bail(fail(SDP_ERR_HIP, "cannot query the device's LDS size"));
+        }
+        if (per_cu > 0) {
+            const int pad = lds_cu / per_cu / 1024 * 1024;
+            if (pad > 0 && pad <= lds_block) c->update_lds_pad = pad;
+        }
+    }
 #define CTX_HIP(expr)                                                                                \
     do {                                                                                             \
         hipError_t e_ = (expr);                                                                      \
@@ -911,7 +928,7 @@ int sdp_probe_update_pattern(sdp_ctx *ctx, const sdp_segment *seg, void *stream)
     a.pb = seg->param_bf16;
     for (int32_t r = 0; r < R; ++r) a.g[r] = seg->grads[r];
     a.n = seg->numel;
-    HIP_TRY(sdp::launch_update_pattern(R, a, (hipStream_t)stream));
+    HIP_TRY(sdp::launch_update_pattern(R, a, ctx->update_lds_pad, (hipStream_t)stream));
     return SDP_OK;
 }
 
