@@ -234,6 +234,41 @@ def test_edge_values(sdp, ctx, case, mode):
         assert np.array_equal(got.param_bf16[0], oracle.bf16(master))
 
 
+@pytest.mark.parametrize("R", [4, 8])
+def test_residency_cap_does_not_change_results(sdp, R, monkeypatch):
+    """The fused update's residency cap (one-wave blocks, at most 8 per
+    compute unit) is a launch shape only: uncapped, capped at 8 and capped
+    at 3 blocks per compute unit give the same bits, also with the capped
+    grid-stride launch of SDP_UPDATE_MAX_BLOCKS."""
+    n = 5 * TILE + 13
+    masters, grads = rand_inputs([n], R, 2, seed=141 + R)
+    outs = []
+    for per_cu, max_blocks in (("0", None), (None, None), ("3", None), (None, "40")):
+        for name, val in (("SDP_UPDATE_BLOCKS_PER_CU", per_cu), ("SDP_UPDATE_MAX_BLOCKS", max_blocks)):
+            if val is None:
+                monkeypatch.delenv(name, raising=False)
+            else:
+                monkeypatch.setenv(name, val)
+        c = sdp.sdp_ctx_create(0, 0, R, 0)  # reads the variables
+        try:
+            dev = DevState(masters, R)
+            for t in (1, 2):
+                hs, _ = hp_pair(sdp, lr=1e-3, weight_decay=0.02, max_grad_norm=0.05, step=t)
+                dev_step(sdp, c, dev, grads[t - 1], hs)
+            outs.append(dev.host())
+        finally:
+            sdp.sdp_ctx_destroy(c)
+    monkeypatch.delenv("SDP_UPDATE_BLOCKS_PER_CU", raising=False)
+    monkeypatch.delenv("SDP_UPDATE_MAX_BLOCKS", raising=False)
+    ref = oracle.State(masters)
+    for t in (1, 2):
+        _, ho = hp_pair(sdp, lr=1e-3, weight_decay=0.02, max_grad_norm=0.05, step=t)
+        oracle.step(ref, grads[t - 1], ho)
+    check_state(outs[0], ref)
+    for o in outs[1:]:
+        assert states_equal(outs[0], o)
+
+
 def test_update_pattern_probe(sdp, ctx):
     """The measurement probe with the update's access pattern runs on device
     segments (and writes its trivial results over the states) and refuses
