@@ -200,6 +200,50 @@ def test_qwen3_14b_layer_device_equals_streamed(sdp):
         pin.close()
 
 
+@pytest.mark.timeout(400)
+def test_qwen3_14b_layer_chunk_sizes_agree(sdp):
+    """Chunk invariance at the full layer: streamed mode with chunks of one
+    tile, 16M and 64M elements gives the device mode's bits and norm (the
+    32M chunking is covered above)."""
+    w = synth.workload(2)
+    n, R = w.numel, w.ranks
+    master = synth.master(w, 0)
+    pin = Pinned(sdp)
+    try:
+        grads = [[pin.array(np.uint16, n) for _ in range(R)]]
+        gen_grads(w, 1, grads)
+        hs = sdp.make_params(**w.hparams(1))
+        dev = DevState([master], R)
+        dev.set_grads(grads)
+        ctx = sdp.sdp_ctx_create(0, 0, R, 0)
+        try:
+            dn = sdp.sdp_agg_adam_step(ctx, dev.segments(sdp), hs, 0, torch.cuda.current_stream().cuda_stream,
+                                       want_norm=True)
+        finally:
+            sdp.sdp_ctx_destroy(ctx)
+        got = pin.state([n])
+        dev_to_host(got, dev)
+        del dev
+        torch.cuda.empty_cache()
+        for chunk in (65536, 1 << 24, 1 << 26):
+            host = HostState(sdp, [master], R)
+            ctx = sdp.sdp_ctx_create(0, chunk, R, 0)
+            try:
+                for r in range(R):
+                    np.copyto(host.g[0][r], grads[0][r])
+                sn = sdp.sdp_stream_step(ctx, host.segments(), hs, chunk)
+                hstate = oracle.State.__new__(oracle.State)
+                hstate.master, hstate.exp_avg, hstate.exp_avg_sq, hstate.param_bf16 = host.p, host.m, host.v, host.pb
+                assert sn == dn, chunk
+                assert states_equal(got, hstate), f"chunk {chunk} differs from device mode"
+                log(f"  chunk {chunk}: streamed == device, norm {sn:.9g}")
+            finally:
+                sdp.sdp_ctx_destroy(ctx)
+                host.close()
+    finally:
+        pin.close()
+
+
 @pytest.mark.timeout(600)
 @pytest.mark.parametrize("fmt", ["f32", "bf16"])
 def test_qwen3_14b_layer_host_route_full(sdp, fmt):
