@@ -20,7 +20,9 @@ JSON line also carries:
                    states in pageable memory, through the staged mode;
   delivery (inside streamed) -- BF16 copies of the layer's FP32 master
                    delivered into a device window, rounded on the host or on
-                   the GPU, from pinned and pageable memory;
+                   the GPU, from pinned and pageable memory; each also three
+                   times back to back with the version gate on the GPU
+                   ("gated");
   chunk_sweep (inside streamed and host_route) -- measured step time at
                    chunk sizes of 4-128 MiB per FP32 array beside the
                    library's step-time model fed with rates measured in
@@ -381,6 +383,20 @@ def stream_leg(args, torch, np, synth, sdp, dres):
                 link_bytes = (2 if mode == sdp.SDP_DELIVER_HOST_CAST else 4) * N
                 deliv[f"{mname}_{sname}"] = dict(ms=el_d * 1e3, params_per_s=N / el_d, bf16_gbs=2 * N / el_d / 1e9,
                                                  link_gbs=link_bytes / el_d / 1e9)
+                # the same deliveries back to back with the gate on the GPU:
+                # the host enqueues the next one while the copies still run
+                consumer = torch.cuda.current_stream()
+                sdp.sdp_deliver_params_async(dctx, src.ctypes.data, window.data_ptr(), N, C, mode,
+                                             consumer_stream=consumer.cuda_stream)
+                consumer.synchronize()
+                t0 = time.perf_counter()
+                for _ in range(3):
+                    sdp.sdp_deliver_params_async(dctx, src.ctypes.data, window.data_ptr(), N, C, mode,
+                                                 consumer_stream=consumer.cuda_stream)
+                consumer.synchronize()
+                el_g = (time.perf_counter() - t0) / 3
+                deliv[f"{mname}_{sname}"]["gated"] = dict(ms=el_g * 1e3, bf16_gbs=2 * N / el_g / 1e9,
+                                                          link_gbs=link_bytes / el_g / 1e9)
         sdp.sdp_ctx_destroy(dctx)
         out["delivery"] = deliv
         del pg, window
