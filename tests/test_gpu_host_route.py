@@ -306,5 +306,16 @@ def test_host_route_argument_errors(sdp, ctx):
         finally:
             sdp.sdp_ctx_destroy(nostage)
         assert states_equal(before, st.state())
+        # gated delivery: the same checks as the blocking one, before any work
+        window = torch.full((n,), 0x5555, dtype=torch.int16, device="cuda")
+        s = torch.cuda.current_stream().cuda_stream
+        deliver = L.sdp_deliver_params_async
+        assert deliver(ctx, h.p[0].ctypes.data, window.data_ptr(), n, TILE, 7, s) == sdp.SDP_ERR_INVALID_ARGUMENT
+        assert deliver(ctx, h.p[0].ctypes.data, window.data_ptr(), n, TILE + 1, 0, s) == sdp.SDP_ERR_INVALID_ARGUMENT
+        assert deliver(ctx, h.p[0].ctypes.data, window.data_ptr(), n, 8 * TILE, 0, s) == sdp.SDP_ERR_CHUNK_TOO_LARGE
+        assert deliver(ctx, h.p[0].ctypes.data, window.data_ptr() + 2, n, TILE, 0, s) == sdp.SDP_ERR_ALIGNMENT
+        assert deliver(ctx, h.p[0].ctypes.data, h.pb[0].ctypes.data, n, TILE, 0, s) == sdp.SDP_ERR_NOT_DEVICE_MEMORY
+        torch.cuda.synchronize()
+        assert np.all(window.cpu().numpy().view(np.uint16) == 0x5555)
     finally:
         st.close()
