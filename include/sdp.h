@@ -158,7 +158,7 @@ typedef struct {
  * max_ranks in 1..SDP_MAX_RANKS bounds R for streamed mode staging.  The
  * context creates two streams (default priority) and its events.  Other
  * workspace (norm partials, cached g_bar) grows on demand.  The fused update
- * keeps at most 8 of its one-wave blocks on a compute unit, through dynamic
+ * keeps at most 10 of its one-wave blocks on a compute unit, through dynamic
  * LDS that it does not use; the environment variable
  * SDP_UPDATE_BLOCKS_PER_CU, read here, sets another cap (0: none). */
 SDP_API int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems,

@@ -67,12 +67,14 @@ constexpr int kNormThreads = 256;
 constexpr int kFinalizeThreads = 1024;
 constexpr int kUpdateThreads = 64;
 // Fused update residency: blocks of one wave, at most kUpdateBlocksPerCU of
-// them per compute unit (two waves per SIMD).  The update's mix of seven read
-// and four write streams runs faster with fewer waves in flight than the
-// registers would allow; the cap is imposed with dynamic LDS that the kernel
-// does not use (the LDS of a compute unit divided by the cap, per block).
-constexpr int kUpdateBlocksPerCU = 8;
-constexpr int kVec = 8;  // elements per lane per access (16 B of BF16, 32 B of FP32)
+// them per compute unit (two or three waves per SIMD).  The update's mix of
+// seven read and four write streams runs faster with fewer waves in flight
+// than the registers would allow; the cap is imposed with dynamic LDS that
+// the kernel does not use (the LDS of a compute unit divided by the cap, per
+// block).
+constexpr int kUpdateBlocksPerCU = 10;
+constexpr int kVec = 8;     // elements per lane per access (16 B of BF16, 32 B of FP32)
+constexpr int kUpdVec = 4;  // fused update: elements per lane (8 B of BF16, 16 B of FP32)
 
 hipError_t launch_norm_partials(int R, const NormArgs &a, hipStream_t s);
 hipError_t launch_norm_finalize(const double *partials /* pairs */, int64_t n_pairs,

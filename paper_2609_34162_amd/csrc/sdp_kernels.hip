@@ -1,7 +1,8 @@
 // gfx950 kernels of the data-parallel update: norm partials over fixed tiles,
 // a one-block fixed-order finalize, and the fused aggregate + clip + AdamW +
-// BF16 re-emit pass.  All of them are bound by HBM bandwidth: every lane moves
-// 16-byte (dwordx4) accesses, eight elements at a time, and no MFMA is used.
+// BF16 re-emit pass.  All of them are bound by HBM bandwidth and use no MFMA.
+// Their lanes move wide accesses: 16-byte (dwordx4) FP32 accesses throughout,
+// and BF16 in 16-byte or 8-byte pieces (eight or four elements per lane).
 //
 // Element arithmetic (the paper names mixed-precision Adam over FP32 master
 // weights and moments, fed by the gradient averaged over the ranks, and BF16
@@ -298,6 +299,25 @@ __device__ __forceinline__ void adamw(float &p, float &m, float &v, float g_bar,
     v = (float)v1;
 }
 
+// g_bar of the 4 elements held as BF16 in raw[r] (one 8-byte load per rank).
+template <int R>
+__device__ __forceinline__ void mean4(const uint2 (&raw)[R], float (&g)[kUpdVec]) {
+#pragma unroll
+    for (int w = 0; w < 2; ++w) {
+        double s_lo = 0.0, s_hi = 0.0;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            uint32_t word = (&raw[r].x)[w];
+            s_lo += (double)bf16_lo(word);
+            s_hi += (double)bf16_hi(word);
+        }
+        g[2 * w] = mean_of<R>(s_lo);
+        g[2 * w + 1] = mean_of<R>(s_hi);
+    }
+}
+
+// Lane t of the grid handles elements 4t .. 4t+3: each access of a wave is
+// one contiguous run (1 KB of every FP32 array, 512 B of every BF16 one).
 template <int R, bool CACHED>
 __global__ __launch_bounds__(kUpdateThreads) void k_update(UpdateArgs a) {
     const NormState *ns = a.ns;
@@ -319,46 +339,40 @@ __global__ __launch_bounds__(kUpdateThreads) void k_update(UpdateArgs a) {
     uint16_t *__restrict__ PB = a.pb;
     const float *__restrict__ GB = a.gbar;
     const int64_t n = a.n;
-    const int64_t groups = n / kVec;
+    const int64_t groups = n / kUpdVec;
     const int64_t gid = (int64_t)blockIdx.x * kUpdateThreads + threadIdx.x;
     const int64_t stride = (int64_t)gridDim.x * kUpdateThreads;
 
     for (int64_t q = gid; q < groups; q += stride) {
-        const int64_t e0 = q * kVec;
-        float g[kVec];
+        const int64_t e0 = q * kUpdVec;
+        float g[kUpdVec];
         if constexpr (CACHED) {
-            const float4 a0 = reinterpret_cast<const float4 *>(GB + e0)[0];
-            const float4 a1 = reinterpret_cast<const float4 *>(GB + e0)[1];
+            const float4 a0 = *reinterpret_cast<const float4 *>(GB + e0);
             g[0] = a0.x; g[1] = a0.y; g[2] = a0.z; g[3] = a0.w;
-            g[4] = a1.x; g[5] = a1.y; g[6] = a1.z; g[7] = a1.w;
         } else {
-            uint4 raw[R];
+            uint2 raw[R];
 #pragma unroll
-            for (int r = 0; r < R; ++r) raw[r] = *reinterpret_cast<const uint4 *>(a.g[r] + e0);
-            mean8<R>(raw, g);
+            for (int r = 0; r < R; ++r) raw[r] = *reinterpret_cast<const uint2 *>(a.g[r] + e0);
+            mean4<R>(raw, g);
         }
         float4 *p4 = reinterpret_cast<float4 *>(P + e0);
         float4 *m4 = reinterpret_cast<float4 *>(M + e0);
         float4 *v4 = reinterpret_cast<float4 *>(V + e0);
-        float4 pv[2] = {p4[0], p4[1]};
-        float4 mv[2] = {m4[0], m4[1]};
-        float4 vv[2] = {v4[0], v4[1]};
-        float *pf = &pv[0].x, *mf = &mv[0].x, *vf = &vv[0].x;
+        float4 pv = *p4, mv = *m4, vv = *v4;
+        float *pf = &pv.x, *mf = &mv.x, *vf = &vv.x;
 #pragma unroll
-        for (int e = 0; e < kVec; ++e) adamw(pf[e], mf[e], vf[e], g[e], k);
-        p4[0] = pv[0]; p4[1] = pv[1];
-        m4[0] = mv[0]; m4[1] = mv[1];
-        v4[0] = vv[0]; v4[1] = vv[1];
-        uint4 b;
+        for (int e = 0; e < kUpdVec; ++e) adamw(pf[e], mf[e], vf[e], g[e], k);
+        *p4 = pv;
+        *m4 = mv;
+        *v4 = vv;
+        uint2 b;
         b.x = pack_bf16(pf[0], pf[1]);
         b.y = pack_bf16(pf[2], pf[3]);
-        b.z = pack_bf16(pf[4], pf[5]);
-        b.w = pack_bf16(pf[6], pf[7]);
-        *reinterpret_cast<uint4 *>(PB + e0) = b;
+        *reinterpret_cast<uint2 *>(PB + e0) = b;
     }
-    // ragged tail of fewer than 8 elements
+    // ragged tail of fewer than 4 elements
     if (gid == 0) {
-        for (int64_t i = groups * kVec; i < n; ++i) {
+        for (int64_t i = groups * kUpdVec; i < n; ++i) {
             float gb;
             if constexpr (CACHED) gb = GB[i];
             else gb = mean1<R>(a.g, i);
@@ -383,40 +397,36 @@ __global__ __launch_bounds__(kUpdateThreads) void k_update_pattern(UpdateArgs a)
     float *__restrict__ V = a.v;
     uint16_t *__restrict__ PB = a.pb;
     const int64_t n = a.n;
-    const int64_t groups = n / kVec;
+    const int64_t groups = n / kUpdVec;
     const int64_t gid = (int64_t)blockIdx.x * kUpdateThreads + threadIdx.x;
     const int64_t stride = (int64_t)gridDim.x * kUpdateThreads;
     for (int64_t q = gid; q < groups; q += stride) {
-        const int64_t e0 = q * kVec;
+        const int64_t e0 = q * kUpdVec;
         uint32_t x = 0;
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-            const uint4 w = *reinterpret_cast<const uint4 *>(a.g[r] + e0);
-            x ^= w.x ^ w.y ^ w.z ^ w.w;
+            const uint2 w = *reinterpret_cast<const uint2 *>(a.g[r] + e0);
+            x ^= w.x ^ w.y;
         }
         const float gx = __uint_as_float((x & 0x007fffffu) | 0x3f800000u);
         float4 *p4 = reinterpret_cast<float4 *>(P + e0);
         float4 *m4 = reinterpret_cast<float4 *>(M + e0);
         float4 *v4 = reinterpret_cast<float4 *>(V + e0);
-        float4 pv[2] = {p4[0], p4[1]};
-        float4 mv[2] = {m4[0], m4[1]};
-        float4 vv[2] = {v4[0], v4[1]};
-        float *pf = &pv[0].x, *mf = &mv[0].x, *vf = &vv[0].x;
+        float4 pv = *p4, mv = *m4, vv = *v4;
+        float *pf = &pv.x, *mf = &mv.x, *vf = &vv.x;
 #pragma unroll
-        for (int e = 0; e < kVec; ++e) {
+        for (int e = 0; e < kUpdVec; ++e) {
             pf[e] += gx;
             mf[e] += pf[e];
             vf[e] += mf[e];
         }
-        p4[0] = pv[0]; p4[1] = pv[1];
-        m4[0] = mv[0]; m4[1] = mv[1];
-        v4[0] = vv[0]; v4[1] = vv[1];
-        uint4 b;
+        *p4 = pv;
+        *m4 = mv;
+        *v4 = vv;
+        uint2 b;
         b.x = (__float_as_uint(pf[0]) >> 16) | (__float_as_uint(pf[1]) & 0xffff0000u);
         b.y = (__float_as_uint(pf[2]) >> 16) | (__float_as_uint(pf[3]) & 0xffff0000u);
-        b.z = (__float_as_uint(pf[4]) >> 16) | (__float_as_uint(pf[5]) & 0xffff0000u);
-        b.w = (__float_as_uint(pf[6]) >> 16) | (__float_as_uint(pf[7]) & 0xffff0000u);
-        *reinterpret_cast<uint4 *>(PB + e0) = b;
+        *reinterpret_cast<uint2 *>(PB + e0) = b;
     }
 }
 
@@ -554,7 +564,7 @@ hipError_t launch_norm_finalize(const double *partials, int64_t n_partials, doub
 }
 
 hipError_t launch_update(int R, const UpdateArgs &a, int max_blocks, int lds_pad, hipStream_t s) {
-    int64_t blocks = cdiv(a.n / kVec, kUpdateThreads);
+    int64_t blocks = cdiv(a.n / kUpdVec, kUpdateThreads);
     if (blocks < 1) blocks = 1;
     if (max_blocks > 0 && blocks > max_blocks) blocks = max_blocks;
     switch (R) {
@@ -566,7 +576,7 @@ hipError_t launch_update(int R, const UpdateArgs &a, int max_blocks, int lds_pad
 }
 
 hipError_t launch_update_pattern(int R, const UpdateArgs &a, int lds_pad, hipStream_t s) {
-    int64_t blocks = cdiv(a.n / kVec, kUpdateThreads);
+    int64_t blocks = cdiv(a.n / kUpdVec, kUpdateThreads);
     if (blocks < 1) blocks = 1;
     switch (R) {
 #define CASE(r) case r: return pattern_r<r>(a, blocks, lds_pad, s);

@@ -236,8 +236,8 @@ def test_edge_values(sdp, ctx, case, mode):
 
 @pytest.mark.parametrize("R", [4, 8])
 def test_residency_cap_does_not_change_results(sdp, R, monkeypatch):
-    """The fused update's residency cap (one-wave blocks, at most 8 per
-    compute unit) is a launch shape only: uncapped, capped at 8 and capped
+    """The fused update's residency cap (one-wave blocks, at most 10 per
+    compute unit) is a launch shape only: uncapped, capped at 10 and capped
     at 3 blocks per compute unit give the same bits, also with the capped
     grid-stride launch of SDP_UPDATE_MAX_BLOCKS."""
     n = 5 * TILE + 13
