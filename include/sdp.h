@@ -158,9 +158,10 @@ typedef struct {
  * max_ranks in 1..SDP_MAX_RANKS bounds R for streamed mode staging.  The
  * context creates two streams (default priority) and its events.  Other
  * workspace (norm partials, cached g_bar) grows on demand.  The fused update
- * keeps at most 10 of its one-wave blocks on a compute unit, through dynamic
- * LDS that it does not use; the environment variable
- * SDP_UPDATE_BLOCKS_PER_CU, read here, sets another cap (0: none). */
+ * keeps at most 10 of its one-wave blocks on a compute unit, and the norm
+ * pass that stores g_bar at most 3 of its blocks, through dynamic LDS that
+ * they do not use; the environment variables SDP_UPDATE_BLOCKS_PER_CU and
+ * SDP_NORM_STORE_BLOCKS_PER_CU, read here, set other caps (0: none). */
 SDP_API int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems,
                    int32_t max_ranks, uint32_t flags);
 SDP_API void sdp_ctx_destroy(sdp_ctx *ctx);

@@ -73,10 +73,14 @@ constexpr int kUpdateThreads = 64;
 // the kernel does not use (the LDS of a compute unit divided by the cap, per
 // block).
 constexpr int kUpdateBlocksPerCU = 10;
+// The norm pass that stores g_bar (16 B read + 4 B written per element at
+// R = 8) is capped the same way at kNormStoreBlocksPerCU blocks of
+// kNormThreads; the plain norm pass, read only, runs uncapped.
+constexpr int kNormStoreBlocksPerCU = 3;
 constexpr int kVec = 8;     // elements per lane per access (16 B of BF16, 32 B of FP32)
 constexpr int kUpdVec = 4;  // fused update: elements per lane (8 B of BF16, 16 B of FP32)
 
-hipError_t launch_norm_partials(int R, const NormArgs &a, hipStream_t s);
+hipError_t launch_norm_partials(int R, const NormArgs &a, int store_lds_pad, hipStream_t s);
 hipError_t launch_norm_finalize(const double *partials /* pairs */, int64_t n_pairs,
                                 double max_grad_norm, NormState *ns, hipStream_t s);
 hipError_t launch_update(int R, const UpdateArgs &a, int max_blocks, int lds_pad, hipStream_t s);

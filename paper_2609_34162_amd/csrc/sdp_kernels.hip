@@ -128,11 +128,10 @@ __device__ __forceinline__ void block_merge(double &hi, double &lo) {
 // Norm partials: each tile is split into kNormSplit spans of kNormSpan
 // elements, and block b sums g_bar^2 over span b of the segment (the grid is
 // kNormSplit blocks per tile, those past the end write a zero pair).  Lanes
-// read V elements per rank at a time: V = 4 (8-byte loads) for the plain
-// pass, V = 8 (16-byte loads) when g_bar is stored, so that a lane's 8 FP32
-// outputs go out as two 16-byte stores.  Lane t handles the V-element groups
-// b*S + 256*j + t (S groups per span) in increasing j, two groups issued
-// before either is consumed.  The gradients are read with non-temporal
+// read 4 elements per rank at a time (8-byte loads); when g_bar is stored,
+// each lane's 4 FP32 results go out as one 16-byte store, contiguous across
+// the wave.  Lane t handles the 4-element groups b*2048 + 256*j + t in
+// increasing j, two groups issued before either is consumed.  The gradients are read with non-temporal
 // loads: they are not reused before the update pass, and the 256 MB
 // last-level cache cannot hold them.  The ragged tail of fewer than V
 // elements is added by lane 0 of its span after the groups.  The per-lane
@@ -156,7 +155,7 @@ __device__ __forceinline__ void load_stream_v(const uint16_t *p, uint32_t (&w)[V
 
 template <int R, bool WRITE_GBAR>
 __global__ __launch_bounds__(kNormThreads) void k_norm_partials(NormArgs a) {
-    constexpr int V = WRITE_GBAR ? 8 : 4;
+    constexpr int V = 4;
     constexpr int kGroupsPerSpan = kNormSpan / V;
     constexpr int kUnroll = 2;
     constexpr int kIters = kGroupsPerSpan / (kNormThreads * kUnroll);
@@ -201,9 +200,7 @@ __global__ __launch_bounds__(kNormThreads) void k_norm_partials(NormArgs a) {
             for (int e = 0; e < V; ++e) dd_add(hi, lo, (double)g[e] * (double)g[e]);
             if constexpr (WRITE_GBAR) {
                 const int64_t e0 = (span0 + (int64_t)(it * kUnroll + u) * kNormThreads + threadIdx.x) * V;
-                float4 *o = reinterpret_cast<float4 *>(a.gbar_out + e0);
-                o[0] = make_float4(g[0], g[1], g[2], g[3]);
-                o[1] = make_float4(g[4], g[5], g[6], g[7]);
+                *reinterpret_cast<float4 *>(a.gbar_out + e0) = make_float4(g[0], g[1], g[2], g[3]);
             }
         }
     }
@@ -510,10 +507,11 @@ __global__ __launch_bounds__(256) void k_fill_u32(uint32_t *__restrict__ dst, in
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 template <int R>
-hipError_t norm_r(const NormArgs &a, hipStream_t s) {
+hipError_t norm_r(const NormArgs &a, int store_lds_pad, hipStream_t s) {
     const int64_t blocks = cdiv(a.n, kTile) * kNormSplit;
     if (a.gbar_out)
-        hipLaunchKernelGGL((k_norm_partials<R, true>), dim3((uint32_t)blocks), dim3(kNormThreads), 0, s, a);
+        hipLaunchKernelGGL((k_norm_partials<R, true>), dim3((uint32_t)blocks), dim3(kNormThreads), store_lds_pad, s,
+                           a);
     else
         hipLaunchKernelGGL((k_norm_partials<R, false>), dim3((uint32_t)blocks), dim3(kNormThreads), 0, s, a);
     return hipGetLastError();
@@ -547,9 +545,9 @@ hipError_t gbar_r(const GbarArgs &a, int64_t blocks, hipStream_t s) {
 
 #define SDP_FOR_EACH_R(X) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15) X(16)
 
-hipError_t launch_norm_partials(int R, const NormArgs &a, hipStream_t s) {
+hipError_t launch_norm_partials(int R, const NormArgs &a, int store_lds_pad, hipStream_t s) {
     switch (R) {
-#define CASE(r) case r: return norm_r<r>(a, s);
+#define CASE(r) case r: return norm_r<r>(a, store_lds_pad, s);
         SDP_FOR_EACH_R(CASE)
 #undef CASE
         default: return hipErrorInvalidValue;

@@ -238,6 +238,7 @@ struct sdp_ctx {
     sdp::NormState *ns_host = nullptr;  // pinned mirror for read-back
     int update_max_blocks = 0;     // 0: one 8-element group per lane
     int update_lds_pad = 0;        // dynamic LDS bytes per update block (residency cap); 0: no cap
+    int norm_store_lds_pad = 0;    // the same for the norm pass that stores g_bar
     bool timing = false;
     std::vector<sdprt::Timed> timed;
     // host lanes of the host-update route, timed on the host clock

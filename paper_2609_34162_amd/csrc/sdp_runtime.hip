@@ -302,7 +302,7 @@ int norm_launch(sdp_ctx *ctx, int32_t R, const uint16_t *const *g, int64_t n, do
     a.partials = partials;
     a.gbar_out = gbar_out;
     hipEvent_t t0 = timed_begin(ctx, s);
-    HIP_TRY(sdp::launch_norm_partials(R, a, s));
+    HIP_TRY(sdp::launch_norm_partials(R, a, ctx->norm_store_lds_pad, s));
     timed_end(ctx, s, t0, kNorm, n);
     return SDP_OK;
 }
@@ -659,21 +659,24 @@ int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems, int32_t m
         return status;
     };
     {
-        // residency cap of the fused update: the compute unit's LDS split
-        // over kUpdateBlocksPerCU blocks (SDP_UPDATE_BLOCKS_PER_CU overrides;
-        // 0 lifts the cap)
-        int per_cu = sdp::kUpdateBlocksPerCU;
-        if (const char *env = std::getenv("SDP_UPDATE_BLOCKS_PER_CU")) per_cu = std::max(0, std::atoi(env));
+        // residency caps: the compute unit's LDS split over the blocks that
+        // may stay on it (SDP_UPDATE_BLOCKS_PER_CU and
+        // SDP_NORM_STORE_BLOCKS_PER_CU override; 0 lifts a cap)
         int lds_cu = 0, lds_block = 0;
         if (hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, device) != hipSuccess ||
             hipDeviceGetAttribute(&lds_block, hipDeviceAttributeMaxSharedMemoryPerBlock, device) != hipSuccess) {
             (void)hipGetLastError();
             return bail(fail(SDP_ERR_HIP, "cannot query the device's LDS size"));
         }
-        if (per_cu > 0) {
-            const int pad = lds_cu / per_cu / 1024 * 1024;
-            if (pad > 0 && pad <= lds_block) c->update_lds_pad = pad;
-        }
+        auto pad_for = [&](const char *env_name, int per_cu, int static_lds) {
+            if (const char *env = std::getenv(env_name)) per_cu = std::max(0, std::atoi(env));
+            if (per_cu <= 0) return 0;
+            const int pad = (lds_cu / per_cu - static_lds) / 1024 * 1024;
+            return pad > 0 && pad + static_lds <= lds_block ? pad : 0;
+        };
+        c->update_lds_pad = pad_for("SDP_UPDATE_BLOCKS_PER_CU", sdp::kUpdateBlocksPerCU, 0);
+        // the norm pass's own LDS: two 4-entry FP64 arrays for the block merge
+        c->norm_store_lds_pad = pad_for("SDP_NORM_STORE_BLOCKS_PER_CU", sdp::kNormStoreBlocksPerCU, 64);
     }
 #define CTX_HIP(expr)                                                                                \
     do {                                                                                             \
