@@ -236,15 +236,17 @@ def test_edge_values(sdp, ctx, case, mode):
 
 @pytest.mark.parametrize("R", [4, 8])
 def test_residency_cap_does_not_change_results(sdp, R, monkeypatch):
-    """The fused update's residency cap (one-wave blocks, at most 10 per
-    compute unit) is a launch shape only: uncapped, capped at 10 and capped
-    at 3 blocks per compute unit give the same bits, also with the capped
-    grid-stride launch of SDP_UPDATE_MAX_BLOCKS."""
+    """The residency caps of the fused update (one-wave blocks, at most 10
+    per compute unit) and of the norm pass that stores g_bar (at most 3) are
+    launch shapes only: uncapped, the default caps and caps of 3 give the
+    same bits and norm, also with the capped grid-stride launch of
+    SDP_UPDATE_MAX_BLOCKS.  At R = 8 the norm pass stores g_bar."""
     n = 5 * TILE + 13
     masters, grads = rand_inputs([n], R, 2, seed=141 + R)
-    outs = []
+    outs, norms = [], []
     for per_cu, max_blocks in (("0", None), (None, None), ("3", None), (None, "40")):
-        for name, val in (("SDP_UPDATE_BLOCKS_PER_CU", per_cu), ("SDP_UPDATE_MAX_BLOCKS", max_blocks)):
+        for name, val in (("SDP_UPDATE_BLOCKS_PER_CU", per_cu), ("SDP_NORM_STORE_BLOCKS_PER_CU", per_cu),
+                          ("SDP_UPDATE_MAX_BLOCKS", max_blocks)):
             if val is None:
                 monkeypatch.delenv(name, raising=False)
             else:
@@ -252,21 +254,24 @@ def test_residency_cap_does_not_change_results(sdp, R, monkeypatch):
         c = sdp.sdp_ctx_create(0, 0, R, 0)  # reads the variables
         try:
             dev = DevState(masters, R)
+            got = []
             for t in (1, 2):
                 hs, _ = hp_pair(sdp, lr=1e-3, weight_decay=0.02, max_grad_norm=0.05, step=t)
-                dev_step(sdp, c, dev, grads[t - 1], hs)
+                got.append(dev_step(sdp, c, dev, grads[t - 1], hs))
             outs.append(dev.host())
+            norms.append(got)
         finally:
             sdp.sdp_ctx_destroy(c)
-    monkeypatch.delenv("SDP_UPDATE_BLOCKS_PER_CU", raising=False)
-    monkeypatch.delenv("SDP_UPDATE_MAX_BLOCKS", raising=False)
+    for name in ("SDP_UPDATE_BLOCKS_PER_CU", "SDP_NORM_STORE_BLOCKS_PER_CU", "SDP_UPDATE_MAX_BLOCKS"):
+        monkeypatch.delenv(name, raising=False)
     ref = oracle.State(masters)
     for t in (1, 2):
         _, ho = hp_pair(sdp, lr=1e-3, weight_decay=0.02, max_grad_norm=0.05, step=t)
         oracle.step(ref, grads[t - 1], ho)
     check_state(outs[0], ref)
-    for o in outs[1:]:
+    for o, nm in zip(outs[1:], norms[1:]):
         assert states_equal(outs[0], o)
+        assert nm == norms[0]
 
 
 def test_update_pattern_probe(sdp, ctx):
