@@ -293,11 +293,12 @@ SDP_API int sdp_deliver_params(sdp_ctx *ctx, const float *host_master, uint16_t 
 /* Parameter delivery with the version gate on the GPU instead of the host:
  * as sdp_deliver_params, but the call returns once every chunk is enqueued
  * (in SDP_DELIVER_HOST_CAST mode, once the host threads have rounded the
- * last chunk), and work enqueued on `consumer_stream` (a hipStream_t; NULL
- * is the null stream) after this call waits until the last copy has landed
- * -- the paper's gate, where dispatch of layer l at iteration t+1 waits for
- * that layer's update from iteration t (Design, completion and buffer
- * reuse).  The caller must keep dev_bf16 alive until then.  In
+ * last chunk), and work enqueued on `consumer_stream` (a hipStream_t of
+ * ctx's GPU; NULL is the null stream) after this call waits until the last
+ * copy has landed.  This is the paper's gate, where dispatch of layer l at
+ * iteration t+1 waits for that layer's update from iteration t (Design,
+ * completion and buffer reuse).  The caller must keep dev_bf16 alive until
+ * then.  In
  * SDP_DELIVER_DEVICE_CAST mode with pinned host_master the DMA reads
  * host_master after the call returns: leave it unchanged until the gate
  * has passed.  Later calls on the context are ordered after this one. */
