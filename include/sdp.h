@@ -97,12 +97,13 @@ extern "C" {
 #define SDP_FLAG_DEBUG_POISON 0x8u
 /* Streamed mode, staged: the host buffers may be ordinary (pageable) memory.
  * Each chunk moves through context-owned pinned bounce buffers: host threads
- * copy it in while the previous chunk's DMA runs, and copy results out while
- * the next chunk's runs.  For host states larger than the pinned memory the
- * system grants.  Needs max_chunk_elems > 0; pins 2 * (28 + 2 * max_ranks) *
- * max_chunk_elems bytes (two incoming bounce buffers shaped like a slot, two
- * outgoing ones of 14 bytes per element); host threads: SDP_STAGING_THREADS,
- * default up to 16. */
+ * copy chunks in ahead of their DMA (up to two chunks ahead in the update
+ * pass), and copy each chunk's results out as soon as they have landed.  For
+ * host states larger than the pinned memory the system grants.  Needs
+ * max_chunk_elems > 0; pins 3 * (28 + 2 * max_ranks) * max_chunk_elems bytes
+ * (three incoming bounce buffers shaped like a slot, three outgoing ones of
+ * 14 bytes per element); host threads: SDP_STAGING_THREADS, default up to
+ * 16. */
 #define SDP_FLAG_STREAM_STAGED 0x10u
 /* Host threads: keep each of the context's worker threads on one CPU of the
  * process's affinity set (the calling thread is left alone). */

@@ -101,14 +101,14 @@ class HostPool {
         }
         for (int i = 0; i < workers; ++i) {
             const int cpu = cpus.empty() ? -1 : cpus[(size_t)(i + 1) % cpus.size()];
-            threads_.emplace_back([this, cpu] {
+            threads_.emplace_back([this, cpu, i] {
                 if (cpu >= 0) {
                     cpu_set_t one;
                     CPU_ZERO(&one);
                     CPU_SET(cpu, &one);
                     (void)pthread_setaffinity_np(pthread_self(), sizeof one, &one);
                 }
-                loop();
+                loop(i);
             });
         }
     }
@@ -122,12 +122,15 @@ class HostPool {
     }
     int size() const { return (int)threads_.size() + 1; }
 
-    void run(size_t n, const std::function<void(size_t)> &fn) {
+    // Runs fn(0) .. fn(n-1) on the calling thread and the workers; width > 0
+    // limits them to the calling thread and the first width - 1 workers.
+    void run(size_t n, const std::function<void(size_t)> &fn, int width = 0) {
         std::unique_lock<std::mutex> g(mu_);
         fn_ = &fn;
         n_ = n;
         next_ = 0;
         left_ = n;
+        width_ = width > 0 ? width : size();
         ++gen_;
         g.unlock();
         cv_work_.notify_all();
@@ -153,16 +156,18 @@ class HostPool {
             if (--left_ == 0) cv_done_.notify_all();
         }
     }
-    void loop() {
+    void loop(int index) {
         uint64_t seen = 0;
         for (;;) {
+            bool join;
             {
                 std::unique_lock<std::mutex> g(mu_);
                 cv_work_.wait(g, [&] { return stop_ || gen_ != seen; });
                 if (stop_) return;
                 seen = gen_;
+                join = index + 1 < width_;
             }
-            work();
+            if (join) work();
         }
     }
 
@@ -171,6 +176,7 @@ class HostPool {
     std::condition_variable cv_work_, cv_done_;
     const std::function<void(size_t)> *fn_ = nullptr;
     size_t n_ = 0, next_ = 0, left_ = 0;
+    int width_ = 0;
     uint64_t gen_ = 0;
     bool stop_ = false;
 };
@@ -185,15 +191,22 @@ struct Job {
     int kind = kCopy;
 };
 
-void pool_jobs(HostPool *pool, const std::vector<Job> &jobs);
+// width > 0: on at most that many threads (see HostPool::run).
+void pool_jobs(HostPool *pool, const std::vector<Job> &jobs, int width = 0);
 
-// Staged mode: outgoing bounce buffers.  Chunk j's results land in buffer
-// j % kOutBufs; the host threads move chunk j-1's out as soon as they have
-// landed, while chunk j's incoming copy runs.  Deferring that by one more
-// chunk (three buffers) lets the host copies overlap the next outgoing DMA,
-// which on the MI355X hosts measured here slowed the DMA enough to lose
-// 25% of the step.
-constexpr int kOutBufs = 2;
+// Staged mode: bounce buffers.  Incoming chunks rotate over kInBufs pinned
+// buffers shaped like a slot, outgoing results over kOutBufs buffers of
+// 14 * max_chunk bytes.  In the update phase the host thread stages and
+// enqueues chunk j + kStageAhead before it drains chunk j, and drains each
+// chunk as soon as its results have landed.  Staging only one chunk ahead
+// put the host copies of a chunk (its drain, then the next chunk's staging)
+// between two device-to-host copies, so each chunk waited for them.  Chunk
+// j + kStageAhead lands in outgoing buffer (j + kStageAhead) % kOutBufs,
+// which chunk j + kStageAhead - kOutBufs used and the host has drained.
+constexpr int kInBufs = 3;
+constexpr int kOutBufs = 3;
+constexpr int kStageAhead = 2;
+static_assert(kStageAhead < kInBufs && kStageAhead < kOutBufs, "staging ahead needs free bounce buffers");
 
 // A host <-> staging-slot transfer of one chunk: `bytes` at byte offset `off`
 // of a slot, from or to `host`.
@@ -220,16 +233,18 @@ struct sdp_ctx {
     char *staging = nullptr;
     size_t slot_bytes = 0;
     // staged streamed mode: pinned bounce buffers shaped like the slots
-    char *bounce_in = nullptr;   // 2 x slot_bytes
+    char *bounce_in = nullptr;   // kInBufs x slot_bytes
     char *bounce_out = nullptr;  // kOutBufs x 14 * max_chunk (master, m, v, bf16 part of a slot)
-    hipEvent_t d2h_done[sdprt::kOutBufs] = {nullptr, nullptr};
-    bool bin_used[2] = {false, false};
+    hipEvent_t bin_done[sdprt::kInBufs] = {};   // copy stream: the copies out of bounce_in[k] are done
+    hipEvent_t d2h_done[sdprt::kOutBufs] = {};  // compute stream: the copies into bounce_out[k] are done
+    bool bin_used[sdprt::kInBufs] = {};
     // parameter delivery and the host-update route: two pinned buffers of
     // 4 * max_chunk bytes each (one chunk of FP32), created on first use
     char *stage = nullptr;
     bool stage_used[2] = {false, false};
     std::vector<sdprt::Xfer> pending_out[sdprt::kOutBufs];
     sdprt::HostPool *copier = nullptr;
+    int staged_copy_threads = 0;   // staged update pass: host copy threads while the DMA runs
     double *partials = nullptr;
     int64_t partials_cap = 0;
     float *gbar = nullptr;
@@ -324,6 +339,14 @@ int stream_norm_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int
 // ---- host threads and pinned stage buffers ------------------------------
 
 int default_host_threads();
+// Staged update pass: how many host threads copy into and out of the bounce
+// buffers while copies in both directions are in flight.  Host memory
+// carries those copies and every DMA byte; on the MI355X hosts measured here
+// (about 400 GB/s of host memory traffic with 16 threads, 50-57 GB/s per
+// thread) five threads let the DMA keep its rate, six or more starved the
+// device-to-host copies and slowed the pass by a quarter.
+constexpr int kStagedCopyThreads = 4;
+int default_staged_copy_threads();
 HostPool *new_pool(const sdp_ctx *ctx, int threads);
 inline size_t stage_bytes(const sdp_ctx *ctx) { return 4 * (size_t)ctx->max_chunk; }
 int ensure_host_stage(sdp_ctx *ctx);

@@ -39,7 +39,7 @@ void cast_bf16_host(const float *src, uint16_t *dst, size_t n) {
     }
 }
 
-void pool_jobs(HostPool *pool, const std::vector<Job> &jobs) {
+void pool_jobs(HostPool *pool, const std::vector<Job> &jobs, int width) {
     constexpr size_t kPiece = 4u << 20;      // bytes per copy piece
     constexpr size_t kCastPiece = 1u << 20;  // elements per rounding piece
     std::vector<Job> pieces;
@@ -59,7 +59,7 @@ void pool_jobs(HostPool *pool, const std::vector<Job> &jobs) {
             cast_bf16_host((const float *)pc.src, (uint16_t *)pc.dst, pc.bytes);
         else
             std::memcpy(pc.dst, pc.src, pc.bytes);
-    });
+    }, width);
 }
 
 // ---- validation ---------------------------------------------------------
@@ -432,6 +432,12 @@ int default_host_threads() {
     return threads;
 }
 
+int default_staged_copy_threads() {
+    int threads = kStagedCopyThreads;
+    if (const char *env = std::getenv("SDP_STAGED_COPY_THREADS")) threads = std::max(1, std::min(256, std::atoi(env)));
+    return threads;
+}
+
 HostPool *new_pool(const sdp_ctx *ctx, int threads) {
     return new HostPool(threads - 1, (ctx->flags & SDP_FLAG_HOST_PIN_THREADS) != 0);
 }
@@ -715,15 +721,18 @@ int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems, int32_t m
         if (max_chunk_elems <= 0)
             return bail(fail(SDP_ERR_INVALID_ARGUMENT, "SDP_FLAG_STREAM_STAGED needs max_chunk_elems > 0"));
         const size_t out_bytes = 14 * (size_t)max_chunk_elems;
-        if (hipHostMalloc(&c->bounce_in, 2 * c->slot_bytes, hipHostMallocDefault) != hipSuccess ||
+        if (hipHostMalloc(&c->bounce_in, kInBufs * c->slot_bytes, hipHostMallocDefault) != hipSuccess ||
             hipHostMalloc(&c->bounce_out, kOutBufs * out_bytes, hipHostMallocDefault) != hipSuccess) {
             (void)hipGetLastError();
             return bail(fail(SDP_ERR_OUT_OF_MEMORY, "cannot allocate %zu bytes of pinned bounce buffers",
-                             2 * c->slot_bytes + kOutBufs * out_bytes));
+                             kInBufs * c->slot_bytes + kOutBufs * out_bytes));
         }
+        for (int k = 0; k < kInBufs; ++k)
+            CTX_HIP(hipEventCreateWithFlags(&c->bin_done[k], hipEventDisableTiming));
         for (int k = 0; k < kOutBufs; ++k)
             CTX_HIP(hipEventCreateWithFlags(&c->d2h_done[k], hipEventDisableTiming));
         c->copier = new_pool(c, default_host_threads());
+        c->staged_copy_threads = default_staged_copy_threads();
     }
     rc = ensure_partials(c, 4096);
     if (rc != SDP_OK) return bail(rc);
@@ -753,6 +762,8 @@ void sdp_ctx_destroy(sdp_ctx *ctx) {
     if (ctx->bounce_in) (void)hipHostFree(ctx->bounce_in);
     if (ctx->stage) (void)hipHostFree(ctx->stage);
     if (ctx->bounce_out) (void)hipHostFree(ctx->bounce_out);
+    for (int k = 0; k < kInBufs; ++k)
+        if (ctx->bin_done[k]) (void)hipEventDestroy(ctx->bin_done[k]);
     for (int k = 0; k < kOutBufs; ++k)
         if (ctx->d2h_done[k]) (void)hipEventDestroy(ctx->d2h_done[k]);
     delete ctx->copier;

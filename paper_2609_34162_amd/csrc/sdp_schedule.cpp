@@ -8,10 +8,11 @@
 //  - phase 2: per chunk, the state copies in after the slot's previous
 //    outgoing copy, the update kernel, and the outgoing copies on the
 //    compute stream, all issued after the read-back;
-//  - staged variant: host-thread copies into the pinned bounce buffer before
-//    each incoming copy (after that buffer's previous copy left it), and out
-//    of outgoing buffer j mod 2 once chunk j+1 is issued, in the host
-//    thread's own order;
+//  - staged variant: host-thread copies into pinned bounce buffer k mod 3
+//    before each incoming copy (after that buffer's previous copy left it);
+//    in phase 2 chunk j's results land in outgoing buffer j mod 3, and the
+//    host thread stages and issues chunk j+2 before it drains chunk j, all
+//    in the host thread's own order;
 //  - host-update route: the norm pass and read-back, then per piece (the
 //    chunks, the first one split into a ramp) the mean-gradient kernel
 //    (after the slot's previous outgoing copy, and issued by the host after
@@ -228,52 +229,57 @@ std::vector<int64_t> route_pieces(const std::vector<int64_t> &chunk_lens) {
 
 namespace {
 
+// The staged runtime's bounce buffers and how far ahead its host thread
+// stages (incoming buffers, outgoing buffers, chunks staged ahead of the
+// drain).
+constexpr int kInBufs = 3, kOutBufs = 3, kStageAhead = 2;
+
 void build_streamed(Graph &g, const std::vector<int64_t> &numels, int R, int64_t C, bool store, bool staged,
                     const Rates &r) {
     const std::vector<Chunk> ch = chunks_of(numels, C);
-    int slot_free[2] = {-1, -1}, bin_h2d[2] = {-1, -1};
+    int slot_free[2] = {-1, -1}, bin_h2d[kInBufs] = {-1, -1, -1};
     for (size_t k = 0; k < ch.size(); ++k) {
-        const int sl = (int)(k & 1);
+        const int sl = (int)(k & 1), bi = (int)(k % kInBufs);
         const double len = (double)ch[k].len;
         int hin = -1;
-        if (staged) hin = g.host(2.0 * 2 * R * len, r.host_gbs, r.host_task_us, {bin_h2d[sl]});
+        if (staged) hin = g.host(2.0 * 2 * R * len, r.host_gbs, r.host_task_us, {bin_h2d[bi]});
         const int cmds = (staged && ch[k].full) ? 1 : R;
         const int h2d = g.add(kCopyS, kH2D, 0, 2.0 * R * len, cmds, {slot_free[sl], hin});
         const int norm = g.add(kCompS, kFixed, kernel_us((2.0 * R + (store ? 4.0 : 0.0)) * len, r.norm_gbs, r), 0, 0,
                                {h2d});
         slot_free[sl] = norm;
-        bin_h2d[sl] = h2d;
+        bin_h2d[bi] = h2d;
     }
     const int fin = g.add(kCompS, kFixed, r.launch_us, 0, 0, {});
     const int rb = g.add(kHostS, kFixed, r.sync_us, 0, 0, {fin});
     const size_t k0 = ch.size();
     int d2h_slot[2] = {-1, -1};
-    // staged: chunk j's results go to outgoing buffer j % 2 and are drained
-    // after chunk j+1 is issued
-    std::vector<int> d2h_of, drain_of;
+    std::vector<int> d2h_of(ch.size(), -1), drain_of(ch.size(), -1);
     const double in_bpe = 12.0 + (store ? 0.0 : 2.0 * R);
-    auto drain = [&](size_t i) {
-        drain_of[i] = g.host(2.0 * 14.0 * (double)ch[i].len, r.host_gbs, r.host_task_us, {d2h_of[i]});
-    };
-    d2h_of.assign(ch.size(), -1);
-    drain_of.assign(ch.size(), -1);
-    for (size_t j = 0; j < ch.size(); ++j) {
-        const int sl = (int)((j + k0) & 1);
+    auto issue = [&](size_t j) {
+        const int sl = (int)((j + k0) & 1), bi = (int)((j + k0) % kInBufs);
         const double len = (double)ch[j].len;
         int hin = -1;
-        if (staged) hin = g.host(2.0 * in_bpe * len, r.host_gbs, r.host_task_us, {rb, bin_h2d[sl]});
+        if (staged) hin = g.host(2.0 * in_bpe * len, r.host_gbs, r.host_task_us, {rb, bin_h2d[bi]});
         const int in_cmds = (staged && ch[j].full) ? 1 : 3 + (store ? 0 : R);
         const int h2d = g.add(kCopyS, kH2D, 0, in_bpe * len, in_cmds, {rb, hin, d2h_slot[sl]});
         const int upd = g.add(kCompS, kFixed, kernel_us((26.0 + (store ? 4.0 : 2.0 * R)) * len, r.update_gbs, r), 0,
                               0, {h2d, rb});
         const int out_cmds = (staged && ch[j].full) ? 1 : 4;
-        const int buf_free = (staged && j >= 2) ? drain_of[j - 2] : -1;
+        const int buf_free = (staged && j >= (size_t)kOutBufs) ? drain_of[j - kOutBufs] : -1;
         d2h_of[j] = g.add(kCompS, kD2H, 0, 14.0 * len, out_cmds, {upd, hin, buf_free});
-        if (staged && j >= 1) drain(j - 1);
-        bin_h2d[sl] = h2d;
+        bin_h2d[bi] = h2d;
         d2h_slot[sl] = d2h_of[j];
+    };
+    if (!staged) {
+        for (size_t j = 0; j < ch.size(); ++j) issue(j);
+        return;
     }
-    if (staged && !ch.empty()) drain(ch.size() - 1);
+    size_t next = 0;
+    for (size_t j = 0; j < ch.size(); ++j) {
+        for (; next < ch.size() && next <= j + kStageAhead; ++next) issue(next);
+        drain_of[j] = g.host(2.0 * 14.0 * (double)ch[j].len, r.host_gbs, r.host_task_us, {d2h_of[j]});
+    }
 }
 
 void build_host_route(Graph &g, const std::vector<int64_t> &numels, int R, int64_t C, bool bf16, const Rates &r) {

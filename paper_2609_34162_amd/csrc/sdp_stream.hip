@@ -35,23 +35,25 @@ std::vector<Xfer> merge_runs(std::vector<Xfer> xs) {
 }
 
 // Host -> slot `sl` copies of one chunk, enqueued on the copy stream.  In the
-// staged mode the host threads first copy into the slot's pinned bounce
-// buffer, after waiting for that buffer's previous copy to leave it.
-int copy_in(sdp_ctx *ctx, int sl, const std::vector<Xfer> &xs) {
+// staged mode the host threads (at most `width` of them, 0: all) first copy
+// into pinned bounce buffer `bi`, after waiting for that buffer's previous
+// copies to leave it.
+int copy_in(sdp_ctx *ctx, int sl, int bi, const std::vector<Xfer> &xs, int width) {
     char *dev = ctx->staging + (size_t)sl * ctx->slot_bytes;
     if (!staged(ctx)) {
         for (const Xfer &x : xs)
             HIP_TRY(hipMemcpyAsync(dev + x.off, x.host, x.bytes, hipMemcpyHostToDevice, ctx->s_copy));
         return SDP_OK;
     }
-    char *bin = ctx->bounce_in + (size_t)sl * ctx->slot_bytes;
-    if (ctx->bin_used[sl]) HIP_TRY(hipEventSynchronize(ctx->h2d_done[sl]));
+    char *bin = ctx->bounce_in + (size_t)bi * ctx->slot_bytes;
+    if (ctx->bin_used[bi]) HIP_TRY(hipEventSynchronize(ctx->bin_done[bi]));
     std::vector<Job> jobs;
     for (const Xfer &x : xs) jobs.push_back({bin + x.off, x.host, x.bytes});
-    pool_jobs(ctx->copier, jobs);
+    pool_jobs(ctx->copier, jobs, width);
     for (const Xfer &r : merge_runs(xs))
         HIP_TRY(hipMemcpyAsync(dev + r.off, bin + r.off, r.bytes, hipMemcpyHostToDevice, ctx->s_copy));
-    ctx->bin_used[sl] = true;
+    HIP_TRY(hipEventRecord(ctx->bin_done[bi], ctx->s_copy));
+    ctx->bin_used[bi] = true;
     return SDP_OK;
 }
 
@@ -74,14 +76,14 @@ int copy_out(sdp_ctx *ctx, int sl, int bo, const std::vector<Xfer> &xs) {
 }
 
 // Staged mode: wait for the outgoing copies into bounce buffer `bo` and move
-// them to their host destinations.
-int drain(sdp_ctx *ctx, int bo) {
+// them to their host destinations on at most `width` host threads (0: all).
+int drain(sdp_ctx *ctx, int bo, int width) {
     if (ctx->pending_out[bo].empty()) return SDP_OK;
     HIP_TRY(hipEventSynchronize(ctx->d2h_done[bo]));
     char *bout = ctx->bounce_out + (size_t)bo * 14 * (size_t)ctx->max_chunk;
     std::vector<Job> jobs;
     for (const Xfer &x : ctx->pending_out[bo]) jobs.push_back({x.host, bout + x.off, x.bytes});
-    pool_jobs(ctx->copier, jobs);
+    pool_jobs(ctx->copier, jobs, width);
     ctx->pending_out[bo].clear();
     return SDP_OK;
 }
@@ -100,7 +102,7 @@ int stream_norm_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int
         for (int32_t r = 0; r < R; ++r)
             xs.push_back({off_in_slot(ctx, sl, slot.g[r]), (char *)(segs[c.seg].grads[r] + c.off), (size_t)c.len * 2});
         if (used[sl]) HIP_TRY(hipStreamWaitEvent(ctx->s_copy, ctx->slot_free[sl], 0));
-        SDP_TRY(copy_in(ctx, sl, xs));
+        SDP_TRY(copy_in(ctx, sl, (int)(k % kInBufs), xs, 0));
         HIP_TRY(hipEventRecord(ctx->h2d_done[sl], ctx->s_copy));
         HIP_TRY(hipStreamWaitEvent(ctx->s_comp, ctx->h2d_done[sl], 0));
         const uint16_t *gp[SDP_MAX_RANKS];
@@ -117,11 +119,18 @@ int stream_norm_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int
 namespace {
 
 // Phase 2: master/m/v in (and the gradients again unless g_bar is stored),
-// fused update, master/m/v and BF16 parameters back out.
+// fused update, master/m/v and BF16 parameters back out.  Chunk j uses slot
+// (j + k0) mod 2, continuing phase 1's alternation.  Staged, the host thread
+// stages and enqueues chunk j + kStageAhead before it drains chunk j.  While
+// copies are in flight the host copies run on staged_copy_threads threads:
+// more of them starve the device-to-host copies of host memory (phase 1,
+// with the link busy in one direction only, is not hurt and uses them all).
+// The first chunk's staging and the last chunk's drain have the link to
+// themselves and use every thread.
 int stream_update_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t R, const Plan &plan,
                         const std::vector<Chunk> &chunks, bool stored_gbar, const sdp_adamw_params *hp, bool used[2],
                         size_t k0) {
-    for (size_t j = 0; j < chunks.size(); ++j) {
+    auto issue = [&](size_t j) -> int {
         const Chunk &c = chunks[j];
         const sdp_segment &g = segs[c.seg];
         const int sl = (int)((j + k0) & 1);
@@ -134,7 +143,7 @@ int stream_update_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t R, const 
             for (int32_t r = 0; r < R; ++r)
                 in.push_back({off_in_slot(ctx, sl, slot.g[r]), (char *)(g.grads[r] + c.off), b2});
         if (used[sl]) HIP_TRY(hipStreamWaitEvent(ctx->s_copy, ctx->slot_free[sl], 0));
-        SDP_TRY(copy_in(ctx, sl, in));
+        SDP_TRY(copy_in(ctx, sl, (int)((j + k0) % kInBufs), in, j == 0 ? 0 : ctx->staged_copy_threads));
         HIP_TRY(hipEventRecord(ctx->h2d_done[sl], ctx->s_copy));
         HIP_TRY(hipStreamWaitEvent(ctx->s_comp, ctx->h2d_done[sl], 0));
         const uint16_t *gp[SDP_MAX_RANKS];
@@ -149,11 +158,17 @@ int stream_update_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t R, const 
         SDP_TRY(poison(ctx, sl));
         HIP_TRY(hipEventRecord(ctx->slot_free[sl], ctx->s_comp));
         used[sl] = true;
-        // staged: move the previous chunk's results out while this one's
-        // incoming copy is in flight
-        if (staged(ctx) && j >= 1) SDP_TRY(drain(ctx, (int)((j - 1) % kOutBufs)));
+        return SDP_OK;
+    };
+    if (!staged(ctx)) {
+        for (size_t j = 0; j < chunks.size(); ++j) SDP_TRY(issue(j));
+        return SDP_OK;
     }
-    if (staged(ctx) && !chunks.empty()) SDP_TRY(drain(ctx, (int)((chunks.size() - 1) % kOutBufs)));
+    size_t next = 0;
+    for (size_t j = 0; j < chunks.size(); ++j) {
+        for (; next < chunks.size() && next <= j + kStageAhead; ++next) SDP_TRY(issue(next));
+        SDP_TRY(drain(ctx, (int)(j % kOutBufs), j + 1 == chunks.size() ? 0 : ctx->staged_copy_threads));
+    }
     return SDP_OK;
 }
 
