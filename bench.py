@@ -361,10 +361,11 @@ def stream_leg(args, torch, np, synth, sdp, dres):
         out["chunk_sweep"] = chunk_sweep(sdp, sdp.SDP_SCHED_STREAMED, [N], R, rates, run_at)
         # the same step with the states in pageable memory, through the staged mode
         log("streamed leg: staged mode on pageable copies of the same state")
+        # the staged context pins its bounce buffers before the pageable state exists
+        sctx = sdp.sdp_ctx_create(0, C, R, sdp.SDP_FLAG_STREAM_STAGED)
         pg = [np.array(x) for x in (p, m, v, pb)] + [np.array(x) for x in g]
         sseg = sdp.Segments([(pg[0].ctypes.data, pg[1].ctypes.data, pg[2].ctypes.data, pg[3].ctypes.data,
                               [x.ctypes.data for x in pg[4:]], N)])
-        sctx = sdp.sdp_ctx_create(0, C, R, sdp.SDP_FLAG_STREAM_STAGED)
         sel = timed(sctx, sseg)
         sdp.sdp_ctx_destroy(sctx)
         out["staged_pageable"] = dict(ms_per_step=sel * 1e3, params_per_s=N / sel, frac_of_link_bound=t_link / sel)

@@ -103,7 +103,10 @@ extern "C" {
  * max_chunk_elems > 0; pins 3 * (28 + 2 * max_ranks) * max_chunk_elems bytes
  * (three incoming bounce buffers shaped like a slot, three outgoing ones of
  * 14 bytes per element); host threads: SDP_STAGING_THREADS, default up to
- * 16. */
+ * 16, of which SDP_STAGED_COPY_THREADS (default 4) copy while transfers are
+ * in flight in both directions.  Create such a context before allocating a
+ * large host state: on the MI355X hosts measured, bounce buffers pinned
+ * after 266 GB of host allocations made the update pass twice as slow. */
 #define SDP_FLAG_STREAM_STAGED 0x10u
 /* Host threads: keep each of the context's worker threads on one CPU of the
  * process's affinity set (the calling thread is left alone). */

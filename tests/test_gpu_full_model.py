@@ -70,6 +70,17 @@ def run_full_model(route):
         samples.append(np.unique(np.concatenate(pts)).astype(np.int64))
     log(f"  {sum(s.size for s in samples)} sample points")
 
+    # the context (and its pinned buffers) first, before the host state
+    # fragments host memory
+    ctx = sdp.sdp_ctx_create(0, C, R, 0 if route else sdp.SDP_FLAG_STREAM_STAGED)
+    try:
+        run_steps(sdp, torch, w, ctx, sizes, samples, route, t0)
+    finally:
+        sdp.sdp_ctx_destroy(ctx)
+
+
+def run_steps(sdp, torch, w, ctx, sizes, samples, route, t0):
+    R, C = w.ranks, w.chunk
     host = PageableState.allocate(sdp, sizes, R)
     for s in range(len(sizes)):
         synth.master(w, s, out=host.p[s])
@@ -82,7 +93,6 @@ def run_full_model(route):
     free = [(synth.master_at(w, s, samples[s]), np.zeros(samples[s].size, np.float32),
              np.zeros(samples[s].size, np.float32)) for s in range(len(sizes))]
     devg = [[torch.empty(n, dtype=torch.int16, device="cuda") for _ in range(R)] for n in sizes] if route else None
-    ctx = sdp.sdp_ctx_create(0, C, R, 0 if route else sdp.SDP_FLAG_STREAM_STAGED)
     try:
         if route:
             segs = sdp.Segments([(host.p[s].ctypes.data, host.m[s].ctypes.data, host.v[s].ctypes.data,
@@ -134,7 +144,6 @@ def run_full_model(route):
             log(f"  step {t}: {sum(x.size for x in samples)} points match, worst relative error {worst:.2e}"
                 f"  {time.time() - t0:.0f}s")
     finally:
-        sdp.sdp_ctx_destroy(ctx)
         host.close()
 
 
