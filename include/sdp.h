@@ -199,9 +199,12 @@ SDP_API int sdp_agg_adam_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_s
  * staging slots ordered by events; then the norm is finalized and read back.
  * Phase 2 copies master/m/v of each chunk in, runs the fused update, and
  * copies master/m/v and the BF16 parameters back to the same host locations
- * on the compute stream, again double-buffered.  Blocks until every copy
- * has landed.  Returns SDP_ERR_NONFINITE (states unchanged) for a
- * non-finite norm.  grad_norm_out may be NULL. */
+ * on the compute stream, again double-buffered.  Device-to-host copies of up
+ * to 64 MiB (SDP_D2H_KERNEL_MAX_BYTES, read at context creation; 0: none)
+ * run as one launch of the library's copy kernel per chunk, which stores
+ * into the pinned host memory directly; larger ones are runtime copies.
+ * Blocks until every copy has landed.  Returns SDP_ERR_NONFINITE (states
+ * unchanged) for a non-finite norm.  grad_norm_out may be NULL. */
 SDP_API int sdp_stream_step(sdp_ctx *ctx, const sdp_segment *host_segs, int32_t n_segs,
                     const sdp_adamw_params *hp, int64_t chunk_elems,
                     double *grad_norm_out);

@@ -60,6 +60,18 @@ struct GbarArgs {
     int bf16;
 };
 
+// Up to kCopyBatchMax copies of `bytes[k]` bytes from src[k] to dst[k] in
+// one launch (the streamed engine's device-to-host copies of a chunk; dst
+// may be pinned host memory).  Every dst and src is 16-byte aligned; any
+// byte count.
+constexpr int kCopyBatchMax = 8;
+struct CopyBatch {
+    int32_t n;
+    char *dst[kCopyBatchMax];
+    const char *src[kCopyBatchMax];
+    int64_t bytes[kCopyBatchMax];
+};
+
 constexpr int kTile = SDP_NORM_TILE;
 constexpr int kNormSplit = 8;                    // norm blocks, and partial pairs, per tile
 constexpr int kNormSpan = kTile / kNormSplit;    // elements per norm block
@@ -88,6 +100,9 @@ hipError_t launch_gbar_out(int R, const GbarArgs &a, hipStream_t s);
 hipError_t launch_update_pattern(int R, const UpdateArgs &a, int lds_pad, hipStream_t s);
 hipError_t launch_cast_bf16(const float *src, uint16_t *dst, int64_t n, hipStream_t s);
 hipError_t launch_copy16(void *dst, const void *src, int64_t n16, int max_blocks, hipStream_t s);
+// blocks_per_copy: blocks given to each copy of the batch (at most; fewer
+// when a copy is short).
+hipError_t launch_copy_batch(const CopyBatch &b, int blocks_per_copy, hipStream_t s);
 hipError_t launch_fill_u32(void *dst, int64_t n_words, uint32_t value, hipStream_t s);
 
 }  // namespace sdp

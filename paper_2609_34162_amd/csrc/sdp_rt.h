@@ -245,6 +245,8 @@ struct sdp_ctx {
     std::vector<sdprt::Xfer> pending_out[sdprt::kOutBufs];
     sdprt::HostPool *copier = nullptr;
     int staged_copy_threads = 0;   // staged update pass: host copy threads while the DMA runs
+    int64_t d2h_kernel_max = 0;    // device-to-host copies up to this many bytes run as k_copy_batch
+    int d2h_kernel_blocks = 0;     // blocks per copy of such a launch
     double *partials = nullptr;
     int64_t partials_cap = 0;
     float *gbar = nullptr;
@@ -347,6 +349,14 @@ int default_host_threads();
 // device-to-host copies and slowed the pass by a quarter.
 constexpr int kStagedCopyThreads = 4;
 int default_staged_copy_threads();
+
+// Streamed engine: device-to-host copies of at most kD2HKernelMaxBytes run as
+// the library's own copy kernel, kD2HKernelBlocks blocks per copy.  The
+// runtime moves copies of a few MiB with DMA copy commands that measured
+// 10-45 GB/s beside host-to-device traffic; larger ones it moves with copy
+// kernels that reach the link's rate.
+constexpr int64_t kD2HKernelMaxBytes = 64ll << 20;
+constexpr int kD2HKernelBlocks = 64;
 HostPool *new_pool(const sdp_ctx *ctx, int threads);
 inline size_t stage_bytes(const sdp_ctx *ctx) { return 4 * (size_t)ctx->max_chunk; }
 int ensure_host_stage(sdp_ctx *ctx);

@@ -709,6 +709,11 @@ int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems, int32_t m
         (void)hipGetLastError();
         return bail(fail(SDP_ERR_OUT_OF_MEMORY, "cannot allocate the pinned norm mirror"));
     }
+    c->d2h_kernel_max = kD2HKernelMaxBytes;
+    if (const char *env = std::getenv("SDP_D2H_KERNEL_MAX_BYTES")) c->d2h_kernel_max = std::atoll(env);
+    c->d2h_kernel_blocks = kD2HKernelBlocks;
+    if (const char *env = std::getenv("SDP_D2H_KERNEL_BLOCKS"))
+        c->d2h_kernel_blocks = std::max(1, std::min(65535, std::atoi(env)));
     if (max_chunk_elems > 0) {
         c->slot_bytes = (size_t)(14 + 2 * max_ranks) * (size_t)max_chunk_elems;
         if (hipMalloc(&c->staging, 2 * c->slot_bytes) != hipSuccess) {

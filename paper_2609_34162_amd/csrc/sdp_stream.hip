@@ -34,6 +34,29 @@ std::vector<Xfer> merge_runs(std::vector<Xfer> xs) {
     return runs;
 }
 
+// Device -> pinned host copies (dst[k] <- src[k], bytes[k]) on the compute
+// stream: those of at most d2h_kernel_max bytes (16-byte aligned) as one
+// launch of the library's copy kernel, the others as runtime copies.  (The
+// same kernel measured slower than the runtime's host-to-device copies at
+// every chunk size, so those stay runtime copies.)
+int d2h_copies(sdp_ctx *ctx, const std::vector<std::pair<char *, const char *>> &ends,
+               const std::vector<size_t> &bytes) {
+    sdp::CopyBatch b{};
+    for (size_t k = 0; k < ends.size(); ++k) {
+        const bool aligned = (((uintptr_t)ends[k].first | (uintptr_t)ends[k].second) % 16) == 0;
+        if ((int64_t)bytes[k] <= ctx->d2h_kernel_max && aligned && b.n < sdp::kCopyBatchMax) {
+            b.dst[b.n] = ends[k].first;
+            b.src[b.n] = ends[k].second;
+            b.bytes[b.n] = (int64_t)bytes[k];
+            ++b.n;
+        } else {
+            HIP_TRY(hipMemcpyAsync(ends[k].first, ends[k].second, bytes[k], hipMemcpyDeviceToHost, ctx->s_comp));
+        }
+    }
+    if (b.n > 0) HIP_TRY(sdp::launch_copy_batch(b, ctx->d2h_kernel_blocks, ctx->s_comp));
+    return SDP_OK;
+}
+
 // Host -> slot `sl` copies of one chunk, enqueued on the copy stream.  In the
 // staged mode the host threads (at most `width` of them, 0: all) first copy
 // into pinned bounce buffer `bi`, after waiting for that buffer's previous
@@ -62,14 +85,21 @@ int copy_in(sdp_ctx *ctx, int sl, int bi, const std::vector<Xfer> &xs, int width
 // their destinations by drain().
 int copy_out(sdp_ctx *ctx, int sl, int bo, const std::vector<Xfer> &xs) {
     char *dev = ctx->staging + (size_t)sl * ctx->slot_bytes;
+    std::vector<std::pair<char *, const char *>> ends;
+    std::vector<size_t> bytes;
     if (!staged(ctx)) {
-        for (const Xfer &x : xs)
-            HIP_TRY(hipMemcpyAsync(x.host, dev + x.off, x.bytes, hipMemcpyDeviceToHost, ctx->s_comp));
-        return SDP_OK;
+        for (const Xfer &x : xs) {
+            ends.push_back({x.host, dev + x.off});
+            bytes.push_back(x.bytes);
+        }
+        return d2h_copies(ctx, ends, bytes);
     }
     char *bout = ctx->bounce_out + (size_t)bo * 14 * (size_t)ctx->max_chunk;
-    for (const Xfer &r : merge_runs(xs))
-        HIP_TRY(hipMemcpyAsync(bout + r.off, dev + r.off, r.bytes, hipMemcpyDeviceToHost, ctx->s_comp));
+    for (const Xfer &r : merge_runs(xs)) {
+        ends.push_back({bout + r.off, dev + r.off});
+        bytes.push_back(r.bytes);
+    }
+    SDP_TRY(d2h_copies(ctx, ends, bytes));
     HIP_TRY(hipEventRecord(ctx->d2h_done[bo], ctx->s_comp));
     ctx->pending_out[bo] = xs;
     return SDP_OK;

@@ -326,6 +326,42 @@ def test_streamed_matches_oracle_and_device(sdp, ctx, ctx_poison, ctx_nostore, c
             host.close()
 
 
+@pytest.mark.parametrize("staged", [False, True])
+def test_d2h_copy_kernel_equals_runtime_copies(sdp, ctx, staged, monkeypatch):
+    """Device-to-host copies through the library's copy kernel (every copy,
+    or those of at most the default 64 MiB) and through the runtime give the
+    same bits, with ragged byte counts (odd element counts of BF16) and one
+    to three chunks per segment, pinned and staged, with the slot poisoning
+    on; all equal device mode."""
+    sizes = [3 * TILE + 5, 1, 70001, 2 * TILE]
+    R = 2
+    masters, grads = rand_inputs(sizes, R, 2, seed=151 + int(staged))
+    dev = DevState(masters, R)
+    hps = [sdp.make_params(lr=1e-3, weight_decay=0.05, max_grad_norm=0.2, step=t) for t in (1, 2)]
+    dev_states, dev_norms = [], []
+    for t in (1, 2):
+        dev_norms.append(dev_step(sdp, ctx, dev, grads[t - 1], hps[t - 1]))
+        dev_states.append(dev.host())
+    flags = sdp.SDP_FLAG_DEBUG_POISON | (sdp.SDP_FLAG_STREAM_STAGED if staged else 0)
+    for limit in ("0", None, str(1 << 40)):
+        if limit is None:
+            monkeypatch.delenv("SDP_D2H_KERNEL_MAX_BYTES", raising=False)
+        else:
+            monkeypatch.setenv("SDP_D2H_KERNEL_MAX_BYTES", limit)
+        c = sdp.sdp_ctx_create(0, 2 * TILE, R, flags)  # reads the variable
+        host = (PageableState if staged else HostState)(sdp, masters, R)
+        try:
+            for t in (1, 2):
+                host.set_grads(grads[t - 1])
+                n = sdp.sdp_stream_step(c, host.segments(), hps[t - 1], 2 * TILE)
+                assert n == dev_norms[t - 1]
+                assert states_equal(host.host(), dev_states[t - 1]), f"limit {limit} step {t}"
+        finally:
+            host.close()
+            sdp.sdp_ctx_destroy(c)
+    monkeypatch.delenv("SDP_D2H_KERNEL_MAX_BYTES", raising=False)
+
+
 @pytest.fixture(scope="module")
 def ctx_staged(sdp):
     c = sdp.sdp_ctx_create(0, 4 * TILE, 16, sdp.SDP_FLAG_STREAM_STAGED | sdp.SDP_FLAG_DEBUG_POISON)
