@@ -36,16 +36,26 @@ std::vector<Xfer> merge_runs(std::vector<Xfer> xs) {
 
 // Device -> pinned host copies (dst[k] <- src[k], bytes[k]) on the compute
 // stream: those of at most d2h_kernel_max bytes (16-byte aligned) as one
-// launch of the library's copy kernel, the others as runtime copies.  (The
-// same kernel measured slower than the runtime's host-to-device copies at
-// every chunk size, so those stay runtime copies.)
+// launch of the library's copy kernel, the others as runtime copies.  The
+// kernel stores through the device's mapping of the host memory, as the
+// runtime reports it: the same address for hipHostMalloc memory, possibly
+// another for registered memory; memory without one takes a runtime copy.
+// (The same kernel measured slower than the runtime's host-to-device copies
+// at every chunk size, so those stay runtime copies.)
 int d2h_copies(sdp_ctx *ctx, const std::vector<std::pair<char *, const char *>> &ends,
                const std::vector<size_t> &bytes) {
     sdp::CopyBatch b{};
     for (size_t k = 0; k < ends.size(); ++k) {
-        const bool aligned = (((uintptr_t)ends[k].first | (uintptr_t)ends[k].second) % 16) == 0;
-        if ((int64_t)bytes[k] <= ctx->d2h_kernel_max && aligned && b.n < sdp::kCopyBatchMax) {
-            b.dst[b.n] = ends[k].first;
+        char *mapped = nullptr;
+        if ((int64_t)bytes[k] <= ctx->d2h_kernel_max && b.n < sdp::kCopyBatchMax) {
+            hipPointerAttribute_t at;
+            if (hipPointerGetAttributes(&at, ends[k].first) == hipSuccess && at.type == hipMemoryTypeHost)
+                mapped = (char *)at.devicePointer;
+            else
+                (void)hipGetLastError();
+        }
+        if (mapped && (((uintptr_t)mapped | (uintptr_t)ends[k].second) % 16) == 0) {
+            b.dst[b.n] = mapped;
             b.src[b.n] = ends[k].second;
             b.bytes[b.n] = (int64_t)bytes[k];
             ++b.n;
