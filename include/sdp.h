@@ -47,8 +47,8 @@
  *  A non-finite norm leaves every state and parameter unchanged.
  *  Results do not depend on the chunk size, on the mode (device or
  *  streamed) or on run-to-run scheduling: the norm is a fixed-order tree
- *  over fixed 8,192-element spans of each segment (eight per 65,536-element
- *  tile, and chunks are whole tiles).  The host-update route
+ *  over fixed 4,096-element spans of each segment (sixteen per
+ *  65,536-element tile, and chunks are whole tiles).  The host-update route
  *  with SDP_GBAR_F32 gives the same norm bits; its host cores evaluate the
  *  same FP64 expression, so its states agree with the other modes up to the
  *  last FP64 rounding before the FP32 one.

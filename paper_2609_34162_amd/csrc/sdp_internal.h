@@ -73,10 +73,15 @@ struct CopyBatch {
 };
 
 constexpr int kTile = SDP_NORM_TILE;
-constexpr int kNormSplit = 8;                    // norm blocks, and partial pairs, per tile
+constexpr int kNormSplit = 16;                   // norm blocks, and partial pairs, per tile
 constexpr int kNormSpan = kTile / kNormSplit;    // elements per norm block
 constexpr int kNormThreads = 256;
 constexpr int kFinalizeThreads = 1024;
+// More than kMergeRun span pairs are merged in two fixed stages: block b of
+// k_norm_merge merges pairs b*kMergeRun .. (b+1)*kMergeRun - 1 into pair b
+// of a second array, and the one-block finalize merges those.
+constexpr int kMergeThreads = 256;
+constexpr int kMergeRun = 2048;
 constexpr int kUpdateThreads = 64;
 // Fused update residency: blocks of one wave, at most kUpdateBlocksPerCU of
 // them per compute unit (two or three waves per SIMD).  The update's mix of
@@ -88,12 +93,13 @@ constexpr int kUpdateBlocksPerCU = 10;
 // The norm pass that stores g_bar (16 B read + 4 B written per element at
 // R = 8) is capped the same way at kNormStoreBlocksPerCU blocks of
 // kNormThreads; the plain norm pass, read only, runs uncapped.
-constexpr int kNormStoreBlocksPerCU = 3;
+constexpr int kNormStoreBlocksPerCU = 4;
 constexpr int kVec = 8;     // elements per lane per access (16 B of BF16, 32 B of FP32)
 constexpr int kUpdVec = 4;  // fused update: elements per lane (8 B of BF16, 16 B of FP32)
 
 hipError_t launch_norm_partials(int R, const NormArgs &a, int store_lds_pad, hipStream_t s);
-hipError_t launch_norm_finalize(const double *partials /* pairs */, int64_t n_pairs,
+// merged: room for ceil(n_pairs / kMergeRun) pairs (used when n_pairs > kMergeRun).
+hipError_t launch_norm_finalize(const double *partials /* pairs */, int64_t n_pairs, double *merged,
                                 double max_grad_norm, NormState *ns, hipStream_t s);
 hipError_t launch_update(int R, const UpdateArgs &a, int max_blocks, int lds_pad, hipStream_t s);
 hipError_t launch_gbar_out(int R, const GbarArgs &a, hipStream_t s);

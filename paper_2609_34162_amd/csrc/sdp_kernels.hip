@@ -219,6 +219,31 @@ __global__ __launch_bounds__(kNormThreads) void k_norm_partials(NormArgs a) {
     }
 }
 
+// First stage of the finalize for many pairs: block b merges the pairs
+// b*kMergeRun + t + kMergeThreads*j (j = 0 .. 7) in increasing j per thread,
+// then the threads by the fixed block tree, into merged pair b.  Pairs past
+// the end count as zero.
+__global__ __launch_bounds__(kMergeThreads) void k_norm_merge(const double *__restrict__ partials,
+                                                              int64_t n_pairs, double *__restrict__ merged) {
+    constexpr int kPer = kMergeRun / kMergeThreads;
+    const double2 *pairs = reinterpret_cast<const double2 *>(partials);
+    const int64_t base = (int64_t)blockIdx.x * kMergeRun + threadIdx.x;
+    double2 b[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        const int64_t i = base + (int64_t)j * kMergeThreads;
+        b[j] = i < n_pairs ? pairs[i] : make_double2(0.0, 0.0);
+    }
+    double hi = b[0].x, lo = b[0].y;
+#pragma unroll
+    for (int j = 1; j < kPer; ++j) dd_merge(hi, lo, b[j].x, b[j].y);
+    block_merge<kMergeThreads>(hi, lo);
+    if (threadIdx.x == 0) {
+        merged[2 * blockIdx.x] = hi;
+        merged[2 * blockIdx.x + 1] = lo;
+    }
+}
+
 // One block: fixed-order sum of all span partials (pairs), then the norm, the
 // clip coefficient and the non-finite flag.  Thread t takes the pairs
 // t + 1024*j; pair j goes to the thread's accumulator j mod 4 (four
@@ -554,8 +579,18 @@ hipError_t launch_norm_partials(int R, const NormArgs &a, int store_lds_pad, hip
     }
 }
 
-hipError_t launch_norm_finalize(const double *partials, int64_t n_partials, double max_grad_norm,
+hipError_t launch_norm_finalize(const double *partials, int64_t n_partials, double *merged, double max_grad_norm,
                                 NormState *ns, hipStream_t s) {
+    if (n_partials > kMergeRun) {
+        if (!merged) return hipErrorInvalidValue;
+        const int64_t blocks = cdiv(n_partials, kMergeRun);
+        hipLaunchKernelGGL(k_norm_merge, dim3((uint32_t)blocks), dim3(kMergeThreads), 0, s, partials, n_partials,
+                           merged);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        partials = merged;
+        n_partials = blocks;
+    }
     hipLaunchKernelGGL(k_norm_finalize, dim3(1), dim3(kFinalizeThreads), 0, s, partials, n_partials,
                        max_grad_norm, ns);
     return hipGetLastError();

@@ -211,8 +211,10 @@ int ensure_partials(sdp_ctx *ctx, int64_t tiles) {
     ctx->partials = nullptr;
     ctx->partials_cap = 0;
     int64_t cap = std::max<int64_t>(n, 4096);
-    // each span partial is a double-double pair
-    if (hipMalloc(&ctx->partials, (size_t)cap * 2 * sizeof(double)) != hipSuccess) {
+    // each span partial is a double-double pair; the finalize's first stage
+    // writes one pair per kMergeRun of them after the last
+    const int64_t pairs = cap + cdiv(cap, sdp::kMergeRun);
+    if (hipMalloc(&ctx->partials, (size_t)pairs * 2 * sizeof(double)) != hipSuccess) {
         (void)hipGetLastError();
         ctx->partials = nullptr;
         return fail(SDP_ERR_OUT_OF_MEMORY, "cannot allocate %lld norm partials", (long long)cap);
@@ -309,7 +311,8 @@ int norm_launch(sdp_ctx *ctx, int32_t R, const uint16_t *const *g, int64_t n, do
 
 int finalize_launch(sdp_ctx *ctx, int64_t tiles, double max_grad_norm, hipStream_t s) {
     hipEvent_t t0 = timed_begin(ctx, s);
-    HIP_TRY(sdp::launch_norm_finalize(ctx->partials, tiles * sdp::kNormSplit, max_grad_norm, ctx->ns, s));
+    HIP_TRY(sdp::launch_norm_finalize(ctx->partials, tiles * sdp::kNormSplit, ctx->partials + 2 * ctx->partials_cap,
+                                      max_grad_norm, ctx->ns, s));
     timed_end(ctx, s, t0, kFinalize, tiles);
     return SDP_OK;
 }
