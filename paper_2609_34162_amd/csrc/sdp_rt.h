@@ -345,8 +345,9 @@ int default_host_threads();
 // buffers while copies in both directions are in flight.  Host memory
 // carries those copies and every DMA byte; on the MI355X hosts measured here
 // (about 400 GB/s of host memory traffic with 16 threads, 50-57 GB/s per
-// thread) five threads let the DMA keep its rate, six or more starved the
-// device-to-host copies and slowed the pass by a quarter.
+// thread) four and five threads let the DMA keep its rate, and six or more
+// starved the device-to-host copies and slowed the pass by a quarter; the
+// default keeps one thread of margin below that cliff.
 constexpr int kStagedCopyThreads = 4;
 int default_staged_copy_threads();
 
