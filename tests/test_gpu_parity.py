@@ -362,6 +362,38 @@ def test_d2h_copy_kernel_equals_runtime_copies(sdp, ctx, staged, monkeypatch):
     monkeypatch.delenv("SDP_D2H_KERNEL_MAX_BYTES", raising=False)
 
 
+def test_staged_copy_threads_do_not_change_results(sdp, ctx, monkeypatch):
+    """The staged mode's cap on copy threads while transfers are in flight
+    (one thread, two, the default four, sixteen) is a schedule only: every
+    cap gives device mode's bits, over five chunks per step."""
+    sizes = [5 * TILE + 9]
+    R = 3
+    masters, grads = rand_inputs(sizes, R, 2, seed=163)
+    dev = DevState(masters, R)
+    hps = [sdp.make_params(lr=1e-3, weight_decay=0.05, max_grad_norm=0.2, step=t) for t in (1, 2)]
+    want = []
+    for t in (1, 2):
+        n = dev_step(sdp, ctx, dev, grads[t - 1], hps[t - 1])
+        want.append((n, dev.host()))
+    for threads in ("1", "2", None, "16"):
+        if threads is None:
+            monkeypatch.delenv("SDP_STAGED_COPY_THREADS", raising=False)
+        else:
+            monkeypatch.setenv("SDP_STAGED_COPY_THREADS", threads)
+        c = sdp.sdp_ctx_create(0, TILE, R, sdp.SDP_FLAG_STREAM_STAGED | sdp.SDP_FLAG_DEBUG_POISON)
+        host = PageableState(sdp, masters, R)
+        try:
+            for t in (1, 2):
+                host.set_grads(grads[t - 1])
+                n = sdp.sdp_stream_step(c, host.segments(), hps[t - 1], TILE)
+                assert n == want[t - 1][0]
+                assert states_equal(host.host(), want[t - 1][1]), f"{threads} copy threads, step {t}"
+        finally:
+            host.close()
+            sdp.sdp_ctx_destroy(c)
+    monkeypatch.delenv("SDP_STAGED_COPY_THREADS", raising=False)
+
+
 @pytest.fixture(scope="module")
 def ctx_staged(sdp):
     c = sdp.sdp_ctx_create(0, 4 * TILE, 16, sdp.SDP_FLAG_STREAM_STAGED | sdp.SDP_FLAG_DEBUG_POISON)
