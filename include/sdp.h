@@ -220,9 +220,10 @@ SDP_API int sdp_stream_step(sdp_ctx *ctx, const sdp_segment *host_segs, int32_t 
  * memory of ctx's GPU; master/exp_avg/exp_avg_sq/param_bf16 are host memory
  * (pinned or pageable; the host threads touch them, no DMA does).
  * Phase 1 runs the norm pass and finalize over the device gradients and
- * reads the norm back.  Phase 2 walks the chunks, the first one split into
- * a ramp of n/16, n/16, n/8, n/4 and n/2 elements when n/16 is at least
- * SDP_NORM_TILE: the GPU writes the piece's mean gradient into a device
+ * reads the norm back.  Phase 2 walks each segment in pieces of at most
+ * chunk_elems elements; at the call's start the pieces grow from
+ * chunk_elems/16 by 6/5 per piece, in whole SDP_NORM_TILEs (no growth when
+ * chunk_elems/16 is less than SDP_NORM_TILE): the GPU writes the piece's mean gradient into a device
  * staging slot, the copy stream moves it into a pinned stage buffer, and
  * the context's host threads run AdamW on the previous piece meanwhile
  * (double-buffered).  gbar_format SDP_GBAR_BF16

@@ -55,7 +55,7 @@ void host_adamw(HostPool *pool, const sdp_host::AdamArgs &a, const sdp_host::Ada
 // by piece: the GPU writes g_bar of piece j (FP32 or BF16) into device slot
 // j%2 on the compute stream, the copy stream moves it into pinned host buffer
 // j%2, and the host threads update piece j-1 from the other buffer meanwhile.
-// The pieces are the chunks, the first one split into a ramp.
+// The pieces grow from C/16 to C over the call's start (route_pieces).
 int host_route(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R, const Plan &plan,
                const sdp_adamw_params *hp, int64_t C, bool bf16, double *grad_norm_out) {
     hipStream_t sc = ctx->s_comp, sy = ctx->s_copy;
@@ -65,21 +65,15 @@ int host_route(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R,
     if (grad_norm_out) *grad_norm_out = st.norm;
     if (st.nonfinite) return fail(SDP_ERR_NONFINITE, "gradient norm is not finite (%g); nothing was updated", st.norm);
     const sdp_host::AdamConsts k = host_consts(hp, st.clip);
-    // the chunks, the first one split into a ramp of short pieces so that the
-    // host threads start after a short first copy
+    // pieces of at most C elements, growing from C/16 so that the host
+    // threads start after a short first copy and each copy hides behind the
+    // host update of the piece before it
     std::vector<Chunk> chunks;
     {
-        const std::vector<Chunk> whole = make_chunks(segs, n_segs, C);
-        std::vector<int64_t> lens;
-        for (const Chunk &c : whole) lens.push_back(c.len);
-        const std::vector<int64_t> pieces = sdp_sched::route_pieces(lens);
-        const size_t head = pieces.size() - (whole.size() - 1);
-        int64_t off = 0;
-        for (size_t j = 0; j < head; ++j) {
-            chunks.push_back({whole[0].seg, whole[0].off + off, pieces[j]});
-            off += pieces[j];
-        }
-        chunks.insert(chunks.end(), whole.begin() + 1, whole.end());
+        std::vector<int64_t> numels;
+        for (int32_t k = 0; k < n_segs; ++k) numels.push_back(segs[k].numel);
+        for (const sdp_sched::RoutePiece &pc : sdp_sched::route_pieces(numels, C))
+            chunks.push_back({pc.seg, pc.off, pc.len});
     }
     const size_t esz = bf16 ? 2 : 4;
     bool used[2] = {false, false};
@@ -101,7 +95,7 @@ int host_route(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R,
         // h2d_done doubles as "g_bar of this slot is written" here
         HIP_TRY(hipEventRecord(ctx->h2d_done[sl], sc));
         HIP_TRY(hipStreamWaitEvent(sy, ctx->h2d_done[sl], 0));
-        HIP_TRY(hipMemcpyAsync(host, dev, (size_t)c.len * esz, hipMemcpyDeviceToHost, sy));
+        SDP_TRY(d2h_copies(ctx, {{host, dev}}, {(size_t)c.len * esz}, sy));
         HIP_TRY(hipEventRecord(ctx->slot_free[sl], sy));  // in the host buffer; the slot is free
         used[sl] = true;
         return SDP_OK;

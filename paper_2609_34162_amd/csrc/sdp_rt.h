@@ -358,6 +358,10 @@ int default_staged_copy_threads();
 // kernels that reach the link's rate.
 constexpr int64_t kD2HKernelMaxBytes = 64ll << 20;
 constexpr int kD2HKernelBlocks = 64;
+// Device -> pinned host copies (dst <- src, bytes) enqueued on stream st,
+// through the copy kernel where they qualify (sdp_stream.hip).
+int d2h_copies(sdp_ctx *ctx, const std::vector<std::pair<char *, const char *>> &ends,
+               const std::vector<size_t> &bytes, hipStream_t st);
 HostPool *new_pool(const sdp_ctx *ctx, int threads);
 inline size_t stage_bytes(const sdp_ctx *ctx) { return 4 * (size_t)ctx->max_chunk; }
 int ensure_host_stage(sdp_ctx *ctx);

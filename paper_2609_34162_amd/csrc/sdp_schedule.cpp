@@ -13,8 +13,8 @@
 //    in phase 2 chunk j's results land in outgoing buffer j mod 3, and the
 //    host thread stages and issues chunk j+2 before it drains chunk j, all
 //    in the host thread's own order;
-//  - host-update route: the norm pass and read-back, then per piece (the
-//    chunks, the first one split into a ramp) the mean-gradient kernel
+//  - host-update route: the norm pass and read-back, then per piece (see
+//    route_pieces: a ramp of growing pieces, then chunks) the mean-gradient kernel
 //    (after the slot's previous outgoing copy, and issued by the host after
 //    it finished the update of piece j-2), its copy to the host on the copy
 //    stream, and the host update after the copy.
@@ -205,25 +205,18 @@ double kernel_us(double bytes, double gbs, const Rates &r) { return bytes / (gbs
 
 }  // namespace
 
-std::vector<int64_t> route_pieces(const std::vector<int64_t> &chunk_lens) {
-    std::vector<int64_t> out;
-    if (chunk_lens.empty()) return out;
-    const int64_t first = chunk_lens[0];
-    int64_t piece = first / 16 / kRampAlign * kRampAlign;
-    if (piece < kRampAlign) {
-        out = chunk_lens;
-        return out;
+std::vector<RoutePiece> route_pieces(const std::vector<int64_t> &numels, int64_t chunk) {
+    std::vector<RoutePiece> out;
+    int64_t size = chunk / 16 / kRampAlign * kRampAlign;
+    if (size < kRampAlign) size = chunk;
+    for (size_t s = 0; s < numels.size(); ++s) {
+        for (int64_t off = 0; off < numels[s];) {
+            const int64_t len = std::min(size, numels[s] - off);
+            out.push_back({(int32_t)s, off, len});
+            off += len;
+            if (size < chunk) size = std::min(chunk, (size * 6 / 5 + kRampAlign - 1) / kRampAlign * kRampAlign);
+        }
     }
-    int64_t done = 0;
-    out.push_back(piece);
-    done += piece;
-    while (done < first) {
-        const int64_t len = std::min(piece, first - done);
-        out.push_back(len);
-        done += len;
-        piece *= 2;
-    }
-    out.insert(out.end(), chunk_lens.begin() + 1, chunk_lens.end());
     return out;
 }
 
@@ -287,12 +280,7 @@ void build_host_route(Graph &g, const std::vector<int64_t> &numels, int R, int64
     const int fin = g.add(kCompS, kFixed, r.launch_us, 0, 0, {});
     const int rb = g.add(kHostS, kFixed, r.sync_us, 0, 0, {fin});
     std::vector<Chunk> ch;
-    {
-        std::vector<int64_t> lens;
-        for (int64_t n : numels)
-            for (int64_t off = 0; off < n; off += C) lens.push_back(std::min(C, n - off));
-        for (int64_t len : route_pieces(lens)) ch.push_back({len, false});
-    }
+    for (const RoutePiece &pc : route_pieces(numels, C)) ch.push_back({pc.len, false});
     const double esz = bf16 ? 2.0 : 4.0;
     std::vector<int> d2h(ch.size(), -1), adam(ch.size(), -1);
     auto issue = [&](size_t j, int host_pred) {

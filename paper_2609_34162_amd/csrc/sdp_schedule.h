@@ -48,13 +48,20 @@ struct Prediction {
     int64_t n_chunks;
 };
 
-// The host-update route's pieces: the call's chunks in order, with the
-// first one split into a ramp of n/16, n/16, n/8, n/4, n/2 elements (each a
-// multiple of kRampAlign; left whole when n/16 is smaller), so that the host
-// threads start after a short first copy and each later copy hides behind
-// the update of the piece before it.
+// The host-update route's pieces, in order: each segment is cut into
+// consecutive pieces of at most `chunk` elements.  The piece size starts at
+// chunk/16 (in whole multiples of kRampAlign; at `chunk` when chunk/16 is
+// smaller than kRampAlign) and grows by 6/5, rounded up to a multiple of
+// kRampAlign, after every piece until it reaches `chunk`; a piece that meets
+// its segment's end is cut there.  The host threads then start after a short
+// first copy, and each copy hides behind the host update of the piece before
+// it while a copy takes at most 5/6 of the update's time per element.
 constexpr int64_t kRampAlign = 65536;
-std::vector<int64_t> route_pieces(const std::vector<int64_t> &chunk_lens);
+struct RoutePiece {
+    int32_t seg;
+    int64_t off, len;
+};
+std::vector<RoutePiece> route_pieces(const std::vector<int64_t> &numels, int64_t chunk);
 
 // store_gbar: streamed mode keeps the mean gradient in device memory
 // between its passes (the default) instead of streaming the gradients twice.

@@ -12,6 +12,39 @@
 
 namespace sdprt {
 
+// Device -> pinned host copies (dst[k] <- src[k], bytes[k]) on stream st:
+// those of at most d2h_kernel_max bytes (16-byte aligned) as one
+// launch of the library's copy kernel, the others as runtime copies.  The
+// kernel stores through the device's mapping of the host memory, as the
+// runtime reports it: the same address for hipHostMalloc memory, possibly
+// another for registered memory; memory without one takes a runtime copy.
+// (The same kernel measured slower than the runtime's host-to-device copies
+// at every chunk size, so those stay runtime copies.)
+int d2h_copies(sdp_ctx *ctx, const std::vector<std::pair<char *, const char *>> &ends,
+               const std::vector<size_t> &bytes, hipStream_t st) {
+    sdp::CopyBatch b{};
+    for (size_t k = 0; k < ends.size(); ++k) {
+        char *mapped = nullptr;
+        if ((int64_t)bytes[k] <= ctx->d2h_kernel_max && b.n < sdp::kCopyBatchMax) {
+            hipPointerAttribute_t at;
+            if (hipPointerGetAttributes(&at, ends[k].first) == hipSuccess && at.type == hipMemoryTypeHost)
+                mapped = (char *)at.devicePointer;
+            else
+                (void)hipGetLastError();
+        }
+        if (mapped && (((uintptr_t)mapped | (uintptr_t)ends[k].second) % 16) == 0) {
+            b.dst[b.n] = mapped;
+            b.src[b.n] = ends[k].second;
+            b.bytes[b.n] = (int64_t)bytes[k];
+            ++b.n;
+        } else {
+            HIP_TRY(hipMemcpyAsync(ends[k].first, ends[k].second, bytes[k], hipMemcpyDeviceToHost, st));
+        }
+    }
+    if (b.n > 0) HIP_TRY(sdp::launch_copy_batch(b, ctx->d2h_kernel_blocks, st));
+    return SDP_OK;
+}
+
 namespace {
 
 int poison(sdp_ctx *ctx, int k) {
@@ -32,39 +65,6 @@ std::vector<Xfer> merge_runs(std::vector<Xfer> xs) {
             runs.push_back({x.off, nullptr, x.bytes});
     }
     return runs;
-}
-
-// Device -> pinned host copies (dst[k] <- src[k], bytes[k]) on the compute
-// stream: those of at most d2h_kernel_max bytes (16-byte aligned) as one
-// launch of the library's copy kernel, the others as runtime copies.  The
-// kernel stores through the device's mapping of the host memory, as the
-// runtime reports it: the same address for hipHostMalloc memory, possibly
-// another for registered memory; memory without one takes a runtime copy.
-// (The same kernel measured slower than the runtime's host-to-device copies
-// at every chunk size, so those stay runtime copies.)
-int d2h_copies(sdp_ctx *ctx, const std::vector<std::pair<char *, const char *>> &ends,
-               const std::vector<size_t> &bytes) {
-    sdp::CopyBatch b{};
-    for (size_t k = 0; k < ends.size(); ++k) {
-        char *mapped = nullptr;
-        if ((int64_t)bytes[k] <= ctx->d2h_kernel_max && b.n < sdp::kCopyBatchMax) {
-            hipPointerAttribute_t at;
-            if (hipPointerGetAttributes(&at, ends[k].first) == hipSuccess && at.type == hipMemoryTypeHost)
-                mapped = (char *)at.devicePointer;
-            else
-                (void)hipGetLastError();
-        }
-        if (mapped && (((uintptr_t)mapped | (uintptr_t)ends[k].second) % 16) == 0) {
-            b.dst[b.n] = mapped;
-            b.src[b.n] = ends[k].second;
-            b.bytes[b.n] = (int64_t)bytes[k];
-            ++b.n;
-        } else {
-            HIP_TRY(hipMemcpyAsync(ends[k].first, ends[k].second, bytes[k], hipMemcpyDeviceToHost, ctx->s_comp));
-        }
-    }
-    if (b.n > 0) HIP_TRY(sdp::launch_copy_batch(b, ctx->d2h_kernel_blocks, ctx->s_comp));
-    return SDP_OK;
 }
 
 // Host -> slot `sl` copies of one chunk, enqueued on the copy stream.  In the
@@ -102,14 +102,14 @@ int copy_out(sdp_ctx *ctx, int sl, int bo, const std::vector<Xfer> &xs) {
             ends.push_back({x.host, dev + x.off});
             bytes.push_back(x.bytes);
         }
-        return d2h_copies(ctx, ends, bytes);
+        return d2h_copies(ctx, ends, bytes, ctx->s_comp);
     }
     char *bout = ctx->bounce_out + (size_t)bo * 14 * (size_t)ctx->max_chunk;
     for (const Xfer &r : merge_runs(xs)) {
         ends.push_back({bout + r.off, dev + r.off});
         bytes.push_back(r.bytes);
     }
-    SDP_TRY(d2h_copies(ctx, ends, bytes));
+    SDP_TRY(d2h_copies(ctx, ends, bytes, ctx->s_comp));
     HIP_TRY(hipEventRecord(ctx->d2h_done[bo], ctx->s_comp));
     ctx->pending_out[bo] = xs;
     return SDP_OK;

@@ -88,9 +88,11 @@ def test_host_route_matches_oracle(sdp, ctx, fmt, chunk_tiles, pinned):
 
 @pytest.mark.parametrize("fmt", ["f32", "bf16"])
 def test_host_route_first_chunk_ramp(sdp, fmt):
-    """A first chunk of 16 tiles runs as a ramp of 1, 1, 2, 4 and 8 tiles;
-    results still match the oracle, and equal those of a chunking too short
-    to ramp (every piece of the update is elementwise)."""
+    """With 16-tile chunks the pieces grow from one tile by 6/5 (1, 2, 3, 4,
+    5 tiles, then the rest of the first segment, 5 tiles and 3 elements, and
+    the 5,000-element second segment whole); results still match the oracle,
+    and equal those of a chunking too short to ramp (every piece of the
+    update is elementwise)."""
     sizes = [20 * TILE + 3, 5000]
     R = 2
     masters, grads = rand_inputs(sizes, R, 2, seed=101)
