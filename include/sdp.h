@@ -394,7 +394,9 @@ SDP_API int sdp_bytes_per_elem(int streamed, int32_t n_ranks, uint32_t flags,
 
 /* ---- measurement support ---------------------------------------------- */
 
-/* Start (enable = 1, also clears) or stop (0) per-kernel event timing. */
+/* Start (enable = 1, also clears) or stop (0) per-kernel event timing.
+ * Starting also creates 256 events in advance, so that timed calls do not
+ * spend host time creating them (more are created when needed). */
 SDP_API int sdp_ctx_set_timing(sdp_ctx *ctx, int enable);
 /* Sum of the recorded kernel times (waits for the recorded events). */
 SDP_API int sdp_ctx_get_timing(sdp_ctx *ctx, sdp_kernel_times *out);

@@ -257,6 +257,10 @@ bool device_gbar(const sdp_ctx *ctx, int32_t R) {
 
 // ---- timing -------------------------------------------------------------
 
+// Timing events kept ready by sdp_ctx_set_timing: two per timed launch,
+// enough for a few host-route calls of a few dozen pieces.
+constexpr size_t kTimingEvents = 256;
+
 hipEvent_t take_event(sdp_ctx *ctx) {
     if (!ctx->pool.empty()) {
         hipEvent_t e = ctx->pool.back();
@@ -889,6 +893,13 @@ int sdp_ctx_set_timing(sdp_ctx *ctx, int enable) {
         ctx->timed.clear();
         ctx->host_adam_ms = ctx->host_wait_ms = 0.0;
         ctx->host_adam_elems = 0;
+        // events ready in advance: creating one takes host time, which a call
+        // on the host-bound route would otherwise spend before its launches
+        while (ctx->pool.size() < kTimingEvents) {
+            hipEvent_t e = nullptr;
+            HIP_TRY(hipEventCreate(&e));
+            ctx->pool.push_back(e);
+        }
     }
     ctx->timing = enable != 0;
     return SDP_OK;
