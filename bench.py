@@ -20,6 +20,9 @@ JSON line also carries:
   streamed      -- one Qwen3-14B layer (330,311,680 parameters, R = 4) in
                    pinned host memory, streamed in 32M-element chunks, against
                    the pinned link bandwidth measured in the same run;
+  host_cast (inside streamed) -- the same step with the BF16 parameters
+                   rounded on the host from the returned master, against its
+                   own link bound (12 B per parameter back instead of 14);
   device_r8     -- one Qwen2.5-72B layer (877,674,496 parameters, R = 8) in
                    device mode, where the norm pass stores the mean gradient;
   staged_pageable (inside streamed) -- the streamed step again with the
@@ -405,6 +408,16 @@ def stream_leg(args, torch, np, synth, sdp, dres):
                link_gbs={"h2d": link[0], "d2h": link[1], "bidir": link[2]},
                t_link_ms=t_link * 1e3, frac_of_link_bound=t_link / el, model_rates=rate_vals,
                predicted_ms=sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, C, 0, rates).predicted_ms)
+    # the same step with the BF16 parameters rounded on the host from the
+    # returned master: 12 B per element back instead of 14
+    log("streamed leg: BF16 parameters rounded on the host")
+    hctx = sdp.sdp_ctx_create(0, C, R, sdp.SDP_FLAG_STREAM_HOST_CAST)
+    hel = timed(hctx, segs)
+    sdp.sdp_ctx_destroy(hctx)
+    t_link_hc = (2 * R * N / (link[0] * 1e9)
+                 + max(12 * N / (link[0] * 1e9), 12 * N / (link[1] * 1e9), 24 * N / (link[2] * 1e9)))
+    out["host_cast"] = dict(ms_per_step=hel * 1e3, params_per_s=N / hel, d2h_bytes_per_param=12,
+                            t_link_ms=t_link_hc * 1e3, frac_of_link_bound=t_link_hc / hel)
     if not args.no_extra:
         log("streamed leg: chunk sweep")
 

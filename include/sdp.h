@@ -111,6 +111,16 @@ extern "C" {
 /* Host threads: keep each of the context's worker threads on one CPU of the
  * process's affinity set (the calling thread is left alone). */
 #define SDP_FLAG_HOST_PIN_THREADS 0x20u
+/* Streamed mode: the BF16 parameters do not cross the link.  Once a chunk's
+ * FP32 master has landed in host memory, host threads round it to BF16 into
+ * param_bf16 (round to nearest even, the device's bits), as the paper's host
+ * rounds FP32 weights to BF16 (Design, chunked overlap).  The update pass
+ * then moves 12 bytes per element each way instead of 12 in and 14 out.
+ * Needs max_chunk_elems > 0; host threads as for SDP_FLAG_STREAM_STAGED.
+ * Without SDP_FLAG_STREAM_STAGED every device-to-host copy then runs as the
+ * library's copy kernel (SDP_D2H_KERNEL_MAX_BYTES overrides).  Combined with
+ * SDP_FLAG_STREAM_STAGED it is correct but measured slower. */
+#define SDP_FLAG_STREAM_HOST_CAST 0x40u
 
 /* ---- types ------------------------------------------------------------- */
 typedef struct sdp_ctx sdp_ctx;
@@ -200,7 +210,8 @@ SDP_API int sdp_agg_adam_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_s
  * Phase 2 copies master/m/v of each chunk in, runs the fused update, and
  * copies master/m/v and the BF16 parameters back to the same host locations
  * on the compute stream, again double-buffered.  Device-to-host copies of up
- * to 64 MiB (SDP_D2H_KERNEL_MAX_BYTES, read at context creation; 0: none)
+ * to 64 MiB (all of them with SDP_FLAG_STREAM_HOST_CAST and pinned memory;
+ * SDP_D2H_KERNEL_MAX_BYTES, read at context creation, overrides; 0: none)
  * run as one launch of the library's copy kernel per chunk, which stores
  * into the pinned host memory directly; larger ones are runtime copies.
  * Blocks until every copy has landed.  Returns SDP_ERR_NONFINITE (states
@@ -388,7 +399,8 @@ SDP_API int sdp_plan(const int64_t *numels, int32_t n_segs, int64_t chunk_elems,
 
 /* Algorithmic bytes per element of one step: device mode HBM traffic, or
  * streamed mode host-link traffic per direction (h2d, d2h), for R ranks and
- * the given context flags' g_bar policy. */
+ * the given context flags' g_bar policy (and, streamed, whether the BF16
+ * parameters are rounded on the host: SDP_FLAG_STREAM_HOST_CAST). */
 SDP_API int sdp_bytes_per_elem(int streamed, int32_t n_ranks, uint32_t flags,
                        double *hbm_or_h2d, double *d2h);
 

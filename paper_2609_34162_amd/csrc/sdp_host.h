@@ -34,6 +34,11 @@ enum Simd { kScalar = 0, kAvx512 = 1 };
 // The best instruction set this CPU runs (kAvx512 needs AVX-512 F/BW/VL/DQ).
 int simd_best();
 
+// dst[i] = BF16 round-to-nearest-even of src[i] for n values: NaN keeps sign
+// and top payload bits and gets the quiet bit, infinities are kept, overflow
+// of the largest values rounds to infinity.  AVX-512 where simd_best() has it.
+void cast_bf16(const float *src, uint16_t *dst, int64_t n);
+
 // Updates elements [i0, i1) of a in place.  simd above simd_best() is
 // lowered to it.  Results do not depend on simd, i0 or i1: each element is
 // computed on its own with the same sequence of IEEE operations, under the

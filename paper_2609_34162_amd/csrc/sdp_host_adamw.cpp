@@ -17,6 +17,11 @@
 // performs exactly the scalar path's operations; the BF16 parameters leave
 // with non-temporal stores (they are written once and read by the next
 // parameter delivery, not by this core).
+//
+// Also here: the host lanes' BF16 rounding of FP32 values on its own
+// (parameter delivery, and streamed mode with the BF16 parameters rounded on
+// the host), integer round-to-nearest-even on the bit pattern, 16 values per
+// AVX-512 step.
 #include "sdp_host.h"
 
 #include <immintrin.h>
@@ -122,7 +127,44 @@ __attribute__((target("avx512f,avx512bw,avx512vl,avx512dq"))) void range_avx512(
     _mm_sfence();
 }
 
+uint16_t bf16_one(uint32_t x) {
+    if ((x & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((x >> 16) | 0x0040u);
+    return (uint16_t)((x + 0x7fffu + ((x >> 16) & 1u)) >> 16);
+}
+
+// Sixteen values per step: the same integer operations as bf16_one, the NaN
+// case chosen by mask.  Finite values cannot carry out of 32 bits: the
+// largest magnitude pattern plus the rounding bias stays below 2^32.
+__attribute__((target("avx512f,avx512bw,avx512vl"))) void cast_avx512(const uint32_t *src, uint16_t *dst,
+                                                                      int64_t n) {
+    const __m512i abs_mask = _mm512_set1_epi32(0x7fffffff), inf = _mm512_set1_epi32(0x7f800000);
+    const __m512i bias = _mm512_set1_epi32(0x7fff), one = _mm512_set1_epi32(1), quiet = _mm512_set1_epi32(0x40);
+    int64_t i = 0;
+    for (; i + 16 <= n; i += 16) {
+        const __m512i x = _mm512_loadu_si512((const void *)(src + i));
+        const __m512i hi = _mm512_srli_epi32(x, 16);
+        const __m512i rne = _mm512_srli_epi32(_mm512_add_epi32(_mm512_add_epi32(x, bias), _mm512_and_si512(hi, one)), 16);
+        const __mmask16 nan = _mm512_cmpgt_epu32_mask(_mm512_and_si512(x, abs_mask), inf);
+        const __m512i r = _mm512_mask_blend_epi32(nan, rne, _mm512_or_si512(hi, quiet));
+        _mm256_storeu_si256((__m256i *)(dst + i), _mm512_cvtepi32_epi16(r));
+    }
+    for (; i < n; ++i) dst[i] = bf16_one(src[i]);
+}
+
 }  // namespace
+
+void cast_bf16(const float *src, uint16_t *dst, int64_t n) {
+    const uint32_t *u = reinterpret_cast<const uint32_t *>(src);
+    if (simd_best() >= kAvx512) {
+        cast_avx512(u, dst, n);
+        return;
+    }
+    for (int64_t i = 0; i < n; ++i) {
+        uint32_t x;
+        std::memcpy(&x, u + i, sizeof x);
+        dst[i] = bf16_one(x);
+    }
+}
 
 int simd_best() {
     static const int best = (__builtin_cpu_supports("avx512f") && __builtin_cpu_supports("avx512bw") &&

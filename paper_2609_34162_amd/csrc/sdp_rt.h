@@ -243,6 +243,9 @@ struct sdp_ctx {
     char *stage = nullptr;
     bool stage_used[2] = {false, false};
     std::vector<sdprt::Xfer> pending_out[sdprt::kOutBufs];
+    // SDP_FLAG_STREAM_HOST_CAST: the BF16 rounding of each chunk whose master
+    // lands with outgoing copies `bo`, run once they have landed
+    std::vector<sdprt::Job> pending_cast[sdprt::kOutBufs];
     sdprt::HostPool *copier = nullptr;
     int staged_copy_threads = 0;   // staged update pass: host copy threads while the DMA runs
     int64_t d2h_kernel_max = 0;    // device-to-host copies up to this many bytes run as k_copy_batch
@@ -332,6 +335,7 @@ struct Chunk {
 };
 std::vector<Chunk> make_chunks(const sdp_segment *segs, int32_t n_segs, int64_t C);
 inline bool staged(const sdp_ctx *ctx) { return (ctx->flags & SDP_FLAG_STREAM_STAGED) != 0; }
+inline bool host_cast(const sdp_ctx *ctx) { return (ctx->flags & SDP_FLAG_STREAM_HOST_CAST) != 0; }
 size_t off_in_slot(const sdp_ctx *ctx, int sl, const void *p);
 int stream_common_checks(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int64_t chunk, bool grads_only,
                          int32_t *R);

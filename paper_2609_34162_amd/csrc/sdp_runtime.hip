@@ -26,18 +26,8 @@ int fail(int status, const char *fmt, ...) {
 }
 
 // Round FP32 values to BF16, nearest even, on the host (the parameter
-// delivery lane).  NaN keeps its sign and top payload bits and gets the quiet
-// bit; infinities are kept; overflow of the largest values rounds to
-// infinity.  Plain integer code that the compiler vectorises.
-void cast_bf16_host(const float *src, uint16_t *dst, size_t n) {
-    for (size_t i = 0; i < n; ++i) {
-        uint32_t x;
-        std::memcpy(&x, src + i, sizeof x);
-        const uint32_t r = ((x & 0x7fffffffu) > 0x7f800000u) ? ((x >> 16) | 0x0040u)
-                                                             : ((x + 0x7fffu + ((x >> 16) & 1u)) >> 16);
-        dst[i] = (uint16_t)r;
-    }
-}
+// delivery lane, and streamed mode's host rounding): the host lanes' routine.
+void cast_bf16_host(const float *src, uint16_t *dst, size_t n) { sdp_host::cast_bf16(src, dst, (int64_t)n); }
 
 void pool_jobs(HostPool *pool, const std::vector<Job> &jobs, int width) {
     constexpr size_t kPiece = 4u << 20;      // bytes per copy piece
@@ -524,7 +514,7 @@ int sdp_bytes_per_elem(int streamed, int32_t n_ranks, uint32_t flags, double *hb
     if (streamed) {
         const bool cache = !(flags & SDP_FLAG_STREAM_GBAR_NEVER);
         *hbm_or_h2d = cache ? 12.0 + 2.0 * R : 12.0 + 4.0 * R;
-        *d2h = 14.0;
+        *d2h = (flags & SDP_FLAG_STREAM_HOST_CAST) ? 12.0 : 14.0;
     } else {
         bool cache = (flags & SDP_FLAG_DEVICE_GBAR_ALWAYS) ? true
                      : (flags & SDP_FLAG_DEVICE_GBAR_NEVER) ? false
@@ -652,7 +642,8 @@ int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems, int32_t m
         return fail(SDP_ERR_INVALID_ARGUMENT, "max_ranks must be in 1..%d", SDP_MAX_RANKS);
     SDP_TRY(check_chunk(max_chunk_elems, true));
     const uint32_t known = SDP_FLAG_DEVICE_GBAR_NEVER | SDP_FLAG_DEVICE_GBAR_ALWAYS | SDP_FLAG_STREAM_GBAR_NEVER |
-                           SDP_FLAG_DEBUG_POISON | SDP_FLAG_STREAM_STAGED | SDP_FLAG_HOST_PIN_THREADS;
+                           SDP_FLAG_DEBUG_POISON | SDP_FLAG_STREAM_STAGED | SDP_FLAG_HOST_PIN_THREADS |
+                           SDP_FLAG_STREAM_HOST_CAST;
     if (flags & ~known) return fail(SDP_ERR_INVALID_ARGUMENT, "unknown context flags 0x%x", flags & ~known);
     if ((flags & SDP_FLAG_DEVICE_GBAR_NEVER) && (flags & SDP_FLAG_DEVICE_GBAR_ALWAYS))
         return fail(SDP_ERR_INVALID_ARGUMENT, "DEVICE_GBAR_NEVER and DEVICE_GBAR_ALWAYS are exclusive");
@@ -716,7 +707,13 @@ int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems, int32_t m
         (void)hipGetLastError();
         return bail(fail(SDP_ERR_OUT_OF_MEMORY, "cannot allocate the pinned norm mirror"));
     }
-    c->d2h_kernel_max = kD2HKernelMaxBytes;
+    // pinned streamed mode with the BF16 parameters rounded on the host waits
+    // on each chunk's returning copies, and then the runtime's large copies
+    // ran slower than the library's kernel (183 against 144 ms per step on
+    // the Qwen3-14B layer at 32M-element chunks): the kernel takes them all
+    c->d2h_kernel_max = ((flags & SDP_FLAG_STREAM_HOST_CAST) && !(flags & SDP_FLAG_STREAM_STAGED))
+                            ? std::numeric_limits<int64_t>::max()
+                            : kD2HKernelMaxBytes;
     if (const char *env = std::getenv("SDP_D2H_KERNEL_MAX_BYTES")) c->d2h_kernel_max = std::atoll(env);
     c->d2h_kernel_blocks = kD2HKernelBlocks;
     if (const char *env = std::getenv("SDP_D2H_KERNEL_BLOCKS"))
@@ -741,6 +738,11 @@ int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems, int32_t m
         }
         for (int k = 0; k < kInBufs; ++k)
             CTX_HIP(hipEventCreateWithFlags(&c->bin_done[k], hipEventDisableTiming));
+    }
+    if (flags & (SDP_FLAG_STREAM_STAGED | SDP_FLAG_STREAM_HOST_CAST)) {
+        if (max_chunk_elems <= 0)
+            return bail(fail(SDP_ERR_INVALID_ARGUMENT, "SDP_FLAG_STREAM_HOST_CAST needs max_chunk_elems > 0"));
+        // the host threads' work on results that have landed waits for these
         for (int k = 0; k < kOutBufs; ++k)
             CTX_HIP(hipEventCreateWithFlags(&c->d2h_done[k], hipEventDisableTiming));
         c->copier = new_pool(c, default_host_threads());

@@ -102,7 +102,9 @@ int copy_out(sdp_ctx *ctx, int sl, int bo, const std::vector<Xfer> &xs) {
             ends.push_back({x.host, dev + x.off});
             bytes.push_back(x.bytes);
         }
-        return d2h_copies(ctx, ends, bytes, ctx->s_comp);
+        SDP_TRY(d2h_copies(ctx, ends, bytes, ctx->s_comp));
+        if (host_cast(ctx)) HIP_TRY(hipEventRecord(ctx->d2h_done[bo], ctx->s_comp));
+        return SDP_OK;
     }
     char *bout = ctx->bounce_out + (size_t)bo * 14 * (size_t)ctx->max_chunk;
     for (const Xfer &r : merge_runs(xs)) {
@@ -115,16 +117,20 @@ int copy_out(sdp_ctx *ctx, int sl, int bo, const std::vector<Xfer> &xs) {
     return SDP_OK;
 }
 
-// Staged mode: wait for the outgoing copies into bounce buffer `bo` and move
-// them to their host destinations on at most `width` host threads (0: all).
+// Wait for outgoing copies `bo` to land, then, on at most `width` host
+// threads (0: all), move them from the bounce buffer to their host
+// destinations (staged mode) and round the chunk's master to BF16
+// (SDP_FLAG_STREAM_HOST_CAST).
 int drain(sdp_ctx *ctx, int bo, int width) {
-    if (ctx->pending_out[bo].empty()) return SDP_OK;
+    if (ctx->pending_out[bo].empty() && ctx->pending_cast[bo].empty()) return SDP_OK;
     HIP_TRY(hipEventSynchronize(ctx->d2h_done[bo]));
     char *bout = ctx->bounce_out + (size_t)bo * 14 * (size_t)ctx->max_chunk;
     std::vector<Job> jobs;
     for (const Xfer &x : ctx->pending_out[bo]) jobs.push_back({x.host, bout + x.off, x.bytes});
+    jobs.insert(jobs.end(), ctx->pending_cast[bo].begin(), ctx->pending_cast[bo].end());
     pool_jobs(ctx->copier, jobs, width);
     ctx->pending_out[bo].clear();
+    ctx->pending_cast[bo].clear();
     return SDP_OK;
 }
 
@@ -159,9 +165,11 @@ int stream_norm_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int
 namespace {
 
 // Phase 2: master/m/v in (and the gradients again unless g_bar is stored),
-// fused update, master/m/v and BF16 parameters back out.  Chunk j uses slot
-// (j + k0) mod 2, continuing phase 1's alternation.  Staged, the host thread
-// stages and enqueues chunk j + kStageAhead before it drains chunk j.  While
+// fused update, master/m/v and BF16 parameters back out (or, with
+// SDP_FLAG_STREAM_HOST_CAST, the BF16 parameters rounded on the host from the
+// returned master).  Chunk j uses slot (j + k0) mod 2, continuing phase 1's
+// alternation.  Staged or rounding on the host, the host thread stages and
+// enqueues chunk j + kStageAhead before it drains chunk j.  While
 // copies are in flight the host copies run on staged_copy_threads threads:
 // more of them starve the device-to-host copies of host memory (phase 1,
 // with the link busy in one direction only, is not hurt and uses them all).
@@ -192,15 +200,24 @@ int stream_update_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t R, const 
                               stored_gbar ? ctx->gbar + plan.gbar_base[c.seg] + c.off : nullptr, c.len, ctx->s_comp));
         std::vector<Xfer> out = {{off_in_slot(ctx, sl, slot.p), (char *)(g.master + c.off), f4},
                                  {off_in_slot(ctx, sl, slot.m), (char *)(g.exp_avg + c.off), f4},
-                                 {off_in_slot(ctx, sl, slot.v), (char *)(g.exp_avg_sq + c.off), f4},
-                                 {off_in_slot(ctx, sl, slot.pb), (char *)(g.param_bf16 + c.off), b2}};
-        SDP_TRY(copy_out(ctx, sl, (int)(j % kOutBufs), out));
+                                 {off_in_slot(ctx, sl, slot.v), (char *)(g.exp_avg_sq + c.off), f4}};
+        const int bo = (int)(j % kOutBufs);
+        if (host_cast(ctx)) {
+            // the master's rounding, from where it lands on the host
+            const void *src = staged(ctx) ? (const void *)(ctx->bounce_out + (size_t)bo * 14 * (size_t)ctx->max_chunk +
+                                                           off_in_slot(ctx, sl, slot.p))
+                                          : (const void *)(g.master + c.off);
+            ctx->pending_cast[bo] = {{g.param_bf16 + c.off, src, (size_t)c.len, Job::kCastBf16}};
+        } else {
+            out.push_back({off_in_slot(ctx, sl, slot.pb), (char *)(g.param_bf16 + c.off), b2});
+        }
+        SDP_TRY(copy_out(ctx, sl, bo, out));
         SDP_TRY(poison(ctx, sl));
         HIP_TRY(hipEventRecord(ctx->slot_free[sl], ctx->s_comp));
         used[sl] = true;
         return SDP_OK;
     };
-    if (!staged(ctx)) {
+    if (!staged(ctx) && !host_cast(ctx)) {
         for (size_t j = 0; j < chunks.size(); ++j) SDP_TRY(issue(j));
         return SDP_OK;
     }
@@ -254,6 +271,7 @@ int sdp_stream_step(sdp_ctx *ctx, const sdp_segment *host_segs, int32_t n_segs, 
     // after a failure, results still waiting in bounce buffers belong to this
     // call only: never let a later call move them
     for (auto &xs : ctx->pending_out) xs.clear();
+    for (auto &js : ctx->pending_cast) js.clear();
     if (rc != SDP_OK) return rc;
     if (rc2 != SDP_OK) return rc2;
     return mark_done(ctx, ctx->s_comp);

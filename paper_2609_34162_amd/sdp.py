@@ -31,6 +31,7 @@ SDP_FLAG_STREAM_GBAR_NEVER = 0x4
 SDP_FLAG_DEBUG_POISON = 0x8
 SDP_FLAG_STREAM_STAGED = 0x10
 SDP_FLAG_HOST_PIN_THREADS = 0x20
+SDP_FLAG_STREAM_HOST_CAST = 0x40
 SDP_DELIVER_HOST_CAST = 0
 SDP_DELIVER_DEVICE_CAST = 1
 SDP_GBAR_F32 = 0

@@ -87,6 +87,9 @@ def test_bytes_per_element(sdp):
     # streamed: each gradient crosses once, states in and out
     assert sdp.sdp_bytes_per_elem(True, 4) == (20.0, 14.0)
     assert sdp.sdp_bytes_per_elem(True, 4, sdp.SDP_FLAG_STREAM_GBAR_NEVER) == (28.0, 14.0)
+    # BF16 parameters rounded on the host: master, m and v come back, 12 B
+    assert sdp.sdp_bytes_per_elem(True, 4, sdp.SDP_FLAG_STREAM_HOST_CAST) == (20.0, 12.0)
+    assert sdp.sdp_bytes_per_elem(True, 2, sdp.SDP_FLAG_STREAM_HOST_CAST | sdp.SDP_FLAG_STREAM_STAGED) == (16.0, 12.0)
 
 
 def test_training_state_bytes_match_paper_table():
@@ -118,5 +121,5 @@ def test_null_arguments_fail_before_any_gpu_call(sdp):
     assert L.sdp_ctx_create(ctypes.byref(out), 0, 0, 0, 0) == sdp.SDP_ERR_INVALID_ARGUMENT  # max_ranks 0
     assert L.sdp_ctx_create(ctypes.byref(out), 0, 1000, 4, 0) == sdp.SDP_ERR_INVALID_ARGUMENT  # chunk
     assert L.sdp_ctx_create(ctypes.byref(out), 0, 0, 4, 3) == sdp.SDP_ERR_INVALID_ARGUMENT  # exclusive flags
-    assert L.sdp_ctx_create(ctypes.byref(out), 0, 0, 4, 0x40) == sdp.SDP_ERR_INVALID_ARGUMENT  # unknown flag
+    assert L.sdp_ctx_create(ctypes.byref(out), 0, 0, 4, 0x80) == sdp.SDP_ERR_INVALID_ARGUMENT  # unknown flag
     assert "unknown" in sdp.sdp_last_error()

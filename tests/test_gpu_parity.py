@@ -362,6 +362,40 @@ def test_d2h_copy_kernel_equals_runtime_copies(sdp, ctx, staged, monkeypatch):
     monkeypatch.delenv("SDP_D2H_KERNEL_MAX_BYTES", raising=False)
 
 
+@pytest.mark.parametrize("staged", [False, True])
+@pytest.mark.parametrize("chunk_tiles", [1, 2])
+def test_streamed_host_cast_equals_device_mode(sdp, ctx, staged, chunk_tiles):
+    """SDP_FLAG_STREAM_HOST_CAST: the BF16 parameters are rounded on the host
+    from the returned master instead of crossing the link.  Pinned and
+    staged, with slot poisoning, ragged sizes and several chunks per segment,
+    every output equals device mode bit for bit, and param_bf16 =
+    bf16(master)."""
+    sizes = [3 * TILE + 5, 1, 70001, 2 * TILE]
+    R = 3
+    masters, grads = rand_inputs(sizes, R, 2, seed=171 + chunk_tiles + 10 * int(staged))
+    dev = DevState(masters, R)
+    hps = [sdp.make_params(lr=1e-3, weight_decay=0.05, max_grad_norm=0.2, step=t) for t in (1, 2)]
+    want = []
+    for t in (1, 2):
+        n = dev_step(sdp, ctx, dev, grads[t - 1], hps[t - 1])
+        want.append((n, dev.host()))
+    flags = sdp.SDP_FLAG_STREAM_HOST_CAST | sdp.SDP_FLAG_DEBUG_POISON | (sdp.SDP_FLAG_STREAM_STAGED if staged else 0)
+    c = sdp.sdp_ctx_create(0, chunk_tiles * TILE, R, flags)
+    host = (PageableState if staged else HostState)(sdp, masters, R)
+    try:
+        for t in (1, 2):
+            host.set_grads(grads[t - 1])
+            n = sdp.sdp_stream_step(c, host.segments(), hps[t - 1], chunk_tiles * TILE)
+            assert n == want[t - 1][0]
+            got = host.host()
+            assert states_equal(got, want[t - 1][1]), f"step {t}"
+            for s in range(len(sizes)):
+                assert np.array_equal(got.param_bf16[s], oracle.bf16(got.master[s]))
+    finally:
+        host.close()
+        sdp.sdp_ctx_destroy(c)
+
+
 def test_staged_copy_threads_do_not_change_results(sdp, ctx, monkeypatch):
     """The staged mode's cap on copy threads while transfers are in flight
     (one thread, two, the default four, sixteen) is a schedule only: every
