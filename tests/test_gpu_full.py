@@ -1,18 +1,19 @@
 """GPU parity at the full workload sizes, in the launch configuration bench.py
 times: one Qwen3-8B layer (192,946,176 params, R = 4, 10 steps) and one
 Qwen2.5-72B layer (877,674,496 params, R = 8, 3 steps) in device mode, and one
-Qwen3-14B layer (330,311,680 params, R = 4, 5 steps) in streamed mode and on
-the host-update route (FP32 mean gradient, 5 steps; BF16 mean gradient, 3
-steps; pageable host states, gradients in device memory), and one segment
+Qwen3-14B layer (330,311,680 params, R = 4, 5 steps) in streamed mode (pinned
+host state; pinned with the BF16 parameters rounded on the host; pageable
+host state through the staged mode) and on the host-update route (FP32 mean
+gradient, 5 steps; BF16 mean gradient, 3 steps; pageable host states,
+gradients in device memory), and one segment
 of 2^31 + 4099 elements in device mode and on the host-update route
 (sampled points, exact norm).
 
 Every element of every output is compared with the oracle at every step,
 teacher-forced (the oracle steps from the GPU's state before the step) and,
 where stated, also free-running (the oracle carries its own state from step
-one).  Criteria as in test_gpu_parity.py.  The full Qwen3-14B model in
-streamed mode (14.8B params, 266 GB of pinned host state) is in
-test_gpu_full_model.py.
+one).  Criteria as in test_gpu_parity.py.  The full Qwen3-14B model
+(14.8B params, 266 GB of pageable host state) is in test_gpu_full_model.py.
 """
 import time
 
@@ -132,14 +133,20 @@ def test_qwen25_72b_layer_device_full(sdp):
 
 
 @pytest.mark.timeout(400)
-def test_qwen3_14b_layer_streamed_full(sdp):
+@pytest.mark.parametrize("mode", ["pinned", "pinned_host_cast", "staged"])
+def test_qwen3_14b_layer_streamed_full(sdp, mode):
+    """The Qwen3-14B layer streamed: pinned host state; pinned with the BF16
+    parameters rounded on the host; pageable host state through the staged
+    mode.  Released slots are poisoned, so a missing wait shows."""
     w = synth.workload(2)
     n = w.numel
-    log(f"full streamed workload {w.name}: N={n} R={w.ranks} chunk={w.chunk} steps={w.steps}")
+    log(f"full streamed workload {w.name} ({mode}): N={n} R={w.ranks} chunk={w.chunk} steps={w.steps}")
     t0 = time.time()
+    flags = sdp.SDP_FLAG_DEBUG_POISON | {"pinned": 0, "pinned_host_cast": sdp.SDP_FLAG_STREAM_HOST_CAST,
+                                         "staged": sdp.SDP_FLAG_STREAM_STAGED}[mode]
+    ctx = sdp.sdp_ctx_create(0, w.chunk, w.ranks, flags)  # its pinned buffers before the host state
     master = synth.master(w, 0)
-    host = HostState(sdp, [master], w.ranks)
-    ctx = sdp.sdp_ctx_create(0, w.chunk, w.ranks, 0)
+    host = (PageableState if mode == "staged" else HostState)(sdp, [master], w.ranks)
     pin = Pinned(sdp)
     try:
         before = pin.state([n])
