@@ -78,7 +78,7 @@ extern "C" {
 #define SDP_ERR_NONFINITE (-8)         /* gradient norm is NaN or Inf; nothing was updated */
 
 /* ---- constants --------------------------------------------------------- */
-#define SDP_NORM_TILE 65536 /* norm tile: the norm sums in a grid fixed per tile (eight partials each); chunk sizes are multiples of it */
+#define SDP_NORM_TILE 65536 /* norm tile: the norm sums in a grid fixed per tile (sixteen partials each); chunk sizes are multiples of it */
 #define SDP_MAX_RANKS 16    /* largest R */
 #define SDP_ALIGN 16        /* byte alignment required of every buffer */
 
@@ -153,7 +153,7 @@ typedef struct {
  * each launch on the stream the launch uses (only while timing is on). */
 typedef struct {
     double norm_ms;       /* norm-partials kernel (first pass over the gradients) */
-    double finalize_ms;   /* norm finalize kernel */
+    double finalize_ms;   /* norm finalize (both of its kernels, one launch each) */
     double update_ms;     /* fused aggregate + clip + AdamW + BF16 kernel */
     int64_t norm_launches, finalize_launches, update_launches;
     int64_t update_elems; /* elements processed by the timed update launches */
@@ -174,7 +174,7 @@ typedef struct {
  * context creates two streams (default priority) and its events.  Other
  * workspace (norm partials, cached g_bar) grows on demand.  The fused update
  * keeps at most 10 of its one-wave blocks on a compute unit, and the norm
- * pass that stores g_bar at most 3 of its blocks, through dynamic LDS that
+ * pass that stores g_bar at most 4 of its blocks, through dynamic LDS that
  * they do not use; the environment variables SDP_UPDATE_BLOCKS_PER_CU and
  * SDP_NORM_STORE_BLOCKS_PER_CU, read here, set other caps (0: none). */
 SDP_API int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems,
@@ -185,7 +185,8 @@ SDP_API void sdp_ctx_destroy(sdp_ctx *ctx);
 
 /* Device mode.  All state and gradient buffers are device memory of ctx's
  * GPU.  Enqueues on `stream`: the norm pass over every tile of every segment
- * (segment order, then tile order), the one-block norm finalize, and the
+ * (segment order, then tile order), the norm finalize (a fixed-order merge of
+ * the span partials, in two stages above 2,048 of them), and the
  * fused update over every element; the update reads the clip coefficient and
  * the non-finite flag from device memory, so nothing returns to the host.
  * chunk_elems (0 or a multiple of SDP_NORM_TILE) names the unit the caller
