@@ -1,6 +1,7 @@
 // gfx950 kernels of the data-parallel update: norm partials over fixed tiles,
-// a one-block fixed-order finalize, and the fused aggregate + clip + AdamW +
-// BF16 re-emit pass.  All of them are bound by HBM bandwidth and use no MFMA.
+// a fixed-order finalize (one block, after a merge stage for many partials),
+// and the fused aggregate + clip + AdamW + BF16 re-emit pass.  All of them
+// are bound by HBM bandwidth and use no MFMA.
 // Their lanes move wide accesses: 16-byte (dwordx4) FP32 accesses throughout,
 // and BF16 in 16-byte or 8-byte pieces (eight or four elements per lane).
 //

@@ -6,8 +6,9 @@
 // step-time model in sdp_schedule.cpp.
 //
 // Device mode (sdp_agg_adam_step): per call, one norm-partials launch per
-// segment, one finalize launch, one fused-update launch per segment, all on
-// the caller's stream.  The clip coefficient stays in device memory.
+// segment, the finalize (one launch, or two above 2,048 span partials) and
+// one fused-update launch per segment, all on the caller's stream.  The clip
+// coefficient stays in device memory.
 #include "sdp_rt.h"
 #include "sdp_schedule.h"
 
