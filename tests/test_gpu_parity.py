@@ -567,7 +567,7 @@ def test_norm_equals_exactly_rounded_sum(sdp, ctx):
         assert got == want and got_s == want, (trial, got, got_s, want)
 
 
-@pytest.mark.parametrize("mode", ["device", "streamed"])
+@pytest.mark.parametrize("mode", ["device", "streamed", "staged", "host_cast"])
 @pytest.mark.parametrize("bad", [np.nan, np.inf])
 def test_nonfinite_gradient_leaves_states_unchanged(sdp, ctx, mode, bad):
     sizes = [TILE + 9]
@@ -590,16 +590,24 @@ def test_nonfinite_gradient_leaves_states_unchanged(sdp, ctx, mode, bad):
         norm, clip, nonfinite = sdp.sdp_ctx_last_norm(ctx)
         assert nonfinite and not np.isfinite(norm)
     else:
-        host = HostState(sdp, masters, R)
+        flags = {"streamed": 0, "staged": sdp.SDP_FLAG_STREAM_STAGED, "host_cast": sdp.SDP_FLAG_STREAM_HOST_CAST}[mode]
+        c = sdp.sdp_ctx_create(0, TILE, R, flags) if flags else ctx
+        host = (PageableState if mode == "staged" else HostState)(sdp, masters, R)
         try:
             host.pb[0][:] = 7
             host.set_grads(g)
             before = host.host()
             with pytest.raises(sdp.SdpNonFinite):
-                sdp.sdp_stream_step(ctx, host.segments(), hs, TILE)
+                sdp.sdp_stream_step(c, host.segments(), hs, TILE)
             assert states_equal(before, host.host())
+            # the context still works afterwards
+            host.set_grads(grads[0])
+            sdp.sdp_stream_step(c, host.segments(), hs, TILE)
+            assert not states_equal(before, host.host())
         finally:
             host.close()
+            if c is not ctx:
+                sdp.sdp_ctx_destroy(c)
 
 
 def test_argument_errors_have_no_side_effects(sdp, ctx):
@@ -647,6 +655,11 @@ def test_argument_errors_have_no_side_effects(sdp, ctx):
     with pytest.raises(sdp.SdpError) as e:
         sdp.sdp_stream_step(ctx, pageable, hs, 8 * TILE)
     assert e.value.status == sdp.SDP_ERR_CHUNK_TOO_LARGE
+    # the host-rounding and staged flags need streamed-mode staging
+    for flag in (sdp.SDP_FLAG_STREAM_HOST_CAST, sdp.SDP_FLAG_STREAM_STAGED):
+        with pytest.raises(sdp.SdpError) as e:
+            sdp.sdp_ctx_create(0, 0, 2, flag)
+        assert e.value.status == sdp.SDP_ERR_INVALID_ARGUMENT
     torch.cuda.synchronize()
     assert states_equal(before, dev.host())
 
