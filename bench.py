@@ -417,7 +417,9 @@ def stream_leg(args, torch, np, synth, sdp, dres):
     t_link_hc = (2 * R * N / (link[0] * 1e9)
                  + max(12 * N / (link[0] * 1e9), 12 * N / (link[1] * 1e9), 24 * N / (link[2] * 1e9)))
     out["host_cast"] = dict(ms_per_step=hel * 1e3, params_per_s=N / hel, d2h_bytes_per_param=12,
-                            t_link_ms=t_link_hc * 1e3, frac_of_link_bound=t_link_hc / hel)
+                            t_link_ms=t_link_hc * 1e3, frac_of_link_bound=t_link_hc / hel,
+                            predicted_ms=sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, C,
+                                                              sdp.SDP_FLAG_STREAM_HOST_CAST, rates).predicted_ms)
     if not args.no_extra:
         log("streamed leg: chunk sweep")
 

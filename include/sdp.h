@@ -368,7 +368,8 @@ typedef struct {
 #define SDP_SCHED_HOST_ROUTE_BF16 3 /* sdp_host_update_step, SDP_GBAR_BF16 */
 
 /* Step time of one call on segments of the given sizes, R ranks, chunk_elems
- * and context flags (only the g_bar policy of streamed mode matters).  The
+ * and context flags (the g_bar policy of streamed mode and
+ * SDP_FLAG_STREAM_HOST_CAST matter).  The
  * paper's step-time model (Design, step-time model) pairs a resource lower
  * bound, max_j W_j / beta_j, with a dependency recurrence f(v) = d_v +
  * max(a_v, f(u) over predecessors u), whose edges are data dependences,

@@ -579,7 +579,8 @@ int sdp_predict_step(int schedule, const int64_t *numels, int32_t n_segs, int32_
     if (!out) return fail(SDP_ERR_INVALID_ARGUMENT, "out is NULL");
     SDP_TRY(model_chunk_ok(sizes, chunk_elems));
     const sdp_sched::Prediction p = sdp_sched::predict(schedule, sizes, n_ranks, chunk_elems,
-                                                       !(flags & SDP_FLAG_STREAM_GBAR_NEVER), to_rates(rates));
+                                                       !(flags & SDP_FLAG_STREAM_GBAR_NEVER),
+                                                       (flags & SDP_FLAG_STREAM_HOST_CAST) != 0, to_rates(rates));
     out->predicted_ms = p.predicted_ms;
     out->bound_ms = p.bound_ms;
     out->h2d_ms = p.h2d_ms;
@@ -604,7 +605,8 @@ int sdp_tune_chunk(int schedule, const int64_t *numels, int32_t n_segs, int32_t 
     double best = std::numeric_limits<double>::infinity();
     for (int32_t k = 0; k < n_candidates; ++k) {
         const double ms = sdp_sched::predict(schedule, sizes, n_ranks, candidates[k],
-                                             !(flags & SDP_FLAG_STREAM_GBAR_NEVER), to_rates(rates))
+                                             !(flags & SDP_FLAG_STREAM_GBAR_NEVER),
+                                             (flags & SDP_FLAG_STREAM_HOST_CAST) != 0, to_rates(rates))
                               .predicted_ms;
         if (predicted_ms_out) predicted_ms_out[k] = ms;
         if (ms < best) {

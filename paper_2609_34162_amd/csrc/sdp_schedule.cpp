@@ -13,6 +13,9 @@
 //    in phase 2 chunk j's results land in outgoing buffer j mod 3, and the
 //    host thread stages and issues chunk j+2 before it drains chunk j, all
 //    in the host thread's own order;
+//  - host rounding of the BF16 parameters (either variant): 12 B per
+//    element back, and after chunk j's copies land a host task reads its
+//    master and writes its BF16 parameters, in the same issue order;
 //  - host-update route: the norm pass and read-back, then per piece (see
 //    route_pieces: a ramp of growing pieces, then chunks) the mean-gradient kernel
 //    (after the slot's previous outgoing copy, and issued by the host after
@@ -224,11 +227,25 @@ namespace {
 
 // The staged runtime's bounce buffers and how far ahead its host thread
 // stages (incoming buffers, outgoing buffers, chunks staged ahead of the
-// drain).
+// drain), and the largest device-to-host copy it moves with its own kernel
+// (one launch for all of a chunk's copies that qualify).
 constexpr int kInBufs = 3, kOutBufs = 3, kStageAhead = 2;
+constexpr double kD2HKernelMaxBytes = 64.0 * 1024 * 1024;
+
+// Commands that carry one chunk's device-to-host copies of `sizes` bytes:
+// one per copy above the kernel's limit, plus one launch for the rest.
+int d2h_commands(const std::vector<double> &sizes, bool all_kernel) {
+    int cmds = 0;
+    bool launch = false;
+    for (double b : sizes) {
+        if (all_kernel || b <= kD2HKernelMaxBytes) launch = true;
+        else ++cmds;
+    }
+    return cmds + (launch ? 1 : 0);
+}
 
 void build_streamed(Graph &g, const std::vector<int64_t> &numels, int R, int64_t C, bool store, bool staged,
-                    const Rates &r) {
+                    bool host_cast, const Rates &r) {
     const std::vector<Chunk> ch = chunks_of(numels, C);
     int slot_free[2] = {-1, -1}, bin_h2d[kInBufs] = {-1, -1, -1};
     for (size_t k = 0; k < ch.size(); ++k) {
@@ -249,6 +266,8 @@ void build_streamed(Graph &g, const std::vector<int64_t> &numels, int R, int64_t
     int d2h_slot[2] = {-1, -1};
     std::vector<int> d2h_of(ch.size(), -1), drain_of(ch.size(), -1);
     const double in_bpe = 12.0 + (store ? 0.0 : 2.0 * R);
+    const double out_bpe = host_cast ? 12.0 : 14.0;
+    const bool ahead = staged || host_cast;  // the host waits for each chunk's results
     auto issue = [&](size_t j) {
         const int sl = (int)((j + k0) & 1), bi = (int)((j + k0) % kInBufs);
         const double len = (double)ch[j].len;
@@ -258,20 +277,29 @@ void build_streamed(Graph &g, const std::vector<int64_t> &numels, int R, int64_t
         const int h2d = g.add(kCopyS, kH2D, 0, in_bpe * len, in_cmds, {rb, hin, d2h_slot[sl]});
         const int upd = g.add(kCompS, kFixed, kernel_us((26.0 + (store ? 4.0 : 2.0 * R)) * len, r.update_gbs, r), 0,
                               0, {h2d, rb});
-        const int out_cmds = (staged && ch[j].full) ? 1 : 4;
-        const int buf_free = (staged && j >= (size_t)kOutBufs) ? drain_of[j - kOutBufs] : -1;
-        d2h_of[j] = g.add(kCompS, kD2H, 0, 14.0 * len, out_cmds, {upd, hin, buf_free});
+        // master, m and v, and the BF16 parameters unless the host rounds them;
+        // staged, a full chunk's arrays sit back to back and leave as one run
+        std::vector<double> sizes = {4.0 * len, 4.0 * len, 4.0 * len};
+        if (!host_cast) sizes.push_back(2.0 * len);
+        if (staged && ch[j].full) sizes = {out_bpe * len};
+        const int out_cmds = d2h_commands(sizes, host_cast && !staged);
+        const int buf_free = (ahead && j >= (size_t)kOutBufs) ? drain_of[j - kOutBufs] : -1;
+        d2h_of[j] = g.add(kCompS, kD2H, 0, out_bpe * len, out_cmds, {upd, hin, buf_free});
         bin_h2d[bi] = h2d;
         d2h_slot[sl] = d2h_of[j];
     };
-    if (!staged) {
+    if (!ahead) {
         for (size_t j = 0; j < ch.size(); ++j) issue(j);
         return;
     }
     size_t next = 0;
     for (size_t j = 0; j < ch.size(); ++j) {
         for (; next < ch.size() && next <= j + kStageAhead; ++next) issue(next);
-        drain_of[j] = g.host(2.0 * 14.0 * (double)ch[j].len, r.host_gbs, r.host_task_us, {d2h_of[j]});
+        // staged: the results move out of the bounce buffer (read and
+        // written); host rounding: the master read, the BF16 parameters written
+        const double len = (double)ch[j].len;
+        const double bytes = (staged ? 2.0 * out_bpe * len : 0.0) + (host_cast ? 6.0 * len : 0.0);
+        drain_of[j] = g.host(bytes, r.host_gbs, r.host_task_us, {d2h_of[j]});
     }
 }
 
@@ -300,10 +328,10 @@ void build_host_route(Graph &g, const std::vector<int64_t> &numels, int R, int64
 }  // namespace
 
 Prediction predict(int schedule, const std::vector<int64_t> &numels, int R, int64_t chunk, bool store_gbar,
-                   const Rates &r) {
+                   bool host_cast, const Rates &r) {
     Graph g;
     if (schedule == kStreamed || schedule == kStreamedStaged)
-        build_streamed(g, numels, R, chunk, store_gbar, schedule == kStreamedStaged, r);
+        build_streamed(g, numels, R, chunk, store_gbar, schedule == kStreamedStaged, host_cast, r);
     else
         build_host_route(g, numels, R, chunk, schedule == kHostRouteBf16, r);
     Prediction p{};

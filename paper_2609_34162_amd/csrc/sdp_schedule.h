@@ -65,7 +65,10 @@ std::vector<RoutePiece> route_pieces(const std::vector<int64_t> &numels, int64_t
 
 // store_gbar: streamed mode keeps the mean gradient in device memory
 // between its passes (the default) instead of streaming the gradients twice.
+// host_cast: streamed mode rounds the BF16 parameters on the host from the
+// returned master (12 B per element back instead of 14, and a host rounding
+// task per chunk once its copies have landed).
 Prediction predict(int schedule, const std::vector<int64_t> &numels, int R, int64_t chunk, bool store_gbar,
-                   const Rates &r);
+                   bool host_cast, const Rates &r);
 
 }  // namespace sdp_sched

@@ -39,7 +39,7 @@ def test_streamed_single_chunk_is_the_serial_sum(sdp):
             + 3.0 + 11.0                             # finalize, read-back
             + 3 * 7.0 + us(12 * N, 50.0)             # states in
             + us(30 * N, 4000.0) + 3.0               # update from stored g_bar
-            + 4 * 7.0 + us(14 * N, 40.0))            # results out
+            + 1 * 7.0 + us(14 * N, 40.0))            # results out: every copy at most 64 MiB, one kernel launch
     assert math.isclose(got.predicted_ms, want / 1e3, rel_tol=1e-12)
     assert got.n_chunks == 1
     # without stored g_bar the gradients cross twice and the update reads them
@@ -141,6 +141,38 @@ def test_host_update_shares_host_memory_with_the_copy(sdp):
     assert math.isclose(got, want, rel_tol=1e-9), (got, want)
     p = sdp.sdp_predict_step(sdp.SDP_SCHED_HOST_ROUTE_BF16, [2 * L], R, L, 0, rt)
     assert math.isclose(p.dram_ms, (2 * W + 2 * esz * L) / (B * 1e9) * 1e3, rel_tol=1e-12)
+
+
+def test_streamed_host_cast_single_chunk_closed_form(sdp):
+    """One chunk with the BF16 parameters rounded on the host: 12 B per
+    element come back in one copy-kernel launch, then one host task reads
+    the master and writes the BF16 parameters (6 B per element), alone on
+    host memory."""
+    N, R = 3 * TILE + 5, 3
+    rt = rates(sdp, copy_cmd_us=7.0, launch_us=3.0, sync_us=11.0, host_gbs=100.0, host_task_us=5.0)
+    got = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, 4 * TILE, sdp.SDP_FLAG_STREAM_HOST_CAST, rt)
+    want = (R * 7.0 + us(2 * R * N, 50.0) + us((2 * R + 4) * N, 5000.0) + 3.0 + 3.0 + 11.0
+            + 3 * 7.0 + us(12 * N, 50.0) + us(30 * N, 4000.0) + 3.0
+            + 1 * 7.0 + us(12 * N, 40.0)             # master, m, v out
+            + 5.0 + us(6 * N, 100.0))                # host rounding
+    assert math.isclose(got.predicted_ms, want / 1e3, rel_tol=1e-12)
+    plain = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, 4 * TILE, 0, rt)
+    assert math.isclose(got.d2h_ms, plain.d2h_ms * 12 / 14, rel_tol=1e-12)
+    assert math.isclose(got.h2d_ms, plain.h2d_ms, rel_tol=1e-12)
+
+
+def test_streamed_host_cast_many_chunks(sdp):
+    """Many chunks: with fast host lanes, rounding on the host beats copying
+    the BF16 parameters back (fewer link bytes); with slow ones it loses."""
+    sizes, R, C = [40 * TILE + 3], 4, 4 * TILE
+    fast = rates(sdp, host_gbs=1e6, host_task_us=0.0)
+    plain = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, sizes, R, C, 0, fast)
+    hc = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, sizes, R, C, sdp.SDP_FLAG_STREAM_HOST_CAST, fast)
+    assert hc.predicted_ms < plain.predicted_ms
+    assert hc.bound_ms <= hc.predicted_ms
+    slow = rates(sdp, host_gbs=2.0, host_task_us=0.0)
+    hc_slow = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, sizes, R, C, sdp.SDP_FLAG_STREAM_HOST_CAST, slow)
+    assert hc_slow.predicted_ms > plain.predicted_ms
 
 
 def test_staged_equals_plain_when_host_lanes_are_free(sdp):
