@@ -266,12 +266,66 @@ def cpu_leg(args, np, synth, oracle, master, host_grads, w):
 SWEEP_CHUNKS = [1 << 20, 1 << 21, 1 << 22, 1 << 23, 1 << 24, 1 << 25]  # 4-128 MiB per FP32 state array
 
 
+def dep_latency_us(torch, n=64, reps=3):
+    """Latency of an event dependency between two GPU streams, as the streamed
+    engine's h2d_done and slot_free events order its copy and compute
+    streams: n rounds of a 1 MiB host-to-device copy on one stream and a
+    one-element kernel on the other, each waiting on the other's event,
+    against each chain alone.  Every chain is queued behind a spin kernel on
+    its first stream, so the GPU-side times leave the host's enqueue cost
+    out.  Best of `reps`."""
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    src = torch.empty(1 << 20, dtype=torch.uint8).pin_memory()
+    dst = torch.empty(1 << 20, dtype=torch.uint8, device="cuda")
+    x = torch.zeros(1, device="cuda")
+    spin = 50_000_000  # GPU clock cycles, about 20 ms: longer than enqueueing a chain
+
+    def timed(first, body):
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(first):
+            torch.cuda._sleep(spin)
+        e0.record(first)
+        body()
+        e1.record(first)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3  # us
+
+    def copies():
+        with torch.cuda.stream(s1):
+            for _ in range(n):
+                dst.copy_(src, non_blocking=True)
+
+    def kernels():
+        with torch.cuda.stream(s2):
+            for _ in range(n):
+                x.add_(1.0)
+
+    def ping_pong():
+        a = [torch.cuda.Event() for _ in range(n)]
+        b = [torch.cuda.Event() for _ in range(n)]
+        for i in range(n):
+            with torch.cuda.stream(s1):
+                dst.copy_(src, non_blocking=True)
+            a[i].record(s1)
+            s2.wait_event(a[i])
+            with torch.cuda.stream(s2):
+                x.add_(1.0)
+            b[i].record(s2)
+            s1.wait_event(b[i])
+
+    t_c = min(timed(s1, copies) for _ in range(reps))
+    t_k = min(timed(s2, kernels) for _ in range(reps))
+    t_pp = min(timed(s1, ping_pong) for _ in range(reps))
+    return max(0.0, (t_pp - t_c - t_k) / (2 * n))
+
+
 def measure_rates(args, torch, np, sdp, ctx, link, dres):
     """The step-time model's inputs, each measured on this machine: link rates
     (passed in), the per-command copy cost, the kernels' HBM rates and the
     launch cost from the device leg, the norm read-back round trip, the host
-    threads' copy bandwidth, their per-hand-off cost and the host AdamW
-    lane's rate alone."""
+    threads' copy bandwidth, their per-hand-off cost, the host AdamW lane's
+    rate alone and the latency of an event between two GPU streams."""
     big, small = 256 << 20, 1 << 20
     ha, hb = sdp.HostBuffer(big), sdp.HostBuffer(big)
     da = torch.empty(big, dtype=torch.uint8, device="cuda")
@@ -321,9 +375,10 @@ def measure_rates(args, torch, np, sdp, ctx, link, dres):
     del st, pb
     kern_ms = dres["update_ms"] + dres["norm_ms"] + dres["finalize_ms"]
     launch_us = max(0.0, (dres["ms_per_step"] - kern_ms) / 3 * 1e3)
+    dep_us = dep_latency_us(torch)
     vals = dict(h2d_gbs=link[0], d2h_gbs=link[1], both_gbs=link[2], copy_cmd_us=copy_cmd_us,
                 norm_gbs=dres["norm_gbs"], update_gbs=dres["update_gbs"], launch_us=launch_us, sync_us=sync_us,
-                host_gbs=host_gbs, host_task_us=host_task_us, host_adam_gbs=host_adam_gbs)
+                host_gbs=host_gbs, host_task_us=host_task_us, host_adam_gbs=host_adam_gbs, dep_us=dep_us)
     log("model rates: " + ", ".join(f"{k} {v:.1f}" for k, v in vals.items()))
     return sdp.make_rates(**vals), vals
 

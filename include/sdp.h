@@ -347,6 +347,8 @@ typedef struct {
     double host_gbs;         /* host memory bandwidth of the host threads' copies (read + written) */
     double host_task_us;     /* fixed cost of one hand-off to the host threads */
     double host_adam_gbs;    /* the host AdamW lane alone (bytes read + written) */
+    double dep_us;           /* latency of an event recorded on the copy stream and waited on
+                                by the compute stream, or the other way round */
 } sdp_rates;
 
 /* What the model predicts for one call. */

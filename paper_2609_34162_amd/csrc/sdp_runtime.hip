@@ -541,7 +541,7 @@ int check_model_args(int schedule, const int64_t *numels, int32_t n_segs, int32_
         return fail(SDP_ERR_INVALID_ARGUMENT, "n_ranks must be in 1..%d", SDP_MAX_RANKS);
     const double pos[] = {r->h2d_gbs,    r->d2h_gbs,  r->both_gbs,     r->norm_gbs,
                           r->update_gbs, r->host_gbs, r->host_adam_gbs};
-    const double nonneg[] = {r->copy_cmd_us, r->launch_us, r->sync_us, r->host_task_us};
+    const double nonneg[] = {r->copy_cmd_us, r->launch_us, r->sync_us, r->host_task_us, r->dep_us};
     for (double x : pos)
         if (!(std::isfinite(x) && x > 0.0)) return fail(SDP_ERR_INVALID_ARGUMENT, "rates must be finite and > 0");
     for (double x : nonneg)
@@ -556,7 +556,7 @@ int check_model_args(int schedule, const int64_t *numels, int32_t n_segs, int32_
 sdp_sched::Rates to_rates(const sdp_rates *r) {
     return sdp_sched::Rates{r->h2d_gbs,   r->d2h_gbs,  r->both_gbs, r->copy_cmd_us,  r->norm_gbs,
                             r->update_gbs, r->launch_us, r->sync_us,  r->host_gbs,     r->host_task_us,
-                            r->host_adam_gbs};
+                            r->host_adam_gbs, r->dep_us};
 }
 
 int model_chunk_ok(const std::vector<int64_t> &sizes, int64_t chunk) {
@@ -843,7 +843,8 @@ int sdp_grad_norm(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int dev
         SDP_TRY(stream_common_checks(ctx, segs, n_segs, chunk_elems, true, &R));
         const Plan p = make_plan(segs, n_segs);
         SDP_TRY(ensure_partials(ctx, p.tiles));
-        const std::vector<Chunk> chunks = make_chunks(segs, n_segs, chunk_elems);
+        const std::vector<Chunk> chunks =
+            make_chunks(segs, n_segs, sdp_sched::norm_phase_chunk(chunk_elems, R, staged(ctx)));
         SDP_TRY(order_after_last(ctx, ctx->s_copy));
         SDP_TRY(order_after_last(ctx, ctx->s_comp));
         bool used[2] = {false, false};

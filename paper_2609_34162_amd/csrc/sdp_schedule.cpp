@@ -1,8 +1,9 @@
 // Step-time model of the chunked schedules; see sdp_schedule.h.
 //
 // The graph mirrors the runtime's issue order:
-//  - streamed mode, phase 1: per chunk k (slot k mod 2) the R gradient
-//    copies on the copy stream, after the slot's previous norm kernel
+//  - streamed mode, phase 1: per chunk k (slot k mod 2; chunks of
+//    norm_phase_chunk elements) the R gradient copies on the copy stream,
+//    after the slot's previous norm kernel
 //    (slot_free); the norm kernel on the compute stream after the copies
 //    (h2d_done); then the finalize and the host's read-back of the norm;
 //  - phase 2: per chunk, the state copies in after the slot's previous
@@ -89,18 +90,32 @@ double evaluate(Graph &g, const Rates &r) {
     double t = 0.0;
     const double h2d = r.h2d_gbs * 1e3, d2h = r.d2h_gbs * 1e3, both = r.both_gbs * 1e3;  // bytes per us
     const double inf = std::numeric_limits<double>::infinity();
+    // an edge between the copy and the compute stream is an event that one
+    // queue records and the other waits on: it takes effect dep_us later
+    auto crosses = [](const Node &u, const Node &v) {
+        return u.stream != v.stream && u.stream != kHostS && v.stream != kHostS;
+    };
     while (done < total) {
+        double wake = inf;  // earliest time a node whose predecessors are done may start
         for (int s = 0; s < kStreams; ++s) {
             if (cur[s] >= 0 || head[s] >= g.fifo[s].size()) continue;
             const int id = g.fifo[s][head[s]];
             Node &v = g.nodes[id];
             bool ready = true;
-            for (int u : v.preds)
-                if (g.nodes[u].state != 3) {
+            double at = t;
+            for (int u : v.preds) {
+                const Node &pu = g.nodes[u];
+                if (pu.state != 3) {
                     ready = false;
                     break;
                 }
+                if (crosses(pu, v)) at = std::max(at, pu.t_end + r.dep_us);
+            }
             if (!ready) continue;
+            if (at > t) {
+                wake = std::min(wake, at);
+                continue;
+            }
             cur[s] = id;
             if (v.kind == kFixed) {
                 v.state = 2;
@@ -156,14 +171,18 @@ double evaluate(Graph &g, const Rates &r) {
                 first = s;
             }
         }
-        if (first < 0) return std::numeric_limits<double>::quiet_NaN();  // nothing can run: not a valid schedule
+        if (wake < next) {
+            next = wake;
+            first = -1;
+        }
+        if (next == inf) return std::numeric_limits<double>::quiet_NaN();  // nothing can run: not a valid schedule
         const double dt = next - t;
         for (int s = 0; s < kStreams; ++s) {
             if (cur[s] < 0) continue;
             Node &v = g.nodes[cur[s]];
             if (v.state == 2 && v.kind != kFixed) v.remaining -= rate(v) * dt;
         }
-        {
+        if (first >= 0) {
             Node &v = g.nodes[cur[first]];
             if (v.state == 2 && v.kind != kFixed) v.remaining = 0.0;
         }
@@ -246,14 +265,14 @@ int d2h_commands(const std::vector<double> &sizes, bool all_kernel) {
 
 void build_streamed(Graph &g, const std::vector<int64_t> &numels, int R, int64_t C, bool store, bool staged,
                     bool host_cast, const Rates &r) {
-    const std::vector<Chunk> ch = chunks_of(numels, C);
+    const std::vector<Chunk> ch1 = chunks_of(numels, norm_phase_chunk(C, R, staged));
     int slot_free[2] = {-1, -1}, bin_h2d[kInBufs] = {-1, -1, -1};
-    for (size_t k = 0; k < ch.size(); ++k) {
+    for (size_t k = 0; k < ch1.size(); ++k) {
         const int sl = (int)(k & 1), bi = (int)(k % kInBufs);
-        const double len = (double)ch[k].len;
+        const double len = (double)ch1[k].len;
         int hin = -1;
         if (staged) hin = g.host(2.0 * 2 * R * len, r.host_gbs, r.host_task_us, {bin_h2d[bi]});
-        const int cmds = (staged && ch[k].full) ? 1 : R;
+        const int cmds = (staged && ch1[k].full) ? 1 : R;
         const int h2d = g.add(kCopyS, kH2D, 0, 2.0 * R * len, cmds, {slot_free[sl], hin});
         const int norm = g.add(kCompS, kFixed, kernel_us((2.0 * R + (store ? 4.0 : 0.0)) * len, r.norm_gbs, r), 0, 0,
                                {h2d});
@@ -262,7 +281,8 @@ void build_streamed(Graph &g, const std::vector<int64_t> &numels, int R, int64_t
     }
     const int fin = g.add(kCompS, kFixed, r.launch_us, 0, 0, {});
     const int rb = g.add(kHostS, kFixed, r.sync_us, 0, 0, {fin});
-    const size_t k0 = ch.size();
+    const size_t k0 = ch1.size();
+    const std::vector<Chunk> ch = chunks_of(numels, C);
     int d2h_slot[2] = {-1, -1};
     std::vector<int> d2h_of(ch.size(), -1), drain_of(ch.size(), -1);
     const double in_bpe = 12.0 + (store ? 0.0 : 2.0 * R);

@@ -37,6 +37,7 @@ struct Rates {
     double host_gbs;                    // host memory bandwidth of the host threads' copies
     double host_task_us;                // fixed cost of one hand-off to the host threads
     double host_adam_gbs;               // host AdamW lane alone (bytes read + written)
+    double dep_us;                      // an event recorded on one GPU stream, waited on by the other
 };
 
 enum Schedule { kStreamed = 0, kStreamedStaged = 1, kHostRouteF32 = 2, kHostRouteBf16 = 3 };
@@ -62,6 +63,21 @@ struct RoutePiece {
     int64_t off, len;
 };
 std::vector<RoutePiece> route_pieces(const std::vector<int64_t> &numels, int64_t chunk);
+
+// Streamed mode's first pass moves only the R BF16 gradient arrays.  From
+// pinned memory its chunks fill the staging slot that the update pass lays
+// out for `chunk` elements: the largest multiple of the 65,536-element norm
+// tile whose R arrays fit in (14 + 2R) * chunk bytes (at least `chunk`), so
+// fewer, larger copies.  Staged, they keep `chunk`: the host threads fill a
+// whole chunk's bounce buffer before its copy can start, and a larger first
+// chunk holds the link back for longer.  The norm does not depend on the
+// chunking.
+inline int64_t norm_phase_chunk(int64_t chunk, int R, bool staged) {
+    constexpr int64_t kTile = 65536;
+    if (staged) return chunk;
+    const int64_t c = (14 + 2 * (int64_t)R) * chunk / (2 * (int64_t)R) / kTile * kTile;
+    return c > chunk ? c : chunk;
+}
 
 // store_gbar: streamed mode keeps the mean gradient in device memory
 // between its passes (the default) instead of streaming the gradients twice.

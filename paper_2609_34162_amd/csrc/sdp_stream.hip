@@ -9,6 +9,7 @@
 // gradients for the global norm; phase 2 streams master/m/v through the
 // fused update and back.
 #include "sdp_rt.h"
+#include "sdp_schedule.h"
 
 namespace sdprt {
 
@@ -137,22 +138,30 @@ int drain(sdp_ctx *ctx, int bo, int width) {
 }  // namespace
 
 // Phase 1: gradients in, norm partials (and stored g_bar) out, then finalize.
+// The chunks are sdp_sched::norm_phase_chunk elements long, larger than the
+// update's from pinned memory.  The R gradient arrays lie back to back from
+// the slot's start, each on a 256-byte boundary, so a staged full chunk
+// crosses the link as one run.
 int stream_norm_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R, const Plan &plan,
                       const std::vector<Chunk> &chunks, bool store_gbar, double max_grad_norm, bool used[2]) {
     (void)n_segs;
     for (size_t k = 0; k < chunks.size(); ++k) {
         const Chunk &c = chunks[k];
         const int sl = (int)(k & 1);
-        Slot slot = slot_at(ctx, sl);
+        char *base = ctx->staging + (size_t)sl * ctx->slot_bytes;
+        const size_t stride = (size_t)((c.len + 127) / 128 * 128) * 2;
+        if ((size_t)R * stride > ctx->slot_bytes)
+            return fail(SDP_ERR_CHUNK_TOO_LARGE, "norm pass chunk of %lld elements does not fit the slot", (long long)c.len);
         std::vector<Xfer> xs;
-        for (int32_t r = 0; r < R; ++r)
-            xs.push_back({off_in_slot(ctx, sl, slot.g[r]), (char *)(segs[c.seg].grads[r] + c.off), (size_t)c.len * 2});
+        const uint16_t *gp[SDP_MAX_RANKS];
+        for (int32_t r = 0; r < R; ++r) {
+            xs.push_back({(size_t)r * stride, (char *)(segs[c.seg].grads[r] + c.off), (size_t)c.len * 2});
+            gp[r] = (const uint16_t *)(base + (size_t)r * stride);
+        }
         if (used[sl]) HIP_TRY(hipStreamWaitEvent(ctx->s_copy, ctx->slot_free[sl], 0));
         SDP_TRY(copy_in(ctx, sl, (int)(k % kInBufs), xs, 0));
         HIP_TRY(hipEventRecord(ctx->h2d_done[sl], ctx->s_copy));
         HIP_TRY(hipStreamWaitEvent(ctx->s_comp, ctx->h2d_done[sl], 0));
-        const uint16_t *gp[SDP_MAX_RANKS];
-        for (int32_t r = 0; r < R; ++r) gp[r] = slot.g[r];
         SDP_TRY(norm_launch(ctx, R, gp, c.len, tile_partials(ctx, plan.tile_base[c.seg] + c.off / SDP_NORM_TILE),
                             store_gbar ? ctx->gbar + plan.gbar_base[c.seg] + c.off : nullptr, ctx->s_comp));
         SDP_TRY(poison(ctx, sl));
@@ -250,10 +259,12 @@ int sdp_stream_step(sdp_ctx *ctx, const sdp_segment *host_segs, int32_t n_segs, 
     SDP_TRY(ensure_partials(ctx, plan.tiles));
     if (store) SDP_TRY(ensure_gbar(ctx, plan.gbar_elems));
     const std::vector<Chunk> chunks = make_chunks(host_segs, n_segs, chunk_elems);
+    const std::vector<Chunk> norm_chunks =
+        make_chunks(host_segs, n_segs, sdp_sched::norm_phase_chunk(chunk_elems, R, staged(ctx)));
     SDP_TRY(order_after_last(ctx, ctx->s_copy));
     SDP_TRY(order_after_last(ctx, ctx->s_comp));
     bool used[2] = {false, false};
-    int rc = stream_norm_phase(ctx, host_segs, n_segs, R, plan, chunks, store, hp->max_grad_norm, used);
+    int rc = stream_norm_phase(ctx, host_segs, n_segs, R, plan, norm_chunks, store, hp->max_grad_norm, used);
     NormState st{};
     if (rc == SDP_OK) rc = read_norm(ctx, ctx->s_comp, &st);
     if (rc != SDP_OK) {
@@ -266,7 +277,7 @@ int sdp_stream_step(sdp_ctx *ctx, const sdp_segment *host_segs, int32_t n_segs, 
         SDP_TRY(mark_done(ctx, ctx->s_comp));
         return fail(SDP_ERR_NONFINITE, "gradient norm is not finite (%g); nothing was updated", st.norm);
     }
-    rc = stream_update_phase(ctx, host_segs, R, plan, chunks, store, hp, used, chunks.size());
+    rc = stream_update_phase(ctx, host_segs, R, plan, chunks, store, hp, used, norm_chunks.size());
     int rc2 = sync_streams(ctx);
     // after a failure, results still waiting in bounce buffers belong to this
     // call only: never let a later call move them

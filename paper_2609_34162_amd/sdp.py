@@ -80,7 +80,7 @@ class sdp_kernel_times(ctypes.Structure):
 class sdp_rates(ctypes.Structure):
     _fields_ = [(n, ctypes.c_double) for n in ("h2d_gbs", "d2h_gbs", "both_gbs", "copy_cmd_us", "norm_gbs",
                                               "update_gbs", "launch_us", "sync_us", "host_gbs", "host_task_us",
-                                              "host_adam_gbs")]
+                                              "host_adam_gbs", "dep_us")]
 
 
 class sdp_prediction(ctypes.Structure):

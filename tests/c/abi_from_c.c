@@ -21,7 +21,7 @@ int main(void) {
     printf("sdp_segment %zu %zu %zu\n", sizeof(sdp_segment), offsetof(sdp_segment, n_ranks),
            offsetof(sdp_segment, numel));
     printf("sdp_kernel_times %zu %zu\n", sizeof(sdp_kernel_times), offsetof(sdp_kernel_times, host_adam_elems));
-    printf("sdp_rates %zu %zu\n", sizeof(sdp_rates), offsetof(sdp_rates, host_adam_gbs));
+    printf("sdp_rates %zu %zu\n", sizeof(sdp_rates), offsetof(sdp_rates, dep_us));
     printf("sdp_prediction %zu %zu\n", sizeof(sdp_prediction), offsetof(sdp_prediction, n_chunks));
 
     /* host-only calls */
@@ -44,7 +44,7 @@ int main(void) {
     FAILIF(pb[0] != 0x3ff3, "BF16 of 1.9");
 
     /* the step-time model */
-    sdp_rates r = {50, 40, 90, 0, 5000, 4000, 0, 0, 1e7, 0, 300};
+    sdp_rates r = {50, 40, 90, 0, 5000, 4000, 0, 0, 1e7, 0, 300, 0};
     sdp_prediction pr;
     FAILIF(sdp_predict_step(SDP_SCHED_STREAMED, numels, 2, 2, SDP_NORM_TILE, 0, &r, &pr) != SDP_OK, "predict");
     FAILIF(!(pr.predicted_ms >= pr.bound_ms && pr.n_chunks == 5), "prediction");

@@ -32,6 +32,6 @@ def test_c_program_uses_the_abi(sdp, tmp_path):
                                     sdp.sdp_segment.numel.offset]
     assert lines["sdp_kernel_times"] == [ctypes.sizeof(sdp.sdp_kernel_times),
                                          sdp.sdp_kernel_times.host_adam_elems.offset]
-    assert lines["sdp_rates"] == [ctypes.sizeof(sdp.sdp_rates), sdp.sdp_rates.host_adam_gbs.offset]
+    assert lines["sdp_rates"] == [ctypes.sizeof(sdp.sdp_rates), sdp.sdp_rates.dep_us.offset]
     assert lines["sdp_prediction"] == [ctypes.sizeof(sdp.sdp_prediction), sdp.sdp_prediction.n_chunks.offset]
     assert out.stdout.strip().endswith("ok")

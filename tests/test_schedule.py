@@ -75,11 +75,9 @@ def test_two_chunk_phase_two_recurrence(sdp):
     rt = rates(sdp, both_gbs=90.0, launch_us=1.0)
     got = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, TILE, 0, rt).predicted_ms * 1e3
     L = TILE
-    g_in = us(2 * R * L, 50.0)
-    norm = us((2 * R + 4) * L, 5000.0) + 1.0
-    # phase one: copies back to back, each norm after its copy
-    n0 = g_in + norm
-    n1 = max(2 * g_in, n0) + norm
+    # phase one moves only the gradients, in chunks that fill the slot laid
+    # out for L elements: floor((14 + 2R) / 2R) = 4 tiles here, so one chunk
+    n1 = us(2 * R * N, 50.0) + us((2 * R + 4) * N, 5000.0) + 1.0
     t1 = n1 + 1.0  # finalize; read-back costs nothing here
     a = us(12 * L, 50.0)
     u = us(30 * L, 4000.0) + 1.0
@@ -87,6 +85,26 @@ def test_two_chunk_phase_two_recurrence(sdp):
     # in_1 and out_0 overlap but both_gbs = h2d + d2h, so neither slows down
     t2 = max(2 * a, a + u + d) + u + d
     assert math.isclose(got, t1 + t2, rel_tol=1e-12)
+
+
+def test_norm_pass_chunks_fill_the_slot(sdp):
+    """From pinned memory, phase one moves only the R gradient arrays, in
+    chunks that fill the slot the update pass lays out for the call's chunk
+    C: the largest tile multiple of (14 + 2R) C / 2R elements.  With the link and the kernels
+    free, a step costs its copy commands: R per phase-one chunk, then three
+    per update chunk on the copy stream, and the last chunk's copy-kernel
+    launch."""
+    fast = dict(h2d_gbs=1e12, d2h_gbs=1e12, both_gbs=2e12, norm_gbs=1e12, update_gbs=1e12, copy_cmd_us=5.0)
+    # (R, C, N, phase-one chunks): 2.75 C -> 2 tiles; 8 C; 3.75 C -> 3 tiles
+    for R, C, N, n1 in ((4, TILE, 8 * TILE, 4), (1, TILE, 16 * TILE, 2), (8, 2 * TILE, 8 * TILE, 3)):
+        n2 = N // C
+        got = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, C, 0, rates(sdp, **fast))
+        assert got.n_chunks == n2
+        assert math.isclose(got.predicted_ms * 1e3, (n1 * R + 3 * n2 + 1) * 5.0, rel_tol=1e-4), (R, C)
+    # staged, phase one keeps the update's chunk, and a full chunk crosses as
+    # one run each way: 8 + 8 copies in and the last chunk's launch out
+    st = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED_STAGED, [8 * TILE], 4, TILE, 0, rates(sdp, **fast))
+    assert math.isclose(st.predicted_ms * 1e3, 17 * 5.0, rel_tol=1e-4)
 
 
 def test_link_contention_slows_overlapping_copies(sdp):
@@ -176,7 +194,8 @@ def test_streamed_host_cast_many_chunks(sdp):
 
 
 def test_staged_equals_plain_when_host_lanes_are_free(sdp):
-    N, R = 10 * TILE + 3, 4
+    # R = 16: (14 + 2R) C / 2R rounds down to C, so both modes chunk phase one alike
+    N, R = 10 * TILE + 3, 16
     rt = rates(sdp, host_gbs=1e9, host_task_us=0.0)
     a = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, 2 * TILE, 0, rt)
     b = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED_STAGED, [N], R, 2 * TILE, 0, rt)
