@@ -208,6 +208,9 @@ SDP_API int sdp_agg_adam_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_s
  * Phase 1 copies each chunk's R gradients host-to-device on the copy
  * stream and runs the norm pass on the compute stream, alternating two
  * staging slots ordered by events; then the norm is finalized and read back.
+ * From pinned memory its chunks fill a slot: the largest multiple of
+ * SDP_NORM_TILE whose R BF16 arrays fit in (14 + 2R) * chunk_elems bytes
+ * (staged, chunk_elems).
  * Phase 2 copies master/m/v of each chunk in, runs the fused update, and
  * copies master/m/v and the BF16 parameters back to the same host locations
  * on the compute stream, again double-buffered.  Device-to-host copies of up
@@ -274,7 +277,8 @@ SDP_API int sdp_ctx_host_threads(sdp_ctx *ctx, int32_t *threads_out);
 /* The global norm of the mean gradient alone (the first pass and finalize of
  * either mode; device_resident selects device or pinned-host buffers; only
  * grads, n_ranks and numel of each segment are read).  Blocks; chunk_elems
- * is used in streamed mode only.  Stores the norm even if it is not finite
+ * is used in streamed mode only, where the pass runs in chunks as phase 1 of
+ * sdp_stream_step does.  Stores the norm even if it is not finite
  * and then returns SDP_ERR_NONFINITE. */
 SDP_API int sdp_grad_norm(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs,
                   int device_resident, int64_t chunk_elems, void *stream,
