@@ -85,6 +85,14 @@ def test_two_chunk_phase_two_recurrence(sdp):
     # in_1 and out_0 overlap but both_gbs = h2d + d2h, so neither slows down
     t2 = max(2 * a, a + u + d) + u + d
     assert math.isclose(got, t1 + t2, rel_tol=1e-12)
+    # an event between the copy and the compute stream takes effect dep_us
+    # later: each kernel after its copy; host edges (the read-back) do not pay it
+    e = 23.0
+    got_e = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, TILE, 0,
+                                 rates(sdp, both_gbs=90.0, launch_us=1.0, dep_us=e)).predicted_ms * 1e3
+    t1e = n1 + e + 1.0
+    t2e = max(2 * a + e, a + e + u + d) + u + d
+    assert math.isclose(got_e, t1e + t2e, rel_tol=1e-12)
 
 
 def test_norm_pass_chunks_fill_the_slot(sdp):
@@ -232,6 +240,7 @@ def test_model_argument_errors(sdp):
     assert L.sdp_predict_step(0, arr, 1, 2, TILE, 0, rates(sdp, h2d_gbs=0.0), out) == sdp.SDP_ERR_INVALID_ARGUMENT
     assert L.sdp_predict_step(0, arr, 1, 2, TILE, 0, rates(sdp, sync_us=float("nan")), out) == \
         sdp.SDP_ERR_INVALID_ARGUMENT
+    assert L.sdp_predict_step(0, arr, 1, 2, TILE, 0, rates(sdp, dep_us=-1.0), out) == sdp.SDP_ERR_INVALID_ARGUMENT
     big = (ctypes.c_int64 * 1)(TILE << 23)
     assert L.sdp_predict_step(0, big, 1, 2, TILE, 0, rt, out) == sdp.SDP_ERR_INVALID_ARGUMENT
     assert "too many" in sdp.sdp_last_error()
