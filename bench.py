@@ -36,6 +36,8 @@ JSON line also carries:
                    chunk sizes of 4-128 MiB per FP32 array beside the
                    library's step-time model fed with rates measured in
                    the same run, and the chunk each would pick;
+  tuned (inside streamed) -- the streamed step at the chunk the model picks
+                   (sdp_tune_chunk), from the sweep;
   host_route    -- the paper's own datapath for the same Qwen3-14B layer:
                    gradients in HBM, states in pageable host memory, the mean
                    gradient copied down (FP32 or BF16) and AdamW on this
@@ -489,6 +491,11 @@ def stream_leg(args, torch, np, synth, sdp, dres):
             finally:
                 sdp.sdp_ctx_destroy(cctx)
         out["chunk_sweep"] = chunk_sweep(sdp, sdp.SDP_SCHED_STREAMED, [N], R, rates, run_at)
+        # the step at the chunk the library's own tuning picks (sdp_tune_chunk)
+        sw = out["chunk_sweep"]
+        out["tuned"] = dict(chunk_elems=sw["model_pick"], ms_per_step=sw["measured_at_model_pick_ms"],
+                            params_per_s=N / (sw["measured_at_model_pick_ms"] / 1e3),
+                            frac_of_link_bound=t_link * 1e3 / sw["measured_at_model_pick_ms"])
         # the same step with the states in pageable memory, through the staged mode
         log("streamed leg: staged mode on pageable copies of the same state")
         # the staged context pins its bounce buffers before the pageable state exists
