@@ -236,7 +236,12 @@ std::vector<RoutePiece> route_pieces(const std::vector<int64_t> &numels, int64_t
             const int64_t len = std::min(size, numels[s] - off);
             out.push_back({(int32_t)s, off, len});
             off += len;
-            if (size < chunk) size = std::min(chunk, (size * 6 / 5 + kRampAlign - 1) / kRampAlign * kRampAlign);
+            if (size < chunk) {
+                // size * 6/5 rounded down, then up to a whole kRampAlign; chunk
+                // is a multiple of kRampAlign, so a size within one of it is chunk
+                const int64_t grown = size + size / 5;
+                size = grown > chunk - kRampAlign ? chunk : (grown + kRampAlign - 1) / kRampAlign * kRampAlign;
+            }
         }
     }
     return out;

@@ -74,7 +74,7 @@ std::vector<RoutePiece> route_pieces(const std::vector<int64_t> &numels, int64_t
 // chunking.
 inline int64_t norm_phase_chunk(int64_t chunk, int R, bool staged) {
     constexpr int64_t kTile = 65536;
-    if (staged) return chunk;
+    if (staged || chunk > INT64_MAX / (14 + 2 * (int64_t)R)) return chunk;
     const int64_t c = (14 + 2 * (int64_t)R) * chunk / (2 * (int64_t)R) / kTile * kTile;
     return c > chunk ? c : chunk;
 }

@@ -241,6 +241,14 @@ def test_model_argument_errors(sdp):
     assert L.sdp_predict_step(0, arr, 1, 2, TILE, 0, rates(sdp, sync_us=float("nan")), out) == \
         sdp.SDP_ERR_INVALID_ARGUMENT
     assert L.sdp_predict_step(0, arr, 1, 2, TILE, 0, rates(sdp, dep_us=-1.0), out) == sdp.SDP_ERR_INVALID_ARGUMENT
+    # host route pieces with a chunk near the int64 limit: the ramp still ends at the segment
+    top = (2 ** 63 - 1) // TILE * TILE
+    ok = sdp.sdp_predict_step(sdp.SDP_SCHED_HOST_ROUTE_F32, [TILE << 46], 2, top, 0, rt)
+    assert math.isfinite(ok.predicted_ms) and ok.predicted_ms > 0
+    # a chunk far beyond any slot: one chunk, as any chunk of at least the segment
+    huge = sdp.sdp_predict_step(0, [TILE], 16, TILE << 45, 0, rt)
+    assert math.isclose(huge.predicted_ms, sdp.sdp_predict_step(0, [TILE], 16, TILE, 0, rt).predicted_ms,
+                        rel_tol=1e-12)
     big = (ctypes.c_int64 * 1)(TILE << 23)
     assert L.sdp_predict_step(0, big, 1, 2, TILE, 0, rt, out) == sdp.SDP_ERR_INVALID_ARGUMENT
     assert "too many" in sdp.sdp_last_error()
