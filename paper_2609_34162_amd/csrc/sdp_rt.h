@@ -249,7 +249,7 @@ struct sdp_ctx {
     sdprt::HostPool *copier = nullptr;
     int staged_copy_threads = 0;   // staged update pass: host copy threads while the DMA runs
     int64_t d2h_kernel_max = 0;    // device-to-host copies up to this many bytes run as k_copy_batch
-    int d2h_kernel_blocks = 0;     // blocks per copy of such a launch
+    int d2h_kernel_blocks = 0;     // blocks per copy of such a launch (0: kD2HLaunchBlocks spread over the copies)
     double *partials = nullptr;
     int64_t partials_cap = 0;
     float *gbar = nullptr;
@@ -356,12 +356,16 @@ constexpr int kStagedCopyThreads = 4;
 int default_staged_copy_threads();
 
 // Streamed engine: device-to-host copies of at most kD2HKernelMaxBytes run as
-// the library's own copy kernel, kD2HKernelBlocks blocks per copy.  The
-// runtime moves copies of a few MiB with DMA copy commands that measured
-// 10-45 GB/s beside host-to-device traffic; larger ones it moves with copy
-// kernels that reach the link's rate.
+// the library's own copy kernel.  The runtime moves copies of a few MiB with
+// DMA copy commands that measured 10-45 GB/s beside host-to-device traffic;
+// larger ones it moves with copy kernels that reach the link's rate.  A
+// launch spreads kD2HLaunchBlocks blocks over its copies, at least
+// kD2HMinBlocksPerCopy each: on the Qwen3-14B layer about 32 blocks writing
+// to host memory at once were fastest (8 per copy for four copies, 32 for
+// one), and 64 per copy cost up to 1% of the step.
 constexpr int64_t kD2HKernelMaxBytes = 64ll << 20;
-constexpr int kD2HKernelBlocks = 64;
+constexpr int kD2HLaunchBlocks = 32;
+constexpr int kD2HMinBlocksPerCopy = 8;
 // Device -> pinned host copies (dst <- src, bytes) enqueued on stream st,
 // through the copy kernel where they qualify (sdp_stream.hip).
 int d2h_copies(sdp_ctx *ctx, const std::vector<std::pair<char *, const char *>> &ends,

@@ -718,7 +718,7 @@ int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems, int32_t m
                             ? std::numeric_limits<int64_t>::max()
                             : kD2HKernelMaxBytes;
     if (const char *env = std::getenv("SDP_D2H_KERNEL_MAX_BYTES")) c->d2h_kernel_max = std::atoll(env);
-    c->d2h_kernel_blocks = kD2HKernelBlocks;
+    c->d2h_kernel_blocks = 0;
     if (const char *env = std::getenv("SDP_D2H_KERNEL_BLOCKS"))
         c->d2h_kernel_blocks = std::max(1, std::min(65535, std::atoi(env)));
     if (max_chunk_elems > 0) {

@@ -42,7 +42,11 @@ int d2h_copies(sdp_ctx *ctx, const std::vector<std::pair<char *, const char *>> 
             HIP_TRY(hipMemcpyAsync(ends[k].first, ends[k].second, bytes[k], hipMemcpyDeviceToHost, st));
         }
     }
-    if (b.n > 0) HIP_TRY(sdp::launch_copy_batch(b, ctx->d2h_kernel_blocks, st));
+    if (b.n > 0) {
+        const int per_copy = ctx->d2h_kernel_blocks > 0 ? ctx->d2h_kernel_blocks
+                                                          : std::max(kD2HMinBlocksPerCopy, kD2HLaunchBlocks / b.n);
+        HIP_TRY(sdp::launch_copy_batch(b, per_copy, st));
+    }
     return SDP_OK;
 }
 
