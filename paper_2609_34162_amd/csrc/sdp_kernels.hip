@@ -375,7 +375,12 @@ __global__ __launch_bounds__(kUpdateThreads) void k_update(UpdateArgs a) {
         } else {
             uint2 raw[R];
 #pragma unroll
-            for (int r = 0; r < R; ++r) raw[r] = *reinterpret_cast<const uint2 *>(a.g[r] + e0);
+            // read once: non-temporal, as in the norm pass
+            for (int r = 0; r < R; ++r) {
+                uint32_t w[2];
+                load_stream_v<4>(a.g[r] + e0, w);
+                raw[r] = make_uint2(w[0], w[1]);
+            }
             mean4<R>(raw, g);
         }
         float4 *p4 = reinterpret_cast<float4 *>(P + e0);
@@ -428,8 +433,9 @@ __global__ __launch_bounds__(kUpdateThreads) void k_update_pattern(UpdateArgs a)
         uint32_t x = 0;
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-            const uint2 w = *reinterpret_cast<const uint2 *>(a.g[r] + e0);
-            x ^= w.x ^ w.y;
+            uint32_t w[2];
+            load_stream_v<4>(a.g[r] + e0, w);
+            x ^= w[0] ^ w[1];
         }
         const float gx = __uint_as_float((x & 0x007fffffu) | 0x3f800000u);
         float4 *p4 = reinterpret_cast<float4 *>(P + e0);
