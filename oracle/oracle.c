@@ -7,10 +7,10 @@
  *
  * What it computes, per call over a list of flat layer segments that all have
  * R gradient buffers:
- *   1. g_bar[i] = fp32( (sum over ranks r of bf16 G_r[i], in FP64) / R )
- *      -- the rank gradients are summed and averaged into one gradient
- *      (Design, shared host state and communication routes: gradient return
- *      by GPU reduction).
+ *   1. g_bar[i] = fp32( (exact sum over ranks r of bf16 G_r[i]) / R ),
+ *      rounded once -- the rank gradients are summed and averaged into one
+ *      gradient (Design, shared host state and communication routes:
+ *      gradient return by GPU reduction).
  *   2. S = sum over every element of every segment of g_bar[i]^2, the
  *      exact sum rounded once to FP64; norm = sqrt(S).  The paper never
  *      mentions clipping; the global L2 norm of the mean gradient is taken
@@ -107,15 +107,170 @@ void orc_bf16_array(const float *x, uint16_t *out, int64_t n)
         out[i] = orc_bf16_from_f32(x[i]);
 }
 
-/* Step 1: mean over ranks of one element's gradients, rounded once to FP32.
- * Ranks are added in rank order in FP64 (exact for BF16 inputs whose
- * magnitudes span less than about 2^45). */
+/* Step 1: the mean over ranks of one element's gradients, rounded once to
+ * FP32: g_bar = fp32(S / R), where S is the exact sum of the R BF16 values
+ * (Design, gradient return by GPU reduction: the reduction sums the ranks'
+ * gradients and averages them).  A sum that is exactly zero gives +0.
+ * If any value is an infinity or a NaN the mean is the IEEE result of the
+ * FP64 sum in rank order divided by R (NaN or an infinity; the norm is then
+ * not finite and no state changes).
+ *
+ * Two routes, both giving that one rounding:
+ *  - when R is a power of two and every addition of the FP64 sum in rank
+ *    order is exact (each TwoSum error term is zero), S is that FP64 sum and
+ *    S / R is exact in FP64, so its conversion to FP32 is the only rounding;
+ *  - otherwise S is formed exactly as a fixed-point integer, divided by R
+ *    with a remainder, and the quotient is rounded to FP32 by hand. */
+
+/* Unsigned fixed-point integer of MEAN_LIMBS little-endian 64-bit limbs whose
+ * bit 0 has weight 2^MEAN_E0.  A BF16 value is M * 2^(k) with an integer
+ * M < 2^8 and k >= -133; at most ORC_MAX_RANKS (2^6) of them, each below
+ * 2^128, sum below 2^134, so 134 - MEAN_E0 = 287 bits suffice.  The 20 bits
+ * below 2^-133 hold the quotient's bits down to 2^-153, under the FP32
+ * rounding position of the smallest subnormal (2^-149). */
+#define MEAN_E0 (-153)
+#define MEAN_LIMBS 5
+typedef struct {
+    uint64_t w[MEAN_LIMBS];
+} orc_fix;
+
+static void fix_add_at(orc_fix *a, int k, uint64_t v)
+{
+    while (v != 0 && k < MEAN_LIMBS) {
+        uint64_t old = a->w[k];
+        a->w[k] = old + v;
+        v = a->w[k] < old; /* carry */
+        ++k;
+    }
+}
+
+/* a += m * 2^b (b >= 0, m < 2^8). */
+static void fix_add_shifted(orc_fix *a, uint64_t m, int b)
+{
+    int k = b >> 6, s = b & 63;
+    fix_add_at(a, k, m << s);
+    if (s > 56)
+        fix_add_at(a, k + 1, m >> (64 - s));
+}
+
+static int fix_cmp(const orc_fix *a, const orc_fix *b)
+{
+    for (int k = MEAN_LIMBS - 1; k >= 0; --k)
+        if (a->w[k] != b->w[k])
+            return a->w[k] < b->w[k] ? -1 : 1;
+    return 0;
+}
+
+/* a -= b, for a >= b. */
+static void fix_sub(orc_fix *a, const orc_fix *b)
+{
+    uint64_t borrow = 0;
+    for (int k = 0; k < MEAN_LIMBS; ++k) {
+        uint64_t x = a->w[k], y = b->w[k];
+        uint64_t d = x - y - borrow;
+        borrow = (x < y) || (x == y && borrow);
+        a->w[k] = d;
+    }
+}
+
+/* a = floor(a / d); returns a mod d (schoolbook division by one word). */
+static uint64_t fix_div_small(orc_fix *a, uint32_t d)
+{
+    unsigned __int128 rem = 0;
+    for (int k = MEAN_LIMBS - 1; k >= 0; --k) {
+        unsigned __int128 cur = (rem << 64) | a->w[k];
+        a->w[k] = (uint64_t)(cur / d);
+        rem = cur % d;
+    }
+    return (uint64_t)rem;
+}
+
+static int fix_msb(const orc_fix *a) /* -1 for zero */
+{
+    for (int k = MEAN_LIMBS - 1; k >= 0; --k)
+        if (a->w[k])
+            return k * 64 + 63 - __builtin_clzll(a->w[k]);
+    return -1;
+}
+
+static int fix_bit(const orc_fix *a, int pos)
+{
+    return pos >= 0 ? (int)((a->w[pos >> 6] >> (pos & 63)) & 1u) : 0;
+}
+
+static int fix_any_below(const orc_fix *a, int pos) /* any bit at index < pos */
+{
+    if (pos <= 0)
+        return 0;
+    int k = pos >> 6, s = pos & 63;
+    for (int j = 0; j < k; ++j)
+        if (a->w[j])
+            return 1;
+    return s ? (a->w[k] & ((1ull << s) - 1)) != 0 : 0;
+}
+
+/* fp32(S / R) for finite BF16 values, through the exact integer S. */
+static float mean_exact(const uint16_t *const *grads, int32_t R, int64_t i)
+{
+    orc_fix pos, neg;
+    memset(&pos, 0, sizeof pos);
+    memset(&neg, 0, sizeof neg);
+    for (int32_t r = 0; r < R; ++r) {
+        uint16_t b = grads[r][i];
+        uint32_t e = (b >> 7) & 0xffu, f = b & 0x7fu;
+        /* value = M * 2^(k): normal M = 1.f (8 bits), k = e - 127 - 7;
+         * subnormal M = 0.f, k = 1 - 127 - 7 */
+        uint64_t M = e ? (0x80u | f) : f;
+        int k = (e ? (int)e : 1) - 134;
+        fix_add_shifted((b & 0x8000u) ? &neg : &pos, M, k - MEAN_E0);
+    }
+    int sign = 0;
+    if (fix_cmp(&pos, &neg) >= 0) {
+        fix_sub(&pos, &neg);
+    } else {
+        fix_sub(&neg, &pos);
+        pos = neg;
+        sign = 1;
+    }
+    uint64_t rem = fix_div_small(&pos, (uint32_t)R);
+    int msb = fix_msb(&pos);
+    if (msb < 0)
+        return 0.0f; /* S = 0 (a nonzero S is at least 2^-133, its quotient at least 2^-139) */
+    /* keep 24 significant bits, or fewer below 2^-126, where the FP32 grid
+     * is fixed at 2^-149 */
+    int lsb = msb + MEAN_E0 >= -126 ? msb - 23 : -149 - MEAN_E0;
+    uint64_t mant = 0;
+    for (int q = msb; q >= lsb; --q)
+        mant = (mant << 1) | (uint64_t)fix_bit(&pos, q);
+    int round = fix_bit(&pos, lsb - 1);
+    int sticky = rem != 0 || fix_any_below(&pos, lsb - 1);
+    if (round && (sticky || (mant & 1u)))
+        ++mant; /* may become 2^24 (or 2^23 below 2^-126): still exact */
+    double mag = ldexp((double)mant, lsb + MEAN_E0);
+    return (float)(sign ? -mag : mag); /* exact: mag is an FP32 value */
+}
+
 float orc_mean_grad(const uint16_t *const *grads, int32_t R, int64_t i)
 {
     double s = 0.0;
-    for (int32_t r = 0; r < R; ++r)
-        s += (double)orc_f32_from_bf16(grads[r][i]);
-    return (float)(s / (double)R);
+    int exact = 1, finite = 1;
+    for (int32_t r = 0; r < R; ++r) {
+        double x = (double)orc_f32_from_bf16(grads[r][i]);
+        if (!isfinite(x))
+            finite = 0;
+        /* TwoSum (Knuth): t + err = s + x exactly */
+        double t = s + x;
+        double xv = t - s;
+        double err = (s - (t - xv)) + (x - xv);
+        if (err != 0.0)
+            exact = 0;
+        s = t;
+    }
+    if (!finite)
+        return (float)(s / (double)R);
+    if (exact && (R & (R - 1)) == 0)
+        return (float)(s / (double)R);
+    return mean_exact(grads, R, i);
 }
 
 void orc_mean_grads(const uint16_t *const *grads, int32_t R, int64_t n, float *out)

@@ -107,13 +107,48 @@ def pin_mean_closed_forms(lib):
     assert np.all(oracle.mean_grads(gs, lib=lib) == np.float32(4.0 / 3.0))
 
 
-def pin_mean_vs_numpy(lib):
-    n = 5000
+def pin_mean_vs_fraction(lib):
+    """Random BF16 gradients: the oracle's mean is the exact rational mean
+    rounded once to FP32 (fractions.Fraction)."""
+    import mean_cases
+    n = 1500
     for R in (1, 2, 3, 4, 7, 8):
-        gs = rand_grads(n, R, seed=R)
-        vals = np.stack([bf16_value(g).astype(np.float64) for g in gs])
-        want = (vals.sum(axis=0) / R).astype(np.float32)
-        assert np.array_equal(oracle.mean_grads(gs, lib=lib), want), R
+        gs = rand_grads(n, R, seed=R, outlier_p=0.01)
+        want = mean_cases.exact_means(np.stack(gs))
+        got = oracle.mean_grads(gs, lib=lib)
+        assert np.array_equal(got.view(np.uint32), want.view(np.uint32)), R
+
+
+def pin_mean_exact_quotient(lib):
+    """Rank sets built to make the single rounding of S / R hard -- quotients
+    on, or a tiny value away from, FP32 midpoints, sums whose FP64 evaluation
+    in rank order is inexact (magnitudes spanning far more than 2^45),
+    every exponent, and subnormal quotients whose rounding only the division's
+    remainder decides -- against fractions.Fraction, bit for bit.  The same
+    sets must also show that an FP64 sum divided in FP64 and rounded again
+    is not the same thing (else they would not test the rounding)."""
+    import mean_cases
+    double_rounding_misses = 0
+    remainder_decides = 0
+    for R in (1, 2, 3, 4, 5, 7, 8, 11, 13, 15, 16):
+        sets = [mean_cases.wide_span(R, 100, seed=R)]
+        if R >= 3:
+            sets.append(mean_cases.near_midpoint(R, 200, seed=100 + R))
+        sub = mean_cases.subnormal_remainder(R)
+        if R in (11, 13, 15):
+            assert sub.shape[1] > 0
+        remainder_decides += mean_cases.remainder_decides(sub)
+        sets.append(sub)
+        ranks = np.concatenate(sets, axis=1)
+        want = mean_cases.exact_means(ranks)
+        got = oracle.mean_grads([ranks[r].copy() for r in range(R)], lib=lib)
+        bad = np.flatnonzero(got.view(np.uint32) != want.view(np.uint32))
+        assert bad.size == 0, (R, [(ranks[:, i].tolist(), float(got[i]), float(want[i])) for i in bad[:3]])
+        if R in (3, 5, 7, 13):
+            naive = mean_cases.rank_order_f64_mean(ranks)
+            double_rounding_misses += int(np.count_nonzero(naive.view(np.uint32) != want.view(np.uint32)))
+    assert double_rounding_misses > 0
+    assert remainder_decides > 0
 
 
 # ---------------------------------------------------------------------------

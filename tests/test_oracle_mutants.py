@@ -26,11 +26,24 @@ MUTATIONS = {
     "no_bias_correction_2": ("double v_hat = v1 / bc2;", "double v_hat = v1;"),
     "step_sign": ("*po = p1 - hp->lr", "*po = p1 + hp->lr"),
     "bias_uses_step_minus_1": ("pow(hp->beta1, (double)hp->step)", "pow(hp->beta1, (double)(hp->step + 1))"),
-    "mean_not_divided": ("return (float)(s / (double)R);", "return (float)s;"),
-    "mean_rank0_only": ("s += (double)orc_f32_from_bf16(grads[r][i]);",
-                        "s += (double)orc_f32_from_bf16(grads[0][i]);"),
-    "mean_fp32_sum": ("double s = 0.0;\n    for (int32_t r = 0; r < R; ++r)\n        s += (double)orc_f32_from_bf16(grads[r][i]);",
-                      "float s = 0.0f;\n    for (int32_t r = 0; r < R; ++r)\n        s += orc_f32_from_bf16(grads[r][i]);"),
+    "mean_not_divided": ("if (exact && (R & (R - 1)) == 0)\n        return (float)(s / (double)R);",
+                         "if (exact && (R & (R - 1)) == 0)\n        return (float)s;"),
+    "mean_rank0_only": ("double x = (double)orc_f32_from_bf16(grads[r][i]);",
+                        "double x = (double)orc_f32_from_bf16(grads[0][i]);"),
+    "mean_fp32_sum": ("        s = t;\n", "        s = (float)t;\n"),
+    "mean_double_rounded": ("if (exact && (R & (R - 1)) == 0)", "if (1)"),
+    "mean_inexact_sum_trusted": ("if (exact && (R & (R - 1)) == 0)", "if ((R & (R - 1)) == 0)"),
+    "mean_exact_not_divided": ("fix_div_small(&pos, (uint32_t)R);", "fix_div_small(&pos, 1u);"),
+    "mean_exact_no_remainder": ("int sticky = rem != 0 || fix_any_below(&pos, lsb - 1);",
+                                "int sticky = fix_any_below(&pos, lsb - 1);"),
+    "mean_exact_truncates": ("        ++mant; /* may become 2^24", "        (void)0; /* may become 2^24"),
+    "mean_exact_sign_lost": ("return (float)(sign ? -mag : mag);", "return (float)mag;"),
+    "mean_exact_negatives_ignored": ("fix_add_shifted((b & 0x8000u) ? &neg : &pos, M, k - MEAN_E0);",
+                                     "fix_add_shifted(&pos, M, k - MEAN_E0);"),
+    "mean_exact_subnormal_bit": ("uint64_t M = e ? (0x80u | f) : f;", "uint64_t M = 0x80u | f;"),
+    "mean_exact_high_part_dropped": ("        fix_add_at(a, k + 1, m >> (64 - s));", "        (void)0;"),
+    "mean_exact_subnormal_grid": ("-149 - MEAN_E0", "-150 - MEAN_E0"),
+    "mean_exact_borrow_dropped": ("borrow = (x < y) || (x == y && borrow);", "borrow = (x < y);"),
     "norm_no_sqrt": ("    return sqrt(acc_round(&total));", "    return acc_round(&total);"),
     "norm_first_segment_only": ("for (int32_t s = 0; s < n_segs; ++s) {\n        const uint16_t *const *g = segs[s].grads;",
                                 "for (int32_t s = 0; s < 1; ++s) {\n        const uint16_t *const *g = segs[s].grads;"),
@@ -66,7 +79,7 @@ ORDER = ["pin_bf16_special_values", "pin_mean_closed_forms", "pin_norm_constant"
          "pin_exact_sum_ties_and_carries", "pin_exact_sum_vs_fsum",
          "pin_clip_coef", "pin_first_step_sign", "pin_zero_gradient", "pin_sign_descent",
          "pin_lr_zero", "pin_identical_ranks", "pin_clip_noop", "pin_nonfinite",
-         "pin_param_is_bf16_of_master", "pin_mean_vs_numpy", "pin_norm_vs_torch",
+         "pin_param_is_bf16_of_master", "pin_mean_vs_fraction", "pin_mean_exact_quotient", "pin_norm_vs_torch",
          "pin_adamw_f64_vs_torch", "pin_bf16_random_vs_torch", "pin_bf16_gradient_route",
          "pin_step_vs_torch",
          "pin_brute_force"]
