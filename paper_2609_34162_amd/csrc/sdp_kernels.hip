@@ -9,7 +9,7 @@
 // weights and moments, fed by the gradient averaged over the ranks, and BF16
 // compute weights; the formulas are AdamW with decoupled decay and
 // Kingma-Ba bias correction):
-//   g_bar = fp32(sum_r bf16 G_r, in FP64 in rank order, / R)
+//   g_bar = fp32(S / R), S the exact sum of the R BF16 values, rounded once
 //   g     = g_bar * c                               (c from the global norm)
 //   p1 = p - lr*wd*p ; m' = b1 m + (1-b1) g ; v' = b2 v + (1-b2) g^2
 //   p' = p1 - lr/(1-b1^t) * m' / (sqrt(v'/(1-b2^t)) + eps)
@@ -49,28 +49,219 @@ __device__ __forceinline__ float mean_of(double s) {
     }
 }
 
-// g_bar of the 8 elements held as BF16 in raw[r] (one dwordx4 per rank).
+// ---------------------------------------------------------------------------
+// Mean gradient g_bar = fp32(S / R): S, the exact sum of the R BF16 values,
+// divided by R and rounded once.
+//
+// Fast route.  Summed in FP64 (from +0, in rank order), R BF16 values give S
+// exactly when their magnitudes are close enough (span_exact below); then
+// fp32(fp64(S / R)) is the single rounding of S / R.  Proof: the two
+// roundings differ only if fp64(S / R) is an FP32 midpoint m with S / R != m.
+// With 2^E <= S / R < 2^(E+1) that needs |S - R m| <= R 2^(E-53).  S - R m is
+// a nonzero multiple of the smaller of S's last-bit weight 2^f and 2^(E-24)
+// (the grid of R m); 2^(E-24) exceeds R 2^(E-53) for every R < 2^29, so
+// 2^f <= R 2^(E-53), and S / 2^f >= R 2^E / (R 2^(E-53)) = 2^53: S would not
+// be an FP64 number.  (Below 2^-126 the FP32 grid is 2^-150 and S's last bit
+// weighs at least 2^-133, so the same holds.)
+//
+// Wide route (magnitudes spread over more binades, which the workloads'
+// gradients practically never reach): S is summed exactly as a fixed-point
+// integer, rounded to odd at 53 bits (truncated, last bit forced to 1 if
+// anything was dropped), and that FP64 value takes the fast route's last two
+// steps.  Rounding to odd keeps S on the same side of every number of at most
+// 52 significant bits; R times an FP32 value or midpoint has at most 30, so
+// fp32 of the quotient is unchanged.
+
+// A lane's values sum exactly in FP64, in any order, when the binade of the
+// largest magnitude exceeds that of the smallest nonzero one by at most
+// 45 - ceil(log2 R): every value is then a multiple of the smallest one's
+// last-bit weight u = 2^(max(e_min, 1) - 134), and every partial sum is
+// below R 2^(e_max - 126) <= 2^53 u.
 template <int R>
-__device__ __forceinline__ void mean8(const uint4 (&raw)[R], float (&g)[kVec]) {
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-        double s_lo = 0.0, s_hi = 0.0;
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            uint32_t word = (&raw[r].x)[w];
-            s_lo += (double)bf16_lo(word);
-            s_hi += (double)bf16_hi(word);
-        }
-        g[2 * w] = mean_of<R>(s_lo);
-        g[2 * w + 1] = mean_of<R>(s_hi);
-    }
+constexpr int kExactSpan = 45 - (R <= 1 ? 0 : R <= 2 ? 1 : R <= 4 ? 2 : R <= 8 ? 3 : 4);
+
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+// Largest magnitude and smallest nonzero magnitude (minus one) of BF16
+// values packed two per word; a zero wraps to 0xffff and so never counts as
+// the smallest.
+struct Span {
+    u16x2 top, low;
+};
+
+__device__ __forceinline__ Span span_init() {
+    Span s;
+    s.top = (u16x2)(0);
+    s.low = (u16x2)(0xffff);
+    return s;
+}
+
+__device__ __forceinline__ void span_add(Span &s, uint32_t word) {
+    const u16x2 m = __builtin_bit_cast(u16x2, word & 0x7fff7fffu);
+    s.top = __builtin_elementwise_max(s.top, m);
+    s.low = __builtin_elementwise_min(s.low, m - (u16x2)(1));
 }
 
 template <int R>
-__device__ __forceinline__ float mean1(const uint16_t *const *g, int64_t i) {
-    double s = 0.0;
+__device__ __forceinline__ bool span_exact(const Span &s) {
+    const uint32_t top = s.top.x > s.top.y ? s.top.x : s.top.y;
+    const uint32_t low = (uint16_t)((s.low.x < s.low.y ? s.low.x : s.low.y) + 1);  // 0: no nonzero value
+    const int e_top = (int)(top >> 7);
+    const int e_low = (int)(low >> 7) > 1 ? (int)(low >> 7) : 1;
+    return e_top - e_low <= kExactSpan<R>;
+}
+
+// The wide route's exact sum: S in two's complement in ten 32-bit words,
+// bit 0 weighing 2^-133 (the smallest BF16 step).  16 values below 2^128 sum
+// below 2^132, so 266 bits with the sign suffice.  The ranks are added one at
+// a time, each as a piece of at most 40 bits carried (or borrowed) through
+// the words above it: a short loop over few registers.
+constexpr int kWideWords = 10;
+
+__device__ __forceinline__ void wide_add(uint32_t (&w)[kWideWords], uint32_t bf16) {
+    const uint32_t e = (bf16 >> 7) & 0xffu, f = bf16 & 0x7fu;
+    const uint32_t mant = e ? (0x80u | f) : f;  // value = mant * 2^(pos - 133)
+    const uint32_t pos = (e ? e : 1u) - 1u;
+    const uint64_t piece = (uint64_t)mant << (pos & 31u);
+    const uint32_t wi = pos >> 5, plo = (uint32_t)piece, phi = (uint32_t)(piece >> 32);
+    const bool sub = (bf16 & 0x8000u) != 0;
+    uint32_t carry = 0;  // carry when adding, borrow when subtracting
 #pragma unroll
-    for (int r = 0; r < R; ++r) s += (double)__uint_as_float((uint32_t)g[r][i] << 16);
+    for (int k = 0; k < kWideWords; ++k) {
+        const uint32_t x = k == (int)wi ? plo : k == (int)wi + 1 ? phi : 0u;
+        const uint64_t t = sub ? (uint64_t)w[k] - x - carry : (uint64_t)w[k] + x + carry;
+        w[k] = (uint32_t)t;
+        carry = (uint32_t)(t >> 32) & 1u;
+    }
+}
+
+// The wide route for one element: rank r's BF16 pattern is g[r][i].
+template <int R>
+__device__ __forceinline__ float mean_wide(const uint16_t *const *g, int64_t i) {
+    uint32_t w[kWideWords];
+#pragma unroll
+    for (int k = 0; k < kWideWords; ++k) w[k] = 0;
+    bool finite = true;
+    double s = 0.0;
+#pragma unroll 1
+    for (int r = 0; r < R; ++r) {
+        const uint32_t v = g[r][i];
+        finite &= (v & 0x7f80u) != 0x7f80u;
+        s += (double)__uint_as_float(v << 16);
+        if ((v & 0x7fffu) != 0) wide_add(w, v);
+    }
+    // NaN or an infinity: the IEEE result of the FP64 sum in rank order
+    if (!finite) return mean_of<R>(s);
+    const bool neg = (w[kWideWords - 1] >> 31) != 0;
+    if (neg) {
+        uint32_t c = 1;
+#pragma unroll
+        for (int k = 0; k < kWideWords; ++k) {
+            const uint64_t t = (uint64_t)(~w[k]) + c;
+            w[k] = (uint32_t)t;
+            c = (uint32_t)(t >> 32);
+        }
+    }
+    int top = -1;
+#pragma unroll
+    for (int k = 0; k < kWideWords; ++k)
+        if (w[k]) top = k;
+    if (top < 0) return 0.0f;
+    // the top three words (zero below word 0) and whether any word under them is nonzero
+    uint32_t hw = 0, mw = 0, lw = 0;
+    bool below = false;
+#pragma unroll
+    for (int k = 0; k < kWideWords; ++k) {
+        hw = k == top ? w[k] : hw;
+        mw = k == top - 1 ? w[k] : mw;
+        lw = k == top - 2 ? w[k] : lw;
+        below |= (k < top - 2) && w[k] != 0;
+    }
+    const int sh = __builtin_clz(hw);
+    uint64_t hi64 = ((uint64_t)hw << 32) | mw;
+    uint32_t rest = lw;
+    if (sh) {
+        hi64 = (hi64 << sh) | (lw >> (32 - sh));
+        rest = lw << sh;
+    }
+    uint64_t m53 = hi64 >> 11;
+    if ((hi64 & 0x7ffu) != 0 || rest != 0 || below) m53 |= 1u;  // round to odd
+    const double mag = ldexp((double)m53, 11 + 32 - sh + 32 * (top - 2) - 133);
+    return mean_of<R>(neg ? -mag : mag);
+}
+
+// The wide route for element i of the R buffers g[r], and for the four
+// elements from e0, loading their inputs again (only the rare lanes that
+// fail span_exact take it).  Inlined: as a function call it gave every
+// kernel a call stack in scratch memory, and the kernels with scratch ran
+// three to four times slower (0.67 against 0.23 ms for the Qwen3-8B layer's
+// norm pass), since scratch caps the waves in flight.  The ranks are added
+// one at a time into ten words, so the route adds few registers.
+template <int R>
+__device__ __forceinline__ float mean_wide_at(const uint16_t *const *g, int64_t i) {
+    return mean_wide<R>(g, i);
+}
+
+template <int R>
+__device__ __forceinline__ float4 mean_wide_at4(const uint16_t *const *g, int64_t e0) {
+    float4 o;
+    o.x = mean_wide_at<R>(g, e0);
+    o.y = mean_wide_at<R>(g, e0 + 1);
+    o.z = mean_wide_at<R>(g, e0 + 2);
+    o.w = mean_wide_at<R>(g, e0 + 3);
+    return o;
+}
+
+// Fast route for the 2W elements held as BF16 in w[r][0..W-1] (two per word,
+// the lower half first).  Returns false if the values fail span_exact: the
+// caller must then take the wide route for them.
+template <int R, int W>
+__device__ __forceinline__ bool means_fast(const uint32_t (&w)[R][W], float (&g)[2 * W]) {
+    Span sp = span_init();
+#pragma unroll
+    for (int j = 0; j < W; ++j) {
+        double s_lo = 0.0, s_hi = 0.0;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            s_lo += (double)bf16_lo(w[r][j]);
+            s_hi += (double)bf16_hi(w[r][j]);
+            if constexpr (R > 1) span_add(sp, w[r][j]);
+        }
+        g[2 * j] = mean_of<R>(s_lo);
+        g[2 * j + 1] = mean_of<R>(s_hi);
+    }
+    if constexpr (R > 1) return span_exact<R>(sp);
+    return true;
+}
+
+// g_bar of the 4 elements from e0 of the R buffers g[r], whose BF16 words
+// (already loaded) are w.
+template <int R>
+__device__ __forceinline__ void mean4(const uint32_t (&w)[R][2], const uint16_t *const *g, int64_t e0,
+                                      float (&out)[4]) {
+    if (__builtin_expect(!means_fast<R, 2>(w, out), 0)) {
+        const float4 t = mean_wide_at4<R>(g, e0);
+        out[0] = t.x;
+        out[1] = t.y;
+        out[2] = t.z;
+        out[3] = t.w;
+    }
+}
+
+// g_bar of element i of the R buffers g[r].
+template <int R>
+__device__ __forceinline__ float mean1(const uint16_t *const *g, int64_t i) {
+    uint32_t v[R];
+    double s = 0.0;
+    Span sp = span_init();
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        v[r] = g[r][i];
+        s += (double)__uint_as_float(v[r] << 16);
+        span_add(sp, v[r]);
+    }
+    if constexpr (R > 1)
+        if (!span_exact<R>(sp)) return mean_wide_at<R>(g, i);
     return mean_of<R>(s);
 }
 
@@ -165,6 +356,7 @@ __global__ __launch_bounds__(kNormThreads) void k_norm_partials(NormArgs a) {
     const int64_t full_groups = n / V;
     const int64_t span0 = (int64_t)blockIdx.x * kGroupsPerSpan;
     double hi = 0.0, lo = 0.0;
+    uint32_t wide = 0;  // bit (it * kUnroll + u): a group that takes the wide route
     for (int it = 0; it < kIters; ++it) {
         uint32_t raw[kUnroll][R][V / 2];
         bool ok[kUnroll];
@@ -186,16 +378,9 @@ __global__ __launch_bounds__(kNormThreads) void k_norm_partials(NormArgs a) {
         for (int u = 0; u < kUnroll; ++u) {
             if (!ok[u]) continue;
             float g[V];
-#pragma unroll
-            for (int w = 0; w < V / 2; ++w) {
-                double s_lo = 0.0, s_hi = 0.0;
-#pragma unroll
-                for (int r = 0; r < R; ++r) {
-                    s_lo += (double)bf16_lo(raw[u][r][w]);
-                    s_hi += (double)bf16_hi(raw[u][r][w]);
-                }
-                g[2 * w] = mean_of<R>(s_lo);
-                g[2 * w + 1] = mean_of<R>(s_hi);
+            if (__builtin_expect(!means_fast<R, V / 2>(raw[u], g), 0)) {
+                wide |= 1u << (it * kUnroll + u);
+                continue;
             }
 #pragma unroll
             for (int e = 0; e < V; ++e) dd_add(hi, lo, (double)g[e] * (double)g[e]);
@@ -204,6 +389,20 @@ __global__ __launch_bounds__(kNormThreads) void k_norm_partials(NormArgs a) {
                 *reinterpret_cast<float4 *>(a.gbar_out + e0) = make_float4(g[0], g[1], g[2], g[3]);
             }
         }
+    }
+    // the groups that failed the span check, in the same order, after the
+    // loop, where the wide route's registers do not add to the loop's
+    static_assert(kIters * kUnroll <= 32, "one bit per group of a lane");
+    while (__builtin_expect(wide != 0, 0)) {
+        const int k = __builtin_ctz(wide);
+        wide &= wide - 1;
+        const int64_t e0 = (span0 + (int64_t)k * kNormThreads + threadIdx.x) * V;
+        const float4 t = mean_wide_at4<R>(a.g, e0);
+        dd_add(hi, lo, (double)t.x * (double)t.x);
+        dd_add(hi, lo, (double)t.y * (double)t.y);
+        dd_add(hi, lo, (double)t.z * (double)t.z);
+        dd_add(hi, lo, (double)t.w * (double)t.w);
+        if constexpr (WRITE_GBAR) *reinterpret_cast<float4 *>(a.gbar_out + e0) = t;
     }
     const int64_t tail0 = full_groups * V;
     if (threadIdx.x == 0 && tail0 < n && tail0 / kNormSpan == (int64_t)blockIdx.x) {
@@ -312,6 +511,7 @@ __device__ __forceinline__ void moments(double pd, double md, double vd, double 
 }
 
 __device__ __forceinline__ void adamw(float &p, float &m, float &v, float g_bar, const Consts &k) {
+#pragma clang fp contract(off)
     const double g = (double)g_bar * k.c;
     double p1, m1, v1;
     moments((double)p, (double)m, (double)v, g, k, p1, m1, v1);
@@ -320,23 +520,6 @@ __device__ __forceinline__ void adamw(float &p, float &m, float &v, float g_bar,
     p = (float)pn;
     m = (float)m1;
     v = (float)v1;
-}
-
-// g_bar of the 4 elements held as BF16 in raw[r] (one 8-byte load per rank).
-template <int R>
-__device__ __forceinline__ void mean4(const uint2 (&raw)[R], float (&g)[kUpdVec]) {
-#pragma unroll
-    for (int w = 0; w < 2; ++w) {
-        double s_lo = 0.0, s_hi = 0.0;
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            uint32_t word = (&raw[r].x)[w];
-            s_lo += (double)bf16_lo(word);
-            s_hi += (double)bf16_hi(word);
-        }
-        g[2 * w] = mean_of<R>(s_lo);
-        g[2 * w + 1] = mean_of<R>(s_hi);
-    }
 }
 
 // Lane t of the grid handles elements 4t .. 4t+3: each access of a wave is
@@ -369,30 +552,31 @@ __global__ __launch_bounds__(kUpdateThreads) void k_update(UpdateArgs a) {
     for (int64_t q = gid; q < groups; q += stride) {
         const int64_t e0 = q * kUpdVec;
         float g[kUpdVec];
+        bool fast = true;
         if constexpr (CACHED) {
             const float4 a0 = *reinterpret_cast<const float4 *>(GB + e0);
             g[0] = a0.x; g[1] = a0.y; g[2] = a0.z; g[3] = a0.w;
         } else {
-            uint2 raw[R];
-#pragma unroll
+            uint32_t raw[R][2];
             // read once: non-temporal, as in the norm pass
-            for (int r = 0; r < R; ++r) {
-                uint32_t w[2];
-                load_stream_v<4>(a.g[r] + e0, w);
-                raw[r] = make_uint2(w[0], w[1]);
-            }
-            mean4<R>(raw, g);
+#pragma unroll
+            for (int r = 0; r < R; ++r) load_stream_v<4>(a.g[r] + e0, raw[r]);
+            fast = means_fast<R, 2>(raw, g);
         }
-        float4 *p4 = reinterpret_cast<float4 *>(P + e0);
-        float4 *m4 = reinterpret_cast<float4 *>(M + e0);
-        float4 *v4 = reinterpret_cast<float4 *>(V + e0);
-        float4 pv = *p4, mv = *m4, vv = *v4;
+        float4 pv = *reinterpret_cast<const float4 *>(P + e0);
+        float4 mv = *reinterpret_cast<const float4 *>(M + e0);
+        float4 vv = *reinterpret_cast<const float4 *>(V + e0);
+        if (__builtin_expect(!fast, 0)) {
+            // the wide route (see means_fast)
+            const float4 t = mean_wide_at4<R>(a.g, e0);
+            g[0] = t.x; g[1] = t.y; g[2] = t.z; g[3] = t.w;
+        }
         float *pf = &pv.x, *mf = &mv.x, *vf = &vv.x;
 #pragma unroll
         for (int e = 0; e < kUpdVec; ++e) adamw(pf[e], mf[e], vf[e], g[e], k);
-        *p4 = pv;
-        *m4 = mv;
-        *v4 = vv;
+        *reinterpret_cast<float4 *>(P + e0) = pv;
+        *reinterpret_cast<float4 *>(M + e0) = mv;
+        *reinterpret_cast<float4 *>(V + e0) = vv;
         uint2 b;
         b.x = pack_bf16(pf[0], pf[1]);
         b.y = pack_bf16(pf[2], pf[3]);
@@ -471,11 +655,20 @@ __global__ __launch_bounds__(256) void k_gbar_out(GbarArgs a) {
     const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
     const int64_t stride = (int64_t)gridDim.x * 256;
     for (int64_t q = gid; q < groups; q += stride) {
-        uint4 raw[R];
+        uint32_t lo4[R][2], hi4[R][2];
 #pragma unroll
-        for (int r = 0; r < R; ++r) raw[r] = load_stream(a.g[r] + q * kVec);
-        float g[kVec];
-        mean8<R>(raw, g);
+        for (int r = 0; r < R; ++r) {
+            const uint4 w = load_stream(a.g[r] + q * kVec);
+            lo4[r][0] = w.x;
+            lo4[r][1] = w.y;
+            hi4[r][0] = w.z;
+            hi4[r][1] = w.w;
+        }
+        float g[kVec], g4[4];
+        mean4<R>(lo4, a.g, q * kVec, g4);
+        g[0] = g4[0]; g[1] = g4[1]; g[2] = g4[2]; g[3] = g4[3];
+        mean4<R>(hi4, a.g, q * kVec + 4, g4);
+        g[4] = g4[0]; g[5] = g4[1]; g[6] = g4[2]; g[7] = g4[3];
         if constexpr (BF16) {
             uint4 b;
             b.x = pack_bf16(g[0], g[1]);

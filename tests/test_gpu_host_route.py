@@ -321,3 +321,28 @@ def test_host_route_argument_errors(sdp, ctx):
         assert np.all(window.cpu().numpy().view(np.uint16) == 0x5555)
     finally:
         st.close()
+
+
+def test_host_route_f32_equals_device_mode_bitwise(sdp, ctx):
+    """The host lane evaluates the fused kernel's FP64 expression with the
+    same per-step constants and no fused multiply-add on either side, so the
+    route with the FP32 mean gradient gives device mode's bits exactly."""
+    sizes = [3 * TILE + 5, 70001]
+    R = 4
+    steps = 3
+    masters, grads = rand_inputs(sizes, R, steps, seed=77)
+    st = RouteState(sdp, masters, R)
+    dev = DevState(masters, R)
+    try:
+        for t in range(1, steps + 1):
+            hs, _ = hp_pair(sdp, lr=1e-3, weight_decay=0.05, max_grad_norm=0.2, step=t)
+            st.set_grads(grads[t - 1])
+            nr = sdp.sdp_host_update_step(ctx, st.segments(sdp), hs, 2 * TILE, sdp.SDP_GBAR_F32)
+            dev.set_grads(grads[t - 1])
+            nd = sdp.sdp_agg_adam_step(ctx, dev.segments(sdp), hs, 0, torch.cuda.current_stream().cuda_stream,
+                                       want_norm=True)
+            torch.cuda.synchronize()
+            assert nr == nd
+            assert states_equal(st.state(), dev.host()), f"step {t}: host route differs from device mode"
+    finally:
+        st.close()

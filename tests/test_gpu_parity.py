@@ -688,3 +688,71 @@ def test_cast_bf16_exhaustive(sdp, ctx):
         y = torch.empty(n, dtype=torch.int16, device="cuda")
         sdp.sdp_cast_bf16(ctx, x.data_ptr(), y.data_ptr(), n, stream())
         assert np.array_equal(y.cpu().numpy().view(np.uint16), oracle.bf16(x.cpu().numpy()))
+
+
+# ---------------------------------------------------------------------------
+# The mean gradient's single rounding, on rank sets built to make it hard
+
+def mean_edge_grads(R, n, seed):
+    """Ordinary N(0, 1e-3) BF16 gradients with mean_cases' stress sets written
+    over scattered elements, the last one (the ragged tail) included."""
+    import mean_cases
+    _, grads = rand_inputs([n], R, 1, seed=seed)
+    g = np.stack(grads[0][0])
+    sets = [mean_cases.wide_span(R, 400, seed=R)]
+    if R >= 3:
+        sets.append(mean_cases.near_midpoint(R, 600, seed=50 + R))
+    sets.append(mean_cases.subnormal_remainder(R))
+    special = np.concatenate(sets, axis=1)
+    rng = np.random.default_rng(seed)
+    pos = np.append(rng.choice(n - 1, special.shape[1] - 1, replace=False), n - 1)
+    g[:, pos] = special
+    return [[g[r].copy() for r in range(R)]]
+
+
+@pytest.mark.parametrize("R", [2, 3, 5, 8, 11, 13, 16])
+def test_mean_exact_quotient_edge_cases(sdp, ctx, ctx_store, ctx_nostore, R):
+    """With beta1 = 0 and no clipping, exp_avg after one step is the mean
+    gradient itself, so every mode's g_bar is compared with the oracle's bit
+    for bit (the oracle's mean is pinned to fractions.Fraction), and the whole
+    step with the oracle's by the usual criteria."""
+    n = 3 * TILE + 5
+    log(f"mean edge cases R={R}")
+    masters, _ = rand_inputs([n], R, 1, seed=300 + R)
+    grads = mean_edge_grads(R, n, seed=400 + R)
+    want = oracle.mean_grads(grads[0])
+    hs, ho = hp_pair(sdp, lr=1e-3, beta1=0.0, weight_decay=0.01, max_grad_norm=0.0, step=1)
+    ref = oracle.State(masters)
+    rc, onorm = oracle.step(ref, grads, ho)
+    assert rc == oracle.ORC_OK
+
+    def check(state, norm, what):
+        check_norm(norm, onorm)
+        assert norm == onorm, f"{what}: norm {norm!r} != exactly rounded {onorm!r}"
+        bad = np.flatnonzero(state.exp_avg[0].view(np.uint32) != want.view(np.uint32))
+        assert bad.size == 0, (f"{what}: g_bar differs on {bad.size} elements, first at {bad[0]}: "
+                               f"gpu {state.exp_avg[0][bad[0]]!r} oracle {want[bad[0]]!r} "
+                               f"ranks {[hex(int(x[bad[0]])) for x in grads[0]]}")
+        check_state(state, ref)
+
+    for c, what in ((ctx, "device"), (ctx_store, "device, stored g_bar"), (ctx_nostore, "device, no g_bar")):
+        dev = DevState(masters, R)
+        norm = dev_step(sdp, c, dev, grads, hs)
+        check(dev.host(), norm, what)
+    # streamed, pinned, in chunks of one tile
+    hst = HostState(sdp, masters, R)
+    try:
+        hst.set_grads(grads)
+        norm = sdp.sdp_stream_step(ctx, hst.segments(), hs, TILE)
+        check(hst.host(), norm, "streamed")
+    finally:
+        hst.close()
+    # host-update route, FP32 mean gradient
+    from test_gpu_host_route import RouteState
+    st = RouteState(sdp, masters, R)
+    try:
+        st.set_grads(grads)
+        norm = sdp.sdp_host_update_step(ctx, st.segments(sdp), hs, 2 * TILE, sdp.SDP_GBAR_F32)
+        check(st.state(), norm, "host route")
+    finally:
+        st.close()
