@@ -33,7 +33,9 @@
  * Numerics (the paper never states the optimizer formulas; these follow
  * AdamW with decoupled decay, Loshchilov & Hutter, and Kingma & Ba bias
  * correction):
- *    g_bar[i] = fp32( (sum_r bf16 G_r[i], summed in FP64 in rank order) / R )
+ *    g_bar[i] = fp32( (exact sum over r of bf16 G_r[i]) / R ), rounded once
+ *               (an exactly zero sum gives +0; a NaN or infinite G_r[i] gives
+ *               the IEEE result of the FP64 sum in rank order divided by R)
  *    norm     = sqrt( sum over all elements of all segments of g_bar^2 ) (FP64)
  *    c        = min(1, max_grad_norm / (norm + 1e-6)) if max_grad_norm > 0, else 1
  *    g        = g_bar * c
@@ -347,12 +349,16 @@ typedef struct {
     double norm_gbs;         /* norm pass and mean-gradient kernel, HBM GB/s */
     double update_gbs;       /* fused update kernel, HBM GB/s */
     double launch_us;        /* fixed cost of one kernel */
-    double sync_us;          /* host round trip of the norm read-back */
+    double sync_us;          /* host round trip of the norm read-back; also the delay before a
+                                host thread waiting on a GPU command learns that it ended */
     double host_gbs;         /* host memory bandwidth of the host threads' copies (read + written) */
     double host_task_us;     /* fixed cost of one hand-off to the host threads */
     double host_adam_gbs;    /* the host AdamW lane alone (bytes read + written) */
     double dep_us;           /* latency of an event recorded on the copy stream and waited on
                                 by the compute stream, or the other way round */
+    double dma_host_cost;    /* host memory bandwidth a host task loses per byte of DMA in
+                                flight (1: the DMA's own bytes; measured from the host AdamW
+                                lane beside a device-to-host copy) */
 } sdp_rates;
 
 /* What the model predicts for one call. */
@@ -385,7 +391,9 @@ typedef struct {
  * link by a fluid model (a direction alone moves at its own rate, both
  * directions together at the bidirectional rate, split in proportion), and
  * host-thread tasks share host memory with the DMA (a task moves at most
- * host_gbs minus the copies' current rate, and at most its own rate). */
+ * host_gbs minus dma_host_cost times the copies' current rate, and at most
+ * its own rate); a host thread waiting on a GPU command starts sync_us after
+ * the command ends. */
 SDP_API int sdp_predict_step(int schedule, const int64_t *numels, int32_t n_segs, int32_t n_ranks,
                      int64_t chunk_elems, uint32_t flags, const sdp_rates *rates,
                      sdp_prediction *out);
@@ -426,6 +434,11 @@ SDP_API int sdp_ctx_get_timing(sdp_ctx *ctx, sdp_kernel_times *out);
  * hardware traffic counters. */
 SDP_API int sdp_probe_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, void *stream);
 
+/* The runtime's own device-to-device copy (hipMemcpyAsync) of `bytes`
+ * bytes on `stream`: a second, independent HBM copy ceiling beside
+ * sdp_probe_copy.  Device memory of ctx's GPU, not overlapping. */
+SDP_API int sdp_probe_memcpy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, void *stream);
+
 /* The fused update's memory access pattern with trivial arithmetic, on one
  * device-mode segment (validated as for sdp_agg_adam_step): the same loads
  * and stores, widths and lane mapping, FP32 adds instead of AdamW.  Its rate
@@ -445,6 +458,21 @@ SDP_API int sdp_probe_update_pattern(sdp_ctx *ctx, const sdp_segment *seg, void 
  * `bytes`.  Blocks. */
 SDP_API int sdp_probe_link(sdp_ctx *ctx, void *host_a, void *host_b, void *dev_a, void *dev_b,
                    int64_t bytes, int64_t chunk_bytes, int32_t reps, double *gbs_out);
+
+/* The same link probe on the streamed engine's other device-to-host path:
+ * as sdp_probe_link, but each device-to-host piece of chunk_bytes is one
+ * launch of the library's copy kernel on the compute stream, storing
+ * straight into host_b through its device mapping, as the engine moves a
+ * chunk's copies of up to 64 MiB (32 blocks per launch, or
+ * SDP_D2H_KERNEL_BLOCKS as read at context creation).  Host-to-device
+ * pieces are runtime copies as in sdp_probe_link.  gbs_out[0] = H2D alone,
+ * [1] = D2H alone (copy kernel), [2] = both at once (sum).  host_b must be
+ * hipHostMalloc memory; dev_b, host_b and chunk_bytes 16-byte aligned.  The
+ * streamed mode's link bound takes, per direction and for both at once, the
+ * faster of the two probes (the paper's resource lower bound needs the rate
+ * of the path the engine can use; Design, step-time model).  Blocks. */
+SDP_API int sdp_probe_link_kernel(sdp_ctx *ctx, void *host_a, void *host_b, void *dev_a, void *dev_b,
+                                  int64_t bytes, int64_t chunk_bytes, int32_t reps, double *gbs_out);
 
 /* Host memory bandwidth of the context's host threads: `bytes` copied from
  * src to dst (host memory, disjoint) `reps` times in 4 MiB pieces over the

@@ -541,7 +541,8 @@ int check_model_args(int schedule, const int64_t *numels, int32_t n_segs, int32_
         return fail(SDP_ERR_INVALID_ARGUMENT, "n_ranks must be in 1..%d", SDP_MAX_RANKS);
     const double pos[] = {r->h2d_gbs,    r->d2h_gbs,  r->both_gbs,     r->norm_gbs,
                           r->update_gbs, r->host_gbs, r->host_adam_gbs};
-    const double nonneg[] = {r->copy_cmd_us, r->launch_us, r->sync_us, r->host_task_us, r->dep_us};
+    const double nonneg[] = {r->copy_cmd_us, r->launch_us, r->sync_us, r->host_task_us, r->dep_us,
+                             r->dma_host_cost};
     for (double x : pos)
         if (!(std::isfinite(x) && x > 0.0)) return fail(SDP_ERR_INVALID_ARGUMENT, "rates must be finite and > 0");
     for (double x : nonneg)
@@ -556,7 +557,7 @@ int check_model_args(int schedule, const int64_t *numels, int32_t n_segs, int32_
 sdp_sched::Rates to_rates(const sdp_rates *r) {
     return sdp_sched::Rates{r->h2d_gbs,   r->d2h_gbs,  r->both_gbs, r->copy_cmd_us,  r->norm_gbs,
                             r->update_gbs, r->launch_us, r->sync_us,  r->host_gbs,     r->host_task_us,
-                            r->host_adam_gbs, r->dep_us};
+                            r->host_adam_gbs, r->dep_us, r->dma_host_cost};
 }
 
 int model_chunk_ok(const std::vector<int64_t> &sizes, int64_t chunk) {
@@ -954,6 +955,19 @@ int sdp_probe_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, void
     return SDP_OK;
 }
 
+int sdp_probe_memcpy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, void *stream) {
+    t_err.clear();
+    if (!ctx || !dst || !src || bytes < 1) return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_probe_memcpy: bad argument");
+    DeviceGuard guard(ctx->device);
+    SDP_TRY(check_device_ptr(ctx, dst, (size_t)bytes, "dst", 0));
+    SDP_TRY(check_device_ptr(ctx, src, (size_t)bytes, "src", 0));
+    const uintptr_t a = (uintptr_t)dst, b = (uintptr_t)src;
+    if (a < b + (size_t)bytes && b < a + (size_t)bytes)
+        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_probe_memcpy: dst and src overlap");
+    HIP_TRY(hipMemcpyAsync(dst, src, (size_t)bytes, hipMemcpyDeviceToDevice, (hipStream_t)stream));
+    return SDP_OK;
+}
+
 int sdp_probe_update_pattern(sdp_ctx *ctx, const sdp_segment *seg, void *stream) {
     t_err.clear();
     if (!ctx) return fail(SDP_ERR_INVALID_ARGUMENT, "context is NULL");
@@ -971,26 +985,53 @@ int sdp_probe_update_pattern(sdp_ctx *ctx, const sdp_segment *seg, void *stream)
     return SDP_OK;
 }
 
-int sdp_probe_link(sdp_ctx *ctx, void *host_a, void *host_b, void *dev_a, void *dev_b, int64_t bytes,
-                   int64_t chunk_bytes, int32_t reps, double *gbs_out) {
-    t_err.clear();
+}  // extern "C"
+
+namespace {
+
+// Both link probes: H2D as runtime copies on the copy stream; D2H as runtime
+// copies, or (kernel_d2h) as the streamed engine's copy kernel, one launch of
+// kD2HLaunchBlocks blocks per piece storing straight into the pinned memory,
+// on the compute stream.
+int probe_link(sdp_ctx *ctx, void *host_a, void *host_b, void *dev_a, void *dev_b, int64_t bytes, int64_t chunk_bytes,
+               int32_t reps, bool kernel_d2h, double *gbs_out, const char *name) {
     if (!ctx || !host_a || !host_b || !dev_a || !dev_b || !gbs_out || bytes < 1 || chunk_bytes < 1 || reps < 1)
-        return fail(SDP_ERR_INVALID_ARGUMENT, "sdp_probe_link: bad argument");
+        return fail(SDP_ERR_INVALID_ARGUMENT, "%s: bad argument", name);
     DeviceGuard guard(ctx->device);
     SDP_TRY(check_pinned_ptr(host_a, (size_t)bytes, "host_a", 0));
     SDP_TRY(check_pinned_ptr(host_b, (size_t)bytes, "host_b", 0));
     SDP_TRY(check_device_ptr(ctx, dev_a, (size_t)bytes, "dev_a", 0));
     SDP_TRY(check_device_ptr(ctx, dev_b, (size_t)bytes, "dev_b", 0));
+    char *mapped_b = nullptr;
+    if (kernel_d2h) {
+        hipPointerAttribute_t at;
+        if (hipPointerGetAttributes(&at, host_b) != hipSuccess || !at.devicePointer) {
+            (void)hipGetLastError();
+            return fail(SDP_ERR_NOT_PINNED, "%s: host_b has no device mapping", name);
+        }
+        mapped_b = (char *)at.devicePointer;
+        if (((uintptr_t)mapped_b | (uintptr_t)dev_b | (uintptr_t)chunk_bytes) % 16 != 0)
+            return fail(SDP_ERR_ALIGNMENT, "%s: buffers and chunk_bytes must be 16-byte aligned", name);
+    }
     HIP_TRY(hipDeviceSynchronize());
     // Each pattern is timed on the host from its first enqueue to the end of
     // both streams, with nothing else in flight; the two directions are
     // issued chunk by chunk, interleaved, as the streamed engine issues them.
     auto copy = [&](bool h2d, int64_t off) -> hipError_t {
         const size_t len = (size_t)std::min(chunk_bytes, bytes - off);
-        return h2d ? hipMemcpyAsync((char *)dev_a + off, (const char *)host_a + off, len, hipMemcpyHostToDevice,
-                                    ctx->s_copy)
-                   : hipMemcpyAsync((char *)host_b + off, (const char *)dev_b + off, len, hipMemcpyDeviceToHost,
-                                    ctx->s_comp);
+        if (h2d)
+            return hipMemcpyAsync((char *)dev_a + off, (const char *)host_a + off, len, hipMemcpyHostToDevice,
+                                  ctx->s_copy);
+        if (!kernel_d2h)
+            return hipMemcpyAsync((char *)host_b + off, (const char *)dev_b + off, len, hipMemcpyDeviceToHost,
+                                  ctx->s_comp);
+        sdp::CopyBatch b{};
+        b.n = 1;
+        b.dst[0] = mapped_b + off;
+        b.src[0] = (const char *)dev_b + off;
+        b.bytes[0] = (int64_t)len;
+        const int per_copy = ctx->d2h_kernel_blocks > 0 ? ctx->d2h_kernel_blocks : kD2HLaunchBlocks;
+        return sdp::launch_copy_batch(b, per_copy, ctx->s_comp);
     };
     auto run = [&](bool do_h2d, bool do_d2h, double *seconds) -> hipError_t {
         const auto t0 = std::chrono::steady_clock::now();
@@ -1014,6 +1055,23 @@ int sdp_probe_link(sdp_ctx *ctx, void *host_a, void *host_b, void *dev_a, void *
     HIP_TRY(run(true, true, &sec));
     gbs_out[2] = 2.0 * total / sec / 1e9;
     return SDP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sdp_probe_link(sdp_ctx *ctx, void *host_a, void *host_b, void *dev_a, void *dev_b, int64_t bytes,
+                   int64_t chunk_bytes, int32_t reps, double *gbs_out) {
+    t_err.clear();
+    return probe_link(ctx, host_a, host_b, dev_a, dev_b, bytes, chunk_bytes, reps, false, gbs_out, "sdp_probe_link");
+}
+
+int sdp_probe_link_kernel(sdp_ctx *ctx, void *host_a, void *host_b, void *dev_a, void *dev_b, int64_t bytes,
+                          int64_t chunk_bytes, int32_t reps, double *gbs_out) {
+    t_err.clear();
+    return probe_link(ctx, host_a, host_b, dev_a, dev_b, bytes, chunk_bytes, reps, true, gbs_out,
+                      "sdp_probe_link_kernel");
 }
 
 int sdp_probe_host_copy(sdp_ctx *ctx, void *dst, const void *src, int64_t bytes, int32_t reps, double *gbs_out) {

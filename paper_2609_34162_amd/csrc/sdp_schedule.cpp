@@ -91,10 +91,13 @@ double evaluate(Graph &g, const Rates &r) {
     const double h2d = r.h2d_gbs * 1e3, d2h = r.d2h_gbs * 1e3, both = r.both_gbs * 1e3;  // bytes per us
     const double inf = std::numeric_limits<double>::infinity();
     // an edge between the copy and the compute stream is an event that one
-    // queue records and the other waits on: it takes effect dep_us later
+    // queue records and the other waits on: it takes effect dep_us later; a
+    // host thread waiting on a GPU command learns of its end sync_us later
+    // (the round trip of the norm read-back)
     auto crosses = [](const Node &u, const Node &v) {
         return u.stream != v.stream && u.stream != kHostS && v.stream != kHostS;
     };
+    auto wakes = [](const Node &u, const Node &v) { return u.stream != kHostS && v.stream == kHostS; };
     while (done < total) {
         double wake = inf;  // earliest time a node whose predecessors are done may start
         for (int s = 0; s < kStreams; ++s) {
@@ -110,6 +113,7 @@ double evaluate(Graph &g, const Rates &r) {
                     break;
                 }
                 if (crosses(pu, v)) at = std::max(at, pu.t_end + r.dep_us);
+                if (wakes(pu, v)) at = std::max(at, pu.t_end + r.sync_us);
             }
             if (!ready) continue;
             if (at > t) {
@@ -144,14 +148,15 @@ double evaluate(Graph &g, const Rates &r) {
             rd = d2h;
         }
         // every DMA byte passes through host memory; the host threads get
-        // what the copies leave of it
+        // what the copies leave of it, each DMA byte costing them
+        // dma_host_cost bytes of host bandwidth
         const double dram = r.host_gbs * 1e3;
         if (rh + rd > dram) {
             const double f = dram / (rh + rd);
             rh *= f;
             rd *= f;
         }
-        const double left = std::max(0.0, dram - rh - rd);
+        const double left = std::max(0.0, dram - r.dma_host_cost * (rh + rd));
         auto rate = [&](const Node &v) {
             if (v.kind == kH2D) return rh / nh;
             if (v.kind == kD2H) return rd / nd;
@@ -285,7 +290,7 @@ void build_streamed(Graph &g, const std::vector<int64_t> &numels, int R, int64_t
         bin_h2d[bi] = h2d;
     }
     const int fin = g.add(kCompS, kFixed, r.launch_us, 0, 0, {});
-    const int rb = g.add(kHostS, kFixed, r.sync_us, 0, 0, {fin});
+    const int rb = g.add(kHostS, kFixed, 0.0, 0, 0, {fin});  // the wake edge carries sync_us
     const size_t k0 = ch1.size();
     const std::vector<Chunk> ch = chunks_of(numels, C);
     int d2h_slot[2] = {-1, -1};
@@ -331,7 +336,7 @@ void build_streamed(Graph &g, const std::vector<int64_t> &numels, int R, int64_t
 void build_host_route(Graph &g, const std::vector<int64_t> &numels, int R, int64_t C, bool bf16, const Rates &r) {
     for (int64_t n : numels) g.add(kCompS, kFixed, kernel_us(2.0 * R * (double)n, r.norm_gbs, r), 0, 0, {});
     const int fin = g.add(kCompS, kFixed, r.launch_us, 0, 0, {});
-    const int rb = g.add(kHostS, kFixed, r.sync_us, 0, 0, {fin});
+    const int rb = g.add(kHostS, kFixed, 0.0, 0, 0, {fin});  // the wake edge carries sync_us
     std::vector<Chunk> ch;
     for (const RoutePiece &pc : route_pieces(numels, C)) ch.push_back({pc.len, false});
     const double esz = bf16 ? 2.0 : 4.0;

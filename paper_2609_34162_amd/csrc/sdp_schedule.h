@@ -16,9 +16,10 @@
 // share host memory with the DMA: every byte a copy moves is read from or
 // written to host memory, so the copies together move at most host_gbs, and
 // while they run at a combined rate r a host task moves at most
-// (host_gbs - r), and never more than its own peak.  With
-// no overlap of copies in both directions and no copy beside a host task,
-// the evaluation is exactly the recurrence with fixed durations.
+// (host_gbs - dma_host_cost * r), and never more than its own peak.  A host
+// thread that waits for a GPU command starts sync_us after the command's
+// end.  With no overlap of copies in both directions and no copy beside a
+// host task, the evaluation is exactly the recurrence with fixed durations.
 #pragma once
 
 #include <stdint.h>
@@ -38,6 +39,7 @@ struct Rates {
     double host_task_us;                // fixed cost of one hand-off to the host threads
     double host_adam_gbs;               // host AdamW lane alone (bytes read + written)
     double dep_us;                      // an event recorded on one GPU stream, waited on by the other
+    double dma_host_cost;               // host memory bytes a host task loses per DMA byte
 };
 
 enum Schedule { kStreamed = 0, kStreamedStaged = 1, kHostRouteF32 = 2, kHostRouteBf16 = 3 };

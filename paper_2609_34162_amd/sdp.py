@@ -80,7 +80,7 @@ class sdp_kernel_times(ctypes.Structure):
 class sdp_rates(ctypes.Structure):
     _fields_ = [(n, ctypes.c_double) for n in ("h2d_gbs", "d2h_gbs", "both_gbs", "copy_cmd_us", "norm_gbs",
                                               "update_gbs", "launch_us", "sync_us", "host_gbs", "host_task_us",
-                                              "host_adam_gbs", "dep_us")]
+                                              "host_adam_gbs", "dep_us", "dma_host_cost")]
 
 
 class sdp_prediction(ctypes.Structure):
@@ -122,6 +122,8 @@ def _load():
         "sdp_probe_copy": (ctypes.c_int, [vp, vp, vp, i64, vp]),
         "sdp_probe_update_pattern": (ctypes.c_int, [vp, vp, vp]),
         "sdp_probe_link": (ctypes.c_int, [vp, vp, vp, vp, vp, i64, i64, i32, P(dbl)]),
+        "sdp_probe_link_kernel": (ctypes.c_int, [vp, vp, vp, vp, vp, i64, i64, i32, P(dbl)]),
+        "sdp_probe_memcpy": (ctypes.c_int, [vp, vp, vp, i64, vp]),
         "sdp_host_alloc": (ctypes.c_int, [P(vp), ctypes.c_size_t]),
         "sdp_host_free": (ctypes.c_int, [vp]),
         "sdp_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -289,6 +291,7 @@ def sdp_ctx_host_threads(ctx) -> int:
 
 def make_rates(**kw) -> sdp_rates:
     r = sdp_rates()
+    r.dma_host_cost = 1.0
     for k, v in kw.items():
         if not hasattr(r, k):
             raise TypeError(f"unknown rate {k}")
@@ -345,6 +348,10 @@ def sdp_probe_copy(ctx, dst: int, src: int, nbytes: int, stream=None) -> None:
     _check(_lib.sdp_probe_copy(ctx, dst, src, nbytes, _stream(stream)))
 
 
+def sdp_probe_memcpy(ctx, dst: int, src: int, nbytes: int, stream=None) -> None:
+    _check(_lib.sdp_probe_memcpy(ctx, dst, src, nbytes, _stream(stream)))
+
+
 def sdp_probe_update_pattern(ctx, segs: Segments, stream=None) -> None:
     if segs.n != 1:
         raise ValueError("sdp_probe_update_pattern takes one segment")
@@ -356,6 +363,14 @@ def sdp_probe_link(ctx, host_a: int, host_b: int, dev_a: int, dev_b: int, nbytes
     out = (ctypes.c_double * 3)()
     _check(_lib.sdp_probe_link(ctx, host_a, host_b, dev_a, dev_b, nbytes, chunk_bytes, reps,
                                ctypes.cast(out, ctypes.POINTER(ctypes.c_double))))
+    return list(out)
+
+
+def sdp_probe_link_kernel(ctx, host_a: int, host_b: int, dev_a: int, dev_b: int, nbytes: int,
+                          chunk_bytes: int, reps: int) -> List[float]:
+    out = (ctypes.c_double * 3)()
+    _check(_lib.sdp_probe_link_kernel(ctx, host_a, host_b, dev_a, dev_b, nbytes, chunk_bytes, reps,
+                                      ctypes.cast(out, ctypes.POINTER(ctypes.c_double))))
     return list(out)
 
 

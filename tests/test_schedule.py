@@ -61,9 +61,9 @@ def test_host_route_two_segments_closed_form(sdp):
         c = [5.0 + us(esz * n, 40.0) for n in sizes]
         h = [us((26 + esz) * n, 300.0) + 17.0 for n in sizes]
         t_c0 = want + g[0] + c[0]
-        t_h0 = t_c0 + h[0]
+        t_h0 = t_c0 + 13.0 + h[0]              # the host learns of each copy's end sync_us later
         t_c1 = max(want + g[0] + g[1], t_c0) + c[1]
-        total = max(t_h0, t_c1) + h[1]
+        total = max(t_h0, t_c1 + 13.0) + h[1]
         assert math.isclose(got.predicted_ms, total / 1e3, rel_tol=1e-12), sched
 
 
@@ -146,20 +146,22 @@ def test_bound_never_exceeds_prediction(sdp):
         assert p.n_chunks == sum(-(-n // chunk) for n in sizes)
 
 
-def test_host_update_shares_host_memory_with_the_copy(sdp):
+@pytest.mark.parametrize("kappa", [1.0, 2.5])
+def test_host_update_shares_host_memory_with_the_copy(sdp, kappa):
     """Host route, two equal chunks: the update of chunk 0 starts with the
-    copy of chunk 1 and runs at min(its own rate, host_gbs - copy rate) until
-    that copy ends, then at its own rate."""
+    copy of chunk 1 and runs at min(its own rate, host_gbs - kappa * copy
+    rate) until that copy ends, then at its own rate; kappa is the host
+    memory a host task loses per DMA byte."""
     L, R = 4 * TILE, 2
     A, B = 300.0, 320.0   # the AdamW lane's own rate; host memory bandwidth
-    rt = rates(sdp, host_gbs=B, host_adam_gbs=A, norm_gbs=1e9)
+    rt = rates(sdp, host_gbs=B, host_adam_gbs=A, norm_gbs=1e9, dma_host_cost=kappa)
     esz = 2
     got = sdp.sdp_predict_step(sdp.SDP_SCHED_HOST_ROUTE_BF16, [2 * L], R, L, 0, rt).predicted_ms * 1e3
     start = us(2 * R * 2 * L, 1e9) + us((2 * R + esz) * L, 1e9)   # norm pass, first mean-gradient kernel
     c = us(esz * L, 40.0)                     # one copy, alone on the link
     W = (26 + esz) * L                        # host bytes of one chunk's update
     # the second kernel ran long ago (its rate is huge), so copy 1 starts with update 0
-    slow = min(A, B - 40.0) * 1e3             # bytes per us while copy 1 runs
+    slow = min(A, B - kappa * 40.0) * 1e3     # bytes per us while copy 1 runs
     done_during = slow * c
     assert done_during < W
     u0 = c + (W - done_during) / (A * 1e3)
@@ -180,7 +182,7 @@ def test_streamed_host_cast_single_chunk_closed_form(sdp):
     want = (R * 7.0 + us(2 * R * N, 50.0) + us((2 * R + 4) * N, 5000.0) + 3.0 + 3.0 + 11.0
             + 3 * 7.0 + us(12 * N, 50.0) + us(30 * N, 4000.0) + 3.0
             + 1 * 7.0 + us(12 * N, 40.0)             # master, m, v out
-            + 5.0 + us(6 * N, 100.0))                # host rounding
+            + 11.0 + 5.0 + us(6 * N, 100.0))         # host rounding, once the host learns the copy ended
     assert math.isclose(got.predicted_ms, want / 1e3, rel_tol=1e-12)
     plain = sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, 4 * TILE, 0, rt)
     assert math.isclose(got.d2h_ms, plain.d2h_ms * 12 / 14, rel_tol=1e-12)
