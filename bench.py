@@ -3,46 +3,44 @@
 
 One step = the whole hot path over one batch of synthetic input: aggregate
 the R ranks' BF16 gradients, global-norm clip, AdamW on the FP32 master and
-moments, BF16 re-emit.  The timed workload is one Qwen3-8B decoder layer
-(192,946,176 parameters, R = 4) with its states in HBM (device mode).  The
-JSON line also carries:
-  roofline      -- the fused update kernel's algorithmic HBM GB/s against
-                   8 TB/s, its duration from HIP events the library records
-                   around each launch on its stream, over a second pass of
-                   the same number of steps (the headline pass runs without
-                   those events, which cost about 20 us per step);
-  torch_eager   -- for comparison, the same step written with PyTorch ops
+moments, BF16 re-emit.  The timed workload is the largest one whose states
+fit in HBM: one Qwen2.5-72B decoder layer (877,674,496 parameters, R = 8)
+with its states in HBM (device mode), where the norm pass stores the mean
+gradient and the fused update reads it back (50 B per parameter).  The JSON
+line also carries:
+  roofline      -- the dominant kernel, the fused update reading the stored
+                   mean gradient (30 B per parameter), against 8 TB/s: its
+                   duration from HIP events the library records around each
+                   launch on its stream, over a second pass of the same
+                   number of steps (the headline pass runs without those
+                   events); traffic from the committed counter record;
+  norm_roofline -- the same for the norm pass that stores the mean gradient;
+  copy_ceiling  -- device copies of 2 GiB measured in the same run: the
+                   library's 16-byte-per-lane copy kernel, the runtime's
+                   hipMemcpyAsync and torch's copy_;
+  qwen3_8b_layer -- one Qwen3-8B layer (192,946,176 parameters, R = 4) in
+                   device mode (42 B per parameter), with its own roofline and
+                   the update's access pattern with trivial arithmetic;
+  torch_eager   -- for comparison, the headline step written with PyTorch ops
                    (FP32 mean gradient, clip_grad_norm_, fused AdamW, BF16
                    cast) on the same GPU;
-  hbm_copy_gbs  -- a 16-byte-per-lane device copy, the practical ceiling;
-  update_pattern_gbs -- the fused update's own loads and stores with trivial
-                   arithmetic: the ceiling of its 20:14 read:write mix;
   streamed      -- one Qwen3-14B layer (330,311,680 parameters, R = 4) in
                    pinned host memory, streamed in 32M-element chunks, against
-                   the pinned link bandwidth measured in the same run;
-  host_cast (inside streamed) -- the same step with the BF16 parameters
-                   rounded on the host from the returned master, against its
-                   own link bound (12 B per parameter back instead of 14);
-  device_r8     -- one Qwen2.5-72B layer (877,674,496 parameters, R = 8) in
-                   device mode, where the norm pass stores the mean gradient;
-  staged_pageable (inside streamed) -- the streamed step again with the
-                   states in pageable memory, through the staged mode;
-  delivery (inside streamed) -- BF16 copies of the layer's FP32 master
-                   delivered into a device window, rounded on the host or on
-                   the GPU, from pinned and pageable memory; each also three
-                   times back to back with the version gate on the GPU
-                   ("gated");
-  chunk_sweep (inside streamed and host_route) -- measured step time at
-                   chunk sizes of 4-128 MiB per FP32 array beside the
-                   library's step-time model fed with rates measured in
-                   the same run, and the chunk each would pick;
-  tuned (inside streamed) -- the streamed step at the chunk the model picks
-                   (sdp_tune_chunk), from the sweep;
+                   the link bound from the faster of the engine's two copy
+                   paths per direction, measured in the same run (runtime
+                   copies; the library's device-to-host copy kernel), with
+                   the BF16 parameters rounded on the host, the staged mode
+                   on pageable memory, parameter delivery, a chunk sweep
+                   beside the step-time model and the model's chunk;
   host_route    -- the paper's own datapath for the same Qwen3-14B layer:
                    gradients in HBM, states in pageable host memory, the mean
                    gradient copied down (FP32 or BF16) and AdamW on this
                    host's cores, with the host AdamW's core scaling;
-  cpu_baseline  -- the CPU oracle on the same layer, on this host's cores.
+  full_model    -- the full Qwen3-14B model (14,768,291,840 parameters,
+                   R = 2, 266 GB of pageable host state): the staged streamed
+                   step against the same link bound, and the host-update
+                   route (inputs generated before the timed steps);
+  cpu_baseline  -- the CPU oracle on the headline layer, on this host's cores.
 Inputs are generated before the timed region and stay resident; the same
 gradient buffers are reused by every timed step.
 """
@@ -58,8 +56,13 @@ sys.path.insert(0, ROOT)
 
 METRIC = "AdamW-step params/s + HBM GB/s (% peak); streamed GB/s vs pinned host link"
 HBM_PEAK_GBS = 8000.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_fused_update_qwen3_8b_layer.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_34162_amd", "csrc", "sdp_kernels.hip")
+# HBM counter records (rocprofv3 FETCH_SIZE / WRITE_SIZE, calibrated against a
+# plain copy); each is valid only for the kernel source it was taken on
+TRAFFIC_FILES = {
+    1: os.path.join(ROOT, "profiles", "traffic_qwen3_8b_layer_device.json"),
+    4: os.path.join(ROOT, "profiles", "traffic_qwen2.5_72b_layer_device.json"),
+}
 
 
 def log(msg):
@@ -70,20 +73,59 @@ def kernel_source_hash() -> str:
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
 
-def measured_traffic(algorithmic_bytes):
-    """HBM bytes per update launch from the committed counter runs, if they
-    were taken on the current kernel source (else None)."""
+def measured_traffic(cid, kernel):
+    """HBM bytes per launch of `kernel` ("update" or "norm") from the committed
+    counter record of workload `cid`, if it was taken on the current kernel
+    source (else None)."""
     try:
-        rec = json.load(open(TRAFFIC_FILE))
-    except (OSError, ValueError):
+        rec = json.load(open(TRAFFIC_FILES[cid]))
+    except (OSError, ValueError, KeyError):
         return None
     if rec.get("kernel_source_sha256_16") != kernel_source_hash():
         return None
-    return rec.get("hbm_bytes_per_launch")
+    return rec.get("kernels", {}).get(kernel, {}).get("hbm_bytes_per_launch")
 
 
-def device_leg(args, torch, np, synth, sdp, cid, steps, warmup, copy_probe):
-    """Times `steps` device-mode steps of workload `cid` after `warmup` ones."""
+def events_ms(torch, stream, fn, reps):
+    """GPU time of `reps` calls of fn() on `stream`, from torch events."""
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1)
+
+
+def copy_ceiling(torch, sdp, ctx, stream):
+    """Device-to-device copies of 2 GiB, ten each after two: the library's
+    16-byte-per-lane copy kernel, the runtime's hipMemcpyAsync and torch's
+    copy_.  GB/s counts bytes read plus bytes written."""
+    nbytes = 2 << 30
+    dev = torch.device("cuda:0")
+    a = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    b = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    a.fill_(1)
+    sh = stream.cuda_stream
+    ways = {
+        "library_copy_kernel": lambda: sdp.sdp_probe_copy(ctx, b.data_ptr(), a.data_ptr(), nbytes, sh),
+        "hip_memcpy_async": lambda: sdp.sdp_probe_memcpy(ctx, b.data_ptr(), a.data_ptr(), nbytes, sh),
+        "torch_copy": lambda: b.copy_(a),
+    }
+    out = {}
+    with torch.cuda.stream(stream):
+        for name, fn in ways.items():
+            events_ms(torch, stream, fn, 2)
+            best = max(2 * nbytes * 10 / (events_ms(torch, stream, fn, 10) * 1e-3) / 1e9 for _ in range(3))
+            out[name] = best
+    del a, b
+    torch.cuda.empty_cache()
+    return out
+
+
+def device_leg(args, torch, np, synth, sdp, cid, steps, warmup, pattern):
+    """Times `steps` device-mode steps of workload `cid` after `warmup` ones,
+    then the same number again with the library's per-launch events."""
     w = synth.workload(cid)
     N, R = w.numel, w.ranks
     log(f"device leg: {w.name} N={N} R={R}; generating inputs")
@@ -108,6 +150,7 @@ def device_leg(args, torch, np, synth, sdp, cid, steps, warmup, copy_probe):
         sdp.sdp_agg_adam_step(ctx, segs, sdp.make_params(**w.hparams(t)), w.chunk, sh)
 
     log(f"device leg: {warmup} warmup + {steps} timed steps, then {steps} steps with per-launch events")
+    torch.cuda.synchronize()
     for t in range(1, warmup + 1):
         step(t)
     torch.cuda.synchronize()
@@ -137,46 +180,44 @@ def device_leg(args, torch, np, synth, sdp, cid, steps, warmup, copy_probe):
     upd_s = kt.update_ms / kt.update_launches / 1e3
     norm_s = kt.norm_ms / kt.norm_launches / 1e3
     res = dict(
-        workload=w.name, N=N, R=R, chunk=w.chunk, steps=steps, elapsed=elapsed,
+        workload=w.name, N=N, R=R, chunk=w.chunk, steps=steps, warmup=warmup, elapsed=elapsed,
         ms_per_step=elapsed / steps * 1e3, params_per_s=N * steps / elapsed,
         ms_per_step_with_events=elapsed_events / steps * 1e3,
         step_bytes_per_elem=step_bytes, step_hbm_gbs=step_bytes * N * steps / elapsed / 1e9,
+        stored_gbar=stored,
         update_ms=upd_s * 1e3, norm_ms=norm_s * 1e3,
         finalize_ms=kt.finalize_ms / max(kt.finalize_launches, 1),
+        update_bytes_per_elem=upd_bytes_per_elem, norm_bytes_per_elem=norm_bytes_per_elem,
         update_gbs=upd_bytes_per_elem * N / upd_s / 1e9, update_bytes=upd_bytes_per_elem * N,
-        norm_gbs=norm_bytes_per_elem * N / norm_s / 1e9, grad_norm=norm, clip=clip,
+        norm_gbs=norm_bytes_per_elem * N / norm_s / 1e9, norm_bytes=norm_bytes_per_elem * N,
+        grad_norm=norm, clip=clip,
     )
-    if copy_probe:
-        # HBM copy ceiling with the same access width (2 x 2 GiB buffers)
-        nbytes = 2 << 30
-        a = torch.empty(nbytes, dtype=torch.uint8, device=dev)
-        b = torch.empty(nbytes, dtype=torch.uint8, device=dev)
-        a.fill_(1)
-        for _ in range(2):
-            sdp.sdp_probe_copy(ctx, b.data_ptr(), a.data_ptr(), nbytes, sh)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        reps = 10
-        for _ in range(reps):
-            sdp.sdp_probe_copy(ctx, b.data_ptr(), a.data_ptr(), nbytes, sh)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        res["copy_gbs"] = 2 * nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
-        del a, b
+    if pattern:
         # the update's own access pattern with trivial arithmetic (overwrites
         # the states, whose results were read above): its traffic-mix ceiling
-        for _ in range(2):
-            sdp.sdp_probe_update_pattern(ctx, segs, sh)
-        e0.record(stream)
-        for _ in range(reps):
-            sdp.sdp_probe_update_pattern(ctx, segs, sh)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        res["pattern_gbs"] = (2 * R + 26) * N * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
-    sdp.sdp_ctx_destroy(ctx)
-    del p, m, v, pb, g
-    torch.cuda.empty_cache()
+        reps = 10
+        with torch.cuda.stream(stream):
+            events_ms(torch, stream, lambda: sdp.sdp_probe_update_pattern(ctx, segs, sh), 2)
+            ms = events_ms(torch, stream, lambda: sdp.sdp_probe_update_pattern(ctx, segs, sh), reps)
+        res["pattern_gbs"] = (2 * R + 26) * N * reps / (ms * 1e-3) / 1e9
+    res["ctx"] = ctx
+    res["_keep"] = (p, m, v, pb, g)
     return res, master, host_grads, w
+
+
+def release(torch, sdp, res):
+    sdp.sdp_ctx_destroy(res.pop("ctx"))
+    res.pop("_keep")
+    torch.cuda.empty_cache()
+
+
+def roofline(res, kernel, cid, kind):
+    """The roofline object of one kernel of a device leg."""
+    ach = res[f"{kernel}_gbs"]
+    return {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS,
+            "traffic": measured_traffic(cid, kernel), "kernel": kind,
+            "algorithmic_bytes_per_launch": res[f"{kernel}_bytes"],
+            "bytes_per_param": res[f"{kernel}_bytes_per_elem"], "launch_ms": res[f"{kernel}_ms"]}
 
 
 def torch_leg(torch, np, w, master, host_grads, steps, warmup):
@@ -225,11 +266,18 @@ def torch_leg(torch, np, w, master, host_grads, steps, warmup):
                 ops="fp32 mean of the R bf16 gradients, clip_grad_norm_, AdamW(fused=True), bf16 cast")
 
 
-def brief(res):
-    """The device-leg figures reported for a non-headline workload."""
-    return {k: res[k] for k in ("workload", "N", "R", "chunk", "steps", "ms_per_step", "params_per_s",
-                                "step_bytes_per_elem", "step_hbm_gbs", "update_ms", "update_gbs", "norm_ms",
-                                "norm_gbs")} | {"step_hbm_frac": res["step_hbm_gbs"] / HBM_PEAK_GBS}
+def brief(res, cid, pattern=False):
+    """The device-leg figures reported for a workload beside the headline."""
+    out = {k: res[k] for k in ("workload", "N", "R", "chunk", "steps", "warmup", "ms_per_step", "params_per_s",
+                               "step_bytes_per_elem", "step_hbm_gbs", "stored_gbar", "update_ms", "update_gbs",
+                               "norm_ms", "norm_gbs", "finalize_ms")}
+    out["step_hbm_frac"] = res["step_hbm_gbs"] / HBM_PEAK_GBS
+    out["roofline"] = roofline(res, "update", cid, "fused aggregate+clip+AdamW+BF16 update")
+    out["norm_roofline"] = roofline(res, "norm", cid, "norm partials")
+    if pattern:
+        out["update_pattern_gbs"] = res["pattern_gbs"]
+        out["update_frac_of_pattern"] = res["update_gbs"] / res["pattern_gbs"]
+    return out
 
 
 def cpu_leg(args, np, synth, oracle, master, host_grads, w):
@@ -326,8 +374,9 @@ def measure_rates(args, torch, np, sdp, ctx, link, dres):
     """The step-time model's inputs, each measured on this machine: link rates
     (passed in), the per-command copy cost, the kernels' HBM rates and the
     launch cost from the device leg, the norm read-back round trip, the host
-    threads' copy bandwidth, their per-hand-off cost, the host AdamW lane's
-    rate alone and the latency of an event between two GPU streams."""
+    threads' copy bandwidth, the host AdamW lane's rate and per-call cost,
+    the host memory a DMA byte takes from that lane, and the latency of an
+    event between two GPU streams."""
     big, small = 256 << 20, 1 << 20
     ha, hb = sdp.HostBuffer(big), sdp.HostBuffer(big)
     da = torch.empty(big, dtype=torch.uint8, device="cuda")
@@ -351,30 +400,61 @@ def measure_rates(args, torch, np, sdp, ctx, link, dres):
     sdp.sdp_probe_host_copy(ctx, dst.ctypes.data, src.ctypes.data, src.nbytes, 1)
     host_gbs = max(sdp.sdp_probe_host_copy(ctx, dst.ctypes.data, src.ctypes.data, src.nbytes, 2) for _ in range(3))
     del src, dst
-    # hand-off cost: an 8-element host update through the context's threads
-    x = [np.zeros(64, np.float32) for _ in range(4)]
-    pbuf = np.zeros(64, np.uint16)
-    hp = sdp.make_params(step=1)
-    call = lambda: sdp.sdp_host_adamw(ctx, x[0].ctypes.data, x[1].ctypes.data, x[2].ctypes.data,  # noqa: E731
-                                      pbuf.ctypes.data, x[3].ctypes.data, sdp.SDP_GBAR_F32, 8, 1.0, hp)
-    call()
-    t0 = time.perf_counter()
-    for _ in range(500):
-        call()
-    host_task_us = (time.perf_counter() - t0) / 500 * 1e6
-    # the host AdamW lane alone on 64M elements (FP32 mean gradient: 30 B per element)
-    n = 1 << 26
-    st = [np.full(n, 1e-2, np.float32) for _ in range(4)]
-    pb = np.zeros(n, np.uint16)
+    # the host AdamW lane alone: time(n) = hand-off + bytes / rate, from calls
+    # of 1M and 16M elements (FP32 mean gradient: 30 B per element); the
+    # intercept is the fixed cost of one hand-off to the host threads
+    # (waking them, and the last task's tail)
     hp3 = sdp.make_params(step=3)
-    lane = lambda: sdp.sdp_host_adamw(ctx, st[0].ctypes.data, st[1].ctypes.data, st[2].ctypes.data,  # noqa: E731
-                                      pb.ctypes.data, st[3].ctypes.data, sdp.SDP_GBAR_F32, n, 1.0, hp3)
-    lane()
+    st = [np.full(1 << 26, 1e-2, np.float32) for _ in range(4)]
+    pb = np.zeros(1 << 26, np.uint16)
+
+    def lane(n):
+        sdp.sdp_host_adamw(ctx, st[0].ctypes.data, st[1].ctypes.data, st[2].ctypes.data, pb.ctypes.data,
+                           st[3].ctypes.data, sdp.SDP_GBAR_F32, n, 1.0, hp3)
+
+    def per_call_us(n, reps):
+        lane(n)
+        best = float("inf")
+        for _ in range(3):
+            t0 = time.perf_counter()
+            for _ in range(reps):
+                lane(n)
+            best = min(best, (time.perf_counter() - t0) / reps * 1e6)
+        return best
+
+    n1, n2 = 1 << 20, 1 << 24
+    t1, t2 = per_call_us(n1, 40), per_call_us(n2, 6)
+    host_adam_gbs = 30 * (n2 - n1) / ((t2 - t1) * 1e3)
+    host_task_us = max(0.0, t1 - 30 * n1 / (host_adam_gbs * 1e3))
+    # the same lane while a device-to-host copy streams into pinned memory (as
+    # in the host-update route): how much host memory bandwidth each DMA byte
+    # takes from it
+    src_d = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    dst_h = torch.empty(1 << 30, dtype=torch.uint8, pin_memory=True)
+    side = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(side):
+        e0.record(side)
+        for _ in range(12):
+            dst_h.copy_(src_d, non_blocking=True)
+        e1.record(side)
+    time.sleep(0.005)  # the copies are running
+    reps = 6
     t0 = time.perf_counter()
-    for _ in range(4):
-        lane()
-    host_adam_gbs = 30 * n * 4 / (time.perf_counter() - t0) / 1e9
-    del st, pb
+    for _ in range(reps):
+        lane(n2)
+    lane_dma_s = (time.perf_counter() - t0) / reps
+    busy = not e1.query()  # the copies outlasted the lane's timing
+    torch.cuda.synchronize()
+    d2h_gbs_meas = 12 * (1 << 30) / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    host_adam_dma_gbs = 30 * n2 / lane_dma_s / 1e9
+    del src_d, dst_h, st, pb
+    dma_host_cost = 1.0
+    if busy and d2h_gbs_meas > 0:
+        dma_host_cost = max(1.0, (host_gbs - host_adam_dma_gbs) / d2h_gbs_meas)
+    else:
+        log("the host lane outlasted the device-to-host copies: DMA cost per byte taken as 1")
     kern_ms = dres["update_ms"] + dres["norm_ms"] + dres["finalize_ms"]
     launch_us = max(0.0, (dres["ms_per_step"] - kern_ms) / 3 * 1e3)
     if hasattr(torch.cuda, "_sleep"):
@@ -384,7 +464,9 @@ def measure_rates(args, torch, np, sdp, ctx, link, dres):
         dep_us = 0.0
     vals = dict(h2d_gbs=link[0], d2h_gbs=link[1], both_gbs=link[2], copy_cmd_us=copy_cmd_us,
                 norm_gbs=dres["norm_gbs"], update_gbs=dres["update_gbs"], launch_us=launch_us, sync_us=sync_us,
-                host_gbs=host_gbs, host_task_us=host_task_us, host_adam_gbs=host_adam_gbs, dep_us=dep_us)
+                host_gbs=host_gbs, host_task_us=host_task_us, host_adam_gbs=host_adam_gbs, dep_us=dep_us,
+                dma_host_cost=dma_host_cost)
+    log(f"host lane beside a {d2h_gbs_meas:.1f} GB/s device-to-host copy: {host_adam_dma_gbs:.1f} GB/s")
     log("model rates: " + ", ".join(f"{k} {v:.1f}" for k, v in vals.items()))
     return sdp.make_rates(**vals), vals
 
@@ -402,10 +484,53 @@ def chunk_sweep(sdp, schedule, numels, R, rates, run_at):
     best_pred, _ = sdp.sdp_tune_chunk(schedule, numels, R, 0, rates, SWEEP_CHUNKS)
     best_meas = min(rows, key=lambda r: r["measured_ms"])
     at_pick = next(r["measured_ms"] for r in rows if r["chunk_elems"] == best_pred)
-    err = [abs(r["predicted_ms"] - r["measured_ms"]) / r["measured_ms"] for r in rows]
+    for r in rows:
+        r["rel_error"] = (r["predicted_ms"] - r["measured_ms"]) / r["measured_ms"]
+    err = [abs(r["rel_error"]) for r in rows]
+    mid = [abs(r["rel_error"]) for r in rows if (1 << 22) <= r["chunk_elems"] <= (1 << 25)]
     return dict(rows=rows, model_pick=best_pred, measured_best=best_meas["chunk_elems"],
                 measured_at_model_pick_ms=at_pick, measured_best_ms=best_meas["measured_ms"],
-                mean_abs_rel_error=sum(err) / len(err), max_abs_rel_error=max(err))
+                mean_abs_rel_error=sum(err) / len(err), max_abs_rel_error=max(err),
+                max_abs_rel_error_4m_to_32m=max(mid))
+
+
+LINK_COPY_BYTES = (32 << 20, 64 << 20, 128 << 20)  # the update pass's copies at 8M, 16M, 32M-element chunks
+
+
+def measure_link(torch, np, sdp, ctx, pinned, runs=4):
+    """Pinned link bandwidth on both of the engine's device-to-host paths, at
+    the copy sizes of the engine's update pass: runtime copies both ways
+    (sdp_probe_link), and runtime copies in with the library's copy kernel
+    out (sdp_probe_link_kernel).  The bound takes, per direction and for both
+    at once, the fastest figure of either path at any of these sizes over
+    `runs` runs: the largest rate, so the tightest bound that is still a
+    bound for whichever path the engine takes."""
+    probe_bytes = 1 << 30
+    ha, hb = pinned(np.uint8, probe_bytes), pinned(np.uint8, probe_bytes)
+    ha[:] = 1
+    da = torch.empty(probe_bytes, dtype=torch.uint8, device="cuda")
+    db = torch.empty(probe_bytes, dtype=torch.uint8, device="cuda")
+    args = (ctx, ha.ctypes.data, hb.ctypes.data, da.data_ptr(), db.data_ptr(), probe_bytes)
+    sdp.sdp_probe_link(*args, LINK_COPY_BYTES[-1], 2)  # first copies on fresh streams do not overlap
+    sdp.sdp_probe_link_kernel(*args, LINK_COPY_BYTES[-1], 2)
+    table = []
+    for cb in LINK_COPY_BYTES:
+        rt = [sdp.sdp_probe_link(*args, cb, 2) for _ in range(runs)]
+        kn = [sdp.sdp_probe_link_kernel(*args, cb, 2) for _ in range(runs)]
+        table.append(dict(copy_bytes=cb, runtime=[max(r[k] for r in rt) for k in range(3)],
+                          copy_kernel=[max(r[k] for r in kn) for k in range(3)]))
+    del da, db
+    best = [max(max(row["runtime"][k], row["copy_kernel"][k]) for row in table) for k in range(3)]
+    return best, table
+
+
+def link_bound_ms(N, R, link, d2h_per_param=14):
+    """The streamed step's resource lower bound (ms): the norm pass's 2R B per
+    parameter in, then the update pass's 12 B in and 14 B (12 with the BF16
+    parameters rounded on the host) out, each direction at its own rate and
+    both together at the bidirectional rate."""
+    h2d, d2h, both = (x * 1e9 for x in link)
+    return 1e3 * (2 * R * N / h2d + max(12 * N / h2d, d2h_per_param * N / d2h, (12 + d2h_per_param) * N / both))
 
 
 def stream_leg(args, torch, np, synth, sdp, dres):
@@ -435,22 +560,8 @@ def stream_leg(args, torch, np, synth, sdp, dres):
     segs = sdp.Segments([(p.ctypes.data, m.ctypes.data, v.ctypes.data, pb.ctypes.data,
                           [x.ctypes.data for x in g], N)])
     ctx = sdp.sdp_ctx_create(0, C, R, 0)
-    # Pinned link bandwidth with the engine's copy path and its largest copy
-    # (one chunk of one FP32 state array).  How much the two directions
-    # overlap varies from run to run (57 to 97 GB/s together), so the best
-    # of ten runs is kept: the bound below is then the tightest one.
-    probe_bytes, copy_bytes = 1 << 30, 4 * C
-    ha, hb = pinned(np.uint8, probe_bytes), pinned(np.uint8, probe_bytes)
-    ha[:] = 1
-    da = torch.empty(probe_bytes, dtype=torch.uint8, device="cuda")
-    db = torch.empty(probe_bytes, dtype=torch.uint8, device="cuda")
-    probe = lambda reps: sdp.sdp_probe_link(ctx, ha.ctypes.data, hb.ctypes.data, da.data_ptr(),  # noqa: E731
-                                            db.data_ptr(), probe_bytes, copy_bytes, reps)
-    probe(2)
-    runs = [probe(2) for _ in range(10)]
-    link = [max(r[k] for r in runs) for k in range(3)]
-    del da, db
-    log(f"streamed leg: link h2d {link[0]:.1f} d2h {link[1]:.1f} both {link[2]:.1f} GB/s")
+    link, link_table = measure_link(torch, np, sdp, ctx, pinned)
+    log(f"streamed leg: link h2d {link[0]:.1f} d2h {link[1]:.1f} both {link[2]:.1f} GB/s (best of both paths)")
     def timed(c, sg):
         sdp.sdp_stream_step(c, sg, sdp.make_params(**w.hparams(1)), C)  # warmup
         t0 = time.perf_counter()
@@ -461,12 +572,11 @@ def stream_leg(args, torch, np, synth, sdp, dres):
     el = timed(ctx, segs)
     rates, rate_vals = measure_rates(args, torch, np, sdp, ctx, link, dres)
     h2d_b, d2h_b = sdp.sdp_bytes_per_elem(True, R, 0)
-    t_link = (2 * R * N / (link[0] * 1e9)
-              + max(12 * N / (link[0] * 1e9), 14 * N / (link[1] * 1e9), 26 * N / (link[2] * 1e9)))
+    t_link = link_bound_ms(N, R, link) / 1e3
     sdp.sdp_ctx_destroy(ctx)
     out = dict(workload=w.name, params=N, ranks=R, chunk_elems=C, ms_per_step=el * 1e3,
                params_per_s=N / el, h2d_gbs=h2d_b * N / el / 1e9, d2h_gbs=d2h_b * N / el / 1e9,
-               link_gbs={"h2d": link[0], "d2h": link[1], "bidir": link[2]},
+               link_gbs={"h2d": link[0], "d2h": link[1], "bidir": link[2]}, link_probe=link_table,
                t_link_ms=t_link * 1e3, frac_of_link_bound=t_link / el, model_rates=rate_vals,
                predicted_ms=sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, C, 0, rates).predicted_ms)
     # the same step with the BF16 parameters rounded on the host from the
@@ -475,8 +585,7 @@ def stream_leg(args, torch, np, synth, sdp, dres):
     hctx = sdp.sdp_ctx_create(0, C, R, sdp.SDP_FLAG_STREAM_HOST_CAST)
     hel = timed(hctx, segs)
     sdp.sdp_ctx_destroy(hctx)
-    t_link_hc = (2 * R * N / (link[0] * 1e9)
-                 + max(12 * N / (link[0] * 1e9), 12 * N / (link[1] * 1e9), 24 * N / (link[2] * 1e9)))
+    t_link_hc = link_bound_ms(N, R, link, d2h_per_param=12) / 1e3
     out["host_cast"] = dict(ms_per_step=hel * 1e3, params_per_s=N / hel, d2h_bytes_per_param=12,
                             t_link_ms=t_link_hc * 1e3, frac_of_link_bound=t_link_hc / hel,
                             predicted_ms=sdp.sdp_predict_step(sdp.SDP_SCHED_STREAMED, [N], R, C,
@@ -597,12 +706,18 @@ def host_route_leg(args, torch, np, synth, sdp, rates):
         el = (time.perf_counter() - t0) / args.stream_steps
         kt = sdp.sdp_ctx_get_timing(ctx)
         sdp.sdp_ctx_set_timing(ctx, 0)
+        # the calling thread's time to enqueue one piece (kernel and copy),
+        # timed by the library around those calls: the model's per-piece
+        # host cost of this schedule
+        issue_us = kt.host_issue_ms * 1e3 / max(kt.host_issues, 1)
+        if rates is not None:
+            rates.host_issue_us = issue_us
         k = args.stream_steps
         host_bytes = (26 + gsz) * N  # p, m, v read and written, g_bar read, BF16 params written
         adam_s = kt.host_adam_ms / k / 1e3
         # host memory carries the host lane's bytes and the copies' bytes
         bound = max((host_bytes + gsz * N) / (host_copy * 1e9), gsz * N / (d2h * 1e9))
-        out[name] = dict(ms_per_step=el * 1e3, params_per_s=N / el, d2h_bytes_per_param=gsz,
+        out[name] = dict(ms_per_step=el * 1e3, params_per_s=N / el, d2h_bytes_per_param=gsz, host_issue_us=issue_us,
                          gpu_norm_ms=(kt.norm_ms + kt.finalize_ms) / k, gbar_kernel_ms=kt.gbar_ms / k,
                          host_adam_ms=kt.host_adam_ms / k, host_wait_ms=kt.host_wait_ms / k,
                          host_adam_gbs=host_bytes / adam_s / 1e9, host_adam_params_per_s=N / adam_s,
@@ -647,20 +762,101 @@ def host_route_leg(args, torch, np, synth, sdp, rates):
     return out
 
 
+def mem_available_gib():
+    with open("/proc/meminfo") as f:
+        for line in f:
+            if line.startswith("MemAvailable:"):
+                return int(line.split()[1]) / (1 << 20)
+    return 0.0
+
+
+def full_model_leg(args, torch, np, synth, sdp, link):
+    """The full Qwen3-14B model (42 segments, R = 2, 32M-element chunks) with
+    every state in pageable host memory: the staged streamed step against the
+    same link bound as the layer, and the host-update route with the BF16
+    mean gradient (its gradients copied to HBM first).  Inputs are generated
+    before the timed steps; one untimed step comes first in each mode."""
+    w = synth.workload(3)
+    sizes = [s.numel for s in w.segments]
+    N, R, C = w.numel, w.ranks, w.chunk
+    need = N * (14 + 2 * R) / (1 << 30) + 8
+    avail = mem_available_gib()
+    if avail < need:
+        log(f"full model leg skipped: needs {need:.0f} GiB of host memory, {avail:.0f} GiB available")
+        return dict(workload=w.name, skipped=f"needs {need:.0f} GiB of host memory, {avail:.0f} GiB available")
+    log(f"full model leg: {w.name} N={N} R={R} chunk={C}, {len(sizes)} segments; {avail:.0f} GiB available")
+    # the staged context pins its bounce buffers before the host state exists
+    ctx = sdp.sdp_ctx_create(0, C, R, sdp.SDP_FLAG_STREAM_STAGED)
+    t0 = time.perf_counter()
+    p, m, v, pb, g = [], [], [], [], []
+    for s, n in enumerate(sizes):
+        p.append(synth.master(w, s))
+        m.append(np.zeros(n, np.float32))
+        v.append(np.zeros(n, np.float32))
+        pb.append(np.zeros(n, np.uint16))
+        g.append([synth.grad_bf16(w, s, 1, r) for r in range(R)])
+        if s % 7 == 6:
+            log(f"full model leg: {s + 1}/{len(sizes)} segments generated, {time.perf_counter() - t0:.0f} s")
+    gen_s = time.perf_counter() - t0
+    log(f"full model leg: inputs generated in {gen_s:.0f} s")
+    segs = sdp.Segments([(p[s].ctypes.data, m[s].ctypes.data, v[s].ctypes.data, pb[s].ctypes.data,
+                          [x.ctypes.data for x in g[s]], sizes[s]) for s in range(len(sizes))])
+    out = dict(workload=w.name, params=N, ranks=R, chunk_elems=C, segments=len(sizes),
+               states="pageable host memory", input_generation_s=gen_s)
+    try:
+        sdp.sdp_stream_step(ctx, segs, sdp.make_params(**w.hparams(1)), C)
+        times = []
+        for t in range(2, args.full_steps + 2):
+            ts = time.perf_counter()
+            sdp.sdp_stream_step(ctx, segs, sdp.make_params(**w.hparams(t)), C)
+            times.append(time.perf_counter() - ts)
+            log(f"full model leg: staged streamed step {times[-1]:.2f} s")
+        el = sum(times) / len(times)
+        t_link = link_bound_ms(N, R, link) / 1e3
+        h2d_b, d2h_b = sdp.sdp_bytes_per_elem(True, R, 0)
+        out["staged_streamed"] = dict(ms_per_step=el * 1e3, steps=len(times), params_per_s=N / el,
+                                      h2d_gbs=h2d_b * N / el / 1e9, d2h_gbs=d2h_b * N / el / 1e9,
+                                      t_link_ms=t_link * 1e3, frac_of_link_bound=t_link / el,
+                                      link_gbs={"h2d": link[0], "d2h": link[1], "bidir": link[2]})
+    finally:
+        sdp.sdp_ctx_destroy(ctx)
+    # the host-update route on the same state, gradients moved to HBM
+    dg = [[torch.from_numpy(x.view(np.int16)).to("cuda") for x in gs] for gs in g]
+    torch.cuda.synchronize()
+    rctx = sdp.sdp_ctx_create(0, C, R, 0)
+    try:
+        rsegs = sdp.Segments([(p[s].ctypes.data, m[s].ctypes.data, v[s].ctypes.data, pb[s].ctypes.data,
+                               [x.data_ptr() for x in dg[s]], sizes[s]) for s in range(len(sizes))])
+        sdp.sdp_host_update_step(rctx, rsegs, sdp.make_params(**w.hparams(1)), C, sdp.SDP_GBAR_BF16)
+        times = []
+        for t in range(2, args.full_steps + 2):
+            ts = time.perf_counter()
+            sdp.sdp_host_update_step(rctx, rsegs, sdp.make_params(**w.hparams(t)), C, sdp.SDP_GBAR_BF16)
+            times.append(time.perf_counter() - ts)
+        el = sum(times) / len(times)
+        out["host_route_bf16"] = dict(ms_per_step=el * 1e3, steps=len(times), params_per_s=N / el,
+                                      grads="device memory", d2h_bytes_per_param=2)
+        log(f"full model leg: host route {el:.2f} s per step")
+    finally:
+        sdp.sdp_ctx_destroy(rctx)
+    del dg, p, m, v, pb, g
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    # the device step takes about 20 steps to settle after the inputs are
-    # uploaded (the fused update runs about 10% slower at first), so the
-    # default warm-up covers that
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=30)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--no-stream", action="store_true", help="skip the streamed-mode leg")
+    ap.add_argument("--no-stream", action="store_true", help="skip the streamed-mode and host-route legs")
+    ap.add_argument("--no-full-model", action="store_true", help="skip the full Qwen3-14B model leg")
     ap.add_argument("--stream-steps", type=int, default=3)
+    ap.add_argument("--full-steps", type=int, default=2, help="timed steps of each full-model mode")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-extra", action="store_true",
-                    help="skip the Qwen2.5-72B layer (R = 8) device leg and the staged streamed run")
+                    help="skip the chunk sweeps, the staged layer run and parameter delivery")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -679,54 +875,62 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     torch.cuda.set_device(0)
-    dres, master, host_grads, w = device_leg(args, torch, np, synth, sdp, 1, args.steps, args.warmup, True)
+    # the headline: the Qwen2.5-72B layer in HBM
+    head, master, host_grads, w = device_leg(args, torch, np, synth, sdp, 4, args.steps, args.warmup, False)
+    ceiling = copy_ceiling(torch, sdp, head["ctx"], torch.cuda.current_stream())
+    log("copy ceiling: " + ", ".join(f"{k} {v:.0f} GB/s" for k, v in ceiling.items()))
+    release(torch, sdp, head)
     tref = torch_leg(torch, np, w, master, host_grads, 10, 3)
     if tref is not None:
-        tref["library_speedup"] = tref["ms_per_step"] / dres["ms_per_step"]
+        tref["library_speedup"] = tref["ms_per_step"] / head["ms_per_step"]
     cpu = None if args.no_cpu else cpu_leg(args, np, synth, oracle, master, host_grads, w)
     del master, host_grads
-    r8 = None
-    if not args.no_extra:
-        r8_res, _, _, _ = device_leg(args, torch, np, synth, sdp, 4, 10, 2, False)
-        r8 = brief(r8_res)
-    streamed, rates = (None, None) if args.no_stream else stream_leg(args, torch, np, synth, sdp, dres)
+    # the Qwen3-8B layer in HBM
+    q8, _, _, _ = device_leg(args, torch, np, synth, sdp, 1, args.steps, args.warmup, True)
+    release(torch, sdp, q8)
+    streamed, rates = (None, None) if args.no_stream else stream_leg(args, torch, np, synth, sdp, q8)
     route = None if args.no_stream else host_route_leg(args, torch, np, synth, sdp, rates)
+    full = None
+    if not args.no_full_model:
+        link = ([streamed["link_gbs"][k] for k in ("h2d", "d2h", "bidir")] if streamed else None)
+        if link is None:
+            full = dict(skipped="needs the streamed leg's link measurement")
+        else:
+            full = full_model_leg(args, torch, np, synth, sdp, link)
 
-    traffic = measured_traffic(dres["update_bytes"])
     out = {
         "metric": METRIC,
-        "value": dres["params_per_s"],
+        "value": head["params_per_s"],
         "unit": "params/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": dres["ms_per_step"],
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f64",
         "data": "synthetic",
-        "config": {"workload": dres["workload"], "params": dres["N"], "ranks": dres["R"],
-                   "mode": "device", "chunk_elems": dres["chunk"],
-                   "states": "fp32 master/exp_avg/exp_avg_sq, bf16 grads and params",
+        "config": {"workload": head["workload"], "params": head["N"], "ranks": head["R"],
+                   "mode": "device", "chunk_elems": head["chunk"],
+                   "states": "fp32 master/exp_avg/exp_avg_sq, bf16 grads and params; mean gradient stored",
                    "parallelism": "single GPU; R rank gradients as separate buffers"},
-        "step_hbm_gbs": dres["step_hbm_gbs"],
-        "step_hbm_frac": dres["step_hbm_gbs"] / HBM_PEAK_GBS,
-        "kernel_ms": {"fused_update": dres["update_ms"], "norm_partials": dres["norm_ms"],
-                      "norm_finalize": dres["finalize_ms"],
+        "step_bytes_per_param": head["step_bytes_per_elem"],
+        "step_hbm_gbs": head["step_hbm_gbs"],
+        "step_hbm_frac": head["step_hbm_gbs"] / HBM_PEAK_GBS,
+        "kernel_ms": {"fused_update": head["update_ms"], "norm_partials": head["norm_ms"],
+                      "norm_finalize": head["finalize_ms"],
                       "timing": f"HIP events around each launch over {args.steps} further steps "
-                                f"({dres['ms_per_step_with_events']:.4f} ms per step with the events)"},
-        "roofline": {"bound": "hbm", "achieved": dres["update_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": dres["update_gbs"] / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "fused aggregate+clip+AdamW+BF16 update",
-                     "algorithmic_bytes_per_launch": dres["update_bytes"]},
-        "hbm_copy_gbs": dres["copy_gbs"],
-        "update_pattern_gbs": dres["pattern_gbs"],
-        "update_frac_of_pattern": dres["update_gbs"] / dres["pattern_gbs"],
-        "grad_norm_last_step": dres["grad_norm"],
+                                f"({head['ms_per_step_with_events']:.4f} ms per step with the events)"},
+        "roofline": roofline(head, "update", 4, "fused update from the stored mean gradient (clip+AdamW+BF16)"),
+        "norm_roofline": roofline(head, "norm", 4, "norm partials storing the mean gradient"),
+        "copy_ceiling_gbs": ceiling,
+        "step_frac_of_copy_ceiling": head["step_hbm_gbs"] / max(ceiling.values()),
+        "grad_norm_last_step": head["grad_norm"],
+        "qwen3_8b_layer": brief(q8, 1, pattern=True),
         "streamed": streamed,
         "host_route": route,
-        "device_r8": r8,
+        "full_model": full,
         "torch_eager": tref,
         "cpu_baseline": cpu,
     }

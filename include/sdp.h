@@ -165,6 +165,8 @@ typedef struct {
     double host_adam_ms;  /* host threads running AdamW (host clock) */
     double host_wait_ms;  /* host waiting for a chunk's g_bar copy to land (host clock) */
     int64_t host_adam_elems;
+    double host_issue_ms; /* the calling thread enqueueing the next piece's kernel and copy (host clock) */
+    int64_t host_issues;  /* pieces so enqueued */
 } sdp_kernel_times;
 
 /* ---- context ----------------------------------------------------------- */
@@ -359,6 +361,8 @@ typedef struct {
     double dma_host_cost;    /* host memory bandwidth a host task loses per byte of DMA in
                                 flight (1: the DMA's own bytes; measured from the host AdamW
                                 lane beside a device-to-host copy) */
+    double host_issue_us;    /* host-update route: the calling thread's time to enqueue one
+                                piece's mean-gradient kernel and copy */
 } sdp_rates;
 
 /* What the model predicts for one call. */

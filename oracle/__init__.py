@@ -10,7 +10,8 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# ORACLE_LIB names another build of oracle.c (the sanitizer run's)
+LIB_PATH = os.environ.get("ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 CFLAGS = ["-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11",
           "-ffp-contract=off", "-fno-fast-math"]
 
@@ -73,6 +74,8 @@ def _declare(L):
     L.orc_update_points.restype = None
     L.orc_update_points.argtypes = [i64, vp, vp, vp, vp, i32, dbl,
                                     ctypes.POINTER(HParams), vp, vp, vp, vp]
+    L.orc_update_given_clip.restype = None
+    L.orc_update_given_clip.argtypes = [i64, vp, vp, vp, vp, vp, i32, dbl, ctypes.POINTER(HParams), i32]
     L.orc_num_threads.restype = ctypes.c_int
     L.orc_num_threads.argtypes = []
     L.orc_set_num_threads.restype = None
@@ -218,6 +221,22 @@ def update_points(p, m, v, g_rows, clip_c: float, hp: HParams, lib=None, gbar_bf
                             g_rows.ctypes.data, R, clip_c, ctypes.byref(hp), int(bool(gbar_bf16)),
                             po.ctypes.data, mo.ctypes.data, vo.ctypes.data, pb.ctypes.data)
     return po, mo, vo, pb
+
+
+def update_given_clip(p, m, v, pb, gs, clip_c: float, hp: HParams, lib=None, gbar_bf16=False):
+    """Update the arrays p, m, v, pb in place from the R gradient arrays gs
+    with a known clip coefficient (no norm pass)."""
+    L = lib or load()
+    n = p.size
+    for a, dt in ((p, np.float32), (m, np.float32), (v, np.float32), (pb, np.uint16)):
+        assert a.size == n
+        _ptr(a, dt)
+    for g in gs:
+        assert g.size == n
+    ptrs = (ctypes.c_void_p * len(gs))(*[_ptr(g, np.uint16) for g in gs])
+    L.orc_update_given_clip(n, p.ctypes.data, m.ctypes.data, v.ctypes.data, pb.ctypes.data,
+                            ctypes.cast(ptrs, ctypes.c_void_p), len(gs), clip_c, ctypes.byref(hp),
+                            int(bool(gbar_bf16)))
 
 
 def num_threads(lib=None) -> int:

@@ -564,6 +564,24 @@ void orc_update_points_fmt(int64_t n, const float *p, const float *m, const floa
     }
 }
 
+/* Steps 1, 4 and 5 over n consecutive elements whose clip coefficient is
+ * already known, in place (for a full check of a state too large to step in
+ * one call: the norm comes from orc_grad_norm over all of it).  grads holds
+ * R pointers, each to the n BF16 gradients of one rank. */
+void orc_update_given_clip(int64_t n, float *p, float *m, float *v, uint16_t *pb,
+                           const uint16_t *const *grads, int32_t R, double clip_coef,
+                           const orc_hparams *hp, int gbar_bf16)
+{
+    if (R < 1 || R > ORC_MAX_RANKS)
+        return;
+    double bc1, bc2;
+    bias_corrections(hp, &bc1, &bc2);
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i)
+        update_one(&p[i], &m[i], &v[i], &pb[i],
+                   update_gradient(orc_mean_grad(grads, R, i), gbar_bf16), clip_coef, hp, bc1, bc2);
+}
+
 /* Threads of the OpenMP loops from now on (n >= 1); for timing only. */
 void orc_set_num_threads(int n)
 {

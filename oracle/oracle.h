@@ -66,6 +66,10 @@ void orc_update_points_fmt(int64_t n, const float *p, const float *m, const floa
                            const orc_hparams *hp, int gbar_bf16, float *p_out,
                            float *m_out, float *v_out, uint16_t *pb_out);
 
+void orc_update_given_clip(int64_t n, float *p, float *m, float *v, uint16_t *pb,
+                           const uint16_t *const *grads, int32_t R, double clip_coef,
+                           const orc_hparams *hp, int gbar_bf16);
+
 int orc_num_threads(void);
 void orc_set_num_threads(int n);
 

@@ -95,7 +95,7 @@ int host_route(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R,
         // h2d_done doubles as "g_bar of this slot is written" here
         HIP_TRY(hipEventRecord(ctx->h2d_done[sl], sc));
         HIP_TRY(hipStreamWaitEvent(sy, ctx->h2d_done[sl], 0));
-        SDP_TRY(d2h_copies(ctx, {{host, dev}}, {(size_t)c.len * esz}, sy));
+        SDP_TRY(d2h_copies(ctx, {{host, dev}}, {(size_t)c.len * esz}, sy, &ctx->stage_map));
         HIP_TRY(hipEventRecord(ctx->slot_free[sl], sy));  // in the host buffer; the slot is free
         used[sl] = true;
         return SDP_OK;
@@ -103,6 +103,7 @@ int host_route(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R,
     if (!chunks.empty()) SDP_TRY(issue(0));
     for (size_t j = 0; j < chunks.size(); ++j) {
         // the next chunk's kernel and copy run while the host updates this one
+        const Clock::time_point ti = Clock::now();
         if (j + 1 < chunks.size()) SDP_TRY(issue(j + 1));
         const int sl = (int)(j & 1);
         const Clock::time_point t0 = Clock::now();
@@ -121,6 +122,10 @@ int host_route(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R,
         if (ctx->timing) {
             const Clock::time_point t2 = Clock::now();
             ctx->host_wait_ms += ms_between(t0, t1);
+            if (j + 1 < chunks.size()) {
+                ctx->host_issue_ms += ms_between(ti, t0);
+                ctx->host_issues += 1;
+            }
             ctx->host_adam_ms += ms_between(t1, t2);
             ctx->host_adam_elems += c.len;
         }

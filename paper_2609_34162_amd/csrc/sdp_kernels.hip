@@ -729,7 +729,8 @@ __global__ __launch_bounds__(256) void k_fill_u32(uint32_t *__restrict__ dst, in
         for (int64_t i = n4 * 4; i < n_words; ++i) dst[i] = value;
 }
 
-inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+// ceil(a / b) for a >= 0, b > 0, without overflow near the int64 limit
+inline int64_t cdiv(int64_t a, int64_t b) { return a / b + (a % b != 0); }
 
 template <int R>
 hipError_t norm_r(const NormArgs &a, int store_lds_pad, hipStream_t s) {

@@ -51,7 +51,8 @@ int fail(int status, const char *fmt, ...);
         if (rc_ != SDP_OK) return rc_; \
     } while (0)
 
-inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+// ceil(a / b) for a >= 0, b > 0, without overflow near the int64 limit
+inline int64_t cdiv(int64_t a, int64_t b) { return a / b + (a % b != 0); }
 inline int64_t round_up(int64_t a, int64_t b) { return cdiv(a, b) * b; }
 
 struct DeviceGuard {
@@ -235,12 +236,14 @@ struct sdp_ctx {
     // staged streamed mode: pinned bounce buffers shaped like the slots
     char *bounce_in = nullptr;   // kInBufs x slot_bytes
     char *bounce_out = nullptr;  // kOutBufs x 14 * max_chunk (master, m, v, bf16 part of a slot)
+    ptrdiff_t bounce_out_map = 0;  // device mapping of bounce_out minus its host address
     hipEvent_t bin_done[sdprt::kInBufs] = {};   // copy stream: the copies out of bounce_in[k] are done
     hipEvent_t d2h_done[sdprt::kOutBufs] = {};  // compute stream: the copies into bounce_out[k] are done
     bool bin_used[sdprt::kInBufs] = {};
     // parameter delivery and the host-update route: two pinned buffers of
     // 4 * max_chunk bytes each (one chunk of FP32), created on first use
     char *stage = nullptr;
+    ptrdiff_t stage_map = 0;  // device mapping of stage minus its host address
     bool stage_used[2] = {false, false};
     std::vector<sdprt::Xfer> pending_out[sdprt::kOutBufs];
     // SDP_FLAG_STREAM_HOST_CAST: the BF16 rounding of each chunk whose master
@@ -262,7 +265,8 @@ struct sdp_ctx {
     bool timing = false;
     std::vector<sdprt::Timed> timed;
     // host lanes of the host-update route, timed on the host clock
-    double host_adam_ms = 0.0, host_wait_ms = 0.0;
+    double host_adam_ms = 0.0, host_wait_ms = 0.0, host_issue_ms = 0.0;
+    int64_t host_issues = 0;
     int64_t host_adam_elems = 0;
     std::vector<hipEvent_t> pool;
 };
@@ -367,9 +371,13 @@ constexpr int64_t kD2HKernelMaxBytes = 64ll << 20;
 constexpr int kD2HLaunchBlocks = 32;
 constexpr int kD2HMinBlocksPerCopy = 8;
 // Device -> pinned host copies (dst <- src, bytes) enqueued on stream st,
-// through the copy kernel where they qualify (sdp_stream.hip).
+// through the copy kernel where they qualify (sdp_stream.hip).  own_map:
+// NULL, or the offset of the device mapping of the destinations, which are a
+// buffer of the context's own (no attribute query then).
 int d2h_copies(sdp_ctx *ctx, const std::vector<std::pair<char *, const char *>> &ends,
-               const std::vector<size_t> &bytes, hipStream_t st);
+               const std::vector<size_t> &bytes, hipStream_t st, const ptrdiff_t *own_map);
+// Offset of the device's mapping of pinned host memory p from p itself.
+int device_map_offset(const void *p, ptrdiff_t *out);
 HostPool *new_pool(const sdp_ctx *ctx, int threads);
 inline size_t stage_bytes(const sdp_ctx *ctx) { return 4 * (size_t)ctx->max_chunk; }
 int ensure_host_stage(sdp_ctx *ctx);

@@ -452,7 +452,23 @@ int ensure_host_stage(sdp_ctx *ctx) {
                         2 * stage_bytes(ctx));
         }
         ctx->stage_used[0] = ctx->stage_used[1] = false;
+        const int rc = device_map_offset(ctx->stage, &ctx->stage_map);
+        if (rc != SDP_OK) {
+            (void)hipHostFree(ctx->stage);
+            ctx->stage = nullptr;
+            return rc;
+        }
     }
+    return SDP_OK;
+}
+
+int device_map_offset(const void *p, ptrdiff_t *out) {
+    hipPointerAttribute_t at;
+    if (hipPointerGetAttributes(&at, p) != hipSuccess || at.type != hipMemoryTypeHost || !at.devicePointer) {
+        (void)hipGetLastError();
+        return fail(SDP_ERR_HIP, "pinned buffer %p has no device mapping", p);
+    }
+    *out = (const char *)at.devicePointer - (const char *)p;
     return SDP_OK;
 }
 
@@ -542,7 +558,7 @@ int check_model_args(int schedule, const int64_t *numels, int32_t n_segs, int32_
     const double pos[] = {r->h2d_gbs,    r->d2h_gbs,  r->both_gbs,     r->norm_gbs,
                           r->update_gbs, r->host_gbs, r->host_adam_gbs};
     const double nonneg[] = {r->copy_cmd_us, r->launch_us, r->sync_us, r->host_task_us, r->dep_us,
-                             r->dma_host_cost};
+                             r->dma_host_cost, r->host_issue_us};
     for (double x : pos)
         if (!(std::isfinite(x) && x > 0.0)) return fail(SDP_ERR_INVALID_ARGUMENT, "rates must be finite and > 0");
     for (double x : nonneg)
@@ -557,7 +573,7 @@ int check_model_args(int schedule, const int64_t *numels, int32_t n_segs, int32_
 sdp_sched::Rates to_rates(const sdp_rates *r) {
     return sdp_sched::Rates{r->h2d_gbs,   r->d2h_gbs,  r->both_gbs, r->copy_cmd_us,  r->norm_gbs,
                             r->update_gbs, r->launch_us, r->sync_us,  r->host_gbs,     r->host_task_us,
-                            r->host_adam_gbs, r->dep_us, r->dma_host_cost};
+                            r->host_adam_gbs, r->dep_us, r->dma_host_cost, r->host_issue_us};
 }
 
 int model_chunk_ok(const std::vector<int64_t> &sizes, int64_t chunk) {
@@ -742,6 +758,8 @@ int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems, int32_t m
         }
         for (int k = 0; k < kInBufs; ++k)
             CTX_HIP(hipEventCreateWithFlags(&c->bin_done[k], hipEventDisableTiming));
+        rc = device_map_offset(c->bounce_out, &c->bounce_out_map);
+        if (rc != SDP_OK) return bail(rc);
     }
     if (flags & (SDP_FLAG_STREAM_STAGED | SDP_FLAG_STREAM_HOST_CAST)) {
         if (max_chunk_elems <= 0)
@@ -898,8 +916,8 @@ int sdp_ctx_set_timing(sdp_ctx *ctx, int enable) {
             ctx->pool.push_back(t.b);
         }
         ctx->timed.clear();
-        ctx->host_adam_ms = ctx->host_wait_ms = 0.0;
-        ctx->host_adam_elems = 0;
+        ctx->host_adam_ms = ctx->host_wait_ms = ctx->host_issue_ms = 0.0;
+        ctx->host_adam_elems = ctx->host_issues = 0;
         // events ready in advance: creating one takes host time, which a call
         // on the host-bound route would otherwise spend before its launches
         while (ctx->pool.size() < kTimingEvents) {
@@ -939,6 +957,8 @@ int sdp_ctx_get_timing(sdp_ctx *ctx, sdp_kernel_times *out) {
     r.host_adam_ms = ctx->host_adam_ms;
     r.host_wait_ms = ctx->host_wait_ms;
     r.host_adam_elems = ctx->host_adam_elems;
+    r.host_issue_ms = ctx->host_issue_ms;
+    r.host_issues = ctx->host_issues;
     *out = r;
     return SDP_OK;
 }

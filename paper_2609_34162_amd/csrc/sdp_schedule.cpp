@@ -19,9 +19,10 @@
 //    master and writes its BF16 parameters, in the same issue order;
 //  - host-update route: the norm pass and read-back, then per piece (see
 //    route_pieces: a ramp of growing pieces, then chunks) the mean-gradient kernel
-//    (after the slot's previous outgoing copy, and issued by the host after
-//    it finished the update of piece j-2), its copy to the host on the copy
-//    stream, and the host update after the copy.
+//    (after the slot's previous outgoing copy, and enqueued by the host
+//    thread, which takes host_issue_us for it, after it finished the update
+//    of piece j-2), its copy to the host on the copy stream, and the host
+//    update after the copy.
 #include "sdp_schedule.h"
 
 #include <algorithm>
@@ -350,7 +351,9 @@ void build_host_route(Graph &g, const std::vector<int64_t> &numels, int R, int64
     };
     if (!ch.empty()) issue(0, -1);
     for (size_t j = 0; j < ch.size(); ++j) {
-        if (j + 1 < ch.size()) issue(j + 1, j >= 1 ? adam[j - 1] : -1);
+        // the calling thread enqueues the next piece, then waits for this
+        // piece's copy and updates it
+        if (j + 1 < ch.size()) issue(j + 1, g.add(kHostS, kFixed, r.host_issue_us, 0, 0, {}));
         adam[j] = g.host((26.0 + esz) * (double)ch[j].len, r.host_adam_gbs, r.host_task_us, {d2h[j]});
     }
 }
@@ -365,7 +368,7 @@ Prediction predict(int schedule, const std::vector<int64_t> &numels, int R, int6
     else
         build_host_route(g, numels, R, chunk, schedule == kHostRouteBf16, r);
     Prediction p{};
-    for (int64_t n : numels) p.n_chunks += (n + chunk - 1) / chunk;
+    for (int64_t n : numels) p.n_chunks += n / chunk + (n % chunk != 0);  // no overflow near the int64 limit
     p.h2d_ms = g.h2d_bytes / (r.h2d_gbs * 1e9) * 1e3;
     p.d2h_ms = g.d2h_bytes / (r.d2h_gbs * 1e9) * 1e3;
     p.link_ms = (g.h2d_bytes + g.d2h_bytes) / (r.both_gbs * 1e9) * 1e3;

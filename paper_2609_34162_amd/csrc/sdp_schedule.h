@@ -40,6 +40,7 @@ struct Rates {
     double host_adam_gbs;               // host AdamW lane alone (bytes read + written)
     double dep_us;                      // an event recorded on one GPU stream, waited on by the other
     double dma_host_cost;               // host memory bytes a host task loses per DMA byte
+    double host_issue_us;               // host route: enqueueing one piece's kernel and copy
 };
 
 enum Schedule { kStreamed = 0, kStreamedStaged = 1, kHostRouteF32 = 2, kHostRouteBf16 = 3 };

@@ -20,15 +20,20 @@ namespace sdprt {
 // runtime reports it: the same address for hipHostMalloc memory, possibly
 // another for registered memory; memory without one takes a runtime copy.
 // (The same kernel measured slower than the runtime's host-to-device copies
-// at every chunk size, so those stay runtime copies.)
+// at every chunk size, so those stay runtime copies.)  own_map: the
+// destinations lie in a buffer of the context's own whose device mapping is
+// offset by *own_map from its host address (looked up once, when the buffer
+// was allocated), so no attribute query is needed per copy.
 int d2h_copies(sdp_ctx *ctx, const std::vector<std::pair<char *, const char *>> &ends,
-               const std::vector<size_t> &bytes, hipStream_t st) {
+               const std::vector<size_t> &bytes, hipStream_t st, const ptrdiff_t *own_map) {
     sdp::CopyBatch b{};
     for (size_t k = 0; k < ends.size(); ++k) {
         char *mapped = nullptr;
         if ((int64_t)bytes[k] <= ctx->d2h_kernel_max && b.n < sdp::kCopyBatchMax) {
             hipPointerAttribute_t at;
-            if (hipPointerGetAttributes(&at, ends[k].first) == hipSuccess && at.type == hipMemoryTypeHost)
+            if (own_map)
+                mapped = ends[k].first + *own_map;
+            else if (hipPointerGetAttributes(&at, ends[k].first) == hipSuccess && at.type == hipMemoryTypeHost)
                 mapped = (char *)at.devicePointer;
             else
                 (void)hipGetLastError();
@@ -107,7 +112,7 @@ int copy_out(sdp_ctx *ctx, int sl, int bo, const std::vector<Xfer> &xs) {
             ends.push_back({x.host, dev + x.off});
             bytes.push_back(x.bytes);
         }
-        SDP_TRY(d2h_copies(ctx, ends, bytes, ctx->s_comp));
+        SDP_TRY(d2h_copies(ctx, ends, bytes, ctx->s_comp, nullptr));
         if (host_cast(ctx)) HIP_TRY(hipEventRecord(ctx->d2h_done[bo], ctx->s_comp));
         return SDP_OK;
     }
@@ -116,7 +121,7 @@ int copy_out(sdp_ctx *ctx, int sl, int bo, const std::vector<Xfer> &xs) {
         ends.push_back({bout + r.off, dev + r.off});
         bytes.push_back(r.bytes);
     }
-    SDP_TRY(d2h_copies(ctx, ends, bytes, ctx->s_comp));
+    SDP_TRY(d2h_copies(ctx, ends, bytes, ctx->s_comp, &ctx->bounce_out_map));
     HIP_TRY(hipEventRecord(ctx->d2h_done[bo], ctx->s_comp));
     ctx->pending_out[bo] = xs;
     return SDP_OK;

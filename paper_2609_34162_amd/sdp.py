@@ -10,7 +10,8 @@ import os
 from typing import List, Optional, Sequence, Tuple
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libsdp.so")
+# SDP_LIB names another build of the same library (the sanitizer run's)
+LIB_PATH = os.environ.get("SDP_LIB") or os.path.join(_HERE, "libsdp.so")
 
 # status codes and constants, as in include/sdp.h
 SDP_OK = 0
@@ -74,13 +75,14 @@ class sdp_kernel_times(ctypes.Structure):
                 ("finalize_launches", ctypes.c_int64), ("update_launches", ctypes.c_int64),
                 ("update_elems", ctypes.c_int64), ("gbar_ms", ctypes.c_double),
                 ("gbar_launches", ctypes.c_int64), ("host_adam_ms", ctypes.c_double),
-                ("host_wait_ms", ctypes.c_double), ("host_adam_elems", ctypes.c_int64)]
+                ("host_wait_ms", ctypes.c_double), ("host_adam_elems", ctypes.c_int64),
+                ("host_issue_ms", ctypes.c_double), ("host_issues", ctypes.c_int64)]
 
 
 class sdp_rates(ctypes.Structure):
     _fields_ = [(n, ctypes.c_double) for n in ("h2d_gbs", "d2h_gbs", "both_gbs", "copy_cmd_us", "norm_gbs",
                                               "update_gbs", "launch_us", "sync_us", "host_gbs", "host_task_us",
-                                              "host_adam_gbs", "dep_us", "dma_host_cost")]
+                                              "host_adam_gbs", "dep_us", "dma_host_cost", "host_issue_us")]
 
 
 class sdp_prediction(ctypes.Structure):

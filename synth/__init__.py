@@ -13,7 +13,8 @@ import numpy as np
 from .configs import NORM_TILE, WORKLOADS, Workload, workload  # noqa: F401
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libsynth.so")
+# SYNTH_LIB names another build of gen.c (the sanitizer run's)
+LIB_PATH = os.environ.get("SYNTH_LIB") or os.path.join(_HERE, "libsynth.so")
 KIND_MASTER = 0
 KIND_GRAD = 1
 

@@ -44,7 +44,7 @@ int main(void) {
     FAILIF(pb[0] != 0x3ff3, "BF16 of 1.9");
 
     /* the step-time model */
-    sdp_rates r = {50, 40, 90, 0, 5000, 4000, 0, 0, 1e7, 0, 300, 0, 1};
+    sdp_rates r = {50, 40, 90, 0, 5000, 4000, 0, 0, 1e7, 0, 300, 0, 1, 0};
     sdp_prediction pr;
     FAILIF(sdp_predict_step(SDP_SCHED_STREAMED, numels, 2, 2, SDP_NORM_TILE, 0, &r, &pr) != SDP_OK, "predict");
     FAILIF(!(pr.predicted_ms >= pr.bound_ms && pr.n_chunks == 5), "prediction");

@@ -445,6 +445,23 @@ def pin_bf16_gradient_route(lib):
     assert np.array_equal(pb, d.param_bf16[0])
 
 
+def pin_update_given_clip_equals_step(lib):
+    """The array update with a known clip coefficient (used to check states
+    too large for one oracle call) is the step with that coefficient."""
+    n, R = 70001, 3
+    grads = [rand_grads(n, R, seed=31, outlier_p=0.01)]
+    master = rand_master(n, seed=31)
+    for t, mgn in ((1, 0.05), (2, 0.0)):
+        hp = oracle.hparams(lr=1e-3, weight_decay=0.02, max_grad_norm=mgn, step=t)
+        st = oracle.State([master])
+        _, norm = oracle.step(st, grads, hp, lib=lib)
+        c = oracle.clip_coef(norm, mgn, lib=lib)
+        p, m, v, pb = master.copy(), np.zeros(n, np.float32), np.zeros(n, np.float32), np.zeros(n, np.uint16)
+        oracle.update_given_clip(p, m, v, pb, grads[0], c, hp, lib=lib)
+        for x, y in ((p, st.master[0]), (m, st.exp_avg[0]), (v, st.exp_avg_sq[0]), (pb, st.param_bf16[0])):
+            assert np.array_equal(x, y), t
+
+
 # ---------------------------------------------------------------------------
 # The whole step against torch (library special case, brute force sizes)
 

@@ -81,7 +81,7 @@ ORDER = ["pin_bf16_special_values", "pin_mean_closed_forms", "pin_norm_constant"
          "pin_lr_zero", "pin_identical_ranks", "pin_clip_noop", "pin_nonfinite",
          "pin_param_is_bf16_of_master", "pin_mean_vs_fraction", "pin_mean_exact_quotient", "pin_norm_vs_torch",
          "pin_adamw_f64_vs_torch", "pin_bf16_random_vs_torch", "pin_bf16_gradient_route",
-         "pin_step_vs_torch",
+         "pin_step_vs_torch", "pin_update_given_clip_equals_step",
          "pin_brute_force"]
 
 

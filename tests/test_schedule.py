@@ -49,9 +49,10 @@ def test_streamed_single_chunk_is_the_serial_sum(sdp):
     assert math.isclose(got2.predicted_ms, want2 / 1e3, rel_tol=1e-12)
 
 
-def test_host_route_two_segments_closed_form(sdp):
+@pytest.mark.parametrize("issue_us", [0.0, 29.0])
+def test_host_route_two_segments_closed_form(sdp, issue_us):
     sizes, R = [TILE + 1, 2 * TILE], 4
-    rt = rates(sdp, copy_cmd_us=5.0, launch_us=2.0, sync_us=13.0, host_task_us=17.0)
+    rt = rates(sdp, copy_cmd_us=5.0, launch_us=2.0, sync_us=13.0, host_task_us=17.0, host_issue_us=issue_us)
     for sched, esz in ((sdp.SDP_SCHED_HOST_ROUTE_F32, 4), (sdp.SDP_SCHED_HOST_ROUTE_BF16, 2)):
         got = sdp.sdp_predict_step(sched, sizes, R, 4 * TILE, 0, rt)
         want = sum(us(2 * R * n, 5000.0) + 2.0 for n in sizes) + 2.0 + 13.0
@@ -60,9 +61,10 @@ def test_host_route_two_segments_closed_form(sdp):
         g = [us((2 * R + esz) * n, 5000.0) + 2.0 for n in sizes]
         c = [5.0 + us(esz * n, 40.0) for n in sizes]
         h = [us((26 + esz) * n, 300.0) + 17.0 for n in sizes]
+        # the host thread enqueues chunk 1 (issue_us) right after the read-back
         t_c0 = want + g[0] + c[0]
-        t_h0 = t_c0 + 13.0 + h[0]              # the host learns of each copy's end sync_us later
-        t_c1 = max(want + g[0] + g[1], t_c0) + c[1]
+        t_h0 = max(want + issue_us, t_c0 + 13.0) + h[0]   # the host learns of a copy's end sync_us later
+        t_c1 = max(want + issue_us + g[1], want + g[0] + g[1], t_c0) + c[1]
         total = max(t_h0, t_c1 + 13.0) + h[1]
         assert math.isclose(got.predicted_ms, total / 1e3, rel_tol=1e-12), sched
 
