@@ -187,8 +187,13 @@ SDP_API void sdp_ctx_destroy(sdp_ctx *ctx);
 
 /* ---- the update -------------------------------------------------------- */
 
-/* Device mode.  All state and gradient buffers are device memory of ctx's
- * GPU.  Enqueues on `stream`: the norm pass over every tile of every segment
+/* Device mode: the update of each layer's FP32 master and moments from the
+ * gradient averaged over the R ranks, which the paper's rank-0 worker makes
+ * once per iteration on the host (Design, shared host state and
+ * communication routes: the update worker and gradient return by GPU
+ * reduction), here on the GPU with the states in HBM; the global-norm clip
+ * before it has no counterpart in the paper.  All state and gradient buffers
+ * are device memory of ctx's GPU.  Enqueues on `stream`: the norm pass over every tile of every segment
  * (segment order, then tile order), the norm finalize (a fixed-order merge of
  * the span partials, in two stages above 2,048 of them), and the
  * fused update over every element; the update reads the clip coefficient and
@@ -205,7 +210,12 @@ SDP_API int sdp_agg_adam_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_s
                       const sdp_adamw_params *hp, int64_t chunk_elems,
                       void *stream, double *grad_norm_out);
 
-/* Streamed mode.  All state and gradient buffers are pinned host memory
+/* Streamed mode: the same update with the states in host memory, as the
+ * paper keeps them, moved through the GPU in chunks whose transfers overlap
+ * the previous chunk's work, a staging buffer being refilled only after its
+ * previous consumer has finished (Design, cross-rank pipelining and chunked
+ * overlap within a layer; completion and buffer reuse).  All state and
+ * gradient buffers are pinned host memory
  * (e.g. from sdp_host_alloc), or any host memory when the context was
  * created with SDP_FLAG_STREAM_STAGED.  chunk_elems: a multiple of SDP_NORM_TILE,
  * at most the context's max_chunk_elems, and n_ranks <= its max_ranks.
@@ -278,7 +288,10 @@ SDP_API int sdp_host_adamw(sdp_ctx *ctx, float *master, float *exp_avg, float *e
 SDP_API int sdp_ctx_set_host_threads(sdp_ctx *ctx, int32_t threads);
 SDP_API int sdp_ctx_host_threads(sdp_ctx *ctx, int32_t *threads_out);
 
-/* The global norm of the mean gradient alone (the first pass and finalize of
+/* The global norm of the mean gradient alone: the L2 norm, over every
+ * element of every segment of the call, of the gradient averaged over the
+ * ranks (Design, gradient return by GPU reduction); the paper never clips,
+ * and this is the quantity the update clips by (the first pass and finalize of
  * either mode; device_resident selects device or pinned-host buffers; only
  * grads, n_ranks and numel of each segment are read).  Blocks; chunk_elems
  * is used in streamed mode only, where the pass runs in chunks as phase 1 of

@@ -12,6 +12,8 @@ if TESTS not in sys.path:
 
 
 def pytest_configure(config):
+    import progress
+    progress.CAPTURE = config.pluginmanager.getplugin("capturemanager")
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
     config.addinivalue_line("markers", "big: full-size workload case (long, large memory)")
 

@@ -23,7 +23,9 @@ def need_gpu():
 
 
 def log(msg):
-    print(f"[gpu-test {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+    """A progress line that shows even while pytest captures the test's output."""
+    import progress
+    progress.say(msg)
 
 
 DEV = "cuda:0"

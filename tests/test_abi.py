@@ -92,15 +92,22 @@ def test_bytes_per_element(sdp):
     assert sdp.sdp_bytes_per_elem(True, 2, sdp.SDP_FLAG_STREAM_HOST_CAST | sdp.SDP_FLAG_STREAM_STAGED) == (16.0, 12.0)
 
 
-def test_training_state_bytes_match_paper_table():
+def test_training_state_bytes_match_paper_table(sdp):
     """Per parameter, the paper's training-state table lists BF16 weights and
     BF16 gradients (2 B each), an FP32 master (4 B) and two FP32 moments
-    (8 B): 16 B.  The library's state layout at R = 1 is the same set."""
+    (8 B): 16 B.  The library's streamed mode moves exactly that state once
+    each way at R = 1 with the mean gradient kept on the GPU: in, the
+    gradient and the FP32 master and moments; out, the FP32 master and
+    moments and the BF16 weights."""
     import json
     fx = json.load(open(os.path.join(ROOT, "tests", "golden", "training_state_bytes.json")))
-    assert fx["total_bytes_per_param"] == sum(fx["bytes_per_param"].values()) == 16
-    layout = {"compute_weights_bf16": 2, "gradients_bf16": 2 * 1, "master_fp32": 4, "adam_moments_fp32": 4 + 4}
-    assert layout == fx["bytes_per_param"]
+    b = fx["bytes_per_param"]
+    assert fx["total_bytes_per_param"] == sum(b.values()) == 16
+    h2d, d2h = sdp.sdp_bytes_per_elem(True, 1, 0)
+    assert h2d == b["gradients_bf16"] + b["master_fp32"] + b["adam_moments_fp32"]
+    assert d2h == b["master_fp32"] + b["adam_moments_fp32"] + b["compute_weights_bf16"]
+    # and every state byte of the table crosses exactly once in one direction or the other
+    assert h2d + d2h - (b["master_fp32"] + b["adam_moments_fp32"]) == fx["total_bytes_per_param"]
 
 
 def test_null_arguments_fail_before_any_gpu_call(sdp):

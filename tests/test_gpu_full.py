@@ -129,7 +129,7 @@ def test_qwen3_8b_layer_device_full(sdp):
 
 @pytest.mark.timeout(400)
 def test_qwen25_72b_layer_device_full(sdp):
-    run_device_workload(sdp, 4, free_running=False)
+    run_device_workload(sdp, 4, free_running=True)
 
 
 @pytest.mark.timeout(400)
