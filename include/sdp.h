@@ -210,6 +210,28 @@ SDP_API int sdp_agg_adam_step(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_s
                       const sdp_adamw_params *hp, int64_t chunk_elems,
                       void *stream, double *grad_norm_out);
 
+/* Device mode for callers that cannot allocate: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation.  As
+ * sdp_agg_adam_step on the GPU current to the calling thread, with no
+ * context: the norm partials, the finalize's merge stage and the norm state
+ * live in a static device array of the library (4 MiB on each GPU it runs
+ * on, held until the process ends; its address on a GPU is looked up on the
+ * first call there).  The call allocates nothing, host or device.  The mean
+ * gradient is not stored: the update reads the R gradient buffers again.
+ * Limits: at most SDP_NOALLOC_MAX_SEGMENTS segments and SDP_NOALLOC_MAX_TILES
+ * norm tiles in all (sum of ceil(numel / SDP_NORM_TILE), up to 2^30
+ * elements); larger calls are rejected with SDP_ERR_INVALID_ARGUMENT before
+ * anything else is checked.  Every call on a GPU uses that GPU's one array:
+ * calls that overlap on one GPU (other streams, other threads) race, calls
+ * on one stream are ordered.  Asynchronous on `stream` unless grad_norm_out
+ * is non-NULL (then it waits and reports the norm, and SDP_ERR_NONFINITE
+ * for a non-finite one, states unchanged).  Results equal sdp_agg_adam_step's
+ * bit for bit. */
+#define SDP_NOALLOC_MAX_SEGMENTS 64
+#define SDP_NOALLOC_MAX_TILES 16384
+SDP_API int sdp_agg_adam_step_noalloc(const sdp_segment *segs, int32_t n_segs, const sdp_adamw_params *hp,
+                                      void *stream, double *grad_norm_out);
+
 /* Streamed mode: the same update with the states in host memory, as the
  * paper keeps them, moved through the GPU in chunks whose transfers overlap
  * the previous chunk's work, a staging buffer being refilled only after its

@@ -9,7 +9,7 @@ ROOT = os.path.dirname(HERE)
 LIB_PATH = os.path.join(HERE, "libsdp.so")
 SOURCES = [os.path.join(HERE, "csrc", f)
            for f in ("sdp_runtime.hip", "sdp_stream.hip", "sdp_host_route.hip", "sdp_kernels.hip",
-                     "sdp_copy.hip")]
+                     "sdp_copy.hip", "sdp_noalloc.hip")]
 # host-only lanes, built with the host compiler: no fused multiply-add, so the
 # FP64 update rounds every product and sum as written
 HOST_SOURCES = [os.path.join(HERE, "csrc", f) for f in ("sdp_host_adamw.cpp", "sdp_schedule.cpp")]

@@ -33,6 +33,8 @@ SDP_FLAG_DEBUG_POISON = 0x8
 SDP_FLAG_STREAM_STAGED = 0x10
 SDP_FLAG_HOST_PIN_THREADS = 0x20
 SDP_FLAG_STREAM_HOST_CAST = 0x40
+SDP_NOALLOC_MAX_SEGMENTS = 64
+SDP_NOALLOC_MAX_TILES = 16384
 SDP_DELIVER_HOST_CAST = 0
 SDP_DELIVER_DEVICE_CAST = 1
 SDP_GBAR_F32 = 0
@@ -126,6 +128,7 @@ def _load():
         "sdp_probe_link": (ctypes.c_int, [vp, vp, vp, vp, vp, i64, i64, i32, P(dbl)]),
         "sdp_probe_link_kernel": (ctypes.c_int, [vp, vp, vp, vp, vp, i64, i64, i32, P(dbl)]),
         "sdp_probe_memcpy": (ctypes.c_int, [vp, vp, vp, i64, vp]),
+        "sdp_agg_adam_step_noalloc": (ctypes.c_int, [vp, i32, vp, vp, P(dbl)]),
         "sdp_host_alloc": (ctypes.c_int, [P(vp), ctypes.c_size_t]),
         "sdp_host_free": (ctypes.c_int, [vp]),
         "sdp_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -215,6 +218,15 @@ def sdp_agg_adam_step(ctx, segs: Segments, hp: sdp_adamw_params, chunk_elems: in
     norm = ctypes.c_double(float("nan"))
     rc = _lib.sdp_agg_adam_step(ctx, segs.ptr, segs.n, ctypes.byref(hp), chunk_elems,
                                 _stream(stream), ctypes.byref(norm) if want_norm else None)
+    _check(rc, norm.value)
+    return norm.value if want_norm else None
+
+
+def sdp_agg_adam_step_noalloc(segs: Segments, hp: sdp_adamw_params, stream=None,
+                              want_norm: bool = False) -> Optional[float]:
+    norm = ctypes.c_double(float("nan"))
+    rc = _lib.sdp_agg_adam_step_noalloc(segs.ptr, segs.n, ctypes.byref(hp), _stream(stream),
+                                        ctypes.byref(norm) if want_norm else None)
     _check(rc, norm.value)
     return norm.value if want_norm else None
 
