@@ -426,18 +426,21 @@ def measure_rates(args, torch, np, sdp, ctx, link, dres):
     t1, t2 = per_call_us(n1, 40), per_call_us(n2, 6)
     host_adam_gbs = 30 * (n2 - n1) / ((t2 - t1) * 1e3)
     host_task_us = max(0.0, t1 - 30 * n1 / (host_adam_gbs * 1e3))
-    # the same lane while a device-to-host copy streams into pinned memory (as
-    # in the host-update route): how much host memory bandwidth each DMA byte
-    # takes from it
-    src_d = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
-    dst_h = torch.empty(1 << 30, dtype=torch.uint8, pin_memory=True)
+    # the same lane while a device-to-host copy streams into pinned memory as
+    # in the host-update route -- 128 MiB copies into two pinned buffers used
+    # in turn, the route's stage buffers at 32M-element chunks: how much host
+    # memory bandwidth each DMA byte takes from it
+    piece = 128 << 20
+    n_copies = 48
+    src_d = torch.empty(piece, dtype=torch.uint8, device="cuda")
+    dst_h = [torch.empty(piece, dtype=torch.uint8, pin_memory=True) for _ in range(2)]
     side = torch.cuda.Stream()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     with torch.cuda.stream(side):
         e0.record(side)
-        for _ in range(12):
-            dst_h.copy_(src_d, non_blocking=True)
+        for k in range(n_copies):
+            dst_h[k % 2].copy_(src_d, non_blocking=True)
         e1.record(side)
     time.sleep(0.005)  # the copies are running
     # timed as the lane alone was (best of three rounds), and per call less
@@ -450,7 +453,7 @@ def measure_rates(args, torch, np, sdp, ctx, link, dres):
         lane_dma_us = min(lane_dma_us, (time.perf_counter() - t0) / 6 * 1e6)
     busy = not e1.query()  # the copies outlasted the lane's timing
     torch.cuda.synchronize()
-    d2h_gbs_meas = 12 * (1 << 30) / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    d2h_gbs_meas = n_copies * piece / (e0.elapsed_time(e1) * 1e-3) / 1e9
     host_adam_dma_gbs = 30 * n2 / (max(lane_dma_us - host_task_us, 1.0) * 1e3)
     del src_d, dst_h, st, pb
     # the model gives a host task min(its own rate, host_gbs - cost * DMA
@@ -718,11 +721,22 @@ def host_route_leg(args, torch, np, synth, sdp, rates):
         # timed by the library around those calls: the model's per-piece
         # host cost of this schedule
         issue_us = kt.host_issue_ms * 1e3 / max(kt.host_issues, 1)
-        if rates is not None:
-            rates.host_issue_us = issue_us
         k = args.stream_steps
         host_bytes = (26 + gsz) * N  # p, m, v read and written, g_bar read, BF16 params written
         adam_s = kt.host_adam_ms / k / 1e3
+        route_rates = None
+        if rates is not None:
+            # The host lane as it runs in this route, beside the route's own
+            # device-to-host copies: its bytes over the host threads' busy
+            # time, from the library's timers.  That rate already carries
+            # what those copies take from host memory, so the model's DMA
+            # cost per byte is the byte itself.  (The lane timed beside
+            # torch's device-to-host copies runs slower than it does here;
+            # that probe's cost stays in the streamed schedules' rates.)
+            route_rates = type(rates).from_buffer_copy(rates)
+            route_rates.host_issue_us = issue_us
+            route_rates.host_adam_gbs = host_bytes / adam_s / 1e9
+            route_rates.dma_host_cost = 1.0
         # host memory carries the host lane's bytes and the copies' bytes
         bound = max((host_bytes + gsz * N) / (host_copy * 1e9), gsz * N / (d2h * 1e9))
         out[name] = dict(ms_per_step=el * 1e3, params_per_s=N / el, d2h_bytes_per_param=gsz, host_issue_us=issue_us,
@@ -731,20 +745,26 @@ def host_route_leg(args, torch, np, synth, sdp, rates):
                          host_adam_gbs=host_bytes / adam_s / 1e9, host_adam_params_per_s=N / adam_s,
                          bound_ms=bound * 1e3, frac_of_bound=bound / el)
         sched = sdp.SDP_SCHED_HOST_ROUTE_BF16 if fmt == sdp.SDP_GBAR_BF16 else sdp.SDP_SCHED_HOST_ROUTE_F32
-        if rates is not None:
-            out[name]["predicted_ms"] = sdp.sdp_predict_step(sched, [N], R, C, 0, rates).predicted_ms
+        if route_rates is not None:
+            out[name]["predicted_ms"] = sdp.sdp_predict_step(sched, [N], R, C, 0, route_rates).predicted_ms
+            out[name]["model_rates"] = {f: getattr(route_rates, f) for f, _ in route_rates._fields_}
         log(f"host route leg {name}: {el * 1e3:.1f} ms/step, host AdamW {kt.host_adam_ms / k:.1f} ms "
             f"({host_bytes / adam_s / 1e9:.1f} GB/s), waits {kt.host_wait_ms / k:.1f} ms")
         if rates is not None and not args.no_extra:
             log(f"host route leg {name}: chunk sweep")
 
             def run_at(c, fmt=fmt):
+                # the median of five steps: a step here takes 30-50 ms of
+                # host work, and a single slow one (other load on the host's
+                # memory) would otherwise move the mean by several percent
                 sdp.sdp_host_update_step(ctx, segs, sdp.make_params(**w.hparams(1)), c, fmt)
-                t0 = time.perf_counter()
-                for t in (2, 3, 4):
+                times = []
+                for t in range(2, 7):
+                    t0 = time.perf_counter()
                     sdp.sdp_host_update_step(ctx, segs, sdp.make_params(**w.hparams(t)), c, fmt)
-                return (time.perf_counter() - t0) / 3 * 1e3
-            out[name]["chunk_sweep"] = chunk_sweep(sdp, sched, [N], R, rates, run_at)
+                    times.append(time.perf_counter() - t0)
+                return sorted(times)[2] * 1e3
+            out[name]["chunk_sweep"] = chunk_sweep(sdp, sched, [N], R, route_rates, run_at)
     # core scaling of the host AdamW alone on the same layer (the paper's
     # CPU Adam scaling microbenchmark)
     gb = np.full(N, 1e-3, np.float32)
@@ -852,6 +872,81 @@ def full_model_leg(args, torch, np, synth, sdp, link):
     return out
 
 
+def clock_trace(torch, np, synth, sdp, cid=4, idle_s=2.0, n_steps=40):
+    """Device-mode steps of workload `cid` right after an idle GPU, each timed
+    by events on the stream, beside the GPU's current core and memory clock
+    levels, read from the driver's sysfs DPM files every 2 ms by a thread.
+    Shows the warm-up ramp and what the clocks do during it."""
+    import glob
+    import threading
+    files = {}
+    for k in ("pp_dpm_sclk", "pp_dpm_mclk"):
+        fs = sorted(glob.glob(f"/sys/class/drm/card*/device/{k}"))
+        if fs:
+            files[k] = fs[0]
+
+    def level(path):
+        try:
+            for line in open(path):
+                if line.strip().endswith("*"):
+                    return float(line.split(":")[1].strip().rstrip("*").strip().lower().rstrip("mhz"))
+        except (OSError, ValueError):
+            return None
+        return None
+
+    w = synth.workload(cid)
+    N, R = w.numel, w.ranks
+    dev = torch.device("cuda:0")
+    p = torch.from_numpy(synth.master(w, 0)).to(dev)
+    m = torch.zeros(N, dtype=torch.float32, device=dev)
+    v = torch.zeros(N, dtype=torch.float32, device=dev)
+    pb = torch.zeros(N, dtype=torch.int16, device=dev)
+    g = [torch.from_numpy(synth.grad_bf16(w, 0, 1, r).view(np.int16)).to(dev) for r in range(R)]
+    ctx = sdp.sdp_ctx_create(0, 0, R, 0)
+    segs = sdp.segments_from_tensors([(p, m, v, pb, g)])
+    s = torch.cuda.current_stream()
+    for t in range(1, 11):  # compiled, resident, then idle
+        sdp.sdp_agg_adam_step(ctx, segs, sdp.make_params(**w.hparams(t)), w.chunk, s.cuda_stream)
+    torch.cuda.synchronize()
+    samples, stop = [], [False]
+    t_base = time.perf_counter()
+
+    def sampler():
+        while not stop[0]:
+            samples.append((time.perf_counter() - t_base, {k: level(f) for k, f in files.items()}))
+            time.sleep(0.002)
+
+    th = threading.Thread(target=sampler)
+    th.start()
+    time.sleep(idle_s)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(n_steps + 1)]
+    t_start = time.perf_counter() - t_base
+    evs[0].record(s)
+    for k in range(n_steps):
+        sdp.sdp_agg_adam_step(ctx, segs, sdp.make_params(**w.hparams(11 + k)), w.chunk, s.cuda_stream)
+        evs[k + 1].record(s)
+    torch.cuda.synchronize()
+    time.sleep(0.02)
+    stop[0] = True
+    th.join()
+    sdp.sdp_ctx_destroy(ctx)
+    ends = [evs[0].elapsed_time(evs[k + 1]) for k in range(n_steps)]
+    rows = []
+    for k in range(n_steps):
+        a = t_start + (ends[k - 1] if k else 0.0) / 1e3
+        b = t_start + ends[k] / 1e3
+        inside = [d for t, d in samples if a <= t <= b] or [min(samples, key=lambda x: abs(x[0] - b))[1]]
+        row = {"step": k + 1, "ms": ends[k] - (ends[k - 1] if k else 0.0)}
+        for key in files:
+            vals = sorted(x[key] for x in inside if x[key] is not None)
+            row[key.replace("pp_dpm_", "") + "_mhz"] = vals[len(vals) // 2] if vals else None
+        rows.append(row)
+    idle = [d for t, d in samples if t < t_start]
+    return {"clock_trace": {"workload": w.name, "params": N, "ranks": R, "idle_s": idle_s,
+                            "dpm_files": files, "samples": len(samples),
+                            "idle_levels": idle[-1] if idle else None, "steps": rows}}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -865,6 +960,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the chunk sweeps, the staged layer run and parameter delivery")
+    ap.add_argument("--clock-trace", action="store_true",
+                    help="only trace the device steps of the Qwen2.5-72B layer after an idle GPU, "
+                         "beside the GPU's clock levels, and print that as JSON")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -883,6 +981,9 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     torch.cuda.set_device(0)
+    if args.clock_trace:
+        print(json.dumps(clock_trace(torch, np, synth, sdp)), flush=True)
+        return
     # the headline: the Qwen2.5-72B layer in HBM
     head, master, host_grads, w = device_leg(args, torch, np, synth, sdp, 4, args.steps, args.warmup, False)
     ceiling = copy_ceiling(torch, sdp, head["ctx"], torch.cuda.current_stream())
