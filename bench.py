@@ -192,6 +192,15 @@ def device_leg(args, torch, np, synth, sdp, cid, steps, warmup, pattern):
         norm_gbs=norm_bytes_per_elem * N / norm_s / 1e9, norm_bytes=norm_bytes_per_elem * N,
         grad_norm=norm, clip=clip,
     )
+    if stored:
+        # the g_bar-storing norm pass's own access pattern with trivial
+        # arithmetic (into the context's workspace; the states are not
+        # touched): its traffic-mix ceiling
+        reps = 10
+        with torch.cuda.stream(stream):
+            events_ms(torch, stream, lambda: sdp.sdp_probe_norm_pattern(ctx, segs, sh), 2)
+            ms = events_ms(torch, stream, lambda: sdp.sdp_probe_norm_pattern(ctx, segs, sh), reps)
+        res["norm_pattern_gbs"] = norm_bytes_per_elem * N * reps / (ms * 1e-3) / 1e9
     if pattern:
         # the update's own access pattern with trivial arithmetic (overwrites
         # the states, whose results were read above): its traffic-mix ceiling
@@ -710,20 +719,33 @@ def host_route_leg(args, torch, np, synth, sdp, rates):
                grads="device memory")
     for name, fmt, gsz in (("f32", sdp.SDP_GBAR_F32, 4), ("bf16", sdp.SDP_GBAR_BF16, 2)):
         sdp.sdp_host_update_step(ctx, segs, sdp.make_params(**w.hparams(1)), C, fmt)  # warmup
-        sdp.sdp_ctx_set_timing(ctx, 1)
-        t0 = time.perf_counter()
-        for t in range(2, args.stream_steps + 2):
+        # Each step timed on its own (the library's timers reset per step);
+        # every figure below is the median over the steps: a step is 30 ms of
+        # host work, and one slowed by other load on the host's memory would
+        # move a mean by several percent.
+        per = []
+        for t in range(2, max(args.stream_steps, 5) + 2):
+            sdp.sdp_ctx_set_timing(ctx, 1)
+            t0 = time.perf_counter()
             sdp.sdp_host_update_step(ctx, segs, sdp.make_params(**w.hparams(t)), C, fmt)
-        el = (time.perf_counter() - t0) / args.stream_steps
-        kt = sdp.sdp_ctx_get_timing(ctx)
+            el_t = time.perf_counter() - t0
+            kt = sdp.sdp_ctx_get_timing(ctx)
+            per.append(dict(el=el_t, adam_ms=kt.host_adam_ms, wait_ms=kt.host_wait_ms,
+                            issue_us=kt.host_issue_ms * 1e3 / max(kt.host_issues, 1),
+                            gpu_norm_ms=kt.norm_ms + kt.finalize_ms, gbar_ms=kt.gbar_ms))
         sdp.sdp_ctx_set_timing(ctx, 0)
+
+        def med(key):
+            v = sorted(x[key] for x in per)
+            return v[len(v) // 2]
+
+        el = med("el")
         # the calling thread's time to enqueue one piece (kernel and copy),
         # timed by the library around those calls: the model's per-piece
         # host cost of this schedule
-        issue_us = kt.host_issue_ms * 1e3 / max(kt.host_issues, 1)
-        k = args.stream_steps
+        issue_us = med("issue_us")
         host_bytes = (26 + gsz) * N  # p, m, v read and written, g_bar read, BF16 params written
-        adam_s = kt.host_adam_ms / k / 1e3
+        adam_s = med("adam_ms") / 1e3
         route_rates = None
         if rates is not None:
             # The host lane as it runs in this route, beside the route's own
@@ -740,16 +762,17 @@ def host_route_leg(args, torch, np, synth, sdp, rates):
         # host memory carries the host lane's bytes and the copies' bytes
         bound = max((host_bytes + gsz * N) / (host_copy * 1e9), gsz * N / (d2h * 1e9))
         out[name] = dict(ms_per_step=el * 1e3, params_per_s=N / el, d2h_bytes_per_param=gsz, host_issue_us=issue_us,
-                         gpu_norm_ms=(kt.norm_ms + kt.finalize_ms) / k, gbar_kernel_ms=kt.gbar_ms / k,
-                         host_adam_ms=kt.host_adam_ms / k, host_wait_ms=kt.host_wait_ms / k,
+                         steps=len(per), statistic="median of single steps",
+                         gpu_norm_ms=med("gpu_norm_ms"), gbar_kernel_ms=med("gbar_ms"),
+                         host_adam_ms=adam_s * 1e3, host_wait_ms=med("wait_ms"),
                          host_adam_gbs=host_bytes / adam_s / 1e9, host_adam_params_per_s=N / adam_s,
                          bound_ms=bound * 1e3, frac_of_bound=bound / el)
         sched = sdp.SDP_SCHED_HOST_ROUTE_BF16 if fmt == sdp.SDP_GBAR_BF16 else sdp.SDP_SCHED_HOST_ROUTE_F32
         if route_rates is not None:
             out[name]["predicted_ms"] = sdp.sdp_predict_step(sched, [N], R, C, 0, route_rates).predicted_ms
             out[name]["model_rates"] = {f: getattr(route_rates, f) for f, _ in route_rates._fields_}
-        log(f"host route leg {name}: {el * 1e3:.1f} ms/step, host AdamW {kt.host_adam_ms / k:.1f} ms "
-            f"({host_bytes / adam_s / 1e9:.1f} GB/s), waits {kt.host_wait_ms / k:.1f} ms")
+        log(f"host route leg {name}: {el * 1e3:.1f} ms/step, host AdamW {adam_s * 1e3:.1f} ms "
+            f"({host_bytes / adam_s / 1e9:.1f} GB/s), waits {med('wait_ms'):.1f} ms")
         if rates is not None and not args.no_extra:
             log(f"host route leg {name}: chunk sweep")
 
@@ -1033,6 +1056,8 @@ def main():
                                 f"({head['ms_per_step_with_events']:.4f} ms per step with the events)"},
         "roofline": roofline(head, "update", 4, "fused update from the stored mean gradient (clip+AdamW+BF16)"),
         "norm_roofline": roofline(head, "norm", 4, "norm partials storing the mean gradient"),
+        "norm_pattern_gbs": head.get("norm_pattern_gbs"),
+        "norm_frac_of_pattern": (head["norm_gbs"] / head["norm_pattern_gbs"]) if head.get("norm_pattern_gbs") else None,
         "copy_ceiling_gbs": ceiling,
         "step_frac_of_copy_ceiling": head["step_hbm_gbs"] / max(ceiling.values()),
         "grad_norm_last_step": head["grad_norm"],

@@ -486,6 +486,16 @@ SDP_API int sdp_probe_memcpy(sdp_ctx *ctx, void *dst, const void *src, int64_t b
  * `stream`. */
 SDP_API int sdp_probe_update_pattern(sdp_ctx *ctx, const sdp_segment *seg, void *stream);
 
+/* The norm pass's memory access pattern when it stores the mean gradient,
+ * with trivial arithmetic, on one device-mode segment's gradients (validated
+ * as for sdp_agg_adam_step; the states are not touched): the same grid, lane
+ * mapping, loads, 16-byte stores and span pairs, into the context's own
+ * workspace, under the same residency cap.  Its rate is the HBM ceiling of
+ * that pass's traffic mix (2R bytes read and 4 written per element).
+ * Measurement only; ordered after the context's previous call, asynchronous
+ * on `stream`. */
+SDP_API int sdp_probe_norm_pattern(sdp_ctx *ctx, const sdp_segment *seg, void *stream);
+
 /* Pinned host link bandwidth with the streamed engine's copy path:
  * hipMemcpyAsync in chunk_bytes pieces over `bytes`, `reps` times, host to
  * device on the context's copy stream and device to host on its compute

@@ -104,6 +104,7 @@ hipError_t launch_norm_finalize(const double *partials /* pairs */, int64_t n_pa
 hipError_t launch_update(int R, const UpdateArgs &a, int max_blocks, int lds_pad, hipStream_t s);
 hipError_t launch_gbar_out(int R, const GbarArgs &a, hipStream_t s);
 hipError_t launch_update_pattern(int R, const UpdateArgs &a, int lds_pad, hipStream_t s);
+hipError_t launch_norm_pattern(int R, const NormArgs &a, int store_lds_pad, hipStream_t s);
 hipError_t launch_cast_bf16(const float *src, uint16_t *dst, int64_t n, hipStream_t s);
 hipError_t launch_copy16(void *dst, const void *src, int64_t n16, int max_blocks, hipStream_t s);
 // blocks_per_copy: blocks given to each copy of the batch (at most; fewer

@@ -658,6 +658,44 @@ __global__ __launch_bounds__(kUpdateThreads) void k_update_pattern(UpdateArgs a)
 }
 
 // ---------------------------------------------------------------------------
+// Measurement: the g_bar-storing norm pass's memory access pattern with
+// trivial arithmetic (xor of the ranks' bits instead of the exact mean and
+// the double-double sum of squares): the same grid, lane mapping, loads,
+// 16-byte stores and span pairs, under the same residency cap.  Its rate is
+// the ceiling that the pass's own traffic mix allows on this part.  The
+// ragged tail of fewer than 4 elements is left out.
+
+template <int R>
+__global__ __launch_bounds__(kNormThreads) void k_norm_pattern(NormArgs a) {
+    constexpr int V = 4;
+    constexpr int kGroupsPerSpan = kNormSpan / V;
+    constexpr int kIters = kGroupsPerSpan / kNormThreads;
+    const int64_t full_groups = a.n / V;
+    const int64_t span0 = (int64_t)blockIdx.x * kGroupsPerSpan;
+    uint32_t acc = 0;
+    for (int it = 0; it < kIters; ++it) {
+        const int64_t q = span0 + (int64_t)it * kNormThreads + threadIdx.x;
+        if (q >= full_groups) break;
+        uint32_t x0 = 0, x1 = 0;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            uint32_t w[2];
+            load_stream_v<V>(a.g[r] + q * V, w);
+            x0 ^= w[0];
+            x1 ^= w[1];
+        }
+        store_nt4(a.gbar_out + q * V, make_float4(bf16_lo(x0), bf16_hi(x0), bf16_lo(x1), bf16_hi(x1)));
+        acc ^= x0 ^ x1;
+    }
+    double hi = (double)acc, lo = 0.0;
+    block_merge<kNormThreads>(hi, lo);
+    if (threadIdx.x == 0) {
+        a.partials[2 * blockIdx.x] = hi;
+        a.partials[2 * blockIdx.x + 1] = lo;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Mean gradient for the host-update route: g_bar of a chunk, FP32 or rounded
 // to BF16, written to a staging slot that the copy engine then moves to host
 // memory.  The rank gradients are read once and not reused (non-temporal).
@@ -773,6 +811,13 @@ hipError_t pattern_r(const UpdateArgs &a, int64_t blocks, int lds_pad, hipStream
 }
 
 template <int R>
+hipError_t norm_pattern_r(const NormArgs &a, int store_lds_pad, hipStream_t s) {
+    const int64_t blocks = cdiv(a.n, kTile) * kNormSplit;
+    hipLaunchKernelGGL((k_norm_pattern<R>), dim3((uint32_t)blocks), dim3(kNormThreads), store_lds_pad, s, a);
+    return hipGetLastError();
+}
+
+template <int R>
 hipError_t gbar_r(const GbarArgs &a, int64_t blocks, hipStream_t s) {
     if (a.bf16)
         hipLaunchKernelGGL((k_gbar_out<R, true>), dim3((uint32_t)blocks), dim3(256), 0, s, a);
@@ -828,6 +873,15 @@ hipError_t launch_update_pattern(int R, const UpdateArgs &a, int lds_pad, hipStr
     if (blocks < 1) blocks = 1;
     switch (R) {
 #define CASE(r) case r: return pattern_r<r>(a, blocks, lds_pad, s);
+        SDP_FOR_EACH_R(CASE)
+#undef CASE
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_norm_pattern(int R, const NormArgs &a, int store_lds_pad, hipStream_t s) {
+    switch (R) {
+#define CASE(r) case r: return norm_pattern_r<r>(a, store_lds_pad, s);
         SDP_FOR_EACH_R(CASE)
 #undef CASE
         default: return hipErrorInvalidValue;

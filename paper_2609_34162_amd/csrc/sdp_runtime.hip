@@ -1005,6 +1005,27 @@ int sdp_probe_update_pattern(sdp_ctx *ctx, const sdp_segment *seg, void *stream)
     return SDP_OK;
 }
 
+int sdp_probe_norm_pattern(sdp_ctx *ctx, const sdp_segment *seg, void *stream) {
+    t_err.clear();
+    if (!ctx) return fail(SDP_ERR_INVALID_ARGUMENT, "context is NULL");
+    DeviceGuard guard(ctx->device);
+    int32_t R = 0;
+    SDP_TRY(validate_segments(ctx, seg, 1, kDeviceMem, kDeviceMem, false, &R));
+    const int64_t tiles = cdiv(seg->numel, SDP_NORM_TILE);
+    SDP_TRY(ensure_partials(ctx, tiles));
+    SDP_TRY(ensure_gbar(ctx, seg->numel));
+    hipStream_t s = (hipStream_t)stream;
+    SDP_TRY(order_after_last(ctx, s));
+    sdp::NormArgs a{};
+    for (int32_t r = 0; r < R; ++r) a.g[r] = seg->grads[r];
+    a.n = seg->numel;
+    a.partials = ctx->partials;
+    a.gbar_out = ctx->gbar;
+    HIP_TRY(sdp::launch_norm_pattern(R, a, ctx->norm_store_lds_pad, s));
+    SDP_TRY(mark_done(ctx, s));
+    return SDP_OK;
+}
+
 }  // extern "C"
 
 namespace {

@@ -125,6 +125,7 @@ def _load():
         "sdp_ctx_get_timing": (ctypes.c_int, [vp, P(sdp_kernel_times)]),
         "sdp_probe_copy": (ctypes.c_int, [vp, vp, vp, i64, vp]),
         "sdp_probe_update_pattern": (ctypes.c_int, [vp, vp, vp]),
+        "sdp_probe_norm_pattern": (ctypes.c_int, [vp, vp, vp]),
         "sdp_probe_link": (ctypes.c_int, [vp, vp, vp, vp, vp, i64, i64, i32, P(dbl)]),
         "sdp_probe_link_kernel": (ctypes.c_int, [vp, vp, vp, vp, vp, i64, i64, i32, P(dbl)]),
         "sdp_probe_memcpy": (ctypes.c_int, [vp, vp, vp, i64, vp]),
@@ -364,6 +365,12 @@ def sdp_probe_copy(ctx, dst: int, src: int, nbytes: int, stream=None) -> None:
 
 def sdp_probe_memcpy(ctx, dst: int, src: int, nbytes: int, stream=None) -> None:
     _check(_lib.sdp_probe_memcpy(ctx, dst, src, nbytes, _stream(stream)))
+
+
+def sdp_probe_norm_pattern(ctx, segs: Segments, stream=None) -> None:
+    if segs.n != 1:
+        raise ValueError("sdp_probe_norm_pattern takes one segment")
+    _check(_lib.sdp_probe_norm_pattern(ctx, segs.ptr, _stream(stream)))
 
 
 def sdp_probe_update_pattern(ctx, segs: Segments, stream=None) -> None:

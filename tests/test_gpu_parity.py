@@ -294,6 +294,33 @@ def test_update_pattern_probe(sdp, ctx):
         host.close()
 
 
+def test_norm_pattern_probe(sdp, ctx):
+    """The measurement probe with the g_bar-storing norm pass's access pattern
+    runs on a device segment's gradients, leaves the states and the gradients
+    alone, and a device step after it on the same context is still exact."""
+    n, R = 3 * TILE + 8, 8
+    masters, grads = rand_inputs([n], R, 1, seed=137)
+    dev = DevState(masters, R)
+    dev.set_grads(grads[0])
+    before = dev.host()
+    sdp.sdp_probe_norm_pattern(ctx, dev.segments(sdp), stream())
+    torch.cuda.synchronize()
+    assert states_equal(dev.host(), before)
+    hs, ho = hp_pair(sdp, lr=1e-3, weight_decay=0.05, max_grad_norm=0.2, step=1)
+    norm = sdp.sdp_agg_adam_step(ctx, dev.segments(sdp), hs, 0, stream(), want_norm=True)
+    ref = oracle.State(masters)
+    _, onorm = oracle.step(ref, grads[0], ho)
+    assert norm == onorm
+    check_state(dev.host(), ref)
+    host = HostState(sdp, masters, R)
+    try:
+        with pytest.raises(sdp.SdpError) as e:
+            sdp.sdp_probe_norm_pattern(ctx, host.segments(), stream())
+        assert e.value.status == sdp.SDP_ERR_NOT_DEVICE_MEMORY
+    finally:
+        host.close()
+
+
 @pytest.mark.parametrize("chunk_tiles", [1, 2, 4])
 def test_streamed_matches_oracle_and_device(sdp, ctx, ctx_poison, ctx_nostore, chunk_tiles):
     sizes = [3 * TILE + 5, 1, 70000]
