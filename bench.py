@@ -491,14 +491,23 @@ def measure_rates(args, torch, np, sdp, ctx, link, dres):
     return sdp.make_rates(**vals), vals
 
 
-def chunk_sweep(sdp, schedule, numels, R, rates, run_at):
+def chunk_sweep(sdp, schedule, numels, R, rates, run_at, passes=1):
     """Measured step time at each chunk size beside the model's prediction,
-    and the chunk each would pick."""
+    and the chunk each would pick.  With passes > 1 the chunk sizes are
+    measured that many times, in alternating order, and each keeps its
+    fastest pass: a stretch of other load on the host slows whatever runs
+    during it, and the model predicts an undisturbed step."""
+    meas = {c: [] for c in SWEEP_CHUNKS}
+    for k in range(passes):
+        for c in (SWEEP_CHUNKS if k % 2 == 0 else SWEEP_CHUNKS[::-1]):
+            meas[c].append(run_at(c))
     rows = []
     for c in SWEEP_CHUNKS:
         pr = sdp.sdp_predict_step(schedule, numels, R, c, 0, rates)
-        ms = run_at(c)
+        ms = min(meas[c])
         rows.append(dict(chunk_elems=c, measured_ms=ms, predicted_ms=pr.predicted_ms, bound_ms=pr.bound_ms))
+        if passes > 1:
+            rows[-1]["passes_ms"] = meas[c]
         log(f"  chunk {c >> 20:3d}M: measured {ms:.2f} ms, predicted {pr.predicted_ms:.2f} ms, "
             f"bound {pr.bound_ms:.2f} ms")
     best_pred, _ = sdp.sdp_tune_chunk(schedule, numels, R, 0, rates, SWEEP_CHUNKS)
@@ -787,7 +796,7 @@ def host_route_leg(args, torch, np, synth, sdp, rates):
                     sdp.sdp_host_update_step(ctx, segs, sdp.make_params(**w.hparams(t)), c, fmt)
                     times.append(time.perf_counter() - t0)
                 return sorted(times)[2] * 1e3
-            out[name]["chunk_sweep"] = chunk_sweep(sdp, sched, [N], R, route_rates, run_at)
+            out[name]["chunk_sweep"] = chunk_sweep(sdp, sched, [N], R, route_rates, run_at, passes=2)
     # core scaling of the host AdamW alone on the same layer (the paper's
     # CPU Adam scaling microbenchmark)
     gb = np.full(N, 1e-3, np.float32)
