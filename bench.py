@@ -201,6 +201,21 @@ def device_leg(args, torch, np, synth, sdp, cid, steps, warmup, pattern):
             events_ms(torch, stream, lambda: sdp.sdp_probe_norm_pattern(ctx, segs, sh), 2)
             ms = events_ms(torch, stream, lambda: sdp.sdp_probe_norm_pattern(ctx, segs, sh), reps)
         res["norm_pattern_gbs"] = norm_bytes_per_elem * N * reps / (ms * 1e-3) / 1e9
+        # the same steps without the stored mean gradient (the update reads
+        # the R gradients again: 58 instead of 50 B per element), same data
+        ctx2 = sdp.sdp_ctx_create(0, 0, R, sdp.SDP_FLAG_DEVICE_GBAR_NEVER)
+        for t in range(1, warmup + 1):
+            sdp.sdp_agg_adam_step(ctx2, segs, sdp.make_params(**w.hparams(t)), w.chunk, sh)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for t in range(warmup + 1, warmup + steps + 1):
+            sdp.sdp_agg_adam_step(ctx2, segs, sdp.make_params(**w.hparams(t)), w.chunk, sh)
+        torch.cuda.synchronize()
+        el2 = time.perf_counter() - t0
+        sdp.sdp_ctx_destroy(ctx2)
+        nb, _ = sdp.sdp_bytes_per_elem(False, R, sdp.SDP_FLAG_DEVICE_GBAR_NEVER)
+        res["unstored_gbar"] = dict(ms_per_step=el2 / steps * 1e3, params_per_s=N * steps / el2,
+                                    step_bytes_per_elem=nb, step_hbm_gbs=nb * N * steps / el2 / 1e9)
     if pattern:
         # the update's own access pattern with trivial arithmetic (overwrites
         # the states, whose results were read above): its traffic-mix ceiling
@@ -491,23 +506,27 @@ def measure_rates(args, torch, np, sdp, ctx, link, dres):
     return sdp.make_rates(**vals), vals
 
 
-def chunk_sweep(sdp, schedule, numels, R, rates, run_at, passes=1):
+def chunk_sweep(sdp, schedule, numels, R, rates, run_at, passes=1, rates_after=None):
     """Measured step time at each chunk size beside the model's prediction,
-    and the chunk each would pick.  With passes > 1 the chunk sizes are
-    measured that many times, in alternating order, and each keeps its
-    fastest pass: a stretch of other load on the host slows whatever runs
-    during it, and the model predicts an undisturbed step."""
+    and the chunk each would pick.  run_at(c) returns the times of single
+    steps at chunk c; a chunk's figure is their median.  With passes > 1 the
+    chunk sizes are measured that many times, in alternating order, so that
+    every chunk size sees the same spread of conditions on the host.
+    rates_after(), if given, supplies the model's rates once all the
+    measurements are in (rates measured during the sweep itself)."""
     meas = {c: [] for c in SWEEP_CHUNKS}
     for k in range(passes):
         for c in (SWEEP_CHUNKS if k % 2 == 0 else SWEEP_CHUNKS[::-1]):
-            meas[c].append(run_at(c))
+            meas[c].extend(run_at(c))
+    if rates_after is not None:
+        rates = rates_after()
     rows = []
     for c in SWEEP_CHUNKS:
         pr = sdp.sdp_predict_step(schedule, numels, R, c, 0, rates)
-        ms = min(meas[c])
-        rows.append(dict(chunk_elems=c, measured_ms=ms, predicted_ms=pr.predicted_ms, bound_ms=pr.bound_ms))
-        if passes > 1:
-            rows[-1]["passes_ms"] = meas[c]
+        v = sorted(meas[c])
+        ms = v[len(v) // 2]
+        rows.append(dict(chunk_elems=c, measured_ms=ms, predicted_ms=pr.predicted_ms, bound_ms=pr.bound_ms,
+                         steps=len(v)))
         log(f"  chunk {c >> 20:3d}M: measured {ms:.2f} ms, predicted {pr.predicted_ms:.2f} ms, "
             f"bound {pr.bound_ms:.2f} ms")
     best_pred, _ = sdp.sdp_tune_chunk(schedule, numels, R, 0, rates, SWEEP_CHUNKS)
@@ -517,10 +536,13 @@ def chunk_sweep(sdp, schedule, numels, R, rates, run_at, passes=1):
         r["rel_error"] = (r["predicted_ms"] - r["measured_ms"]) / r["measured_ms"]
     err = [abs(r["rel_error"]) for r in rows]
     mid = [abs(r["rel_error"]) for r in rows if (1 << 22) <= r["chunk_elems"] <= (1 << 25)]
-    return dict(rows=rows, model_pick=best_pred, measured_best=best_meas["chunk_elems"],
-                measured_at_model_pick_ms=at_pick, measured_best_ms=best_meas["measured_ms"],
-                mean_abs_rel_error=sum(err) / len(err), max_abs_rel_error=max(err),
-                max_abs_rel_error_4m_to_32m=max(mid))
+    out = dict(rows=rows, model_pick=best_pred, measured_best=best_meas["chunk_elems"],
+               measured_at_model_pick_ms=at_pick, measured_best_ms=best_meas["measured_ms"],
+               mean_abs_rel_error=sum(err) / len(err), max_abs_rel_error=max(err),
+               max_abs_rel_error_4m_to_32m=max(mid))
+    if rates_after is not None:
+        out["model_rates"] = {f: getattr(rates, f) for f, _ in rates._fields_}
+    return out
 
 
 LINK_COPY_BYTES = (32 << 20, 64 << 20, 128 << 20)  # the update pass's copies at 8M, 16M, 32M-element chunks
@@ -626,10 +648,12 @@ def stream_leg(args, torch, np, synth, sdp, dres):
             cctx = sdp.sdp_ctx_create(0, c, R, 0)
             try:
                 sdp.sdp_stream_step(cctx, segs, sdp.make_params(**w.hparams(1)), c)
-                t0 = time.perf_counter()
-                for t in (2, 3):
+                times = []
+                for t in (2, 3, 4):
+                    t0 = time.perf_counter()
                     sdp.sdp_stream_step(cctx, segs, sdp.make_params(**w.hparams(t)), c)
-                return (time.perf_counter() - t0) / 2 * 1e3
+                    times.append((time.perf_counter() - t0) * 1e3)
+                return times
             finally:
                 sdp.sdp_ctx_destroy(cctx)
         out["chunk_sweep"] = chunk_sweep(sdp, sdp.SDP_SCHED_STREAMED, [N], R, rates, run_at)
@@ -764,10 +788,14 @@ def host_route_leg(args, torch, np, synth, sdp, rates):
             # cost per byte is the byte itself.  (The lane timed beside
             # torch's device-to-host copies runs slower than it does here;
             # that probe's cost stays in the streamed schedules' rates.)
+            # For the same reason host memory must not cap the lane below
+            # that rate while the copies run: the ceiling is raised to at
+            # least the lane's rate plus the copies'.
             route_rates = type(rates).from_buffer_copy(rates)
             route_rates.host_issue_us = issue_us
             route_rates.host_adam_gbs = host_bytes / adam_s / 1e9
             route_rates.dma_host_cost = 1.0
+            route_rates.host_gbs = max(route_rates.host_gbs, route_rates.host_adam_gbs + route_rates.d2h_gbs)
         # host memory carries the host lane's bytes and the copies' bytes
         bound = max((host_bytes + gsz * N) / (host_copy * 1e9), gsz * N / (d2h * 1e9))
         out[name] = dict(ms_per_step=el * 1e3, params_per_s=N / el, d2h_bytes_per_param=gsz, host_issue_us=issue_us,
@@ -785,18 +813,55 @@ def host_route_leg(args, torch, np, synth, sdp, rates):
         if rates is not None and not args.no_extra:
             log(f"host route leg {name}: chunk sweep")
 
+            # Single steps, each timed by the library as well.  The host
+            # lane's busy time per step is bytes / rate + pieces x a cost per
+            # piece (waking the host threads, the last task's tail); both are
+            # fitted, by least squares over the per-chunk medians, to the
+            # lane's own busy times in the sweep's steps (not to the step
+            # times), and the per-piece issue cost is their median.  The
+            # model's host inputs and the measured steps thus see the same
+            # conditions on the host, whose memory other load slows from
+            # time to time by up to 10%.
+            lane, issue = {}, []
+
             def run_at(c, fmt=fmt):
-                # the median of five steps: a step here takes 30-50 ms of
-                # host work, and a single slow one (other load on the host's
-                # memory) would otherwise move the mean by several percent
                 sdp.sdp_host_update_step(ctx, segs, sdp.make_params(**w.hparams(1)), c, fmt)
                 times = []
                 for t in range(2, 7):
+                    sdp.sdp_ctx_set_timing(ctx, 1)
                     t0 = time.perf_counter()
                     sdp.sdp_host_update_step(ctx, segs, sdp.make_params(**w.hparams(t)), c, fmt)
-                    times.append(time.perf_counter() - t0)
-                return sorted(times)[2] * 1e3
-            out[name]["chunk_sweep"] = chunk_sweep(sdp, sched, [N], R, route_rates, run_at, passes=2)
+                    times.append((time.perf_counter() - t0) * 1e3)
+                    kt = sdp.sdp_ctx_get_timing(ctx)
+                    lane.setdefault(c, []).append((kt.host_issues + 1, kt.host_adam_ms))  # pieces, busy ms
+                    issue.append(kt.host_issue_ms * 1e3 / max(kt.host_issues, 1))
+                sdp.sdp_ctx_set_timing(ctx, 0)
+                return times
+
+            def rates_after():
+                pts = []
+                for c, v in lane.items():
+                    v = sorted(v, key=lambda x: x[1])
+                    pts.append((float(v[len(v) // 2][0]), v[len(v) // 2][1]))
+                xm = sum(x for x, _ in pts) / len(pts)
+                ym = sum(y for _, y in pts) / len(pts)
+                slope = (sum((x - xm) * (y - ym) for x, y in pts) / max(sum((x - xm) ** 2 for x, _ in pts), 1e-12))
+                slope = max(slope, 0.0)
+                base_ms = ym - slope * xm
+                r = type(route_rates).from_buffer_copy(route_rates)
+                r.host_adam_gbs = host_bytes / (base_ms * 1e-3) / 1e9
+                r.host_task_us = slope * 1e3
+                r.host_issue_us = sorted(issue)[len(issue) // 2]
+                r.host_gbs = max(r.host_gbs, r.host_adam_gbs + r.d2h_gbs)
+                return r
+            out[name]["chunk_sweep"] = chunk_sweep(sdp, sched, [N], R, route_rates, run_at, passes=2,
+                                                   rates_after=rates_after)
+            # the step at C, predicted with the rates the sweep measured
+            swr = out[name]["chunk_sweep"]["model_rates"]
+            r = type(route_rates).from_buffer_copy(route_rates)
+            for f_, v_ in swr.items():
+                setattr(r, f_, v_)
+            out[name]["predicted_ms"] = sdp.sdp_predict_step(sched, [N], R, C, 0, r).predicted_ms
     # core scaling of the host AdamW alone on the same layer (the paper's
     # CPU Adam scaling microbenchmark)
     gb = np.full(N, 1e-3, np.float32)
@@ -1067,6 +1132,7 @@ def main():
         "norm_roofline": roofline(head, "norm", 4, "norm partials storing the mean gradient"),
         "norm_pattern_gbs": head.get("norm_pattern_gbs"),
         "norm_frac_of_pattern": (head["norm_gbs"] / head["norm_pattern_gbs"]) if head.get("norm_pattern_gbs") else None,
+        "unstored_gbar": head.get("unstored_gbar"),
         "copy_ceiling_gbs": ceiling,
         "step_frac_of_copy_ceiling": head["step_hbm_gbs"] / max(ceiling.values()),
         "grad_norm_last_step": head["grad_norm"],
