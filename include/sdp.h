@@ -123,6 +123,16 @@ extern "C" {
  * library's copy kernel (SDP_D2H_KERNEL_MAX_BYTES overrides).  Combined with
  * SDP_FLAG_STREAM_STAGED it is correct but measured slower. */
 #define SDP_FLAG_STREAM_HOST_CAST 0x40u
+/* Debug aid for the streamed mode, the host-update route and parameter
+ * delivery: before each of their copies and kernels the engines enqueue, on
+ * that stream, a one-wave kernel that sleeps a random 0-200 us, and the
+ * calling thread sleeps a random 0-200 us before each of its waits, host
+ * copies and host updates.  It shifts the timing between the copy stream,
+ * the compute stream and the host, so that a missing wait shows up (with
+ * SDP_FLAG_DEBUG_POISON) as wrong results; results are unchanged otherwise.
+ * The delays come from a per-context generator seeded by SDP_JITTER_SEED
+ * (an unsigned integer; a fixed seed by default). */
+#define SDP_FLAG_DEBUG_JITTER 0x80u
 
 /* ---- types ------------------------------------------------------------- */
 typedef struct sdp_ctx sdp_ctx;

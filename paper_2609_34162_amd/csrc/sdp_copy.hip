@@ -1,6 +1,7 @@
 // gfx950 copy kernel of the streamed engine: a batch of device-to-host
 // copies of one chunk (master, exp_avg, exp_avg_sq and BF16 parameters) in
-// one launch, written straight into pinned host memory.
+// one launch, written straight into pinned host memory.  Also the debug
+// jitter's sleeping kernel.
 #include "sdp_internal.h"
 
 namespace sdp {
@@ -20,7 +21,19 @@ __global__ __launch_bounds__(256) void k_copy_batch(CopyBatch b) {
     if (blockIdx.x == 0 && threadIdx.x < tail) b.dst[k][n16 * 16 + threadIdx.x] = b.src[k][n16 * 16 + threadIdx.x];
 }
 
+// The debug jitter's delay: a fixed number of s_sleep 64 (about 4,096
+// clocks each), then the wave ends.
+__global__ __launch_bounds__(64) void k_sleep(int sleeps) {
+    for (int i = 0; i < sleeps; ++i) __builtin_amdgcn_s_sleep(64);
+}
+
 }  // namespace
+
+hipError_t launch_sleep(int sleeps, hipStream_t s) {
+    if (sleeps < 0 || sleeps > 4096) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_sleep, dim3(1), dim3(64), 0, s, sleeps);
+    return hipGetLastError();
+}
 
 hipError_t launch_copy_batch(const CopyBatch &b, int blocks_per_copy, hipStream_t s) {
     if (b.n < 1 || b.n > kCopyBatchMax || blocks_per_copy < 1) return hipErrorInvalidValue;

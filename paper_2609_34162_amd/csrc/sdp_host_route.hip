@@ -89,12 +89,14 @@ int host_route(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R,
         a.n = c.len;
         a.out = dev;
         a.bf16 = bf16 ? 1 : 0;
+        SDP_TRY(jitter_stream(ctx, sc));
         hipEvent_t t0 = timed_begin(ctx, sc);
         HIP_TRY(sdp::launch_gbar_out(R, a, sc));
         timed_end(ctx, sc, t0, kGbar, c.len);
         // h2d_done doubles as "g_bar of this slot is written" here
         HIP_TRY(hipEventRecord(ctx->h2d_done[sl], sc));
         HIP_TRY(hipStreamWaitEvent(sy, ctx->h2d_done[sl], 0));
+        SDP_TRY(jitter_stream(ctx, sy));
         SDP_TRY(d2h_copies(ctx, {{host, dev}}, {(size_t)c.len * esz}, sy, &ctx->stage_map));
         HIP_TRY(hipEventRecord(ctx->slot_free[sl], sy));  // in the host buffer; the slot is free
         used[sl] = true;
@@ -106,6 +108,7 @@ int host_route(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R,
         const Clock::time_point ti = Clock::now();
         if (j + 1 < chunks.size()) SDP_TRY(issue(j + 1));
         const int sl = (int)(j & 1);
+        jitter_host(ctx);
         const Clock::time_point t0 = Clock::now();
         HIP_TRY(hipEventSynchronize(ctx->slot_free[sl]));
         const Clock::time_point t1 = Clock::now();
@@ -184,6 +187,8 @@ int deliver(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf16, int64_t 
         const int sl = (int)(k & 1);
         const int64_t len = std::min(chunk_elems, n - off);
         char *bin = ctx->stage ? ctx->stage + (size_t)sl * stage_bytes(ctx) : nullptr;
+        jitter_host(ctx);
+        if ((rc = jitter_stream(ctx, ctx->s_copy)) != SDP_OK) break;
         if (mode == SDP_DELIVER_HOST_CAST) {
             // host threads round chunk k while the DMA still moves chunk k-1
             if (ctx->stage_used[sl] && hipEventSynchronize(ctx->h2d_done[sl]) != hipSuccess) {
@@ -219,6 +224,7 @@ int deliver(sdp_ctx *ctx, const float *host_master, uint16_t *dev_bf16, int64_t 
             if (rc != SDP_OK) break;
             if (hipEventRecord(ctx->h2d_done[sl], ctx->s_copy) != hipSuccess ||
                 hipStreamWaitEvent(ctx->s_comp, ctx->h2d_done[sl], 0) != hipSuccess ||
+                jitter_stream(ctx, ctx->s_comp) != SDP_OK ||
                 sdp::launch_cast_bf16(slot.p, dev_bf16 + off, len, ctx->s_comp) != hipSuccess ||
                 hipEventRecord(ctx->slot_free[sl], ctx->s_comp) != hipSuccess)
                 rc = fail(SDP_ERR_HIP, "sdp_deliver_params: enqueue failed");

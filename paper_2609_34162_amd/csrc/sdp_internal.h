@@ -111,5 +111,8 @@ hipError_t launch_copy16(void *dst, const void *src, int64_t n16, int max_blocks
 // when a copy is short).
 hipError_t launch_copy_batch(const CopyBatch &b, int blocks_per_copy, hipStream_t s);
 hipError_t launch_fill_u32(void *dst, int64_t n_words, uint32_t value, hipStream_t s);
+// One wave that sleeps `sleeps` times for about 64 x 64 clocks each (a fixed
+// count: it always ends); the debug jitter's delay on a stream.
+hipError_t launch_sleep(int sleeps, hipStream_t s);
 
 }  // namespace sdp

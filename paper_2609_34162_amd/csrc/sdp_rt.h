@@ -225,6 +225,7 @@ struct sdp_ctx {
     int64_t max_chunk = 0;
     int32_t max_ranks = 0;
     uint32_t flags = 0;
+    uint64_t jitter_state = 0;  // SDP_FLAG_DEBUG_JITTER's generator (xorshift64*)
     hipStream_t s_copy = nullptr, s_comp = nullptr;
     hipEvent_t h2d_done[2] = {nullptr, nullptr};
     hipEvent_t slot_free[2] = {nullptr, nullptr};
@@ -324,6 +325,12 @@ int read_norm(sdp_ctx *ctx, hipStream_t s, NormState *out);
 int device_norm(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int32_t R, const Plan &plan, bool store_gbar,
                 double max_grad_norm, hipStream_t s);
 int sync_streams(sdp_ctx *ctx);
+
+// SDP_FLAG_DEBUG_JITTER: a random delay of 0-200 us enqueued on stream s
+// (jitter_stream), or slept by the calling thread (jitter_host); nothing
+// without the flag.
+int jitter_stream(sdp_ctx *ctx, hipStream_t s);
+void jitter_host(sdp_ctx *ctx);
 
 // ---- chunks and staging slots -------------------------------------------
 

@@ -357,6 +357,32 @@ int mark_done(sdp_ctx *ctx, hipStream_t s) {
     return SDP_OK;
 }
 
+namespace {
+// xorshift64* (Vigna): the next draw of the context's jitter generator, as
+// a number in [0, bound)
+uint32_t jitter_draw(sdp_ctx *ctx, uint32_t bound) {
+    uint64_t x = ctx->jitter_state;
+    x ^= x >> 12;
+    x ^= x << 25;
+    x ^= x >> 27;
+    ctx->jitter_state = x;
+    return (uint32_t)(((x * 2685821657736338717ull) >> 32) % bound);
+}
+}  // namespace
+
+int jitter_stream(sdp_ctx *ctx, hipStream_t s) {
+    if (!(ctx->flags & SDP_FLAG_DEBUG_JITTER)) return SDP_OK;
+    // s_sleep 64 is about 4,096 clocks, 1.7-1.8 us at the clocks measured:
+    // up to 116 of them is up to about 200 us
+    HIP_TRY(sdp::launch_sleep((int)jitter_draw(ctx, 117), s));
+    return SDP_OK;
+}
+
+void jitter_host(sdp_ctx *ctx) {
+    if (!(ctx->flags & SDP_FLAG_DEBUG_JITTER)) return;
+    std::this_thread::sleep_for(std::chrono::microseconds(jitter_draw(ctx, 201)));
+}
+
 int read_norm(sdp_ctx *ctx, hipStream_t s, NormState *out) {
     HIP_TRY(hipMemcpyAsync(ctx->ns_host, ctx->ns, sizeof(NormState), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
@@ -663,7 +689,7 @@ int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems, int32_t m
     SDP_TRY(check_chunk(max_chunk_elems, true));
     const uint32_t known = SDP_FLAG_DEVICE_GBAR_NEVER | SDP_FLAG_DEVICE_GBAR_ALWAYS | SDP_FLAG_STREAM_GBAR_NEVER |
                            SDP_FLAG_DEBUG_POISON | SDP_FLAG_STREAM_STAGED | SDP_FLAG_HOST_PIN_THREADS |
-                           SDP_FLAG_STREAM_HOST_CAST;
+                           SDP_FLAG_STREAM_HOST_CAST | SDP_FLAG_DEBUG_JITTER;
     if (flags & ~known) return fail(SDP_ERR_INVALID_ARGUMENT, "unknown context flags 0x%x", flags & ~known);
     if ((flags & SDP_FLAG_DEVICE_GBAR_NEVER) && (flags & SDP_FLAG_DEVICE_GBAR_ALWAYS))
         return fail(SDP_ERR_INVALID_ARGUMENT, "DEVICE_GBAR_NEVER and DEVICE_GBAR_ALWAYS are exclusive");
@@ -676,6 +702,9 @@ int sdp_ctx_create(sdp_ctx **out, int device, int64_t max_chunk_elems, int32_t m
     c->max_chunk = max_chunk_elems;
     c->max_ranks = max_ranks;
     c->flags = flags;
+    c->jitter_state = 0x9E3779B97F4A7C15ull;
+    if (const char *env = std::getenv("SDP_JITTER_SEED")) c->jitter_state ^= std::strtoull(env, nullptr, 10);
+    if (c->jitter_state == 0) c->jitter_state = 1;  // xorshift's one fixed point
     if (const char *env = std::getenv("SDP_UPDATE_MAX_BLOCKS")) c->update_max_blocks = std::max(0, std::atoi(env));
     int rc = SDP_OK;
     auto bail = [&](int status) {

@@ -83,6 +83,8 @@ std::vector<Xfer> merge_runs(std::vector<Xfer> xs) {
 // copies to leave it.
 int copy_in(sdp_ctx *ctx, int sl, int bi, const std::vector<Xfer> &xs, int width) {
     char *dev = ctx->staging + (size_t)sl * ctx->slot_bytes;
+    jitter_host(ctx);
+    SDP_TRY(jitter_stream(ctx, ctx->s_copy));
     if (!staged(ctx)) {
         for (const Xfer &x : xs)
             HIP_TRY(hipMemcpyAsync(dev + x.off, x.host, x.bytes, hipMemcpyHostToDevice, ctx->s_copy));
@@ -107,6 +109,7 @@ int copy_out(sdp_ctx *ctx, int sl, int bo, const std::vector<Xfer> &xs) {
     char *dev = ctx->staging + (size_t)sl * ctx->slot_bytes;
     std::vector<std::pair<char *, const char *>> ends;
     std::vector<size_t> bytes;
+    SDP_TRY(jitter_stream(ctx, ctx->s_comp));
     if (!staged(ctx)) {
         for (const Xfer &x : xs) {
             ends.push_back({x.host, dev + x.off});
@@ -133,6 +136,7 @@ int copy_out(sdp_ctx *ctx, int sl, int bo, const std::vector<Xfer> &xs) {
 // (SDP_FLAG_STREAM_HOST_CAST).
 int drain(sdp_ctx *ctx, int bo, int width) {
     if (ctx->pending_out[bo].empty() && ctx->pending_cast[bo].empty()) return SDP_OK;
+    jitter_host(ctx);
     HIP_TRY(hipEventSynchronize(ctx->d2h_done[bo]));
     char *bout = ctx->bounce_out + (size_t)bo * 14 * (size_t)ctx->max_chunk;
     std::vector<Job> jobs;
@@ -171,6 +175,7 @@ int stream_norm_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t n_segs, int
         SDP_TRY(copy_in(ctx, sl, (int)(k % kInBufs), xs, 0));
         HIP_TRY(hipEventRecord(ctx->h2d_done[sl], ctx->s_copy));
         HIP_TRY(hipStreamWaitEvent(ctx->s_comp, ctx->h2d_done[sl], 0));
+        SDP_TRY(jitter_stream(ctx, ctx->s_comp));
         SDP_TRY(norm_launch(ctx, R, gp, c.len, tile_partials(ctx, plan.tile_base[c.seg] + c.off / SDP_NORM_TILE),
                             store_gbar ? ctx->gbar + plan.gbar_base[c.seg] + c.off : nullptr, ctx->s_comp));
         SDP_TRY(poison(ctx, sl));
@@ -214,6 +219,7 @@ int stream_update_phase(sdp_ctx *ctx, const sdp_segment *segs, int32_t R, const 
         HIP_TRY(hipStreamWaitEvent(ctx->s_comp, ctx->h2d_done[sl], 0));
         const uint16_t *gp[SDP_MAX_RANKS];
         for (int32_t r = 0; r < R; ++r) gp[r] = slot.g[r];
+        SDP_TRY(jitter_stream(ctx, ctx->s_comp));
         SDP_TRY(update_launch(ctx, R, hp, slot.p, slot.m, slot.v, slot.pb, gp,
                               stored_gbar ? ctx->gbar + plan.gbar_base[c.seg] + c.off : nullptr, c.len, ctx->s_comp));
         std::vector<Xfer> out = {{off_in_slot(ctx, sl, slot.p), (char *)(g.master + c.off), f4},

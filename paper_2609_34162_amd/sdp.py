@@ -33,6 +33,7 @@ SDP_FLAG_DEBUG_POISON = 0x8
 SDP_FLAG_STREAM_STAGED = 0x10
 SDP_FLAG_HOST_PIN_THREADS = 0x20
 SDP_FLAG_STREAM_HOST_CAST = 0x40
+SDP_FLAG_DEBUG_JITTER = 0x80
 SDP_NOALLOC_MAX_SEGMENTS = 64
 SDP_NOALLOC_MAX_TILES = 16384
 SDP_DELIVER_HOST_CAST = 0

@@ -128,5 +128,5 @@ def test_null_arguments_fail_before_any_gpu_call(sdp):
     assert L.sdp_ctx_create(ctypes.byref(out), 0, 0, 0, 0) == sdp.SDP_ERR_INVALID_ARGUMENT  # max_ranks 0
     assert L.sdp_ctx_create(ctypes.byref(out), 0, 1000, 4, 0) == sdp.SDP_ERR_INVALID_ARGUMENT  # chunk
     assert L.sdp_ctx_create(ctypes.byref(out), 0, 0, 4, 3) == sdp.SDP_ERR_INVALID_ARGUMENT  # exclusive flags
-    assert L.sdp_ctx_create(ctypes.byref(out), 0, 0, 4, 0x80) == sdp.SDP_ERR_INVALID_ARGUMENT  # unknown flag
+    assert L.sdp_ctx_create(ctypes.byref(out), 0, 0, 4, 0x100) == sdp.SDP_ERR_INVALID_ARGUMENT  # unknown flag
     assert "unknown" in sdp.sdp_last_error()
