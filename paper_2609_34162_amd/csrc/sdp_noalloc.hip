@@ -17,7 +17,6 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
-#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <mutex>
@@ -30,6 +29,7 @@ namespace sdprt {
 int fail(int status, const char *fmt, ...);
 extern thread_local std::string t_err;
 int check_hparams(const sdp_adamw_params *hp);
+void fill_consts(const sdp_adamw_params *hp, sdp::UpdateArgs &a);
 }  // namespace sdprt
 
 namespace {
@@ -222,9 +222,8 @@ int sdp_agg_adam_step_noalloc(const sdp_segment *segs, int32_t n_segs, const sdp
         tile_base += (segs[s].numel / SDP_NORM_TILE + (segs[s].numel % SDP_NORM_TILE != 0));
     }
     NA_HIP(sdp::launch_norm_finalize(partials, tiles * sdp::kNormSplit, merged, hp->max_grad_norm, ns, st));
-    // the fused update, reading the clip coefficient from the norm state
-    const double t = (double)hp->step;
-    const double bc1 = 1.0 - std::pow(hp->beta1, t), bc2 = 1.0 - std::pow(hp->beta2, t);
+    // the fused update, reading the clip coefficient from the norm state,
+    // with the per-step constants computed as for every other mode
     for (int32_t s = 0; s < n_segs; ++s) {
         const sdp_segment &g = segs[s];
         sdp::UpdateArgs a{};
@@ -236,14 +235,7 @@ int sdp_agg_adam_step_noalloc(const sdp_segment *segs, int32_t n_segs, const sdp
         a.gbar = nullptr;
         a.n = g.numel;
         a.ns = ns;
-        a.lr_wd = hp->lr * hp->weight_decay;
-        a.beta1 = hp->beta1;
-        a.one_minus_beta1 = 1.0 - hp->beta1;
-        a.beta2 = hp->beta2;
-        a.one_minus_beta2 = 1.0 - hp->beta2;
-        a.step_size = hp->lr / bc1;
-        a.inv_bc2 = 1.0 / bc2;
-        a.eps = hp->eps;
+        sdprt::fill_consts(hp, a);
         NA_HIP(sdp::launch_update(R, a, 0, dev.update_lds_pad, st));
     }
     if (grad_norm_out) {
