@@ -81,3 +81,42 @@ def test_qwen2_5_72b_layer_full_size_equals_context_step():
         assert states_equal(b.host(), a.host())
     finally:
         sdp.sdp_ctx_destroy(ctx)
+
+
+@pytest.mark.gpu
+@pytest.mark.big
+def test_at_the_tile_limit_equals_context_step():
+    """Exactly SDP_NOALLOC_MAX_TILES norm tiles (16,383 of one segment, whose
+    last is ragged, and one of a second): the workspace's last span pairs and
+    merge-stage pairs are used.  Bit for bit against sdp_agg_adam_step, two
+    steps, inputs generated on the GPU."""
+    sdp = need_gpu()
+    stream = torch.cuda.current_stream().cuda_stream
+    sizes = [(sdp.SDP_NOALLOC_MAX_TILES - 1) * TILE - 3, 3]
+    R = 2
+    log(f"no-alloc step at the tile limit: sizes {sizes} R={R}")
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    grads = [[(torch.randn(n, generator=gen, device="cuda") * 1e-3).to(torch.bfloat16).view(torch.int16)
+              for _ in range(R)] for n in sizes]
+    masters = [torch.randn(n, generator=gen, device="cuda") * 0.02 for n in sizes]
+
+    def fresh():
+        return [(p.clone(), torch.zeros_like(p), torch.zeros_like(p), torch.zeros(p.numel(), dtype=torch.int16,
+                                                                                device="cuda"), g)
+                for p, g in zip(masters, grads)]
+
+    a, b = fresh(), fresh()
+    ctx = sdp.sdp_ctx_create(0, 0, R, 0)
+    try:
+        for t in (1, 2):
+            hs = sdp.make_params(lr=1e-3, weight_decay=0.05, max_grad_norm=0.2, step=t)
+            n_ctx = sdp.sdp_agg_adam_step(ctx, sdp.segments_from_tensors(a), hs, 0, stream, want_norm=True)
+            n_na = sdp.sdp_agg_adam_step_noalloc(sdp.segments_from_tensors(b), hs, stream, want_norm=True)
+            torch.cuda.synchronize()
+            assert n_na == n_ctx, t
+            for sa, sb in zip(a, b):
+                for x, y in zip(sa[:4], sb[:4]):
+                    assert torch.equal(x.view(torch.int32) if x.dtype == torch.float32 else x,
+                                       y.view(torch.int32) if y.dtype == torch.float32 else y), f"step {t}"
+    finally:
+        sdp.sdp_ctx_destroy(ctx)
