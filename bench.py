@@ -334,7 +334,34 @@ def cpu_leg(args, np, synth, oracle, master, host_grads, w):
     return dict(value=w.numel * steps / el, unit="params/s", cores=cores, kind="oracle",
                 sample=f"{steps} full oracle steps of the {w.name} workload "
                        f"({w.numel} params, R={w.ranks}), {el:.1f} s",
-                one_thread=dict(workload=t.name, params_per_s=one, steps=t.steps))
+                one_thread=dict(workload=t.name, params_per_s=one, steps=t.steps),
+                host=host_cpus())
+
+
+def host_cpus():
+    """The host's CPUs as this process sees them: model, logical CPUs, the
+    CPUs this process may run on, sockets and NUMA nodes (from /proc and
+    /sys; nothing is bound)."""
+    out = {"logical_cpus": os.cpu_count(), "affinity_cpus": len(os.sched_getaffinity(0))}
+    try:
+        sockets, model = set(), None
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                k, _, v = line.partition(":")
+                k = k.strip()
+                if k == "model name" and model is None:
+                    model = v.strip()
+                elif k == "physical id":
+                    sockets.add(v.strip())
+        out["model"] = model
+        out["sockets"] = len(sockets) or None
+    except OSError:
+        pass
+    try:
+        out["numa_nodes"] = len([d for d in os.listdir("/sys/devices/system/node") if d.startswith("node")])
+    except OSError:
+        pass
+    return out
 
 
 SWEEP_CHUNKS = [1 << 20, 1 << 21, 1 << 22, 1 << 23, 1 << 24, 1 << 25]  # 4-128 MiB per FP32 state array
