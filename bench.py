@@ -223,7 +223,7 @@ def device_leg(args, torch, np, synth, sdp, cid, steps, warmup, pattern):
         with torch.cuda.stream(stream):
             events_ms(torch, stream, lambda: sdp.sdp_probe_update_pattern(ctx, segs, sh), 2)
             ms = events_ms(torch, stream, lambda: sdp.sdp_probe_update_pattern(ctx, segs, sh), reps)
-        res["pattern_gbs"] = (2 * R + 26) * N * reps / (ms * 1e-3) / 1e9
+        res["pattern_gbs"] = upd_bytes_per_elem * N * reps / (ms * 1e-3) / 1e9
     res["ctx"] = ctx
     res["_keep"] = (p, m, v, pb, g)
     return res, master, host_grads, w
@@ -1109,7 +1109,7 @@ def main():
         print(json.dumps(clock_trace(torch, np, synth, sdp)), flush=True)
         return
     # the headline: the Qwen2.5-72B layer in HBM
-    head, master, host_grads, w = device_leg(args, torch, np, synth, sdp, 4, args.steps, args.warmup, False)
+    head, master, host_grads, w = device_leg(args, torch, np, synth, sdp, 4, args.steps, args.warmup, True)
     ceiling = copy_ceiling(torch, sdp, head["ctx"], torch.cuda.current_stream())
     log("copy ceiling: " + ", ".join(f"{k} {v:.0f} GB/s" for k, v in ceiling.items()))
     release(torch, sdp, head)
@@ -1162,6 +1162,8 @@ def main():
         "norm_pattern_gbs": head.get("norm_pattern_gbs"),
         "norm_frac_of_pattern": (head["norm_gbs"] / head["norm_pattern_gbs"]) if head.get("norm_pattern_gbs") else None,
         "unstored_gbar": head.get("unstored_gbar"),
+        "update_pattern_gbs": head["pattern_gbs"],
+        "update_frac_of_pattern": head["update_gbs"] / head["pattern_gbs"],
         "copy_ceiling_gbs": ceiling,
         "step_frac_of_copy_ceiling": head["step_hbm_gbs"] / max(ceiling.values()),
         "grad_norm_last_step": head["grad_norm"],

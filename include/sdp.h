@@ -490,10 +490,11 @@ SDP_API int sdp_probe_memcpy(sdp_ctx *ctx, void *dst, const void *src, int64_t b
 
 /* The fused update's memory access pattern with trivial arithmetic, on one
  * device-mode segment (validated as for sdp_agg_adam_step): the same loads
- * and stores, widths and lane mapping, FP32 adds instead of AdamW.  Its rate
- * is the HBM ceiling of the update's own traffic mix.  Measurement only: it
- * overwrites the segment's states and BF16 params.  Asynchronous on
- * `stream`. */
+ * and stores, widths and lane mapping, FP32 adds instead of AdamW; from the
+ * R gradients, or from stored g_bar (the context's workspace) where the
+ * context's device mode stores it (R > 4 by default).  Its rate is the HBM
+ * ceiling of the update's own traffic mix.  Measurement only: it overwrites
+ * the segment's states and BF16 params.  Asynchronous on `stream`. */
 SDP_API int sdp_probe_update_pattern(sdp_ctx *ctx, const sdp_segment *seg, void *stream);
 
 /* The norm pass's memory access pattern when it stores the mean gradient,

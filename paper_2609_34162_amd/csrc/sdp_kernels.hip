@@ -618,10 +618,11 @@ __global__ __launch_bounds__(kUpdateThreads) void k_update(UpdateArgs a) {
 // ---------------------------------------------------------------------------
 // Measurement: the fused update's memory access pattern with trivial
 // arithmetic (integer and FP32 adds instead of the FP64 AdamW), the same
-// loads, stores, widths and lane mapping.  Its rate is the ceiling that the
-// update's own traffic mix allows on this part.  Overwrites the states.
+// loads, stores, widths and lane mapping, from the R gradients or (CACHED)
+// from stored g_bar.  Its rate is the ceiling that the update's own traffic
+// mix allows on this part.  Overwrites the states.
 
-template <int R>
+template <int R, bool CACHED>
 __global__ __launch_bounds__(kUpdateThreads) void k_update_pattern(UpdateArgs a) {
     float *__restrict__ P = a.p;
     float *__restrict__ M = a.m;
@@ -634,11 +635,16 @@ __global__ __launch_bounds__(kUpdateThreads) void k_update_pattern(UpdateArgs a)
     for (int64_t q = gid; q < groups; q += stride) {
         const int64_t e0 = q * kUpdVec;
         uint32_t x = 0;
+        if constexpr (CACHED) {
+            const float4 t = load_nt4(a.gbar + e0);
+            x = __float_as_uint(t.x) ^ __float_as_uint(t.y) ^ __float_as_uint(t.z) ^ __float_as_uint(t.w);
+        } else {
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-            uint32_t w[2];
-            load_stream_v<4>(a.g[r] + e0, w);
-            x ^= w[0] ^ w[1];
+            for (int r = 0; r < R; ++r) {
+                uint32_t w[2];
+                load_stream_v<4>(a.g[r] + e0, w);
+                x ^= w[0] ^ w[1];
+            }
         }
         const float gx = __uint_as_float((x & 0x007fffffu) | 0x3f800000u);
         float4 pv = load_nt4(P + e0), mv = load_nt4(M + e0), vv = load_nt4(V + e0);
@@ -806,7 +812,10 @@ hipError_t update_r(const UpdateArgs &a, int64_t blocks, int lds_pad, hipStream_
 
 template <int R>
 hipError_t pattern_r(const UpdateArgs &a, int64_t blocks, int lds_pad, hipStream_t s) {
-    hipLaunchKernelGGL((k_update_pattern<R>), dim3((uint32_t)blocks), dim3(kUpdateThreads), lds_pad, s, a);
+    if (a.gbar)
+        hipLaunchKernelGGL((k_update_pattern<1, true>), dim3((uint32_t)blocks), dim3(kUpdateThreads), lds_pad, s, a);
+    else
+        hipLaunchKernelGGL((k_update_pattern<R, false>), dim3((uint32_t)blocks), dim3(kUpdateThreads), lds_pad, s, a);
     return hipGetLastError();
 }
 

@@ -1030,7 +1030,16 @@ int sdp_probe_update_pattern(sdp_ctx *ctx, const sdp_segment *seg, void *stream)
     a.pb = seg->param_bf16;
     for (int32_t r = 0; r < R; ++r) a.g[r] = seg->grads[r];
     a.n = seg->numel;
-    HIP_TRY(sdp::launch_update_pattern(R, a, ctx->update_lds_pad, (hipStream_t)stream));
+    hipStream_t s = (hipStream_t)stream;
+    if (device_gbar(ctx, R)) {
+        // the update as device mode runs it here: from stored g_bar (the
+        // context's workspace; its contents do not matter to the pattern)
+        SDP_TRY(ensure_gbar(ctx, seg->numel));
+        SDP_TRY(order_after_last(ctx, s));
+        a.gbar = ctx->gbar;
+    }
+    HIP_TRY(sdp::launch_update_pattern(R, a, ctx->update_lds_pad, s));
+    if (a.gbar) SDP_TRY(mark_done(ctx, s));
     return SDP_OK;
 }
 

@@ -274,17 +274,27 @@ def test_residency_cap_does_not_change_results(sdp, R, monkeypatch):
         assert nm == norms[0]
 
 
-def test_update_pattern_probe(sdp, ctx):
+@pytest.mark.parametrize("R", [4, 8])
+def test_update_pattern_probe(sdp, ctx, R):
     """The measurement probe with the update's access pattern runs on device
-    segments (and writes its trivial results over the states) and refuses
-    host memory."""
-    n, R = 3 * TILE + 8, 4
+    segments (and writes its trivial results over the states), from the
+    gradients at R = 4 and from the context's stored g_bar at R = 8, and
+    refuses host memory; a device step after it is still exact."""
+    n = 3 * TILE + 8
     masters, grads = rand_inputs([n], R, 1, seed=131)
     dev = DevState(masters, R)
     dev.set_grads(grads[0])
     sdp.sdp_probe_update_pattern(ctx, dev.segments(sdp), stream())
     torch.cuda.synchronize()
     assert not np.array_equal(dev.host().master[0], masters[0])
+    after = DevState(masters, R)
+    after.set_grads(grads[0])
+    hs, ho = hp_pair(sdp, lr=1e-3, weight_decay=0.05, max_grad_norm=0.2, step=1)
+    norm = sdp.sdp_agg_adam_step(ctx, after.segments(sdp), hs, 0, stream(), want_norm=True)
+    ref = oracle.State(masters)
+    _, onorm = oracle.step(ref, grads[0], ho)
+    assert norm == onorm
+    check_state(after.host(), ref)
     host = HostState(sdp, masters, R)
     try:
         with pytest.raises(sdp.SdpError) as e:
