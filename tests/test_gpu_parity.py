@@ -363,6 +363,32 @@ def test_streamed_matches_oracle_and_device(sdp, ctx, ctx_poison, ctx_nostore, c
             host.close()
 
 
+@pytest.mark.parametrize("R", [1, 5, 8, 16])
+@pytest.mark.parametrize("flags", ["plain", "gbar_never", "staged"])
+def test_streamed_ranks_equal_device_mode(sdp, ctx, R, flags):
+    """Streamed mode over the rank counts the slot layout depends on (the
+    norm pass's R arrays back to back, the update's R gradient arrays when
+    g_bar is not kept), with the slots poisoned: device mode's bits."""
+    sizes = [2 * TILE + 7, 33]
+    masters, grads = rand_inputs(sizes, R, 2, seed=171 + R)
+    f = sdp.SDP_FLAG_DEBUG_POISON | {"plain": 0, "gbar_never": sdp.SDP_FLAG_STREAM_GBAR_NEVER,
+                                     "staged": sdp.SDP_FLAG_STREAM_STAGED}[flags]
+    c = sdp.sdp_ctx_create(0, TILE, 16, f)
+    dev = DevState(masters, R)
+    host = PageableState(sdp, masters, R) if flags == "staged" else HostState(sdp, masters, R)
+    try:
+        for t in (1, 2):
+            hs = sdp.make_params(lr=1e-3, weight_decay=0.05, max_grad_norm=0.2, step=t)
+            dn = dev_step(sdp, ctx, dev, grads[t - 1], hs)
+            host.set_grads(grads[t - 1])
+            sn = sdp.sdp_stream_step(c, host.segments(), hs, TILE)
+            assert sn == dn
+            assert states_equal(host.host(), dev.host()), f"R={R} {flags} step {t}"
+    finally:
+        host.close()
+        sdp.sdp_ctx_destroy(c)
+
+
 @pytest.mark.parametrize("staged", [False, True])
 def test_d2h_copy_kernel_equals_runtime_copies(sdp, ctx, staged, monkeypatch):
     """Device-to-host copies through the library's copy kernel (every copy,
